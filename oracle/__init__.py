@@ -1,0 +1,177 @@
+"""CPU oracle for the PULSE patch codec -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The GPU library never imports, links or
+calls it, and it imports nothing from the GPU library.
+
+The arithmetic lives in ``oracle.c`` (plain single-threaded C, one function per
+passage of the paper, see its header).  This module only compiles it with gcc
+and marshals numpy arrays into it with ctypes.
+
+    bf16_rne(x)                      App. A.2 / App. D round-to-nearest-even cast
+    cast(w)                          Sec. 3: the BF16 view of an FP32 tensor
+    encode(w_new, snap, ...)         Sec. 4.2 Alg. 1 Encode, App. H.5 Alg. 3
+    apply(dst, idx, val, ...)        Sec. 4.2 Alg. 1 Decode, App. H.5 Alg. 4
+    loco(delta, residual, tau, ...)  Sec. 4.3 Alg. 2 (s = Delta + e, selection, error feedback)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_CFLAGS = ["-O2", "-ffp-contract=off", "-fno-fast-math", "-std=c11", "-shared", "-fPIC"]
+
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c into liboracle.so next to it (gcc, no FP contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", *_CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            lib = ctypes.CDLL(build())
+            u64, u32, f32, vp = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_float, ctypes.c_void_p
+            lib.oracle_bf16_rne.argtypes = [f32]
+            lib.oracle_bf16_rne.restype = ctypes.c_uint16
+            lib.oracle_bf16_value.argtypes = [ctypes.c_uint16]
+            lib.oracle_bf16_value.restype = ctypes.c_double
+            lib.oracle_cast.argtypes = [vp, vp, u64]
+            lib.oracle_cast.restype = None
+            lib.oracle_encode.argtypes = [vp, vp, u64, u32, vp, vp, u64, u64, vp]
+            lib.oracle_encode.restype = u64
+            lib.oracle_apply.argtypes = [vp, u64, vp, vp, u64, u64, u32]
+            lib.oracle_apply.restype = u64
+            lib.oracle_loco.argtypes = [vp, vp, u64, f32, vp, u32, vp, vp, u64, u64]
+            lib.oracle_loco.restype = u64
+            _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle arrays must be C-contiguous"
+    return a.ctypes.data
+
+
+def _f32(a) -> np.ndarray:
+    a = np.asarray(a)
+    assert a.dtype == np.float32, a.dtype
+    return np.ascontiguousarray(a)
+
+
+def _u16(a) -> np.ndarray:
+    a = np.asarray(a)
+    assert a.dtype == np.uint16, a.dtype
+    return np.ascontiguousarray(a)
+
+
+def bf16_rne(x: float) -> int:
+    """BF16 bit pattern of one FP32 value (round to nearest, ties to even)."""
+    return int(_load().oracle_bf16_rne(float(np.float32(x))))
+
+
+def bf16_value(b: int) -> float:
+    """The real value of a BF16 bit pattern."""
+    return float(_load().oracle_bf16_value(int(b) & 0xFFFF))
+
+
+def cast(w: np.ndarray) -> np.ndarray:
+    """Dense BF16 view (uint16 bit patterns) of an FP32 array."""
+    w = _f32(w)
+    out = np.empty(w.shape, dtype=np.uint16)
+    _load().oracle_cast(_ptr(w), _ptr(out), w.size)
+    return out
+
+
+def cast_u32(bits: np.ndarray) -> np.ndarray:
+    """Same as cast(), for FP32 given as raw uint32 bit patterns (any pattern, NaNs included)."""
+    bits = np.ascontiguousarray(bits, dtype=np.uint32)
+    return cast(bits.view(np.float32))
+
+
+def encode(w_new, snap, index_base: int = 0, capacity: int | None = None, count_in: int = 0,
+           idx_out: np.ndarray | None = None, val_out: np.ndarray | None = None,
+           refresh: np.ndarray | None = None):
+    """Alg. 1 Encode on one tensor.
+
+    Returns (count, idx, val): ``count`` is the true total (count_in + changed),
+    ``idx``/``val`` are the output arrays (only entries below ``capacity`` are written).
+    """
+    w_new, snap = _f32(w_new).ravel(), _u16(snap).ravel()
+    assert w_new.size == snap.size
+    n = w_new.size
+    if capacity is None:
+        capacity = count_in + n
+    if idx_out is None:
+        idx_out = np.zeros(capacity, dtype=np.uint32)
+    if val_out is None:
+        val_out = np.zeros(capacity, dtype=np.uint16)
+    assert idx_out.dtype == np.uint32 and val_out.dtype == np.uint16
+    assert idx_out.size >= capacity and val_out.size >= capacity
+    if refresh is not None:
+        assert refresh.dtype == np.uint16 and refresh.size == n and refresh.flags["C_CONTIGUOUS"]
+    assert 0 <= index_base and index_base + n <= 2**32
+    count = _load().oracle_encode(_ptr(w_new), _ptr(snap), n, index_base, _ptr(idx_out),
+                                  _ptr(val_out), capacity, count_in, _ptr(refresh))
+    return int(count), idx_out, val_out
+
+
+def apply(dst: np.ndarray, idx, val, begin: int = 0, end: int | None = None,
+          index_base: int = 0) -> int:
+    """Alg. 1 Decode in place: dst[idx[k]-index_base] = val[k] for k in [begin, end).
+
+    Returns the number of entries skipped because their index lies outside dst.
+    """
+    assert dst.dtype == np.uint16 and dst.flags["C_CONTIGUOUS"]
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    val = _u16(val)
+    if end is None:
+        end = idx.size
+    assert 0 <= begin <= end <= min(idx.size, val.size)
+    return int(_load().oracle_apply(_ptr(dst), dst.size, _ptr(idx), _ptr(val), begin, end,
+                                    index_base))
+
+
+def loco(delta, residual: np.ndarray, tau: float, theta=None, index_base: int = 0,
+         capacity: int | None = None, count_in: int = 0,
+         idx_out: np.ndarray | None = None, val_out: np.ndarray | None = None):
+    """Alg. 2 sparsification with error feedback; ``residual`` is updated in place.
+
+    Returns (count, idx, val) like :func:`encode`.
+    """
+    delta = _f32(delta).ravel()
+    assert residual.dtype == np.float32 and residual.flags["C_CONTIGUOUS"]
+    assert residual.size == delta.size
+    n = delta.size
+    if theta is not None:
+        theta = _f32(theta).ravel()
+        assert theta.size == n
+    if capacity is None:
+        capacity = count_in + n
+    if idx_out is None:
+        idx_out = np.zeros(capacity, dtype=np.uint32)
+    if val_out is None:
+        val_out = np.zeros(capacity, dtype=np.float32)
+    assert idx_out.size >= capacity and val_out.size >= capacity
+    assert 0 <= index_base and index_base + n <= 2**32
+    count = _load().oracle_loco(_ptr(delta), _ptr(residual), n, float(np.float32(tau)),
+                                _ptr(theta), index_base, _ptr(idx_out), _ptr(val_out),
+                                capacity, count_in)
+    return int(count), idx_out, val_out

@@ -1,0 +1,184 @@
+/*
+ * oracle.c -- plain, single-threaded CPU oracle for the PULSE patch codec.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the reference the GPU library is
+ * checked against.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load it.  It shares no code, header, table or constant
+ * generator with the GPU library and must never be linked into it.
+ *
+ * Every function below follows a passage of the paper (arXiv 2602.03839,
+ * "PULSE: compute-visible sparsification") and is written as the plain
+ * definition of what that passage computes, not as a fast kernel:
+ *
+ *   oracle_bf16_rne      App. A.2, Def. "Update Absorption" (RNE cell rule) and
+ *                        App. D (round-to-nearest-even is the rounding mode).
+ *   oracle_cast          Sec. 3 "Sparsity metric": the BF16 view of the FP32 master.
+ *   oracle_encode        Sec. 4.2, Alg. 1 Encode (changed set and its values) and
+ *                        App. H.5, Alg. 3 (per-tensor mask, bitwise compare).
+ *   oracle_apply         Sec. 4.2, Alg. 1 Decode (W_t[I] <- V) and App. H.5,
+ *                        Alg. 4 (direct value assignment, no FP arithmetic).
+ *   oracle_loco          Sec. 4.3, Alg. 2: s = Delta + e, the selection, and the
+ *                        error-feedback update e[I] <- 0, e[not I] <- s.
+ *
+ * Readings where the paper is silent (all listed in the design notes):
+ *   - A NaN input casts to a quiet NaN that keeps the sign and the leading
+ *     payload bits (IEEE 754-2019 6.2.3 NaN propagation; the paper never meets NaN).
+ *   - Overflow rounds to +-inf exactly as IEEE RNE with an unbounded exponent.
+ *   - Subnormals are rounded like any other value (no flush to zero).
+ *   - Equality of BF16 values is bitwise, so +0 and -0 differ (Sec. 3 metric).
+ *   - Output entries beyond `capacity` are not written; the returned count is
+ *     still the true total.  `refresh` is written only for emitted entries.  In
+ *     the sparsifier an entry that was selected but not emitted stays in the
+ *     residual (it was not sent, so error feedback keeps it).
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -shared -fPIC -o liboracle.so oracle.c -lm
+ * (no FMA contraction is possible: the only FP arithmetic is one add or one
+ * subtract per element, and exact double-precision distance comparisons).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+static float float_from_bits(uint32_t u)
+{
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+static uint32_t bits_from_float(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return u;
+}
+
+/* Value of a BF16 bit pattern, as a double (every BF16 value is exact in double). */
+double oracle_bf16_value(uint16_t b)
+{
+    return (double)float_from_bits((uint32_t)b << 16);
+}
+
+/*
+ * FP32 -> BF16, round to nearest, ties to even (App. A.2 and App. D).
+ *
+ * By definition: take the two BF16 values that bracket x in magnitude -- the
+ * truncation `lo` (upper 16 bits of x) and the next BF16 magnitude `hi` --
+ * measure both distances exactly in double, return the nearer one, and on a
+ * tie return the one whose last mantissa bit is 0.  When `lo` is the largest
+ * finite BF16, `hi` is infinity and its distance is measured to 2^128, the
+ * value the next step would have with an unbounded exponent (IEEE overflow
+ * rule for round-to-nearest).
+ */
+uint16_t oracle_bf16_rne(float x)
+{
+    uint32_t u = bits_from_float(x);
+    if (isnan(x))
+        return (uint16_t)((u >> 16) | 0x0040); /* keep sign and top payload, set the quiet bit */
+    uint16_t lo = (uint16_t)(u >> 16);
+    if (isinf(x))
+        return lo;
+    uint16_t hi = (uint16_t)(lo + 1); /* next magnitude, same sign */
+
+    double ax = fabs((double)x);
+    double alo = fabs(oracle_bf16_value(lo));
+    double ahi = ((hi & 0x7FFF) == 0x7F80) ? ldexp(1.0, 128) : fabs(oracle_bf16_value(hi));
+    double d_lo = ax - alo; /* both differences are exact in double */
+    double d_hi = ahi - ax;
+
+    if (d_lo < d_hi)
+        return lo;
+    if (d_hi < d_lo)
+        return hi;
+    return (lo & 1) ? hi : lo;
+}
+
+/* Dense BF16 view of an FP32 tensor: dst[i] = bf16(src[i]). */
+void oracle_cast(const float *src, uint16_t *dst, uint64_t n)
+{
+    for (uint64_t i = 0; i < n; i++)
+        dst[i] = oracle_bf16_rne(src[i]);
+}
+
+/*
+ * Encode one tensor (Alg. 1 Encode, Alg. 3 per-tensor body):
+ *   I = { i : bf16(w_new[i]) != snap[i] }   (bitwise),   V = bf16(w_new)[I],
+ * emitted in ascending i as (index_base + i, value) at positions
+ * count_in, count_in + 1, ...  Returns count_in + |I|.
+ */
+uint64_t oracle_encode(const float *w_new, const uint16_t *snap, uint64_t n, uint32_t index_base,
+                       uint32_t *idx, uint16_t *val, uint64_t capacity, uint64_t count_in,
+                       uint16_t *refresh)
+{
+    uint64_t count = count_in;
+    for (uint64_t i = 0; i < n; i++) {
+        uint16_t b = oracle_bf16_rne(w_new[i]);
+        if (b != snap[i]) {
+            if (count < capacity) {
+                idx[count] = (uint32_t)(index_base + i);
+                val[count] = b;
+                if (refresh)
+                    refresh[i] = b;
+            }
+            count++;
+        }
+    }
+    return count;
+}
+
+/*
+ * Apply a patch (Alg. 1 Decode, Alg. 4): dst[idx[k] - index_base] = val[k]
+ * for k in [begin, end).  Entries whose index falls outside the tensor are
+ * skipped and counted; the function returns that count.
+ */
+uint64_t oracle_apply(uint16_t *dst, uint64_t n, const uint32_t *idx, const uint16_t *val,
+                      uint64_t begin, uint64_t end, uint32_t index_base)
+{
+    uint64_t rejected = 0;
+    for (uint64_t k = begin; k < end; k++) {
+        if (idx[k] < index_base || (uint64_t)(idx[k] - index_base) >= n) {
+            rejected++;
+            continue;
+        }
+        dst[idx[k] - index_base] = val[k];
+    }
+    return rejected;
+}
+
+/*
+ * PULSELoCo-style sparsification with error feedback (Alg. 2, lines forming
+ * s, the selected set, and the residual update):
+ *   a_i = fl32(delta_i + e_i)
+ *   selected iff |a_i| >= tau                                  (theta == NULL)
+ *   selected iff bf16(theta_i) != bf16(fl32(theta_i - a_i))    (theta != NULL,
+ *                                          the compute-visibility gate, Sec. 4.1)
+ *   selected and emitted:  (index_base + i, a_i) is written, e_i = +0
+ *   otherwise:             e_i = a_i
+ * Returns count_in + number selected.
+ */
+uint64_t oracle_loco(const float *delta, float *residual, uint64_t n, float tau,
+                     const float *theta, uint32_t index_base, uint32_t *idx, float *val,
+                     uint64_t capacity, uint64_t count_in)
+{
+    uint64_t count = count_in;
+    for (uint64_t i = 0; i < n; i++) {
+        float a = delta[i] + residual[i];
+        int selected;
+        if (theta) {
+            float after = theta[i] - a;
+            selected = oracle_bf16_rne(theta[i]) != oracle_bf16_rne(after);
+        } else {
+            selected = fabsf(a) >= tau;
+        }
+        if (selected && count < capacity) {
+            idx[count] = (uint32_t)(index_base + i);
+            val[count] = a;
+            residual[i] = 0.0f;
+        } else {
+            residual[i] = a;
+        }
+        if (selected)
+            count++;
+    }
+    return count;
+}

@@ -1,0 +1,256 @@
+"""Pins for the oracle's encode / apply / sparsify (CPU only).
+
+References used here, none of them the oracle itself:
+* torch's CPU BF16 cast (library) for every non-NaN value that decides a mask;
+* numpy fancy-index assignment (library) for apply;
+* numpy FP32 addition (library) for s = Delta + e;
+* brute force over every change mask of tiny tensors;
+* the lossless proposition of App. H.6 (Decode(W_{t-1}, Encode(W_t, W_{t-1})) == W_t
+  bitwise, also along chains);
+* the error-feedback identity of Alg. 2 on exactly representable inputs: after
+  any number of rounds, the sum of everything sent plus the residual equals the
+  sum of all pseudo-gradients.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2602_03839_amd import workloads as wl
+
+
+def tcast(f32: np.ndarray) -> np.ndarray:
+    """torch CPU cast to BF16 bit patterns (library reference; only used on non-NaN)."""
+    f32 = np.ascontiguousarray(f32, dtype=np.float32)
+    return torch.from_numpy(f32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def bits(*vals):
+    return np.array(vals, dtype=np.uint32).view(np.float32)
+
+
+# special FP32 values: grid point, ties (even / odd neighbours), +-0, subnormal,
+# +-max finite, +-inf.  (NaN is exercised separately.)
+SPECIAL = bits(0x3F800000, 0x3F808000, 0x3F818000, 0x00000000, 0x80000000, 0x00018000,
+               0x007F8000, 0x7F7F0000, 0xFF7F0000, 0x7F7F8000, 0x7F800000, 0xFF800000,
+               0xBE4CCCCD, 0x3C23D70A)
+
+
+# --------------------------------------------------------------------------- encode
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 10])
+def test_encode_brute_force_all_masks(oracle_mod, n):
+    """Every subset of positions as the change set, over special values."""
+    rng = np.random.default_rng(n)
+    for mask_bits in range(1 << n):
+        w = SPECIAL[rng.integers(0, SPECIAL.size, n)]
+        s = tcast(w)
+        changed = np.array([(mask_bits >> i) & 1 for i in range(n)], dtype=bool)
+        # perturb the snapshot where a change is wanted (flip the last bit, or +-0)
+        s_prev = s.copy()
+        s_prev[changed] ^= np.uint16(1)
+        base = int(rng.integers(0, 1000))
+        count, idx, val = oracle_mod.encode(w, s_prev, index_base=base)
+        want_i = np.flatnonzero(changed)
+        assert count == want_i.size
+        np.testing.assert_array_equal(idx[:count], want_i + base)
+        np.testing.assert_array_equal(val[:count], s[want_i])
+
+
+def test_encode_counts_and_lossless_on_c1(oracle_mod):
+    """Config c1: nnz == mismatch count, ascending unique indices, lossless apply."""
+    w, w_new = wl.c1_inputs()
+    snap = tcast(w)
+    target = tcast(w_new)
+    count, idx, val = oracle_mod.encode(w_new, snap)
+    mism = np.flatnonzero(target != snap)
+    assert count == mism.size
+    np.testing.assert_array_equal(idx[:count], mism)
+    np.testing.assert_array_equal(val[:count], target[mism])
+    assert np.all(np.diff(idx[:count].astype(np.int64)) > 0)
+    r = snap.copy()
+    assert oracle_mod.apply(r, idx, val, 0, count) == 0
+    np.testing.assert_array_equal(r, target)            # App. H.6, Prop. lossless
+    # density of the configuration: "roughly 1%" (variance reading of N(0, x))
+    assert 0.008 < count / w.size < 0.011
+
+
+def test_encode_chain_lossless(oracle_mod):
+    """Prop. lossless along a chain of 12 patches (snapshot refreshed in place)."""
+    rng = np.random.default_rng(7)
+    n = 50_000
+    w = rng.normal(0, math.sqrt(wl.W_VAR), n).astype(np.float32)
+    snap = tcast(w)
+    receiver = snap.copy()
+    for _ in range(12):
+        w = wl.adam_step_np(w, wl.adam_direction_np(rng, n), 3e-6)
+        count, idx, val = oracle_mod.encode(w, snap, refresh=snap)
+        oracle_mod.apply(receiver, idx, val, 0, count)
+        np.testing.assert_array_equal(snap, tcast(w))
+        np.testing.assert_array_equal(receiver, tcast(w))
+
+
+def test_encode_capacity_append_refresh(oracle_mod):
+    rng = np.random.default_rng(3)
+    n = 4096
+    w = rng.normal(0, 0.1, n).astype(np.float32)
+    snap = tcast(w)
+    flip = rng.random(n) < 0.2
+    snap[flip] ^= np.uint16(0x0004)
+    truth = np.flatnonzero(flip)
+    target = tcast(w)
+    # append after 5 existing entries, capacity cuts the patch short
+    cap = 5 + truth.size // 2
+    idx = np.full(cap, 0xDEADBEEF, np.uint32)
+    val = np.full(cap, 0xABCD, np.uint16)
+    ref = snap.copy()
+    count, _, _ = oracle_mod.encode(w, snap, index_base=100, capacity=cap, count_in=5,
+                                    idx_out=idx, val_out=val, refresh=ref)
+    assert count == 5 + truth.size                     # true total despite the overflow
+    assert np.all(idx[:5] == 0xDEADBEEF) and np.all(val[:5] == 0xABCD)
+    emitted = truth[: cap - 5]
+    np.testing.assert_array_equal(idx[5:], emitted + 100)
+    np.testing.assert_array_equal(val[5:], target[emitted])
+    # refresh only for emitted entries
+    want_ref = snap.copy()
+    want_ref[emitted] = target[emitted]
+    np.testing.assert_array_equal(ref, want_ref)
+
+
+def test_encode_nan_and_signed_zero(oracle_mod):
+    w = bits(0x7FC00001, 0xFF800001, 0x00000000, 0x80000000)
+    snap = np.array([0x7FC0, 0xFFC0, 0x8000, 0x8000], np.uint16)
+    count, idx, val = oracle_mod.encode(w, snap)
+    # +0 vs -0 differ bitwise (Sec. 3: equality is bitwise); NaNs with equal bits are equal
+    assert count == 1 and idx[0] == 2 and val[0] == 0x0000
+
+
+# --------------------------------------------------------------------------- apply
+
+def test_apply_matches_numpy_and_rejects_out_of_range(oracle_mod):
+    rng = np.random.default_rng(4)
+    n = 10_000
+    dst = rng.integers(0, 1 << 16, n, dtype=np.uint16)
+    k = 777
+    j = np.sort(rng.choice(n, k, replace=False)).astype(np.uint32)
+    v = rng.integers(0, 1 << 16, k, dtype=np.uint16)
+    base = 12345
+    idx = j + base
+    bad = np.array([base - 1, base + n, 0xFFFFFFFF], dtype=np.uint32)
+    idx_all = np.concatenate([idx[:300], bad, idx[300:]])
+    val_all = np.concatenate([v[:300], np.zeros(3, np.uint16), v[300:]])
+    want = dst.copy()
+    want[j] = v
+    got = dst.copy()
+    rej = oracle_mod.apply(got, idx_all, val_all, 0, idx_all.size, index_base=base)
+    assert rej == 3
+    np.testing.assert_array_equal(got, want)
+    # a sub-range [begin, end) touches only those entries
+    got2 = dst.copy()
+    oracle_mod.apply(got2, idx, v, 100, 200, index_base=base)
+    want2 = dst.copy()
+    want2[j[100:200]] = v[100:200]
+    np.testing.assert_array_equal(got2, want2)
+
+
+# --------------------------------------------------------------------------- PULSELoCo
+
+def test_loco_partition_and_values(oracle_mod):
+    """a = fl32(Delta + e) (numpy add); selected iff |a| >= tau; exactly one of
+    (emitted, value a, residual +0) / (not emitted, residual a) per entry."""
+    rng = np.random.default_rng(5)
+    n = 200_000
+    tau = wl.loco_tau()
+    e = (wl.loco_delta_np(rng, n) * np.float32(0.5)).astype(np.float32)
+    d = wl.loco_delta_np(rng, n)
+    a = (d + e).astype(np.float32)
+    res = e.copy()
+    count, idx, val = oracle_mod.loco(d, res, tau, index_base=9)
+    keep = np.abs(a) >= np.float32(tau)
+    ki = np.flatnonzero(keep)
+    assert count == ki.size
+    np.testing.assert_array_equal(idx[:count], ki + 9)
+    np.testing.assert_array_equal(val[:count].view(np.uint32), a[ki].view(np.uint32))
+    want_res = np.where(keep, np.float32(0.0), a).astype(np.float32)
+    np.testing.assert_array_equal(res.view(np.uint32), want_res.view(np.uint32))
+    assert np.all(res[keep].view(np.uint32) == 0)       # +0, not -0
+
+
+def test_loco_special_thresholds(oracle_mod):
+    d = bits(0x3F800000, 0x00000001, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0xBF000000)
+    # tau = 0 keeps every non-NaN entry, including +-0 and subnormals
+    r = np.zeros(d.size, np.float32)
+    c, idx, _ = oracle_mod.loco(d, r, 0.0)
+    assert list(idx[:c]) == [0, 1, 2, 3, 4, 6]
+    assert np.isnan(r[5]) and np.all(r[[0, 1, 2, 3, 4, 6]].view(np.uint32) == 0)
+    # tau = +inf keeps only the infinities; NaN is never selected and stays in e
+    r = np.zeros(d.size, np.float32)
+    c, idx, _ = oracle_mod.loco(d, r, np.inf)
+    assert list(idx[:c]) == [3, 4]
+    assert np.isnan(r[5])
+
+
+def test_loco_overflow_keeps_unsent_in_residual(oracle_mod):
+    rng = np.random.default_rng(6)
+    n = 5000
+    d = wl.loco_delta_np(rng, n)
+    tau = float(np.quantile(np.abs(d), 0.9))
+    res = np.zeros(n, np.float32)
+    cap = 100
+    c, idx, val = oracle_mod.loco(d, res, tau, capacity=cap)
+    ki = np.flatnonzero(np.abs(d) >= np.float32(tau))
+    assert c == ki.size > cap
+    sent = ki[:cap]
+    want = d.copy()
+    want[sent] = 0.0
+    np.testing.assert_array_equal(res.view(np.uint32), want.view(np.uint32))
+    np.testing.assert_array_equal(idx[:cap], sent)
+
+
+def test_loco_error_feedback_identity(oracle_mod):
+    """Alg. 2 over 10 rounds on dyadic values (all sums exact in FP32):
+    sum_r Delta_r == sum of sent values + final residual, entry by entry."""
+    rng = np.random.default_rng(8)
+    n = 20_000
+    res = np.zeros(n, np.float32)
+    total_d = np.zeros(n, np.float64)
+    total_sent = np.zeros(n, np.float64)
+    for r in range(10):
+        d = (rng.integers(-64, 65, n) * 2.0 ** -20).astype(np.float32)
+        total_d += d
+        c, idx, val = oracle_mod.loco(d, res, 40 * 2.0 ** -20)
+        np.add.at(total_sent, idx[:c].astype(np.int64), val[:c].astype(np.float64))
+    np.testing.assert_array_equal(total_sent + res.astype(np.float64), total_d)
+
+
+def test_loco_gate_matches_torch_cast(oracle_mod):
+    """theta given: selected iff bf16(theta) != bf16(theta - a) (Sec. 4.1 gate, Alg. 2)."""
+    rng = np.random.default_rng(9)
+    n = 100_000
+    theta = rng.normal(0, math.sqrt(wl.W_VAR), n).astype(np.float32)
+    d = (wl.loco_delta_np(rng, n) * np.float32(30)).astype(np.float32)
+    res = np.zeros(n, np.float32)
+    c, idx, val = oracle_mod.loco(d, res, 0.0, theta=theta)
+    a = d  # residual started at 0
+    sel = tcast(theta) != tcast((theta - a).astype(np.float32))
+    ki = np.flatnonzero(sel)
+    assert c == ki.size and 0 < c < n
+    np.testing.assert_array_equal(idx[:c], ki)
+    np.testing.assert_array_equal(val[:c].view(np.uint32), a[ki].view(np.uint32))
+
+
+def test_loco_density_grows_with_fixed_tau(oracle_mod):
+    """With tau fixed at the round-1 98th percentile, round 1 keeps ~2% and the
+    residual makes later rounds keep more (App. B reports 3.6-5.2% sent per round)."""
+    rng = np.random.default_rng(10)
+    n = 1 << 20
+    tau = wl.loco_tau()
+    res = np.zeros(n, np.float32)
+    dens = []
+    for _ in range(10):
+        c, _, _ = oracle_mod.loco(wl.loco_delta_np(rng, n), res, tau)
+        dens.append(c / n)
+    assert abs(dens[0] - 0.02) < 0.001
+    assert all(b >= a - 1e-3 for a, b in zip(dens, dens[1:]))
+    assert 0.03 < dens[-1] < 0.06
