@@ -1,0 +1,201 @@
+/*
+ * pulse.h -- C ABI of libpulse, the MI355X (gfx950) PULSE patch codec.
+ *
+ * The library implements the data-parallel hot path of compute-visible
+ * sparsification (arXiv 2602.03839):
+ *   - the BF16 view of FP32 master weights (Sec. 3 "Sparsity metric"),
+ *   - the sparse value patch of PULSESync: encode (Sec. 4.2, Alg. 1 Encode;
+ *     App. H.5, Alg. 3) and apply (Alg. 1 Decode; App. H.5, Alg. 4),
+ *   - PULSELoCo's error-feedback sparsification of FP32 pseudo-gradients
+ *     (Sec. 4.3, Alg. 2).
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers (HIP device memory of the current device)
+ *     unless the argument says "host".  BF16 values travel as uint16_t bit
+ *     patterns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Work is enqueued on it and the call returns without synchronising; the
+ *     caller owns every buffer and keeps it alive until the stream has run
+ *     the work.  The library allocates no device memory.
+ *   - Return value: PULSE_OK, or a negative pulse_status for an argument error
+ *     found on the host (nothing is enqueued then) or a failed launch.
+ *     pulse_strerror() names it; pulse_last_error() gives the detail message
+ *     of the calling thread's last failure.
+ *   - n == 0 (or an empty batch) enqueues nothing that changes outputs.
+ *
+ * Patch layout (Sec. 4.2 "Encoding and decoding": store index and new value,
+ * not a difference; App. H.2: indices ascending): struct-of-arrays
+ * `uint32_t idx[capacity]` + value array, entries in ascending index order,
+ * tensors in the order given.  Index of element i of a tensor = index_base + i,
+ * so a whole model below 2^32 parameters can use one flat index space
+ * (index_base = offset of the tensor), and larger models use per-tensor local
+ * indices (index_base = 0) with per-tensor segment offsets (seg_begin).
+ *
+ * Running count: `count` is a device uint64.  On entry it holds the number of
+ * entries already in the patch (the append position); the kernel adds the
+ * number of entries this call selects, also those that did not fit.  Entries
+ * whose position is >= capacity are not written; the caller detects overflow
+ * as *count > capacity after synchronising.
+ *
+ * Workspace: encode and sparsify need `pulse_workspace_bytes()` bytes of
+ * device memory, 256-byte aligned, ZERO-FILLED ONCE before its first use and
+ * then reused unchanged by every call (the kernels leave it valid for the next
+ * call).  Calls that share a workspace must be ordered on one stream; give
+ * concurrent streams separate workspaces.  A call that faulted leaves it
+ * undefined: zero it again.
+ */
+#ifndef PULSE_H
+#define PULSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pulse_status {
+    PULSE_OK = 0,
+    PULSE_EINVAL = -1, /* NULL required pointer, bad size, workspace too small */
+    PULSE_ERANGE = -2, /* index_base + n > 2^32 */
+    PULSE_EALIGN = -3, /* a dense stream pointer is not 16-byte aligned */
+    PULSE_EHIP = -4    /* the HIP runtime rejected a launch */
+} pulse_status;
+
+/* Size in bytes of the workspace that encode and sparsify calls use. */
+size_t pulse_workspace_bytes(void);
+
+/* Human-readable name of a pulse_status value (static string). */
+const char *pulse_strerror(int status);
+
+/* Detail message of the calling thread's last failed call ("" if none). */
+const char *pulse_last_error(void);
+
+/*
+ * pulse_cast_bf16 -- the BF16 view of an FP32 tensor (Sec. 3 "Sparsity
+ * metric": the dtype of the next forward pass), dst[i] = bf16(src[i]),
+ * round to nearest, ties to even (App. A.2, App. D).  A NaN becomes a quiet
+ * NaN with the same sign and leading payload bits.  Used for the first
+ * snapshot / full anchor of a chain.
+ *   src  FP32 [n], 16-byte aligned.      dst  BF16 bits [n], 16-byte aligned.
+ */
+int pulse_cast_bf16(const float *src, uint16_t *dst, uint64_t n, void *stream);
+
+/*
+ * pulse_encode -- PULSESync encode of one tensor (Sec. 4.2, Alg. 1 Encode;
+ * App. H.5, Alg. 3).  I = { i : bf16(w_new[i]) != snap[i] } compared bitwise
+ * (Sec. 3: equality is bitwise, so +0 != -0), V = bf16(w_new)[I]; entry k of
+ * this tensor's part of the patch is written at position (*count on entry) + k
+ * as idx = index_base + i, val = bf16(w_new[i]).
+ *   w_new       FP32 master after the step [n], 16-byte aligned.
+ *   snap        previous BF16 snapshot [n], 16-byte aligned; read only, unless
+ *               it is also `refresh`.
+ *   n           elements; index_base + n <= 2^32 (else PULSE_ERANGE).
+ *   idx, val    patch arrays with room for `capacity` entries.
+ *   count       device uint64, in: append position, out: += entries selected.
+ *   refresh     NULL, or BF16 [n] that receives bf16(w_new[i]) for every
+ *               EMITTED entry (position < capacity); may equal `snap`, which
+ *               advances the snapshot in place (App. H.3).
+ *   workspace   pulse_workspace_bytes() bytes, see above.
+ */
+int pulse_encode(const float *w_new, const uint16_t *snap, uint64_t n,
+                 uint32_t *idx, uint16_t *val, uint64_t capacity, uint64_t *count,
+                 uint32_t index_base, uint16_t *refresh,
+                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* One tensor of a batched encode (fields as in pulse_encode). */
+typedef struct pulse_encode_tensor {
+    const float *w_new;
+    const uint16_t *snap;
+    uint16_t *refresh; /* may be NULL */
+    uint64_t n;
+    uint32_t index_base;
+} pulse_encode_tensor;
+
+/*
+ * pulse_encode_batch -- Alg. 3's loop over parameter tensors in one pass: the
+ * tensors' patches are appended one after another, in the order given, to one
+ * patch.  Equivalent to calling pulse_encode on each tensor in order.
+ *   tensors     HOST array [ntensors]; read during the call only.
+ *   seg_begin   NULL, or device uint64 [ntensors]: position in the patch where
+ *               tensor t's entries begin (the end of tensor t is seg_begin[t+1],
+ *               and *count for the last one).  Values may exceed capacity.
+ */
+int pulse_encode_batch(const pulse_encode_tensor *tensors, uint32_t ntensors,
+                       uint32_t *idx, uint16_t *val, uint64_t capacity, uint64_t *count,
+                       uint64_t *seg_begin, void *workspace, size_t workspace_bytes,
+                       void *stream);
+
+/*
+ * pulse_apply -- PULSESync decode of one tensor (Sec. 4.2, Alg. 1 Decode;
+ * App. H.5, Alg. 4): dst[idx[k] - index_base] = val[k] for k in
+ * [*begin, min(*end, capacity)).  A direct copy of bit patterns, no
+ * arithmetic; dst is not read.  Indices must be unique (encode's are); entries
+ * whose index is outside [index_base, index_base + n) are skipped and, if
+ * `rejected` is not NULL, counted into the device uint64 *rejected.
+ *   dst       BF16 [n] receiving the patch in place (App. H.3).
+ *   begin/end device uint64 positions (e.g. a saved count and encode's count),
+ *             so no host synchronisation is needed between encode and apply.
+ */
+int pulse_apply(uint16_t *dst, uint64_t n, const uint32_t *idx, const uint16_t *val,
+                uint64_t capacity, const uint64_t *begin, const uint64_t *end,
+                uint32_t index_base, uint64_t *rejected, void *stream);
+
+/* One tensor of a batched apply. */
+typedef struct pulse_apply_tensor {
+    uint16_t *dst;
+    uint64_t n;
+    uint32_t index_base;
+} pulse_apply_tensor;
+
+/*
+ * pulse_apply_batch -- Alg. 4's loop over tensors: tensor t takes the entries
+ * [seg_begin[t], seg_begin[t+1]) (the last one up to *end), clipped to
+ * capacity, as produced by pulse_encode_batch.
+ *   tensors    HOST array [ntensors].
+ *   seg_begin  device uint64 [ntensors], non-decreasing.
+ */
+int pulse_apply_batch(const pulse_apply_tensor *tensors, uint32_t ntensors,
+                      const uint32_t *idx, const uint16_t *val, uint64_t capacity,
+                      const uint64_t *seg_begin, const uint64_t *end, uint64_t *rejected,
+                      void *stream);
+
+/*
+ * pulse_loco_sparsify -- PULSELoCo sparsification with error feedback
+ * (Sec. 4.3, Alg. 2): a = fl32(delta[i] + residual[i]) (s = Delta + e), then
+ *   theta == NULL: selected iff |a| >= tau (threshold form);
+ *   theta != NULL: selected iff bf16(theta[i]) != bf16(fl32(theta[i] - a)),
+ *                  the compute-visibility gate G_BF16(theta, s) of Sec. 4.1
+ *                  (tau is ignored).
+ * A selected entry at position < capacity is emitted as (index_base + i, a)
+ * and its residual becomes +0 (e[I] <- 0); every other entry -- not selected,
+ * or selected but beyond capacity, hence not sent -- keeps residual = a
+ * (e[not I] <- s).  NaN is never selected by the threshold form.
+ *   delta, residual (in/out), theta: FP32 [n], 16-byte aligned.
+ *   idx, val   FP32 patch with room for `capacity` entries.
+ */
+int pulse_loco_sparsify(const float *delta, float *residual, uint64_t n, float tau,
+                        const float *theta, uint32_t *idx, float *val, uint64_t capacity,
+                        uint64_t *count, uint32_t index_base,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/* One tensor of a batched sparsify. */
+typedef struct pulse_loco_tensor {
+    const float *delta;
+    float *residual;
+    const float *theta; /* may be NULL: threshold form */
+    uint64_t n;
+    uint32_t index_base;
+} pulse_loco_tensor;
+
+/* pulse_loco_sparsify over tensors in order, appended to one patch (see pulse_encode_batch). */
+int pulse_loco_sparsify_batch(const pulse_loco_tensor *tensors, uint32_t ntensors, float tau,
+                              uint32_t *idx, float *val, uint64_t capacity, uint64_t *count,
+                              uint64_t *seg_begin, void *workspace, size_t workspace_bytes,
+                              void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PULSE_H */

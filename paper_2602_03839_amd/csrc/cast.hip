@@ -1,0 +1,39 @@
+// cast.hip -- the dense BF16 view of an FP32 tensor (Sec. 3 "Sparsity
+// metric"; RNE per App. A.2 / App. D).  Eight elements per lane per step:
+// two 16-byte loads, one 16-byte store.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace pulse {
+
+constexpr int kCastTB = 256;
+
+__global__ __launch_bounds__(kCastTB) void cast_kernel(const float* __restrict__ src,
+                                                       uint16_t* __restrict__ dst, uint64_t n) {
+  const uint64_t groups = n / 8;
+  const uint64_t gid = (uint64_t)blockIdx.x * kCastTB + threadIdx.x;
+  const uint64_t stride = (uint64_t)gridDim.x * kCastTB;
+  for (uint64_t g = gid; g < groups; g += stride) {
+    const uint4 a = load16(src + g * 8);
+    const uint4 b = load16(src + g * 8 + 4);
+    uint4 o;
+    o.x = bf16_rne_bits(a.x) | (bf16_rne_bits(a.y) << 16);
+    o.y = bf16_rne_bits(a.z) | (bf16_rne_bits(a.w) << 16);
+    o.z = bf16_rne_bits(b.x) | (bf16_rne_bits(b.y) << 16);
+    o.w = bf16_rne_bits(b.z) | (bf16_rne_bits(b.w) << 16);
+    store16(dst + g * 8, o);
+  }
+  const uint64_t e = groups * 8 + gid;
+  if (e < n) dst[e] = (uint16_t)bf16_rne_bits(__float_as_uint(src[e]));
+}
+
+hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream) {
+  const uint64_t groups = (n + 7) / 8;
+  uint64_t blocks = (groups + kCastTB - 1) / kCastTB;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks == 0) blocks = 1;
+  hipLaunchKernelGGL(cast_kernel, dim3((uint32_t)blocks), dim3(kCastTB), 0, stream, src, dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace pulse

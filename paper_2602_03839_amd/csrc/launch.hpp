@@ -1,0 +1,91 @@
+// launch.hpp -- kernel parameter blocks and launcher declarations shared by
+// the kernels and the C ABI layer.  Parameter blocks travel as kernel
+// arguments (they stay below the 4 KiB kernel-argument limit), so a batched
+// call needs no device-side descriptor table and no extra copy.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pulse {
+
+constexpr int kMaxBatch = 64;  // tensors per launch; larger batches are split
+
+// Tile shapes (threads per block, 8-element groups per thread).
+constexpr int kEncodeTB = 512;
+constexpr int kEncodeU = 4;
+constexpr int kLocoTB = 256;
+constexpr int kLocoU = 4;
+
+struct EncodeTensorDesc {
+  const float* w_new;
+  const uint16_t* snap;
+  uint16_t* refresh;
+  uint64_t n;
+  uint32_t index_base;
+};
+
+struct EncodeParams {
+  uint64_t* ws;
+  uint32_t* idx;
+  uint16_t* val;
+  uint64_t capacity;
+  uint64_t* count;
+  uint64_t* seg_begin;  // already offset to this launch's first tensor; may be null
+  uint32_t ntiles;
+  int ntensors;
+  uint32_t tile_begin[kMaxBatch + 1];
+  EncodeTensorDesc t[kMaxBatch];
+};
+
+struct LocoTensorDesc {
+  const float* delta;
+  float* residual;
+  const float* theta;
+  uint64_t n;
+  uint32_t index_base;
+};
+
+struct LocoParams {
+  uint64_t* ws;
+  uint32_t* idx;
+  float* val;
+  uint64_t capacity;
+  uint64_t* count;
+  uint64_t* seg_begin;
+  float tau;
+  uint32_t ntiles;
+  int ntensors;
+  uint32_t tile_begin[kMaxBatch + 1];
+  LocoTensorDesc t[kMaxBatch];
+};
+
+struct ApplyTensorDesc {
+  uint16_t* dst;
+  uint64_t n;
+  uint32_t index_base;
+};
+
+struct ApplyParams {
+  const uint32_t* idx;
+  const uint16_t* val;
+  uint64_t capacity;
+  const uint64_t* seg_begin;  // device [ntensors] (batched form), or the single `begin`
+  const uint64_t* end;
+  uint64_t* rejected;
+  int ntensors;
+  ApplyTensorDesc t[kMaxBatch];
+};
+
+static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
+static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
+static_assert(sizeof(ApplyParams) < 4096, "kernel argument block too large");
+
+uint32_t encode_tile_elems();
+uint32_t loco_tile_elems();
+hipError_t launch_encode(EncodeParams& p, hipStream_t stream);
+hipError_t launch_loco(LocoParams& p, hipStream_t stream);
+hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);
+hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream);
+
+}  // namespace pulse

@@ -1,0 +1,275 @@
+// pulse_abi.hip -- the extern "C" entry points of libpulse (declared in
+// include/pulse.h): argument validation on the host, splitting of batches
+// into launches, and kernel launch on the caller's stream.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/pulse.h"
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace {
+
+thread_local char g_last_error[512];
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return PULSE_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(PULSE_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+int check_workspace(void* ws, size_t bytes) {
+  if (!ws) return fail(PULSE_EINVAL, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(PULSE_EALIGN, "workspace is not 256-byte aligned");
+  if (bytes < pulse::kWorkspaceBytes)
+    return fail(PULSE_EINVAL, "workspace has %zu bytes, needs %zu", bytes,
+                (size_t)pulse::kWorkspaceBytes);
+  return PULSE_OK;
+}
+
+int check_range(uint64_t n, uint32_t index_base, const char* who, uint32_t t) {
+  if ((uint64_t)index_base + n > (1ull << 32))
+    return fail(PULSE_ERANGE, "%s tensor %u: index_base %u + n %llu exceeds 2^32", who, t,
+                index_base, (unsigned long long)n);
+  return PULSE_OK;
+}
+
+uint32_t tiles_for(uint64_t n, uint32_t tile) { return (uint32_t)((n + tile - 1) / tile); }
+
+}  // namespace
+
+extern "C" {
+
+size_t pulse_workspace_bytes(void) { return pulse::kWorkspaceBytes; }
+
+const char* pulse_strerror(int status) {
+  switch (status) {
+    case PULSE_OK: return "PULSE_OK";
+    case PULSE_EINVAL: return "PULSE_EINVAL: invalid argument";
+    case PULSE_ERANGE: return "PULSE_ERANGE: index range exceeds 32 bits";
+    case PULSE_EALIGN: return "PULSE_EALIGN: pointer not aligned";
+    case PULSE_EHIP: return "PULSE_EHIP: HIP launch failed";
+    default: return "unknown pulse status";
+  }
+}
+
+const char* pulse_last_error(void) { return g_last_error; }
+
+int pulse_cast_bf16(const float* src, uint16_t* dst, uint64_t n, void* stream) {
+  if (n == 0) return ok();
+  if (!src || !dst) return fail(PULSE_EINVAL, "cast: NULL pointer");
+  if (!aligned16(src) || !aligned16(dst)) return fail(PULSE_EALIGN, "cast: src/dst not 16-byte aligned");
+  return hip_status(pulse::launch_cast(src, dst, n, (hipStream_t)stream), "cast launch");
+}
+
+int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, uint32_t* idx,
+                       uint16_t* val, uint64_t capacity, uint64_t* count, uint64_t* seg_begin,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  if (ntensors == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "encode: tensors is NULL");
+  if (!count) return fail(PULSE_EINVAL, "encode: count is NULL");
+  if (capacity > 0 && (!idx || !val)) return fail(PULSE_EINVAL, "encode: idx/val NULL with capacity > 0");
+  if (!aligned(count, 8) || (seg_begin && !aligned(seg_begin, 8)))
+    return fail(PULSE_EALIGN, "encode: count/seg_begin not 8-byte aligned");
+  if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 2)))
+    return fail(PULSE_EALIGN, "encode: idx/val misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_encode_tensor& d = tensors[t];
+    if (d.n == 0) continue;
+    if (!d.w_new || !d.snap) return fail(PULSE_EINVAL, "encode tensor %u: NULL w_new/snap", t);
+    if (!aligned16(d.w_new) || !aligned16(d.snap))
+      return fail(PULSE_EALIGN, "encode tensor %u: w_new/snap not 16-byte aligned", t);
+    if (d.refresh && !aligned(d.refresh, 2))
+      return fail(PULSE_EALIGN, "encode tensor %u: refresh misaligned", t);
+    if (int rc = check_range(d.n, d.index_base, "encode", t)) return rc;
+  }
+
+  const uint32_t tile = pulse::encode_tile_elems();
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::EncodeParams p;
+    memset(&p, 0, sizeof p);
+    p.ws = (uint64_t*)workspace;
+    p.idx = idx;
+    p.val = val;
+    p.capacity = capacity;
+    p.count = count;
+    p.seg_begin = seg_begin ? seg_begin + t0 : nullptr;
+    uint32_t tiles = 0;
+    int k = 0;
+    while (t0 + k < ntensors && k < pulse::kMaxBatch) {
+      const pulse_encode_tensor& d = tensors[t0 + k];
+      const uint32_t nt = tiles_for(d.n, tile);
+      if (k > 0 && (uint64_t)tiles + nt > pulse::kMaxTilesPerLaunch) break;
+      p.tile_begin[k] = tiles;
+      p.t[k].w_new = d.w_new;
+      p.t[k].snap = d.snap;
+      p.t[k].refresh = d.refresh;
+      p.t[k].n = d.n;
+      p.t[k].index_base = d.index_base;
+      tiles += nt;
+      ++k;
+    }
+    p.tile_begin[k] = tiles;
+    p.ntensors = k;
+    p.ntiles = tiles;
+    if (int rc = hip_status(pulse::launch_encode(p, (hipStream_t)stream), "encode launch")) return rc;
+    t0 += k;
+  }
+  return ok();
+}
+
+int pulse_encode(const float* w_new, const uint16_t* snap, uint64_t n, uint32_t* idx,
+                 uint16_t* val, uint64_t capacity, uint64_t* count, uint32_t index_base,
+                 uint16_t* refresh, void* workspace, size_t workspace_bytes, void* stream) {
+  if (n == 0) return ok();
+  pulse_encode_tensor d;
+  d.w_new = w_new;
+  d.snap = snap;
+  d.refresh = refresh;
+  d.n = n;
+  d.index_base = index_base;
+  return pulse_encode_batch(&d, 1, idx, val, capacity, count, nullptr, workspace,
+                            workspace_bytes, stream);
+}
+
+int pulse_apply_batch(const pulse_apply_tensor* tensors, uint32_t ntensors, const uint32_t* idx,
+                      const uint16_t* val, uint64_t capacity, const uint64_t* seg_begin,
+                      const uint64_t* end, uint64_t* rejected, void* stream) {
+  if (ntensors == 0 || capacity == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "apply: tensors is NULL");
+  if (!idx || !val) return fail(PULSE_EINVAL, "apply: idx/val is NULL");
+  if (!seg_begin || !end) return fail(PULSE_EINVAL, "apply: seg_begin/end is NULL");
+  if (!aligned(seg_begin, 8) || !aligned(end, 8) || (rejected && !aligned(rejected, 8)))
+    return fail(PULSE_EALIGN, "apply: counters not 8-byte aligned");
+  if (!aligned(idx, 4) || !aligned(val, 2)) return fail(PULSE_EALIGN, "apply: idx/val misaligned");
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_apply_tensor& d = tensors[t];
+    if (d.n > 0 && !d.dst) return fail(PULSE_EINVAL, "apply tensor %u: dst is NULL", t);
+    if (d.dst && !aligned(d.dst, 2)) return fail(PULSE_EALIGN, "apply tensor %u: dst misaligned", t);
+    if (int rc = check_range(d.n, d.index_base, "apply", t)) return rc;
+  }
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::ApplyParams p;
+    memset(&p, 0, sizeof p);
+    const uint32_t k = (ntensors - t0) < (uint32_t)pulse::kMaxBatch ? (ntensors - t0)
+                                                                     : (uint32_t)pulse::kMaxBatch;
+    p.idx = idx;
+    p.val = val;
+    p.capacity = capacity;
+    p.seg_begin = seg_begin + t0;
+    p.end = (t0 + k < ntensors) ? seg_begin + t0 + k : end;
+    p.rejected = rejected;
+    p.ntensors = (int)k;
+    for (uint32_t i = 0; i < k; ++i) {
+      p.t[i].dst = tensors[t0 + i].dst;
+      p.t[i].n = tensors[t0 + i].n;
+      p.t[i].index_base = tensors[t0 + i].index_base;
+    }
+    if (int rc = hip_status(pulse::launch_apply(p, (hipStream_t)stream), "apply launch")) return rc;
+    t0 += k;
+  }
+  return ok();
+}
+
+int pulse_apply(uint16_t* dst, uint64_t n, const uint32_t* idx, const uint16_t* val,
+                uint64_t capacity, const uint64_t* begin, const uint64_t* end,
+                uint32_t index_base, uint64_t* rejected, void* stream) {
+  pulse_apply_tensor d;
+  d.dst = dst;
+  d.n = n;
+  d.index_base = index_base;
+  return pulse_apply_batch(&d, 1, idx, val, capacity, begin, end, rejected, stream);
+}
+
+int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensors, float tau,
+                              uint32_t* idx, float* val, uint64_t capacity, uint64_t* count,
+                              uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  if (ntensors == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "loco: tensors is NULL");
+  if (!count) return fail(PULSE_EINVAL, "loco: count is NULL");
+  if (capacity > 0 && (!idx || !val)) return fail(PULSE_EINVAL, "loco: idx/val NULL with capacity > 0");
+  if (!aligned(count, 8) || (seg_begin && !aligned(seg_begin, 8)))
+    return fail(PULSE_EALIGN, "loco: count/seg_begin not 8-byte aligned");
+  if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 4)))
+    return fail(PULSE_EALIGN, "loco: idx/val misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_loco_tensor& d = tensors[t];
+    if (d.n == 0) continue;
+    if (!d.delta || !d.residual) return fail(PULSE_EINVAL, "loco tensor %u: NULL delta/residual", t);
+    if (!aligned16(d.delta) || !aligned16(d.residual) || (d.theta && !aligned16(d.theta)))
+      return fail(PULSE_EALIGN, "loco tensor %u: delta/residual/theta not 16-byte aligned", t);
+    if (int rc = check_range(d.n, d.index_base, "loco", t)) return rc;
+  }
+  const uint32_t tile = pulse::loco_tile_elems();
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::LocoParams p;
+    memset(&p, 0, sizeof p);
+    p.ws = (uint64_t*)workspace;
+    p.idx = idx;
+    p.val = val;
+    p.capacity = capacity;
+    p.count = count;
+    p.seg_begin = seg_begin ? seg_begin + t0 : nullptr;
+    p.tau = tau;
+    uint32_t tiles = 0;
+    int k = 0;
+    while (t0 + k < ntensors && k < pulse::kMaxBatch) {
+      const pulse_loco_tensor& d = tensors[t0 + k];
+      const uint32_t nt = tiles_for(d.n, tile);
+      if (k > 0 && (uint64_t)tiles + nt > pulse::kMaxTilesPerLaunch) break;
+      p.tile_begin[k] = tiles;
+      p.t[k].delta = d.delta;
+      p.t[k].residual = d.residual;
+      p.t[k].theta = d.theta;
+      p.t[k].n = d.n;
+      p.t[k].index_base = d.index_base;
+      tiles += nt;
+      ++k;
+    }
+    p.tile_begin[k] = tiles;
+    p.ntensors = k;
+    p.ntiles = tiles;
+    if (int rc = hip_status(pulse::launch_loco(p, (hipStream_t)stream), "loco launch")) return rc;
+    t0 += k;
+  }
+  return ok();
+}
+
+int pulse_loco_sparsify(const float* delta, float* residual, uint64_t n, float tau,
+                        const float* theta, uint32_t* idx, float* val, uint64_t capacity,
+                        uint64_t* count, uint32_t index_base, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (n == 0) return ok();
+  pulse_loco_tensor d;
+  d.delta = delta;
+  d.residual = residual;
+  d.theta = theta;
+  d.n = n;
+  d.index_base = index_base;
+  return pulse_loco_sparsify_batch(&d, 1, tau, idx, val, capacity, count, nullptr, workspace,
+                                   workspace_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,246 @@
+"""ctypes binding to libpulse.so (C ABI in include/pulse.h).
+
+Argument marshalling only: every function takes torch tensors that already
+live on the GPU, passes their device pointers and the current HIP stream to
+the C entry point of the same name, and raises on a non-zero status.  All
+arithmetic runs in the library's HIP kernels.  If libpulse.so has not been
+built (``python -m paper_2602_03839_amd.build``) the first call raises.
+
+BF16 data is passed as any 2-byte tensor (torch.bfloat16, int16 or uint16):
+only bit patterns move through the codec.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpulse.so")
+
+_lock = threading.Lock()
+_lib = None
+
+
+class PulseError(RuntimeError):
+    pass
+
+
+class _EncodeTensor(ctypes.Structure):
+    _fields_ = [("w_new", ctypes.c_void_p), ("snap", ctypes.c_void_p),
+                ("refresh", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("index_base", ctypes.c_uint32)]
+
+
+class _ApplyTensor(ctypes.Structure):
+    _fields_ = [("dst", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("index_base", ctypes.c_uint32)]
+
+
+class _LocoTensor(ctypes.Structure):
+    _fields_ = [("delta", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("theta", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("index_base", ctypes.c_uint32)]
+
+
+EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
+           "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
+           "pulse_loco_sparsify", "pulse_loco_sparsify_batch")
+
+
+def lib():
+    """Load libpulse.so once; raise if it is missing."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise PulseError(f"{LIB_PATH} is not built; run `python -m paper_2602_03839_amd.build`")
+            L = ctypes.CDLL(LIB_PATH)
+            vp, u64, u32, f32, i32 = (ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                                      ctypes.c_float, ctypes.c_int)
+            sz = ctypes.c_size_t
+            L.pulse_workspace_bytes.argtypes = []
+            L.pulse_workspace_bytes.restype = sz
+            L.pulse_strerror.argtypes = [i32]
+            L.pulse_strerror.restype = ctypes.c_char_p
+            L.pulse_last_error.argtypes = []
+            L.pulse_last_error.restype = ctypes.c_char_p
+            L.pulse_cast_bf16.argtypes = [vp, vp, u64, vp]
+            L.pulse_encode.argtypes = [vp, vp, u64, vp, vp, u64, vp, u32, vp, vp, sz, vp]
+            L.pulse_encode_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
+            L.pulse_apply.argtypes = [vp, u64, vp, vp, u64, vp, vp, u32, vp, vp]
+            L.pulse_apply_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, vp]
+            L.pulse_loco_sparsify.argtypes = [vp, vp, u64, f32, vp, vp, vp, u64, vp, u32, vp, sz, vp]
+            L.pulse_loco_sparsify_batch.argtypes = [vp, u32, f32, vp, vp, u64, vp, vp, vp, sz, vp]
+            for name in EXPORTS[3:]:
+                getattr(L, name).restype = i32
+            _lib = L
+    return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        L = lib()
+        raise PulseError(f"{what}: {L.pulse_strerror(rc).decode()} ({L.pulse_last_error().decode()})")
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise PulseError("libpulse takes device tensors")
+    return t.data_ptr()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _is16(t: torch.Tensor) -> bool:
+    return t.element_size() == 2
+
+
+def _capacity(idx: torch.Tensor, val: torch.Tensor, capacity: Optional[int]) -> int:
+    room = min(idx.numel(), val.numel())
+    if capacity is None:
+        return room
+    if not 0 <= capacity <= room:
+        raise PulseError(f"capacity {capacity} exceeds the patch buffers ({room} entries)")
+    return capacity
+
+
+def workspace_bytes() -> int:
+    return int(lib().pulse_workspace_bytes())
+
+
+def workspace(device=None) -> torch.Tensor:
+    """A zero-filled workspace; reuse it for every call ordered on one stream."""
+    return torch.zeros(workspace_bytes(), dtype=torch.uint8, device=device or "cuda")
+
+
+def cast_bf16(src: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    assert src.dtype == torch.float32 and src.is_contiguous()
+    if out is None:
+        out = torch.empty(src.shape, dtype=torch.int16, device=src.device)
+    assert _is16(out) and out.numel() == src.numel() and out.is_contiguous()
+    _check(lib().pulse_cast_bf16(_p(src), _p(out), src.numel(), _stream(stream)), "pulse_cast_bf16")
+    return out
+
+
+def encode(w_new: torch.Tensor, snap: torch.Tensor, idx: torch.Tensor, val: torch.Tensor,
+           count: torch.Tensor, ws: torch.Tensor, index_base: int = 0,
+           refresh: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
+           stream=None) -> None:
+    assert w_new.dtype == torch.float32 and _is16(snap) and _is16(val)
+    assert idx.element_size() == 4 and count.element_size() == 8
+    assert w_new.numel() == snap.numel()
+    cap = _capacity(idx, val, capacity)
+    _check(lib().pulse_encode(_p(w_new), _p(snap), w_new.numel(), _p(idx), _p(val),
+                              cap, _p(count), index_base,
+                              _p(refresh), _p(ws), ws.numel(), _stream(stream)), "pulse_encode")
+
+
+@dataclass
+class EncodeTensor:
+    w_new: torch.Tensor
+    snap: torch.Tensor
+    refresh: Optional[torch.Tensor] = None
+    index_base: int = 0
+
+
+class EncodeBatch:
+    """Descriptor array for pulse_encode_batch, built once and reused."""
+
+    def __init__(self, tensors: Sequence[EncodeTensor]):
+        self.n = len(tensors)
+        arr = (_EncodeTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert t.w_new.dtype == torch.float32 and _is16(t.snap)
+            assert t.w_new.numel() == t.snap.numel()
+            arr[i] = _EncodeTensor(_p(t.w_new), _p(t.snap), _p(t.refresh), t.w_new.numel(),
+                                   t.index_base)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_encode_batch(self.arr, self.n, _p(idx), _p(val), cap, _p(count),
+                                        _p(seg_begin), _p(ws), ws.numel(), _stream(stream)),
+               "pulse_encode_batch")
+
+
+def apply(dst: torch.Tensor, idx: torch.Tensor, val: torch.Tensor, begin: torch.Tensor,
+          end: torch.Tensor, index_base: int = 0, rejected: Optional[torch.Tensor] = None,
+          capacity: Optional[int] = None, stream=None) -> None:
+    assert _is16(dst) and _is16(val) and idx.element_size() == 4
+    cap = _capacity(idx, val, capacity)
+    _check(lib().pulse_apply(_p(dst), dst.numel(), _p(idx), _p(val), cap, _p(begin), _p(end),
+                             index_base, _p(rejected), _stream(stream)), "pulse_apply")
+
+
+@dataclass
+class ApplyTensor:
+    dst: torch.Tensor
+    index_base: int = 0
+
+
+class ApplyBatch:
+    def __init__(self, tensors: Sequence[ApplyTensor]):
+        self.n = len(tensors)
+        arr = (_ApplyTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert _is16(t.dst)
+            arr[i] = _ApplyTensor(_p(t.dst), t.dst.numel(), t.index_base)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, idx, val, seg_begin, end, rejected=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_apply_batch(self.arr, self.n, _p(idx), _p(val), cap, _p(seg_begin),
+                                       _p(end), _p(rejected), _stream(stream)), "pulse_apply_batch")
+
+
+def loco_sparsify(delta: torch.Tensor, residual: torch.Tensor, tau: float, idx: torch.Tensor,
+                  val: torch.Tensor, count: torch.Tensor, ws: torch.Tensor,
+                  theta: Optional[torch.Tensor] = None, index_base: int = 0,
+                  capacity: Optional[int] = None, stream=None) -> None:
+    assert delta.dtype == torch.float32 and residual.dtype == torch.float32
+    assert val.dtype == torch.float32 and idx.element_size() == 4
+    assert delta.numel() == residual.numel()
+    cap = _capacity(idx, val, capacity)
+    _check(lib().pulse_loco_sparsify(_p(delta), _p(residual), delta.numel(), float(tau),
+                                     _p(theta), _p(idx), _p(val), cap,
+                                     _p(count), index_base, _p(ws), ws.numel(), _stream(stream)),
+           "pulse_loco_sparsify")
+
+
+@dataclass
+class LocoTensor:
+    delta: torch.Tensor
+    residual: torch.Tensor
+    theta: Optional[torch.Tensor] = None
+    index_base: int = 0
+
+
+class LocoBatch:
+    def __init__(self, tensors: Sequence[LocoTensor]):
+        self.n = len(tensors)
+        arr = (_LocoTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert t.delta.dtype == torch.float32 and t.residual.dtype == torch.float32
+            assert t.delta.numel() == t.residual.numel()
+            arr[i] = _LocoTensor(_p(t.delta), _p(t.residual), _p(t.theta), t.delta.numel(),
+                                 t.index_base)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, tau, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_loco_sparsify_batch(self.arr, self.n, float(tau), _p(idx), _p(val),
+                                               cap, _p(count), _p(seg_begin), _p(ws), ws.numel(),
+                                               _stream(stream)), "pulse_loco_sparsify_batch")

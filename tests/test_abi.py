@@ -1,0 +1,106 @@
+"""C ABI checks that need no GPU: libpulse.so loads, exports every function that
+include/pulse.h declares, and rejects bad arguments on the host before any
+launch (the pointers below are never dereferenced: validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2602_03839_amd import pulse
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pulse.h")
+
+OK, EINVAL, ERANGE, EALIGN = 0, -1, -2, -3
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pulse_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(pulse.LIB_PATH):
+        from paper_2602_03839_amd import build
+        build.build()
+    return pulse.lib()
+
+
+def test_exports_every_declared_function(L):
+    names = declared_functions()
+    assert len(names) == 10, names
+    assert set(names) == set(pulse.EXPORTS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_strerror_and_workspace(L):
+    assert L.pulse_workspace_bytes() >= 8 * (1 << 16)
+    for rc in (OK, EINVAL, ERANGE, EALIGN, -4):
+        assert L.pulse_strerror(rc).decode().startswith("PULSE_")
+
+
+A = 1 << 20  # fake, 16-byte-aligned "device" address (never touched)
+
+
+def ws_args(L):
+    return A * 8, L.pulse_workspace_bytes()
+
+
+def test_encode_validation(L):
+    ws, wsb = ws_args(L)
+    enc = L.pulse_encode
+    # n == 0: nothing to do
+    assert enc(None, None, 0, None, None, 0, None, 0, None, None, 0, None) == OK
+    # missing count
+    assert enc(A, A, 10, A, A, 10, None, 0, None, ws, wsb, None) == EINVAL
+    assert b"count" in L.pulse_last_error()
+    # misaligned master / snapshot
+    assert enc(A + 4, A, 10, A, A, 10, A, 0, None, ws, wsb, None) == EALIGN
+    assert enc(A, A + 2, 10, A, A, 10, A, 0, None, ws, wsb, None) == EALIGN
+    # index range beyond 2^32
+    assert enc(A, A, 10, A, A, 10, A, (1 << 32) - 5, None, ws, wsb, None) == ERANGE
+    # workspace missing / too small / misaligned
+    assert enc(A, A, 10, A, A, 10, A, 0, None, None, wsb, None) == EINVAL
+    assert enc(A, A, 10, A, A, 10, A, 0, None, ws, wsb - 8, None) == EINVAL
+    assert enc(A, A, 10, A, A, 10, A, 0, None, ws + 8, wsb, None) == EALIGN
+    # capacity > 0 but no patch buffers
+    assert enc(A, A, 10, None, A, 10, A, 0, None, ws, wsb, None) == EINVAL
+
+
+def test_batch_validation(L):
+    ws, wsb = ws_args(L)
+    arr = (pulse._EncodeTensor * 2)()
+    arr[0] = pulse._EncodeTensor(A, A, None, 100, 0)
+    arr[1] = pulse._EncodeTensor(A, A + 6, None, 100, 100)
+    assert L.pulse_encode_batch(arr, 2, A, A, 10, A, None, ws, wsb, None) == EALIGN
+    assert b"tensor 1" in L.pulse_last_error()
+    assert L.pulse_encode_batch(None, 0, None, None, 0, None, None, None, 0, None) == OK
+    arr[1] = pulse._EncodeTensor(A, A, None, 100, (1 << 32) - 99)
+    assert L.pulse_encode_batch(arr, 2, A, A, 10, A, None, ws, wsb, None) == ERANGE
+
+
+def test_apply_validation(L):
+    assert L.pulse_apply(A, 10, A, A, 10, None, A, 0, None, None) == EINVAL
+    assert L.pulse_apply(A, 10, A, A + 1, 10, A, A, 0, None, None) == EALIGN
+    assert L.pulse_apply(A, 10, A, A, 10, A, A, (1 << 32) - 1, None, None) == ERANGE
+    assert L.pulse_apply(A, 10, A, A, 0, A, A, 0, None, None) == OK  # empty patch
+
+
+def test_loco_validation(L):
+    ws, wsb = ws_args(L)
+    f = L.pulse_loco_sparsify
+    assert f(A, A, 0, 0.0, None, None, None, 0, None, 0, None, 0, None) == OK
+    assert f(A + 8, A, 16, 0.0, None, A, A, 16, A, 0, ws, wsb, None) == EALIGN
+    assert f(A, A, 16, 0.0, A + 4, A, A, 16, A, 0, ws, wsb, None) == EALIGN
+    assert f(A, None, 16, 0.0, None, A, A, 16, A, 0, ws, wsb, None) == EINVAL
+    assert f(A, A, 16, 0.0, None, A, A, 16, A, (1 << 32) - 8, ws, wsb, None) == ERANGE
+
+
+def test_cast_validation(L):
+    assert L.pulse_cast_bf16(None, None, 0, None) == OK
+    assert L.pulse_cast_bf16(None, A, 5, None) == EINVAL
+    assert L.pulse_cast_bf16(A + 4, A, 5, None) == EALIGN

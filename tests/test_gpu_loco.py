@@ -1,0 +1,149 @@
+"""GPU parity for PULSELoCo sparsification (Alg. 2) against the oracle, bit-exact:
+emitted indices, FP32 values and the FP32 residual, over shapes, thresholds,
+the BF16-gate form, overflow, batches, and a 10-round error-feedback chain."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_03839_amd import pulse
+from paper_2602_03839_amd import workloads as wl
+from tests.gpu_helpers import counter, dev, h32, hf32, read_count
+
+pytestmark = pytest.mark.gpu
+
+TILE = 256 * 4 * 8  # sparsify tile (elements)
+
+
+@pytest.fixture(scope="module")
+def ws():
+    return pulse.workspace()
+
+
+def run_loco(delta, res, tau, ws, theta=None, capacity=None, index_base=0, count_in=0):
+    n = delta.size
+    cap = n + count_in if capacity is None else capacity
+    o_res = res.copy()
+    o_idx = np.full(max(cap, 1), 0xA5A5A5A5, np.uint32)
+    o_val = np.full(max(cap, 1), -7.0, np.float32)
+    o_cnt, _, _ = oracle.loco(delta, o_res, tau, theta=theta, index_base=index_base, capacity=cap,
+                              count_in=count_in, idx_out=o_idx, val_out=o_val)
+    g_res = dev(res)
+    g_idx = torch.full((max(cap, 1),), 0xA5A5A5A5 - (1 << 32), dtype=torch.int32, device="cuda")
+    g_val = torch.full((max(cap, 1),), -7.0, dtype=torch.float32, device="cuda")
+    g_cnt = counter(count_in)
+    pulse.loco_sparsify(dev(delta), g_res, tau, g_idx, g_val, g_cnt, ws,
+                        theta=None if theta is None else dev(theta), index_base=index_base,
+                        capacity=cap)
+    torch.cuda.synchronize()
+    assert read_count(g_cnt) == o_cnt
+    np.testing.assert_array_equal(h32(g_idx), o_idx)
+    np.testing.assert_array_equal(hf32(g_val).view(np.uint32), o_val.view(np.uint32))
+    np.testing.assert_array_equal(hf32(g_res).view(np.uint32), o_res.view(np.uint32))
+    return o_cnt, o_res
+
+
+@pytest.mark.parametrize("n", [1, 9, TILE - 1, TILE, TILE + 1, 4 * TILE + 3, 123_457])
+def test_loco_threshold_shapes(ws, n):
+    rng = np.random.default_rng(n)
+    tau = wl.loco_tau()
+    d = wl.loco_delta_np(rng, n)
+    e = (wl.loco_delta_np(rng, n) * np.float32(0.5)).astype(np.float32)
+    run_loco(d, e, tau, ws)
+
+
+def test_loco_special_thresholds_and_values(ws):
+    rng = np.random.default_rng(3)
+    n = 2 * TILE + 17
+    d = wl.loco_delta_np(rng, n)
+    sp = np.array([0x7FC00000, 0x7F800000, 0xFF800000, 0x80000000, 0x00000001],
+                  np.uint32).view(np.float32)
+    pos = rng.random(n) < 0.05
+    d[pos] = sp[rng.integers(0, sp.size, pos.sum())]
+    e = np.zeros(n, np.float32)
+    for tau in (0.0, float("inf"), wl.loco_tau(), 1e-30):
+        run_loco(d, e, tau, ws)
+
+
+def test_loco_gate_form(ws):
+    rng = np.random.default_rng(4)
+    n = 3 * TILE + 5
+    theta = rng.normal(0, math.sqrt(wl.W_VAR), n).astype(np.float32)
+    d = (wl.loco_delta_np(rng, n) * np.float32(30)).astype(np.float32)
+    e = (wl.loco_delta_np(rng, n) * np.float32(10)).astype(np.float32)
+    cnt, _ = run_loco(d, e, 0.0, ws, theta=theta)
+    assert 0 < cnt < n
+
+
+def test_loco_overflow_append_base(ws):
+    rng = np.random.default_rng(5)
+    n = 5 * TILE + 99
+    d = wl.loco_delta_np(rng, n)
+    e = np.zeros(n, np.float32)
+    tau = wl.loco_tau()
+    nnz = int((np.abs(d) >= np.float32(tau)).sum())
+    for cap in (7 + nnz, 7 + nnz // 3, 7):
+        run_loco(d, e, tau, ws, capacity=cap, count_in=7, index_base=999)
+
+
+def test_loco_ten_round_chain(ws):
+    """Config c5's recipe at 2^20 elements: 10 rounds, residual carried on each side."""
+    rng = np.random.default_rng(12)
+    n = 1 << 20
+    tau = wl.loco_tau()
+    e_or = np.zeros(n, np.float32)
+    g_res = torch.zeros(n, dtype=torch.float32, device="cuda")
+    g_idx = torch.empty(n, dtype=torch.int32, device="cuda")
+    g_val = torch.empty(n, dtype=torch.float32, device="cuda")
+    dens = []
+    for r in range(10):
+        d = wl.loco_delta_np(rng, n)
+        o_cnt, o_idx, o_val = oracle.loco(d, e_or, tau)
+        g_cnt = counter(0)
+        pulse.loco_sparsify(dev(d), g_res, tau, g_idx, g_val, g_cnt, ws)
+        torch.cuda.synchronize()
+        assert read_count(g_cnt) == o_cnt
+        np.testing.assert_array_equal(h32(g_idx)[:o_cnt], o_idx[:o_cnt])
+        np.testing.assert_array_equal(hf32(g_val)[:o_cnt].view(np.uint32),
+                                      o_val[:o_cnt].view(np.uint32))
+        np.testing.assert_array_equal(hf32(g_res).view(np.uint32), e_or.view(np.uint32))
+        dens.append(o_cnt / n)
+    assert abs(dens[0] - 0.02) < 0.002 and dens[-1] > dens[0]
+
+
+def test_loco_batch_with_empty_tensors(ws):
+    rng = np.random.default_rng(13)
+    sizes = [0, 3, TILE + 1, 0, 50_001, 8, 0] + [int(rng.integers(0, 5000)) for _ in range(66)]
+    tau = wl.loco_tau()
+    descs, host = [], []
+    base = 0
+    for n in sizes:
+        d = wl.loco_delta_np(rng, n)
+        e = (wl.loco_delta_np(rng, n) * np.float32(0.7)).astype(np.float32)
+        th = rng.normal(0, 0.1, n).astype(np.float32) if rng.random() < 0.3 else None
+        host.append((d, e.copy(), th, base))
+        mk = (lambda a: dev(a)) if n else (lambda a: torch.empty(0, dtype=torch.float32, device="cuda"))
+        descs.append(pulse.LocoTensor(mk(d), mk(e), None if th is None else mk(th), base))
+        base += n
+    cap = base
+    o_idx = np.zeros(cap, np.uint32)
+    o_val = np.zeros(cap, np.float32)
+    cnt, o_seg = 0, []
+    for d, e, th, b in host:
+        o_seg.append(cnt)
+        cnt, _, _ = oracle.loco(d, e, tau, theta=th, index_base=b, capacity=cap, count_in=cnt,
+                                idx_out=o_idx, val_out=o_val)
+    g_idx = torch.zeros(cap, dtype=torch.int32, device="cuda")
+    g_val = torch.zeros(cap, dtype=torch.float32, device="cuda")
+    g_cnt = counter(0)
+    g_seg = torch.full((len(sizes),), -1, dtype=torch.int64, device="cuda")
+    pulse.LocoBatch(descs)(tau, g_idx, g_val, g_cnt, ws, seg_begin=g_seg)
+    torch.cuda.synchronize()
+    assert read_count(g_cnt) == cnt
+    np.testing.assert_array_equal(g_seg.cpu().numpy(), np.array(o_seg, np.int64))
+    np.testing.assert_array_equal(h32(g_idx)[:cnt], o_idx[:cnt])
+    np.testing.assert_array_equal(hf32(g_val)[:cnt].view(np.uint32), o_val[:cnt].view(np.uint32))
+    for (d, e, th, b), desc in zip(host, descs):
+        np.testing.assert_array_equal(hf32(desc.residual).view(np.uint32), e.view(np.uint32))
