@@ -16,19 +16,23 @@ namespace pulse {
 
 // ---------------------------------------------------------------- workspace
 //
+// word 0: ticket counter = (G0 << 24) | c, where c counts the chunks of
+//         kChunk consecutive tiles drawn in the current launch and G0 is the
+//         global sequence number of that launch's first tile.  Blocks are
+//         persistent and draw chunks until they get one past the launch's last
+//         tile.  A single device-wide counter sustains only ~75M atomics/s on
+//         MI355X, so tiles are handed out kChunk at a time.
 // word 1: set to 1 if a look-back ever gave up waiting (see look_back).
-// word 0: ticket counter = (G0 << 24) | t, where t counts the tickets taken in
-//         the current launch and G0 is the global sequence number of that
-//         launch's first tile.  The block that draws the launch's last ticket
-//         stores ((G0 + ntiles) << 24), so the next launch starts at t = 0 with
-//         no reset kernel.  All other blocks drew their tickets before it (the
-//         counter's modification order), so none of them can see that store.
+// word 2: number of blocks of the current launch that have finished.  The last
+//         block out (every other block has made its final draw before it
+//         counted itself out) stores ((G0 + ntiles) << 24) into word 0 and 0
+//         here, so the next launch starts at t = 0 with no reset kernel.
 // words 32 ..: a ring of kSlots status words.  Tile with global sequence g uses
 //         slot g mod kSlots and tags its word with (g / kSlots) mod 256.  Every
 //         sequence number is published exactly once, in order of use, so a
 //         slot holds either the current lap's word or the previous lap's, whose
 //         tag differs; a stale word reads as "not ready".  A slot is reused only
-//         kSlots tickets later; since at most R <= 8192 tiles are resident at
+//         kSlots tickets later; since at most R <= 8192 tiles are in flight at
 //         once and a tile looks back at most R tiles, kSlots > 2R + 2 ensures a
 //         word is never overwritten while a reader still needs it.
 constexpr int kTicketBits = 24;
@@ -38,7 +42,7 @@ constexpr int kSlotBits = 16;
 constexpr uint64_t kSlots = 1ull << kSlotBits;
 constexpr int kStatusOffsetWords = 32;            // 256-byte header
 constexpr size_t kWorkspaceBytes = (kStatusOffsetWords + kSlots) * sizeof(uint64_t);
-constexpr uint32_t kMaxTilesPerLaunch = (1u << kTicketBits) - 1;
+constexpr uint32_t kMaxTilesPerLaunch = (1u << kTicketBits) - 1;  // < kNoTicket
 
 // status word: [63:62] flag, [61:54] lap tag, [53:0] value
 constexpr uint64_t kFlagAggregate = 1;  // value = this tile's own count
@@ -47,10 +51,15 @@ constexpr uint64_t kValueMask = (1ull << 54) - 1;
 
 // A predecessor is always resident or finished, so a look-back normally waits
 // microseconds.  Only a workspace that was not zero-filled can make a tile
-// wait for one that never runs; after this many polls (about a second) the
-// wave stops waiting, counts the missing tiles as empty and raises word 1 of
-// the workspace, so a misuse yields a wrong patch instead of a hung GPU.
-constexpr uint32_t kMaxPolls = 1u << 20;
+// wait for one that never runs; after this many polls (well under a second)
+// the wave stops waiting, counts the missing tiles as empty and raises word 1
+// of the workspace, after which no wave of the device waits any more: a
+// misuse yields a wrong patch and a raised flag instead of a hung GPU.
+constexpr uint32_t kMaxPolls = 1u << 18;
+
+#ifndef PULSE_LOOKBACK_K
+#define PULSE_LOOKBACK_K 1
+#endif
 
 __device__ __forceinline__ uint64_t status_word(uint64_t flag, uint64_t g, uint64_t value) {
   return (flag << 62) | (((g >> kSlotBits) & 0xFFull) << 54) | (value & kValueMask);
@@ -107,16 +116,38 @@ struct Ticket {
   uint64_t seq;   // global sequence number of this tile (mod 2^40)
 };
 
-// Called by one thread per block.  `ntiles` is the launch's tile count.
-__device__ __forceinline__ uint64_t draw_ticket(uint64_t* ws, uint32_t ntiles) {
-  const uint64_t c =
-      __hip_atomic_fetch_add(ws, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint32_t t = (uint32_t)(c & kTicketMask);
-  if (t == ntiles - 1) {
-    const uint64_t next = (((c >> kTicketBits) + ntiles) & kSeqMask) << kTicketBits;
-    __hip_atomic_store(ws, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Called by one thread of the block.
+__device__ __forceinline__ uint64_t draw_ticket(uint64_t* ws) {
+  return __hip_atomic_fetch_add(ws, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Called by one thread per block after its last draw.  The acquire-release
+// increment orders every block's draws before the reset done by the last one.
+__device__ __forceinline__ void finish_launch(uint64_t* ws, uint64_t g0, uint32_t ntiles,
+                                              uint32_t nblocks) {
+  const uint64_t d =
+      __hip_atomic_fetch_add(ws + 2, 1ull, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  if (d == nblocks - 1) {
+    __hip_atomic_store(ws + 2, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ws, ((g0 + ntiles) & kSeqMask) << kTicketBits, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   }
-  return c;
+}
+
+// A ticket value whose tile field is past any launch: "no tile".
+constexpr uint64_t kNoTicket = kTicketMask;
+
+// Tiles per ticket.  A chunk's tiles are processed in consecutive iterations,
+// so the chunk's last aggregate appears kChunk - 1 iterations after its first;
+// with kChunk <= kDefer later tiles never wait for it at resolution time.
+#ifndef PULSE_CHUNK
+#define PULSE_CHUNK 2
+#endif
+constexpr uint32_t kChunk = PULSE_CHUNK;
+
+// Ticket word of tile `tile` of the launch whose first tile has sequence g0.
+__device__ __forceinline__ uint64_t make_ticket(uint64_t g0, uint32_t tile, uint32_t ntiles) {
+  return tile < ntiles ? ((g0 << kTicketBits) | tile) : kNoTicket;
 }
 
 __device__ __forceinline__ Ticket decode_ticket(uint64_t c) {
@@ -128,59 +159,114 @@ __device__ __forceinline__ Ticket decode_ticket(uint64_t c) {
 
 // ---------------------------------------------------------------- look-back
 //
-// Executed by one full wave of the block of tile `tile` (tile > 0), after it
-// has published its aggregate.  Returns the exclusive prefix of the tile: the
-// inclusive prefix of the nearest predecessor that has published one, plus the
-// aggregates of the tiles in between.  Lane i inspects tile (j - i); a window
-// is consumed only when every tile up to the nearest prefix is ready.  The wait
-// ends because tickets are handed out in order: every predecessor belongs to a
-// block that is already running, and tile 0 always publishes a prefix.
-__device__ uint64_t look_back(uint64_t* ws, const Ticket& tk) {
+// Computes the exclusive prefix of tile `tk` (tile > 0) after it has published
+// its aggregate: the inclusive prefix of the nearest predecessor that has
+// published one, plus the aggregates of the tiles in between.  A window of
+// 64 * LK predecessors is read at once (lane i, slot m inspects tile
+// j - (m*64 + i)) and consumed only when every tile up to the nearest prefix
+// is ready.  The first window is issued early by the caller (look_back_issue)
+// so its latency overlaps other work.  If a needed tile is not ready, only
+// lane 0 polls that tile's word, with a growing pause, before the window is
+// read again: device-scope loads bypass the per-XCD L2 caches, and hundreds
+// of waves re-reading whole windows would flood the memory side.  The wait
+// ends because tickets are handed out in order: every predecessor belongs to
+// a block that is already running, and tile 0 always publishes a prefix.
+template <int LK>
+struct LookWindow {
+  uint64_t w[LK];
+};
+
+template <int LK>
+__device__ __forceinline__ void look_back_issue(uint64_t* ws, const Ticket& tk, int64_t j,
+                                                LookWindow<LK>& win) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int m = 0; m < LK; ++m) {
+    const int64_t tj = j - (m * 64 + lane);
+    win.w[m] = 0;
+    if (tj >= 0) {
+      const uint64_t gj = (tk.seq - (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
+      win.w[m] = __hip_atomic_load(status_slot(ws, gj), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+template <int LK>
+__device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win) {
   const int lane = lane_id();
   uint64_t excl = 0;
   int64_t j = (int64_t)tk.tile - 1;
   uint32_t polls = 0;
   for (;;) {
-    const int64_t tj = j - lane;
-    const bool in_range = tj >= 0;
-    uint64_t w = 0, flag = 0;
-    if (in_range) {
+    uint64_t pm[LK], xm[LK];
+#pragma unroll
+    for (int m = 0; m < LK; ++m) {
+      const int64_t tj = j - (m * 64 + lane);
       const uint64_t gj = (tk.seq - (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
-      w = __hip_atomic_load(status_slot(ws, gj), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      flag = w >> 62;
-      if (((w >> 54) & 0xFFull) != ((gj >> kSlotBits) & 0xFFull)) flag = 0;
+      if (tj >= 0 && ((win.w[m] >> 54) & 0xFFull) != ((gj >> kSlotBits) & 0xFFull))
+        win.w[m] = 0;  // stale lap: not ready
+      const uint64_t flag = win.w[m] >> 62;
+      pm[m] = __ballot(tj >= 0 && flag == kFlagPrefix);
+      xm[m] = __ballot(tj >= 0 && flag == 0);
     }
-    const uint64_t pmask = __ballot(in_range && flag == kFlagPrefix);
-    const uint64_t xmask = __ballot(in_range && flag == 0);
-    const int first_p = pmask ? __builtin_ctzll(pmask) : 64;
-    const uint64_t need = first_p >= 63 ? ~0ull : ((2ull << first_p) - 1);
-    if ((xmask & need) && ++polls < kMaxPolls) {
-      __builtin_amdgcn_s_sleep(1);
+    // nearest prefix in window order (m, then lane)
+    int first_m = LK, first_l = 64;
+#pragma unroll
+    for (int m = LK - 1; m >= 0; --m)
+      if (pm[m]) { first_m = m; first_l = __builtin_ctzll(pm[m]); }
+    // nearest tile that is needed but not ready
+    int wait_q = -1;
+#pragma unroll
+    for (int m = LK - 1; m >= 0; --m) {
+      uint64_t need;
+      if (m < first_m) need = ~0ull;
+      else if (m == first_m) need = first_l >= 63 ? ~0ull : ((2ull << first_l) - 1);
+      else need = 0;
+      if (xm[m] & need) wait_q = m * 64 + __builtin_ctzll(xm[m] & need);
+    }
+    if (wait_q >= 0) {
+      // wait for that one tile, then read the window again
+      const int64_t tq = j - wait_q;
+      const uint64_t gq = (tk.seq - (uint64_t)((int64_t)tk.tile - tq)) & kSeqMask;
+      uint32_t pause = 0;
+      bool ready = false;
+      bool gave_up = false;
+      while (!ready && !gave_up) {
+        if (lane == 0) {
+          const uint64_t x =
+              __hip_atomic_load(status_slot(ws, gq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ready = (x >> 62) != 0 && ((x >> 54) & 0xFFull) == ((gq >> kSlotBits) & 0xFFull);
+          // once any wave of the device has given up, nobody waits any more
+          if (!ready && (++polls >= kMaxPolls ||
+                         __hip_atomic_load(ws + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)))
+            gave_up = true;
+        }
+        ready = __shfl(ready ? 1 : 0, 0, 64) != 0;
+        gave_up = __shfl(gave_up ? 1 : 0, 0, 64) != 0;
+        if (!ready && !gave_up) {
+          if (pause < 8) ++pause;
+          for (uint32_t z = 0; z < pause; ++z) __builtin_amdgcn_s_sleep(2);
+        }
+      }
+      if (!ready) {
+        // gave up: only a workspace that was not zero-filled gets here
+        if (lane == 0) __hip_atomic_store(ws + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return excl;
+      }
+      look_back_issue<LK>(ws, tk, j, win);
       continue;
     }
-    if (xmask & need) {
-      if (lane == 0) __hip_atomic_store(ws + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return excl;
+    uint64_t v = 0;
+#pragma unroll
+    for (int m = 0; m < LK; ++m) {
+      const bool take = m < first_m || (m == first_m && lane <= first_l);
+      if (take) v += win.w[m] & kValueMask;
     }
-    const uint64_t v = (in_range && lane <= first_p) ? (w & kValueMask) : 0;
     excl += wave_sum_u64(v);
-    if (first_p < 64) return excl;
-    j -= 64;
+    if (first_m < LK) return excl;
+    j -= 64 * LK;
+    look_back_issue<LK>(ws, tk, j, win);
   }
-}
-
-// ---------------------------------------------------------------- loads
-
-__device__ __forceinline__ uint4 load16(const void* p) {
-  return *reinterpret_cast<const uint4*>(p);
-}
-
-__device__ __forceinline__ void store16(void* p, uint4 v) {
-  *reinterpret_cast<uint4*>(p) = v;
-}
-
-__device__ __forceinline__ uint32_t get_u32(const uint4& v, int i) {
-  return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
 }
 
 // Smallest k in [0, count) with begin[k + 1] > t, for a non-decreasing begin[]
@@ -193,6 +279,180 @@ __device__ __forceinline__ int find_owner(const Arr& begin, int count, uint32_t 
     if (begin[mid] <= t) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+// ---------------------------------------------------------------- scan wave
+//
+// The loop run by the one scan wave of a persistent encode/sparsify block.
+// Blocks synchronise once per iteration.  Tile T(i) is the tile whose data
+// the compute waves turn into wave totals in iteration i (its loads were
+// issued during iteration i - 1).  For each tile:
+//   iteration i            compute waves publish its wave totals
+//                          (s_wtot[i & 1]); after the barrier the scan wave
+//                          combines them (group-major) into s_wexcl[i & 3]
+//                          and publishes the tile aggregate (tile 0 of the
+//                          launch publishes its inclusive prefix, folding in
+//                          the append position *count);
+//   iteration i + kResolve the scan wave resolves the tile: the first
+//                          look-back window is read before the barrier,
+//                          overlapping the compute, and is consumed after it;
+//                          it publishes the inclusive prefix and stores the
+//                          exclusive prefix in s_excl[i & 1];
+//   iteration i + kDefer   after the barrier the compute waves write its
+//                          entries.
+// Tiles computed in the same iteration by different blocks publish their
+// aggregates at about the same time, so a tile is resolved kResolve = 2
+// iterations later, when every predecessor has long published: the look-back
+// then reads one window and never waits.  The scan wave's work of iteration i
+// only has to be done before barrier i + 1, so it does not hold the compute
+// waves up while it waits on memory.  Tickets: s_tk[i % 3] holds T(i); before
+// barrier i the scan wave stores T(i + 2), which the compute waves need at the
+// top of iteration i + 1 to start that tile's loads.  The last tile stores the
+// new *count; the first tile of each tensor stores the tensor's segment
+// start.  Both loops run while any tile is still to be computed, resolved or
+// written.
+constexpr int kResolve = 2;            // iterations from compute to resolution
+constexpr int kDefer = kResolve + 1;   // iterations from compute to write-out
+constexpr int kValBufs = kDefer + 2;   // LDS value buffers (ring)
+
+struct ScanState {
+  Ticket tk;
+  uint64_t agg;
+  int k;
+  bool valid;
+};
+
+template <int U, int NW, typename Params>
+__device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot2,
+                               uint32_t* s_wexcl4, uint64_t* s_excl2) {
+  const int lane = lane_id();
+  // tiles come in chunks of kChunk consecutive tiles, one atomic per chunk;
+  // next_tile / left: the unused part of the block's current chunk
+  uint64_t g0 = 0;
+  uint32_t next_tile = 0, left = 0;
+  auto take = [&]() -> uint64_t {  // lane 0 only
+    if (left == 0) {
+      const uint64_t c = draw_ticket(p.ws);
+      g0 = c >> kTicketBits;
+      next_tile = (uint32_t)(c & kTicketMask) * kChunk;
+      left = kChunk;
+    }
+    --left;
+    return make_ticket(g0, next_tile++, p.ntiles);
+  };
+  if (lane == 0) {
+    s_tk[0] = take();
+    s_tk[1] = take();
+  }
+  __syncthreads();  // first two tickets
+  // g0 (lane 0 only) comes from the counter itself: a ticket slot may hold
+  // kNoTicket when the block's first chunk lies past the last tile, and the
+  // sequence base must never move backwards
+  uint64_t count_in = 0;
+  ScanState hist[kDefer];  // hist[d]: T(i - 1 - d)
+#pragma unroll
+  for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
+  for (int it = 0;; ++it) {
+    const Ticket cur = decode_ticket(s_tk[it % 3]);
+    const bool have_cur = cur.tile < p.ntiles;
+    bool pending = have_cur;
+#pragma unroll
+    for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
+    if (!pending) break;
+    const bool have_next = decode_ticket(s_tk[(it + 1) % 3]).tile < p.ntiles;
+    if (lane == 0) s_tk[(it + 2) % 3] = have_next ? take() : kNoTicket;
+    // first look-back window of T(i - kResolve), overlapping the compute of T(i)
+    const ScanState res = hist[kResolve - 1];
+    LookWindow<PULSE_LOOKBACK_K> win;
+    const bool walk = res.valid && res.tk.tile != 0;
+    if (walk) look_back_issue<PULSE_LOOKBACK_K>(p.ws, res.tk, (int64_t)res.tk.tile - 1, win);
+    __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + 2) is in s_tk
+    ScanState now;
+    now.valid = have_cur;
+    if (have_cur) {
+      const uint32_t v = lane < U * NW ? s_wtot2[(it & 1) * U * NW + lane] : 0u;
+      const uint32_t incl = wave_incl_scan(v);
+      if (lane < U * NW) s_wexcl4[(it & 3) * U * NW + lane] = incl - v;
+      now.tk = cur;
+      now.agg = __shfl(incl, 63, 64);
+      now.k = find_owner(p.tile_begin, p.ntensors, cur.tile);
+      if (cur.tile == 0) {
+        count_in = *p.count;  // append position, written by an earlier call
+        if (lane == 0) status_publish(p.ws, cur.seq, kFlagPrefix, count_in + now.agg);
+      } else if (lane == 0) {
+        status_publish(p.ws, cur.seq, kFlagAggregate, now.agg);
+      }
+    }
+    if (res.valid) {
+      uint64_t excl;
+      if (!walk) {
+        excl = count_in;
+      } else {
+        excl = look_back<PULSE_LOOKBACK_K>(p.ws, res.tk, win);
+        if (lane == 0) status_publish(p.ws, res.tk.seq, kFlagPrefix, excl + res.agg);
+      }
+      if (lane == 0) {
+        s_excl2[(it - kResolve) & 1] = excl;
+        if (res.tk.tile == p.ntiles - 1) *p.count = excl + res.agg;
+        if (p.seg_begin) {
+          // segment starts of this tensor and of the empty tensors just before it
+          if (p.tile_begin[res.k] == res.tk.tile) {
+            for (int kk = res.k; kk >= 0 && p.tile_begin[kk] == res.tk.tile; --kk)
+              p.seg_begin[kk] = excl;
+          }
+          // empty tensors at the end of the batch start where the patch ends
+          if (res.tk.tile == p.ntiles - 1) {
+            for (int kk = res.k + 1; kk < p.ntensors; ++kk) p.seg_begin[kk] = excl + res.agg;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int d = kDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
+    hist[0] = now;
+  }
+  if (lane == 0) finish_launch(p.ws, g0, p.ntiles, gridDim.x);
+}
+
+// ---------------------------------------------------------------- loads
+
+__device__ __forceinline__ uint4 load16(const void* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte load with the non-temporal hint: streamed data that is read once
+// should not displace what the caches hold.
+__device__ __forceinline__ uint4 load16_stream(const void* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store16_stream(void* p, uint4 v) {
+  u32x4_t w;
+  w.x = v.x; w.y = v.y; w.z = v.z; w.w = v.w;
+  __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
+}
+
+__device__ __forceinline__ void store16(void* p, uint4 v) {
+  *reinterpret_cast<uint4*>(p) = v;
+}
+
+__device__ __forceinline__ uint32_t get_u32(const uint4& v, int i) {
+  return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+
+// Blocks of `kernel` (launched with `block` threads) that fit on the current
+// device at once: the grid of a persistent launch.  Cached per device.
+inline int persistent_grid(const void* kernel, int block) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, 0) != hipSuccess) return 0;
+  return cus * (per_cu > 0 ? per_cu : 1);
 }
 
 }  // namespace pulse

@@ -11,11 +11,27 @@ namespace pulse {
 
 constexpr int kMaxBatch = 64;  // tensors per launch; larger batches are split
 
-// Tile shapes (threads per block, 8-element groups per thread).
-constexpr int kEncodeTB = 512;
-constexpr int kEncodeU = 4;
-constexpr int kLocoTB = 256;
-constexpr int kLocoU = 4;
+// Tile shapes: compute threads per block (a multiple of 64; one more wave is
+// added for the scan) and 8-element groups per thread.  The defaults give
+// 16-wave blocks (15 compute + 1 scan), one per CU: waves are handed out to
+// the SIMDs in fours, and the LDS value ring of one block takes 150 KiB of the
+// CU's 160 KiB.  Overridable at build time for tuning sweeps.
+#ifndef PULSE_ENCODE_TB
+#define PULSE_ENCODE_TB 960
+#endif
+#ifndef PULSE_ENCODE_U
+#define PULSE_ENCODE_U 2
+#endif
+#ifndef PULSE_LOCO_TB
+#define PULSE_LOCO_TB 960
+#endif
+#ifndef PULSE_LOCO_U
+#define PULSE_LOCO_U 1
+#endif
+constexpr int kEncodeTB = PULSE_ENCODE_TB;
+constexpr int kEncodeU = PULSE_ENCODE_U;
+constexpr int kLocoTB = PULSE_LOCO_TB;
+constexpr int kLocoU = PULSE_LOCO_U;
 
 struct EncodeTensorDesc {
   const float* w_new;

@@ -4,177 +4,245 @@
 // selected (index, FP32 value) pairs in index order, and rewrite the residual
 // (0 where sent, s elsewhere) -- one pass over Delta and e.
 //
-// Same tile structure and ordered compaction as encode.hip; the residual is
-// stored densely right after the selection, and the rare selected-but-beyond-
-// capacity entries are patched back to s in the write phase (same lane, same
-// address, so program order keeps the later store).
+// Same persistent, pipelined tile structure and ordered compaction as
+// encode.hip (NW compute waves + 1 scan wave; the next tile's loads are in
+// flight while the scan wave walks back).  The residual of a tile is stored
+// densely right after the selection; the rare selected-but-beyond-capacity
+// entries are patched back to s in the write phase (same lane, same address,
+// so program order keeps the later store).
 #include "device_common.hpp"
 #include "launch.hpp"
 
 namespace pulse {
 
-template <int TB, int U>
-__global__ __launch_bounds__(TB) void loco_kernel(LocoParams p) {
-  constexpr int NW = TB / 64;
-  constexpr uint32_t TILE = TB * U * 8;
-  __shared__ uint64_t s_ticket;
-  __shared__ uint64_t s_excl;
-  __shared__ uint32_t s_wtot[U * NW];
-  __shared__ uint32_t s_wexcl[U * NW];
-  __shared__ uint4 s_vals[U * TB * 2];
+namespace {
+
+struct LocoCtx {
+  const float* d;
+  float* r;
+  const float* th;
+  uint64_t e0;
+  uint64_t n;
+  int k;
+  uint32_t tile_in_tensor;
+};
+
+__device__ __forceinline__ LocoCtx locate(const LocoParams& p, uint32_t tile, uint32_t tile_elems) {
+  LocoCtx c;
+  c.k = find_owner(p.tile_begin, p.ntensors, tile);
+  c.tile_in_tensor = tile - p.tile_begin[c.k];
+  c.e0 = (uint64_t)c.tile_in_tensor * tile_elems;
+  c.n = p.t[c.k].n;
+  c.d = p.t[c.k].delta;
+  c.r = p.t[c.k].residual;
+  c.th = p.t[c.k].theta;
+  return c;
+}
+
+// Registers of one tile: Delta, residual and (gate form only) theta.
+template <int U, bool GATE>
+struct LocoRegs {
+  uint4 d0[U], d1[U], r0[U], r1[U];
+  uint4 t0[GATE ? U : 1], t1[GATE ? U : 1];
+};
+
+// Loads of group u of a tile for lane `cl`; whole tiles (`full`, uniform
+// across the block) take the straight-line 16-byte path.  In the gate form a
+// tensor without theta loads nothing for it (its selection uses tau).
+template <int TBC, int U, bool GATE>
+__device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const LocoCtx& c, int cl,
+                                           bool full) {
+  const uint64_t e = c.e0 + (uint64_t)(u * TBC + cl) * 8;
+  if (full) {
+    g.d0[u] = load16_stream(c.d + e);
+    g.d1[u] = load16_stream(c.d + e + 4);
+    g.r0[u] = load16_stream(c.r + e);
+    g.r1[u] = load16_stream(c.r + e + 4);
+    if (GATE && c.th) {
+      g.t0[u] = load16_stream(c.th + e);
+      g.t1[u] = load16_stream(c.th + e + 4);
+    }
+  } else {
+    uint32_t dv[8], rv[8], tv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const bool ok = e + i < c.n;
+      dv[i] = ok ? __float_as_uint(c.d[e + i]) : 0u;
+      rv[i] = ok ? __float_as_uint(c.r[e + i]) : 0u;
+      tv[i] = (ok && GATE && c.th) ? __float_as_uint(c.th[e + i]) : 0u;
+    }
+    g.d0[u] = make_uint4(dv[0], dv[1], dv[2], dv[3]);
+    g.d1[u] = make_uint4(dv[4], dv[5], dv[6], dv[7]);
+    g.r0[u] = make_uint4(rv[0], rv[1], rv[2], rv[3]);
+    g.r1[u] = make_uint4(rv[4], rv[5], rv[6], rv[7]);
+    if (GATE) {
+      g.t0[u] = make_uint4(tv[0], tv[1], tv[2], tv[3]);
+      g.t1[u] = make_uint4(tv[4], tv[5], tv[6], tv[7]);
+    }
+  }
+}
+
+}  // namespace
+
+template <int NW, int U, bool GATE>
+__global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
+  constexpr int TBC = NW * 64;
+  constexpr uint32_t TILE = TBC * U * 8;
+  __shared__ uint64_t s_tk[3];
+  __shared__ uint64_t s_excl[2];
+  __shared__ uint32_t s_wtot[2 * U * NW];
+  __shared__ uint32_t s_wexcl[4 * U * NW];
+  __shared__ uint4 s_vals[kValBufs][U * TBC * 2];
+  static_assert(U * NW <= 64, "block scan runs on one wave");
+  static_assert(U <= 4, "masks of all groups are packed into one register");
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid >> 6;
-
-  if (tid == 0) s_ticket = draw_ticket(p.ws, p.ntiles);
-  __syncthreads();
-  const Ticket tk = decode_ticket(s_ticket);
-
-  const int k = find_owner(p.tile_begin, p.ntensors, tk.tile);
-  const uint32_t tile_in_tensor = tk.tile - p.tile_begin[k];
-  const uint64_t n = p.t[k].n;
-  const uint64_t e0 = (uint64_t)tile_in_tensor * TILE;
-  const float* __restrict__ d = p.t[k].delta;
-  float* __restrict__ r = p.t[k].residual;
-  const float* __restrict__ th = p.t[k].theta;
   const float tau = p.tau;
-  const bool full = e0 + TILE <= n;
 
-  uint32_t mask[U];
-  uint32_t cnt[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint64_t e = e0 + (uint64_t)(u * TB + tid) * 8;
-    const bool vec = full || e + 8 <= n;
-    float dv[8], rv[8], tv[8];
-    if (vec) {
-      const uint4 d0 = load16(d + e), d1 = load16(d + e + 4);
-      const uint4 r0 = load16(r + e), r1 = load16(r + e + 4);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dv[i] = __uint_as_float(get_u32(d0, i));
-        dv[4 + i] = __uint_as_float(get_u32(d1, i));
-        rv[i] = __uint_as_float(get_u32(r0, i));
-        rv[4 + i] = __uint_as_float(get_u32(r1, i));
-      }
-      if (th) {
-        const uint4 t0 = load16(th + e), t1 = load16(th + e + 4);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          tv[i] = __uint_as_float(get_u32(t0, i));
-          tv[4 + i] = __uint_as_float(get_u32(t1, i));
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const bool ok = e + i < n;
-        dv[i] = ok ? d[e + i] : 0.0f;
-        rv[i] = ok ? r[e + i] : 0.0f;
-        tv[i] = (ok && th) ? th[e + i] : 0.0f;
-      }
-    }
-    uint32_t m = 0;
-    float a[8], nr[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      a[i] = dv[i] + rv[i];
-      bool sel;
-      if (th) {
-        const float after = tv[i] - a[i];
-        sel = bf16_rne_bits(__float_as_uint(tv[i])) != bf16_rne_bits(__float_as_uint(after));
-      } else {
-        sel = fabsf(a[i]) >= tau;
-      }
-      if (!vec && !(e + i < n)) sel = false;
-      m |= (uint32_t)sel << i;
-      nr[i] = sel ? 0.0f : a[i];
-    }
-    if (vec) {
-      store16(r + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
-                                __float_as_uint(nr[2]), __float_as_uint(nr[3])));
-      store16(r + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
-                                    __float_as_uint(nr[6]), __float_as_uint(nr[7])));
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (e + i < n) r[e + i] = nr[i];
-    }
-    mask[u] = m;
-    cnt[u] = __builtin_popcount(m);
-    s_vals[(u * TB + tid) * 2] = make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]),
-                                            __float_as_uint(a[2]), __float_as_uint(a[3]));
-    s_vals[(u * TB + tid) * 2 + 1] = make_uint4(__float_as_uint(a[4]), __float_as_uint(a[5]),
-                                                __float_as_uint(a[6]), __float_as_uint(a[7]));
+  if (wid == NW) {
+    scan_wave_loop<U, NW>(p, s_tk, s_wtot, s_wexcl, s_excl);
+    return;
   }
 
-  uint32_t lane_excl[U];
+  // ---------------- compute waves (same schedule as encode_kernel: compute
+  // `cur` group by group while refilling the registers with the next tile,
+  // then write the entries of the tile computed kDefer iterations earlier)
+  __syncthreads();  // first two tickets
+  LocoRegs<U, GATE> g;
+  LocoCtx cc;
+  {
+    const Ticket t0 = decode_ticket(s_tk[0]);
+    if (t0.tile < p.ntiles) {
+      cc = locate(p, t0.tile, TILE);
+      const bool full = cc.e0 + TILE <= cc.n;
 #pragma unroll
-  for (int u = 0; u < U; u += 2) {
-    const uint32_t packed = cnt[u] | (u + 1 < U ? (cnt[u + 1] << 16) : 0u);
-    const uint32_t incl = wave_incl_scan(packed);
-    const uint32_t excl = incl - packed;
-    lane_excl[u] = excl & 0xFFFFu;
-    if (u + 1 < U) lane_excl[u + 1] = excl >> 16;
-    if (lane == 63) {
-      s_wtot[u * NW + wid] = incl & 0xFFFFu;
-      if (u + 1 < U) s_wtot[(u + 1) * NW + wid] = incl >> 16;
+      for (int u = 0; u < U; ++u) load_group<TBC, U, GATE>(g, u, cc, tid, full);
     }
   }
-  __syncthreads();
-
-  if (wid == 0) {
-    const uint32_t v = lane < U * NW ? s_wtot[lane] : 0u;
-    const uint32_t incl = wave_incl_scan(v);
-    if (lane < U * NW) s_wexcl[lane] = incl - v;
-    const uint64_t agg = __shfl(incl, 63, 64);
-    uint64_t excl;
-    if (tk.tile == 0) {
-      excl = *p.count;
-      if (lane == 0) status_publish(p.ws, tk.seq, kFlagPrefix, excl + agg);
-    } else {
-      if (lane == 0) status_publish(p.ws, tk.seq, kFlagAggregate, agg);
-      excl = look_back(p.ws, tk);
-      if (lane == 0) status_publish(p.ws, tk.seq, kFlagPrefix, excl + agg);
-    }
-    if (lane == 0) {
-      s_excl = excl;
-      if (tk.tile == p.ntiles - 1) *p.count = excl + agg;
-      if (p.seg_begin) {
-        if (tile_in_tensor == 0) {
-          for (int kk = k; kk >= 0 && p.tile_begin[kk] == tk.tile; --kk) p.seg_begin[kk] = excl;
+  LocoCtx hctx[kDefer];
+  uint32_t hmask[kDefer], hexcl[kDefer][(U + 1) / 2];
+  bool hvalid[kDefer];
+#pragma unroll
+  for (int d = 0; d < kDefer; ++d) hvalid[d] = false;
+  for (int it = 0;; ++it) {
+    const Ticket cur = decode_ticket(s_tk[it % 3]);
+    const Ticket nxt = decode_ticket(s_tk[(it + 1) % 3]);
+    const bool have_cur = cur.tile < p.ntiles;
+    bool pending = have_cur;
+#pragma unroll
+    for (int d = 0; d < kDefer; ++d) pending |= hvalid[d];
+    if (!pending) break;
+    const bool have_next = nxt.tile < p.ntiles;
+    const LocoCtx cn = have_next ? locate(p, nxt.tile, TILE) : cc;
+    const bool next_full = cn.e0 + TILE <= cn.n;
+    uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
+    if (have_cur) {
+      uint32_t cnt[U];
+      const bool full = cc.e0 + TILE <= cc.n;
+      const bool gate = GATE && cc.th != nullptr;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint64_t e = cc.e0 + (uint64_t)(u * TBC + tid) * 8;
+        const bool vec = full || e + 8 <= cc.n;
+        uint32_t m = 0;
+        float a[8], nr[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float dv = __uint_as_float(i < 4 ? get_u32(g.d0[u], i) : get_u32(g.d1[u], i - 4));
+          const float rv = __uint_as_float(i < 4 ? get_u32(g.r0[u], i) : get_u32(g.r1[u], i - 4));
+          a[i] = dv + rv;
+          bool sel;
+          if (gate) {
+            const float tv = __uint_as_float(i < 4 ? get_u32(g.t0[GATE ? u : 0], i)
+                                                   : get_u32(g.t1[GATE ? u : 0], i - 4));
+            const float after = tv - a[i];
+            sel = bf16_rne_bits(__float_as_uint(tv)) != bf16_rne_bits(__float_as_uint(after));
+          } else {
+            sel = fabsf(a[i]) >= tau;
+          }
+          if (!vec && !(e + i < cc.n)) sel = false;
+          m |= (uint32_t)sel << i;
+          nr[i] = sel ? 0.0f : a[i];
         }
-        if (tk.tile == p.ntiles - 1) {
-          for (int kk = k + 1; kk < p.ntensors; ++kk) p.seg_begin[kk] = excl + agg;
+        if (vec) {
+          store16_stream(cc.r + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
+                                              __float_as_uint(nr[2]), __float_as_uint(nr[3])));
+          store16_stream(cc.r + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
+                                                  __float_as_uint(nr[6]), __float_as_uint(nr[7])));
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            if (e + i < cc.n) cc.r[e + i] = nr[i];
+        }
+        mask_packed |= m << (8 * u);
+        cnt[u] = __builtin_popcount(m);
+        s_vals[it % kValBufs][(u * TBC + tid) * 2] =
+            make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
+                       __float_as_uint(a[3]));
+        s_vals[it % kValBufs][(u * TBC + tid) * 2 + 1] =
+            make_uint4(__float_as_uint(a[4]), __float_as_uint(a[5]), __float_as_uint(a[6]),
+                       __float_as_uint(a[7]));
+        // this group's registers are free: start the next tile's loads into them
+        if (have_next) load_group<TBC, U, GATE>(g, u, cn, tid, next_full);
+      }
+#pragma unroll
+      for (int u = 0; u < U; u += 2) {
+        const uint32_t packed = cnt[u] | (u + 1 < U ? (cnt[u + 1] << 16) : 0u);
+        const uint32_t incl = wave_incl_scan(packed);
+        excl_packed[u >> 1] = incl - packed;
+        if (lane == 63) {
+          s_wtot[(it & 1) * U * NW + u * NW + wid] = incl & 0xFFFFu;
+          if (u + 1 < U) s_wtot[(it & 1) * U * NW + (u + 1) * NW + wid] = incl >> 16;
         }
       }
     }
-  }
-  __syncthreads();
+    __syncthreads();  // wave totals of `cur` published; prefix of `old` resolved
 
-  const uint64_t tile_excl = s_excl;
-  const uint64_t cap = p.capacity;
-  const uint32_t base = p.t[k].index_base;
-  const float* vals = reinterpret_cast<const float*>(s_vals);
+    if (hvalid[kDefer - 1]) {
+      const LocoCtx& oc = hctx[kDefer - 1];
+      const int oi = it - kDefer;
+      const uint64_t tile_excl = s_excl[oi & 1];
+      const uint64_t cap = p.capacity;
+      const uint32_t base = p.t[oc.k].index_base;
+      const float* vals = reinterpret_cast<const float*>(s_vals[oi % kValBufs]);
+      const uint32_t* wexcl = s_wexcl + (oi & 3) * U * NW;
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    uint32_t m = mask[u];
-    if (m == 0) continue;
-    uint64_t pos = tile_excl + s_wexcl[u * NW + wid] + lane_excl[u];
-    const uint64_t e = e0 + (uint64_t)(u * TB + tid) * 8;
-    while (m) {
-      const int i = __builtin_ctz(m);
-      m &= m - 1;
-      const float v = vals[(u * TB + tid) * 8 + i];
-      if (pos < cap) {
-        p.idx[pos] = base + (uint32_t)(e + i);
-        p.val[pos] = v;
-      } else {
-        r[e + i] = v;  // selected but not sent: error feedback keeps it
+      for (int u = 0; u < U; ++u) {
+        uint32_t m = (hmask[kDefer - 1] >> (8 * u)) & 0xFFu;
+        if (m == 0) continue;
+        uint64_t pos = tile_excl + wexcl[u * NW + wid] +
+                       ((hexcl[kDefer - 1][u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        const uint64_t e = oc.e0 + (uint64_t)(u * TBC + tid) * 8;
+        while (m) {
+          const int i = __builtin_ctz(m);
+          m &= m - 1;
+          const float v = vals[(u * TBC + tid) * 8 + i];
+          if (pos < cap) {
+            p.idx[pos] = base + (uint32_t)(e + i);
+            p.val[pos] = v;
+          } else {
+            oc.r[e + i] = v;  // selected but not sent: error feedback keeps it
+          }
+          ++pos;
+        }
       }
-      ++pos;
     }
+#pragma unroll
+    for (int d = kDefer - 1; d > 0; --d) {
+      hctx[d] = hctx[d - 1];
+      hmask[d] = hmask[d - 1];
+      hvalid[d] = hvalid[d - 1];
+#pragma unroll
+      for (int q = 0; q < (U + 1) / 2; ++q) hexcl[d][q] = hexcl[d - 1][q];
+    }
+    hctx[0] = cc;
+    hmask[0] = mask_packed;
+    hvalid[0] = have_cur;
+#pragma unroll
+    for (int q = 0; q < (U + 1) / 2; ++q) hexcl[0][q] = excl_packed[q];
+    cc = cn;
   }
 }
 
@@ -183,6 +251,8 @@ __global__ void loco_empty_segments_kernel(const uint64_t* count, uint64_t* seg_
   const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nseg) seg_begin[i] = *count;
 }
+
+constexpr int kLocoNW = kLocoTB / 64;
 
 uint32_t loco_tile_elems() { return kLocoTB * kLocoU * 8; }
 
@@ -193,8 +263,19 @@ hipError_t launch_loco(LocoParams& p, hipStream_t stream) {
                        (const uint64_t*)p.count, p.seg_begin, (uint32_t)p.ntensors);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((loco_kernel<kLocoTB, kLocoU>), dim3(p.ntiles), dim3(kLocoTB), 0, stream,
-                     p);
+  bool gate = false;
+  for (int k = 0; k < p.ntensors; ++k) gate |= p.t[k].theta != nullptr;
+  const void* fn = gate ? (const void*)loco_kernel<kLocoNW, kLocoU, true>
+                        : (const void*)loco_kernel<kLocoNW, kLocoU, false>;
+  const int grid_cap = persistent_grid(fn, (kLocoNW + 1) * 64);
+  if (grid_cap <= 0) return hipErrorInvalidConfiguration;
+  const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
+  if (gate)
+    hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, true>), dim3(grid), dim3((kLocoNW + 1) * 64),
+                       0, stream, p);
+  else
+    hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, false>), dim3(grid),
+                       dim3((kLocoNW + 1) * 64), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -20,7 +20,8 @@ from typing import Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libpulse.so")
+# PULSE_LIB may name another build of the same library (tuning sweeps).
+LIB_PATH = os.environ.get("PULSE_LIB") or os.path.join(_HERE, "libpulse.so")
 
 _lock = threading.Lock()
 _lib = None

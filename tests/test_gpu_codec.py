@@ -20,7 +20,9 @@ from tests.gpu_helpers import counter, dev, h16, h32, read_count
 
 pytestmark = pytest.mark.gpu
 
-TILE = 512 * 4 * 8  # encode tile (elements)
+TILE = 960 * 2 * 8  # encode tile (elements) of the default build
+# boundaries of every tile size a tuning build may use (4096 .. 32768 elements)
+EDGES = sorted({m * t + d for t in (7680, 15360, 30720) for m in (1, 3) for d in (-1, 0, 1)})
 
 
 @pytest.fixture(scope="module")
@@ -135,8 +137,7 @@ def test_encode_c1(ws):
     np.testing.assert_array_equal(r_or, oracle.cast(w_new))
 
 
-@pytest.mark.parametrize("n", [1, 7, 8, 9, 63, 4095, TILE - 1, TILE, TILE + 1, 3 * TILE - 1,
-                               3 * TILE + 5, 5 * TILE, 200_003])
+@pytest.mark.parametrize("n", [1, 7, 8, 9, 63] + EDGES + [5 * TILE + 5, 200_003])
 @pytest.mark.parametrize("density", [0.0, 0.005, 0.5, 1.0])
 def test_encode_shapes_and_densities(ws, n, density):
     rng = np.random.default_rng(n * 7 + int(density * 1000))
@@ -195,6 +196,23 @@ def test_encode_max_index_base(ws):
     flip = rng.random(n) < 0.2
     s_or, s_d = snapshots(w_new, flip)
     run_encode(w_new, s_or, s_d, ws, index_base=(1 << 32) - n)
+
+
+def test_workspace_sequence_base_only_grows():
+    """Tiny launches (more blocks than chunks of tiles) followed by a large one:
+    the tile sequence base kept in the workspace must strictly increase."""
+    ws = pulse.workspace()
+    rng = np.random.default_rng(21)
+    seen = []
+    for n in [1, 3 * TILE, 5, 7 * TILE + 1, 2, 1 << 24]:
+        w_new = rng.normal(0, 0.1, n).astype(np.float32)
+        flip = rng.random(n) < 0.02
+        s_or, s_d = snapshots(w_new, flip)
+        run_encode(w_new, s_or, s_d, ws)
+        seen.append(int(ws.view(torch.int64)[0].item()) >> 24)
+    assert all(b > a for a, b in zip(seen, seen[1:])), seen
+    assert int(ws.view(torch.int64)[1].item()) == 0  # no look-back gave up
+    assert int(ws.view(torch.int64)[2].item()) == 0  # every launch finished
 
 
 def test_encode_workspace_ring_wraps(ws):

@@ -14,7 +14,8 @@ from tests.gpu_helpers import counter, dev, h32, hf32, read_count
 
 pytestmark = pytest.mark.gpu
 
-TILE = 256 * 4 * 8  # sparsify tile (elements)
+TILE = 960 * 1 * 8  # sparsify tile (elements) of the default build
+EDGES = sorted({m * t + d for t in (7680, 15360) for m in (1, 3) for d in (-1, 0, 1)})
 
 
 @pytest.fixture(scope="module")
@@ -45,7 +46,7 @@ def run_loco(delta, res, tau, ws, theta=None, capacity=None, index_base=0, count
     return o_cnt, o_res
 
 
-@pytest.mark.parametrize("n", [1, 9, TILE - 1, TILE, TILE + 1, 4 * TILE + 3, 123_457])
+@pytest.mark.parametrize("n", [1, 9] + EDGES + [4 * TILE + 3, 123_457])
 def test_loco_threshold_shapes(ws, n):
     rng = np.random.default_rng(n)
     tau = wl.loco_tau()
