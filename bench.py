@@ -1,15 +1,23 @@
 #!/usr/bin/env python3
-"""Benchmark: PULSESync encode + apply over a whole synthetic parameter set on one MI355X.
+"""Benchmark: the PULSESync patch codec over a whole synthetic parameter set on one MI355X.
 
-One step = one pass of the hot path over every tensor of the parameter set:
-  encode (FP32 master -> BF16 RNE, bitwise compare with the previous BF16
-  snapshot, ordered compaction into a (uint32 index, bf16 value) patch), then
-  apply (scatter the patch into the inference-side BF16 copy).
-All inputs are generated on the GPU before timing and stay resident in HBM.
+One step = one pass of the hot path over every tensor of the parameter set
+(default: the 32B-shaped set, 32,763,417,600 FP32 parameters in 579 tensors):
+the fused encode, which casts the FP32 masters to BF16 (RNE), compares them
+bitwise with the previous BF16 snapshot, compacts the changed positions into
+an index-ordered (uint32 index, bf16 value) patch with its device-side count,
+and writes the changed values into the inference-side BF16 copy in the same
+pass.  That step is the headline.
+
+Also measured, outside the headline: the unfused form (encode, then the
+standalone scatter apply of the patch into the inference copy) and the
+PULSELoCo error-feedback sparsification over the 7B-shaped set (10 rounds,
+fixed threshold).  All inputs are generated on the GPU before timing and stay
+resident in HBM.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
-    python bench.py [--steps K] [--warmup W] [--workload 32b|7b|0.5b] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload 32b|7b|0.5b] [--no-cpu-baseline] [--no-loco]
 """
 from __future__ import annotations
 
@@ -27,6 +35,9 @@ if ROOT not in sys.path:
 METRIC = "encode+apply GB/s of weights scanned, % of MI355X HBM peak; patch density"
 HBM_PEAK_GBS = 8000.0
 WORKLOAD_IDS = {"0.5b": 2, "7b": 3, "32b": 4}
+CHUNK = 64  # tensors per launch (the library's batch limit)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "encode_fused_32b_traffic.txt")
+CALIB_WORDS = 1 << 28  # int32 words of the plain copy kernel run for counter calibration
 
 
 def log(*a):
@@ -92,6 +103,11 @@ def chunks(n, k):
     return [(a, min(a + k, n)) for a in range(0, n, k)]
 
 
+def event_pair():
+    import torch
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -103,11 +119,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=1.0e9,
                     help="elements of the parameter set the oracle baseline encodes")
+    ap.add_argument("--no-loco", action="store_true", help="skip the PULSELoCo leg")
+    ap.add_argument("--loco-rounds", type=int, default=10)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the patch codec needs no collectives, and this "
-              "build measures a single MI355X (see the design notes for how it would shard).",
+              "build measures a single MI355X (the design notes describe how it would shard).",
               file=sys.stderr)
         sys.exit(2)
 
@@ -118,6 +136,16 @@ def main():
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     pulse.lib()
+    stream = torch.cuda.current_stream()
+
+    # A plain copy kernel of known size (bitwise_not over 1 GiB of int32 reads
+    # 1 GiB and writes 1 GiB), run once so that a counter-collection run of this
+    # script can calibrate the HBM byte counters against it.
+    calib = torch.empty(CALIB_WORDS, dtype=torch.int32, device=device).random_()
+    torch.bitwise_not(calib, out=torch.empty_like(calib))
+    torch.cuda.synchronize()
+    del calib
+    torch.cuda.empty_cache()
 
     ps = ParamSet(args.workload, args.lr, device)
     T = len(ps.specs)
@@ -129,87 +157,82 @@ def main():
     ws = pulse.workspace(device)
     log(f"[bench] patch capacity {cap:,} entries ({cap * 6 / 1e9:.2f} GB)")
 
-    # one launch per chunk of <= 64 tensors; each chunk is its own batch so its
-    # kernel can be bracketed by events
-    parts = chunks(T, 64)
-    enc = [pulse.EncodeBatch([pulse.EncodeTensor(ps.view(ps.w, i), ps.view(ps.S, i), None, ps.base(i))
-                              for i in range(a, b)]) for a, b in parts]
+    parts = chunks(T, CHUNK)
+    n_launch = len(parts)
     enc_fused = [pulse.EncodeBatch([pulse.EncodeTensor(ps.view(ps.w, i), ps.view(ps.S, i),
                                                        ps.view(ps.R, i), ps.base(i))
                                     for i in range(a, b)]) for a, b in parts]
+    enc_plain = [pulse.EncodeBatch([pulse.EncodeTensor(ps.view(ps.w, i), ps.view(ps.S, i), None, ps.base(i))
+                                    for i in range(a, b)]) for a, b in parts]
     app = pulse.ApplyBatch([pulse.ApplyTensor(ps.view(ps.R, i), ps.base(i)) for i in range(T)])
-    stream = torch.cuda.current_stream()
 
-    def new_events():
-        return [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                for _ in parts]
-
-    def step(enc_events=None, app_events=None, fused=False):
+    def encode_pass(batches, events=None):
         count.zero_()
-        batches = enc_fused if fused else enc
         for c, ((a, _b), b) in enumerate(zip(parts, batches)):
-            if enc_events:
-                enc_events[c][0].record(stream)
+            if events:
+                events[c][0].record(stream)
             b(idx, val, count, ws, seg_begin=seg[a:])
-            if enc_events:
-                enc_events[c][1].record(stream)
-        if not fused:
-            if app_events:
-                app_events[0].record(stream)
-            app(idx, val, seg, count)
-            if app_events:
-                app_events[1].record(stream)
+            if events:
+                events[c][1].record(stream)
 
-    # ---- headline: encode + apply
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev_enc = [new_events() for _ in range(args.steps)]
-    ev_app = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(ev_enc[k], ev_app[k])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    def timed_steps(step_fn, make_events):
+        for _ in range(args.warmup):
+            step_fn(None)
+        torch.cuda.synchronize()
+        evs = [make_events() for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            step_fn(evs[k])
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / args.steps, evs
+
+    # ---- headline: fused encode + refresh of the inference copy
+    fused_ms, fused_ev = timed_steps(lambda ev: encode_pass(enc_fused, ev),
+                                     lambda: [event_pair() for _ in parts])
     nnz = int(count.item())
+    sent = min(nnz, cap)
     if nnz > cap:
         log(f"[bench] WARNING: patch overflow ({nnz:,} > capacity {cap:,})")
-    enc_ms = [[s.elapsed_time(e) for s, e in evs] for evs in ev_enc]
-    app_ms = [s.elapsed_time(e) for s, e in ev_app]
-    n_launch = len(parts)
-    enc_avg_ms = float(np.mean([np.mean(x) for x in enc_ms]))
-    enc_step_ms = float(np.mean([np.sum(x) for x in enc_ms]))
-    app_avg_ms = float(np.mean(app_ms))
-    enc_bytes_per_launch = (6.0 * ps.N + 6.0 * min(nnz, cap)) / n_launch
-    achieved = enc_bytes_per_launch / (enc_avg_ms * 1e-3) / 1e9
-    value = 6.0 * ps.N / (ms_step * 1e-3) / 1e9
-    step_frac = (6.0 * ps.N + 14.0 * min(nnz, cap)) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS
-    log(f"[bench] encode+apply {ms_step:.3f} ms/step  ({value:.0f} GB/s scanned); "
-        f"encode {enc_step_ms:.3f} ms ({n_launch} launches, avg {enc_avg_ms:.3f} ms), "
-        f"apply {app_avg_ms:.3f} ms; nnz {nnz:,} density {nnz / ps.N:.4%}")
+    launch_ms = np.array([[s.elapsed_time(e) for s, e in ev] for ev in fused_ev])  # steps x launches
+    fused_kernel_ms = float(launch_ms.sum(axis=1).mean())
+    fused_avg_launch_ms = float(launch_ms.mean())
+    value = 6.0 * ps.N / (fused_ms * 1e-3) / 1e9
+    fused_bytes = 6.0 * ps.N + 8.0 * sent  # FP32 + BF16 read; idx + val + refresh written per entry
+    achieved = fused_bytes / n_launch / (fused_avg_launch_ms * 1e-3) / 1e9
+    log(f"[bench] fused encode+refresh {fused_ms:.3f} ms/step ({value:.0f} GB/s scanned); "
+        f"kernels {fused_kernel_ms:.3f} ms over {n_launch} launches; nnz {nnz:,} density {nnz / ps.N:.4%}")
+    seg_fused = seg.clone()
+    idx_head = idx[: min(sent, 1 << 24)].clone()
+    val_head = val[: min(sent, 1 << 24)].clone()
 
-    # ---- fused variant: encode writes the inference copy directly (no separate apply)
-    for _ in range(max(1, args.warmup)):
-        step(fused=True)
-    torch.cuda.synchronize()
-    tf0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(fused=True)
-    torch.cuda.synchronize()
-    fused_ms = (time.perf_counter() - tf0) * 1e3 / args.steps
-    log(f"[bench] fused encode+refresh {fused_ms:.3f} ms/step ({6.0 * ps.N / fused_ms / 1e6:.0f} GB/s)")
+    # ---- encode, then the standalone scatter apply (receiver side)
+    def unfused(ev):
+        encode_pass(enc_plain, ev[0] if ev else None)
+        if ev:
+            ev[1][0].record(stream)
+        app(idx, val, seg, count)
+        if ev:
+            ev[1][1].record(stream)
 
-    # ---- sanity: the inference copy equals the BF16 view of the new masters
+    unf_ms, unf_ev = timed_steps(unfused, lambda: ([event_pair() for _ in parts], event_pair()))
+    enc_ms = float(np.mean([sum(s.elapsed_time(e) for s, e in ev[0]) for ev in unf_ev]))
+    app_ms = float(np.mean([ev[1][0].elapsed_time(ev[1][1]) for ev in unf_ev]))
+    log(f"[bench] encode then apply {unf_ms:.3f} ms/step: encode {enc_ms:.3f} ms, apply {app_ms:.3f} ms")
+
+    # ---- sanity: both forms give the same patch; the inference copy equals bf16(w')
+    assert int(count.item()) == nnz, "fused and plain encode disagree on the count"
+    assert torch.equal(seg, seg_fused), "fused and plain encode disagree on the segments"
+    assert torch.equal(idx[: idx_head.numel()], idx_head) and torch.equal(val[: val_head.numel()], val_head)
     check = pulse.cast_bf16(ps.w[: min(ps.N, 1 << 28)])
     assert torch.equal(check, ps.R[: check.numel()]), "inference copy differs from bf16(w')"
-    del check
+    del check, idx_head, val_head
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(ps, args.cpu_sample, idx, val, seg, nnz, cap)
 
+    from paper_2602_03839_amd.traffic import read_summary
+    traffic = read_summary(TRAFFIC_FILE) if args.workload == "32b" else None
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -217,47 +240,106 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": round(fused_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": f"pulsesync-{args.workload}-shaped",
+            "workload": f"pulsesync-{args.workload}-shaped fused encode+refresh",
             "params": ps.N,
             "tensors": T,
             "lr": args.lr,
             "nnz": nnz,
             "patch_density": round(nnz / ps.N, 6),
-            "hbm_frac_of_peak": round(step_frac, 4),
+            "hbm_frac_of_peak": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "index_form": "flat uint32" if ps.flat_index else "per-tensor uint32 + segment offsets",
             "patch_capacity": cap,
-            "encode_ms_per_step": round(enc_step_ms, 4),
-            "apply_ms_per_step": round(app_avg_ms, 4),
-            "fused_encode_refresh_ms_per_step": round(fused_ms, 4),
-            "fused_GBps_scanned": round(6.0 * ps.N / fused_ms / 1e6, 2),
+            "launches_per_step": n_launch,
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "encode_kernel",
+            "kernel": "encode_kernel (refresh form)",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
-            "bytes_per_launch": enc_bytes_per_launch,
-            "avg_launch_ms": round(enc_avg_ms, 5),
+            "traffic": None if traffic is None else round(traffic, 0),
+            "bytes_per_launch": fused_bytes / n_launch,
+            "avg_launch_ms": round(fused_avg_launch_ms, 5),
         },
         "cpu_baseline": cpu,
+        "legs": {
+            "encode_then_apply": {
+                "ms_per_step": round(unf_ms, 4),
+                "GBps_scanned": round(6.0 * ps.N / (unf_ms * 1e-3) / 1e9, 2),
+                "encode_ms": round(enc_ms, 4),
+                "apply_ms": round(app_ms, 4),
+                "hbm_frac_of_peak": round((6.0 * ps.N + 14.0 * sent) / (unf_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            },
+        },
     }
+    del enc_fused, enc_plain, app, idx, val, ps
+    torch.cuda.empty_cache()
+    if not args.no_loco:
+        out["legs"]["loco_7b"] = loco_leg(args, device, stream)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
-    """The oracle (single-threaded C) on a bounded sample of the same step."""
+def loco_leg(args, device, stream):
+    """PULSELoCo sparsification with error feedback over the 7B-shaped set, fixed threshold."""
     import numpy as np
     import torch
+    from paper_2602_03839_amd import pulse
+    from paper_2602_03839_amd import workloads as wl
+
+    specs = wl.SHAPES["7b"].tensors()
+    sizes = [s.numel for s in specs]
+    offs = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    N = offs[-1]
+    tau = wl.loco_tau()
+    delta = torch.empty(N, dtype=torch.float32, device=device)
+    resid = torch.zeros(N, dtype=torch.float32, device=device)
+    cap = N // 10
+    idx = torch.empty(cap, dtype=torch.int32, device=device)
+    val = torch.empty(cap, dtype=torch.float32, device=device)
+    count = torch.zeros(1, dtype=torch.int64, device=device)
+    ws = pulse.workspace(device)
+    parts = chunks(len(sizes), CHUNK)
+    batches = [pulse.LocoBatch([pulse.LocoTensor(delta[offs[i]:offs[i + 1]], resid[offs[i]:offs[i + 1]],
+                                                 None, 0) for i in range(a, b)]) for a, b in parts]
+    ms, dens = [], []
+    for r in range(args.loco_rounds):
+        for i in range(len(sizes)):
+            wl.loco_delta_(delta[offs[i]:offs[i + 1]], 5, r, i)
+        count.zero_()
+        torch.cuda.synchronize()
+        a, e = event_pair()
+        a.record(stream)
+        for b in batches:
+            b(tau, idx, val, count, ws)
+        e.record(stream)
+        e.synchronize()
+        ms.append(a.elapsed_time(e))
+        dens.append(int(count.item()) / N)
+    med = float(np.median(ms[1:] if len(ms) > 1 else ms))
+    log(f"[bench] loco 7b: median {med:.3f} ms/round ({12.0 * N / med / 1e6:.0f} GB/s at 12 B/param); "
+        f"density {dens[0]:.4%} -> {dens[-1]:.4%}")
+    return {
+        "params": N,
+        "tau": tau,
+        "rounds": args.loco_rounds,
+        "ms_per_round_median": round(med, 4),
+        "GBps_12B_per_param": round(12.0 * N / med / 1e6, 2),
+        "kernel": "loco_kernel (threshold form)",
+        "density_first_last": [round(dens[0], 6), round(dens[-1], 6)],
+    }
+
+
+def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
+    """The oracle (single-threaded C) on a bounded sample of the same step: encode with refresh."""
+    import numpy as np
     import oracle
 
     oracle.build()
@@ -268,37 +350,31 @@ def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
         take.append(i)
         tot += n
     segs = seg.cpu().numpy().tolist() + [min(nnz, cap)]
-    t_enc = t_app = 0.0
+    t_enc = 0.0
     parity = True
     for i in take:
         w = ps.view(ps.w, i).cpu().numpy()
         s = ps.view(ps.S, i).cpu().numpy().view(np.uint16)
-        c0 = time.perf_counter_ns()
-        cnt, o_idx, o_val = oracle.encode(w, s, index_base=ps.base(i))
-        c1 = time.perf_counter_ns()
         r = s.copy()
-        oracle.apply(r, o_idx, o_val, 0, cnt, index_base=ps.base(i))
-        c2 = time.perf_counter_ns()
-        t_enc += (c1 - c0) * 1e-9
-        t_app += (c2 - c1) * 1e-9
+        c0 = time.perf_counter_ns()
+        cnt, o_idx, o_val = oracle.encode(w, s, index_base=ps.base(i), refresh=r)
+        t_enc += (time.perf_counter_ns() - c0) * 1e-9
         b, e = segs[i], segs[i + 1]
         if e <= cap:
             g_idx = idx[b:e].cpu().numpy().view(np.uint32)
             g_val = val[b:e].cpu().numpy().view(np.uint16)
             parity &= (e - b == cnt and np.array_equal(g_idx, o_idx[:cnt])
                        and np.array_equal(g_val, o_val[:cnt]))
+        parity &= np.array_equal(r, ps.view(ps.R, i).cpu().numpy().view(np.uint16))
         log(f"[bench] cpu baseline: tensor {i} ({ps.sizes[i]:,} elems) done")
-    t = t_enc + t_app
     return {
-        "value": round(6.0 * tot / t / 1e9, 4),
+        "value": round(6.0 * tot / t_enc / 1e9, 4),
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
         "sample": f"first {len(take)} tensors in model order ({tot:,} of {ps.N:,} params): "
-                  f"oracle encode + apply, single-threaded C",
-        "seconds": round(t, 3),
-        "encode_s": round(t_enc, 3),
-        "apply_s": round(t_app, 3),
+                  f"oracle fused encode + refresh, single-threaded C",
+        "seconds": round(t_enc, 3),
         "host_cpu": cpu_model(),
         "host_nproc": os.cpu_count(),
         "sample_parity_with_gpu": bool(parity),

@@ -17,14 +17,14 @@ __global__ __launch_bounds__(kCastTB) void cast_kernel(const float* __restrict__
     const uint4 a = load16(src + g * 8);
     const uint4 b = load16(src + g * 8 + 4);
     uint4 o;
-    o.x = bf16_rne_bits(a.x) | (bf16_rne_bits(a.y) << 16);
-    o.y = bf16_rne_bits(a.z) | (bf16_rne_bits(a.w) << 16);
-    o.z = bf16_rne_bits(b.x) | (bf16_rne_bits(b.y) << 16);
-    o.w = bf16_rne_bits(b.z) | (bf16_rne_bits(b.w) << 16);
+    o.x = bf16x2_rne(a.x, a.y);
+    o.y = bf16x2_rne(a.z, a.w);
+    o.z = bf16x2_rne(b.x, b.y);
+    o.w = bf16x2_rne(b.z, b.w);
     store16(dst + g * 8, o);
   }
   const uint64_t e = groups * 8 + gid;
-  if (e < n) dst[e] = (uint16_t)bf16_rne_bits(__float_as_uint(src[e]));
+  if (e < n) dst[e] = (uint16_t)bf16x2_rne(__float_as_uint(src[e]), 0u);
 }
 
 hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream) {

@@ -12,35 +12,44 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 namespace pulse {
 
 // ---------------------------------------------------------------- workspace
 //
-// word 0: ticket counter = (G0 << 24) | c, where c counts the chunks of
-//         kChunk consecutive tiles drawn in the current launch and G0 is the
+// The header holds three words, each on its own 128-byte cache line so that
+// polls of one never contend with the atomics on another:
+// word kWordTicket: ticket counter = (G0 << 24) | c, where c counts the chunks
+//         of kChunk consecutive tiles drawn in the current launch and G0 is the
 //         global sequence number of that launch's first tile.  Blocks are
 //         persistent and draw chunks until they get one past the launch's last
 //         tile.  A single device-wide counter sustains only ~75M atomics/s on
 //         MI355X, so tiles are handed out kChunk at a time.
-// word 1: set to 1 if a look-back ever gave up waiting (see look_back).
-// word 2: number of blocks of the current launch that have finished.  The last
-//         block out (every other block has made its final draw before it
-//         counted itself out) stores ((G0 + ntiles) << 24) into word 0 and 0
-//         here, so the next launch starts at t = 0 with no reset kernel.
-// words 32 ..: a ring of kSlots status words.  Tile with global sequence g uses
-//         slot g mod kSlots and tags its word with (g / kSlots) mod 256.  Every
-//         sequence number is published exactly once, in order of use, so a
-//         slot holds either the current lap's word or the previous lap's, whose
-//         tag differs; a stale word reads as "not ready".  A slot is reused only
-//         kSlots tickets later; since at most R <= 8192 tiles are in flight at
-//         once and a tile looks back at most R tiles, kSlots > 2R + 2 ensures a
-//         word is never overwritten while a reader still needs it.
+// word kWordGaveUp: set to 1 if a look-back ever gave up waiting (see look_back).
+// word kWordDone: number of blocks of the current launch that have finished.
+//         The last block out (every other block has made its final draw before
+//         it counted itself out) stores ((G0 + ntiles) << 24) into the ticket
+//         counter and 0 here, so the next launch starts at c = 0 with no reset
+//         kernel.
+// words kStatusOffsetWords ..: a ring of kSlots status words.  Tile with global
+//         sequence g uses slot g mod kSlots and tags its word with (g / kSlots)
+//         mod 256.  Every sequence number is published exactly once, in order
+//         of use, so a slot holds either the current lap's word or the previous
+//         lap's, whose tag differs; a stale word reads as "not ready".  A slot
+//         is reused only kSlots tickets later; since at most R <= 8192 tiles
+//         are in flight at once and a tile looks back at most R tiles,
+//         kSlots > 2R + 2 ensures a word is never overwritten while a reader
+//         still needs it.
+constexpr int kWordTicket = 0;
+constexpr int kWordGaveUp = 16;
+constexpr int kWordDone = 32;
 constexpr int kTicketBits = 24;
 constexpr uint64_t kTicketMask = (1ull << kTicketBits) - 1;
 constexpr uint64_t kSeqMask = (1ull << 40) - 1;  // G0 is kept modulo 2^40
 constexpr int kSlotBits = 16;
 constexpr uint64_t kSlots = 1ull << kSlotBits;
-constexpr int kStatusOffsetWords = 32;            // 256-byte header
+constexpr int kStatusOffsetWords = 64;            // 512-byte header
 constexpr size_t kWorkspaceBytes = (kStatusOffsetWords + kSlots) * sizeof(uint64_t);
 constexpr uint32_t kMaxTilesPerLaunch = (1u << kTicketBits) - 1;  // < kNoTicket
 
@@ -77,29 +86,50 @@ __device__ __forceinline__ void status_publish(uint64_t* ws, uint64_t g, uint64_
 
 // ---------------------------------------------------------------- BF16 RNE
 //
-// Round-to-nearest-even to the upper 16 bits: adding 0x7FFF plus the last kept
-// bit carries into bit 16 exactly when the dropped half is above the midpoint,
-// or at the midpoint with an odd kept part.  Overflow carries into the
-// exponent and yields +-inf, as IEEE RNE does.  A NaN is made quiet, keeping
-// its sign and leading payload (the carry trick would turn some NaNs to inf).
-__device__ __forceinline__ uint32_t bf16_rne_bits(uint32_t u) {
-  const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t q = (u >> 16) | 0x40u;
-  return ((u & 0x7FFFFFFFu) > 0x7F800000u) ? q : r;
+// FP32 -> BF16 with round-to-nearest-even, two elements at a time, on the
+// gfx950 conversion unit (v_cvt_pk_bf16_f32).  With the IEEE denormal mode
+// these kernels run in, it computes exactly the reference rounding: the
+// nearest BF16 value, ties to the even mantissa, overflow to +-inf,
+// subnormals kept, and a NaN made quiet with its sign and leading payload
+// bits kept.  The exhaustive cast test compares it with the CPU reference on
+// all 2^32 FP32 patterns.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// BF16 bits of the FP32 patterns lo (bits 15:0) and hi (bits 31:16).
+__device__ __forceinline__ uint32_t bf16x2_rne(uint32_t lo, uint32_t hi) {
+  const f32x2_t v = {__uint_as_float(lo), __uint_as_float(hi)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// Change mask of two packed BF16 pairs: bit 0 = low halves differ, bit 1 =
+// high halves differ (bitwise, so +0 and -0 differ and equal NaN bits match).
+__device__ __forceinline__ uint32_t diff2(uint32_t a, uint32_t b) {
+  const uint32_t d = a ^ b;
+  return (uint32_t)((d & 0xFFFFu) != 0u) | ((uint32_t)((d >> 16) != 0u) << 1);
 }
 
 // ---------------------------------------------------------------- wave64 helpers
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
-// Inclusive prefix sum over the 64 lanes of a wave.
+// Lane move with a DPP pattern; lanes without a source (or outside the enabled
+// rows) read 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_or_zero(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave, without LDS: shifts by
+// 1, 2, 4, 8 inside each 16-lane row, then the row totals are carried across
+// rows by the row_bcast:15 and row_bcast:31 patterns.
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t o = __shfl_up(v, d, 64);
-    if (lane >= d) v += o;
-  }
+  v += dpp_or_zero<0x111, 0xF>(v);  // row_shr:1
+  v += dpp_or_zero<0x112, 0xF>(v);  // row_shr:2
+  v += dpp_or_zero<0x114, 0xF>(v);  // row_shr:4
+  v += dpp_or_zero<0x118, 0xF>(v);  // row_shr:8
+  v += dpp_or_zero<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_or_zero<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
   return v;
 }
 
@@ -118,7 +148,8 @@ struct Ticket {
 
 // Called by one thread of the block.
 __device__ __forceinline__ uint64_t draw_ticket(uint64_t* ws) {
-  return __hip_atomic_fetch_add(ws, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_fetch_add(ws + kWordTicket, 1ull, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Called by one thread per block after its last draw.  The acquire-release
@@ -126,11 +157,11 @@ __device__ __forceinline__ uint64_t draw_ticket(uint64_t* ws) {
 __device__ __forceinline__ void finish_launch(uint64_t* ws, uint64_t g0, uint32_t ntiles,
                                               uint32_t nblocks) {
   const uint64_t d =
-      __hip_atomic_fetch_add(ws + 2, 1ull, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_add(ws + kWordDone, 1ull, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
   if (d == nblocks - 1) {
-    __hip_atomic_store(ws + 2, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(ws, ((g0 + ntiles) & kSeqMask) << kTicketBits, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ws + kWordDone, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(ws + kWordTicket, ((g0 + ntiles) & kSeqMask) << kTicketBits,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -141,9 +172,22 @@ constexpr uint64_t kNoTicket = kTicketMask;
 // so the chunk's last aggregate appears kChunk - 1 iterations after its first;
 // with kChunk <= kDefer later tiles never wait for it at resolution time.
 #ifndef PULSE_CHUNK
-#define PULSE_CHUNK 2
+#define PULSE_CHUNK 4
 #endif
 constexpr uint32_t kChunk = PULSE_CHUNK;
+
+// Tiles whose loads a block keeps in flight: while a block computes tile T(i),
+// the loads of T(i + 1) .. T(i + kAhead) are outstanding.  A tile is 90 KiB
+// of input at the default shape; one CU needs well over 100 KiB in flight to
+// cover the HBM latency under full load.
+#ifndef PULSE_AHEAD
+#define PULSE_AHEAD 2
+#endif
+constexpr int kAhead = PULSE_AHEAD;
+// LDS ring of tickets: T(i) lives in slot i mod kTkRing.  Compute waves read
+// slots i and i + kAhead in iteration i while the scan wave fills i + kAhead + 1.
+constexpr int kTkRing = kAhead + 2 <= 4 ? 4 : 8;
+static_assert(kAhead >= 1 && kAhead + 2 <= kTkRing, "ticket ring too small");
 
 // Ticket word of tile `tile` of the launch whose first tile has sequence g0.
 __device__ __forceinline__ uint64_t make_ticket(uint64_t g0, uint32_t tile, uint32_t ntiles) {
@@ -155,6 +199,15 @@ __device__ __forceinline__ Ticket decode_ticket(uint64_t c) {
   tk.tile = (uint32_t)(c & kTicketMask);
   tk.seq = ((c >> kTicketBits) + tk.tile) & kSeqMask;
   return tk;
+}
+
+// T(i) from the LDS ticket ring, as a wave-uniform (scalar) value, so that
+// the tensor lookup and the per-tile bookkeeping stay out of vector registers.
+__device__ __forceinline__ Ticket ticket_at(const uint64_t* s_tk, int i) {
+  const uint64_t c = s_tk[i & (kTkRing - 1)];
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)c);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(c >> 32));
+  return decode_ticket(((uint64_t)hi << 32) | lo);
 }
 
 // ---------------------------------------------------------------- look-back
@@ -237,8 +290,11 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
               __hip_atomic_load(status_slot(ws, gq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           ready = (x >> 62) != 0 && ((x >> 54) & 0xFFull) == ((gq >> kSlotBits) & 0xFFull);
           // once any wave of the device has given up, nobody waits any more
+          // (checked every 64th poll: the flag is only a safety net)
           if (!ready && (++polls >= kMaxPolls ||
-                         __hip_atomic_load(ws + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)))
+                         ((polls & 63) == 0 &&
+                          __hip_atomic_load(ws + kWordGaveUp, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT))))
             gave_up = true;
         }
         ready = __shfl(ready ? 1 : 0, 0, 64) != 0;
@@ -250,7 +306,8 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
       }
       if (!ready) {
         // gave up: only a workspace that was not zero-filled gets here
-        if (lane == 0) __hip_atomic_store(ws + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0)
+          __hip_atomic_store(ws + kWordGaveUp, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return excl;
       }
       look_back_issue<LK>(ws, tk, j, win);
@@ -269,16 +326,24 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
   }
 }
 
-// Smallest k in [0, count) with begin[k + 1] > t, for a non-decreasing begin[]
-// with begin[0] <= t < begin[count] (the tensor that owns tile t).
-template <typename Arr>
-__device__ __forceinline__ int find_owner(const Arr& begin, int count, uint32_t t) {
-  int lo = 0, hi = count - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (begin[mid] <= t) lo = mid; else hi = mid - 1;
-  }
-  return lo;
+// Owner of a tile.  Lane k of a wave holds tile_begin[k] for k < ntensors
+// (<= 64 tensors per launch) and ~0 elsewhere; the tensor that owns tile t is
+// the highest lane whose begin is <= t (begins never decrease, and an empty
+// tensor shares its begin with the next tensor, which wins).  One compare and
+// one ballot, no memory access on the way.
+template <typename Params>
+__device__ __forceinline__ uint32_t owner_lane_begin(const Params& p) {
+  uint32_t v = ~0u;
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 0; k < 64; ++k)
+    if (k < p.ntensors && lane == k) v = p.tile_begin[k];
+  return v;
+}
+
+__device__ __forceinline__ int owner_of(uint32_t lane_begin, uint32_t t) {
+  const uint64_t b = __ballot(lane_begin <= t);  // lane 0 holds 0 <= t
+  return 63 - __builtin_clzll(b);
 }
 
 // ---------------------------------------------------------------- scan wave
@@ -286,10 +351,11 @@ __device__ __forceinline__ int find_owner(const Arr& begin, int count, uint32_t 
 // The loop run by the one scan wave of a persistent encode/sparsify block.
 // Blocks synchronise once per iteration.  Tile T(i) is the tile whose data
 // the compute waves turn into wave totals in iteration i (its loads were
-// issued during iteration i - 1).  For each tile:
+// issued during iteration i - kAhead).  For each tile:
 //   iteration i            compute waves publish its wave totals
 //                          (s_wtot[i & 1]); after the barrier the scan wave
-//                          combines them (group-major) into s_wexcl[i & 3]
+//                          combines them (group-major) into s_wexcl (ring
+//                          of kWexclRing)
 //                          and publishes the tile aggregate (tile 0 of the
 //                          launch publishes its inclusive prefix, folding in
 //                          the append position *count);
@@ -301,19 +367,29 @@ __device__ __forceinline__ int find_owner(const Arr& begin, int count, uint32_t 
 //   iteration i + kDefer   after the barrier the compute waves write its
 //                          entries.
 // Tiles computed in the same iteration by different blocks publish their
-// aggregates at about the same time, so a tile is resolved kResolve = 2
-// iterations later, when every predecessor has long published: the look-back
-// then reads one window and never waits.  The scan wave's work of iteration i
-// only has to be done before barrier i + 1, so it does not hold the compute
-// waves up while it waits on memory.  Tickets: s_tk[i % 3] holds T(i); before
-// barrier i the scan wave stores T(i + 2), which the compute waves need at the
-// top of iteration i + 1 to start that tile's loads.  The last tile stores the
-// new *count; the first tile of each tensor stores the tensor's segment
-// start.  Both loops run while any tile is still to be computed, resolved or
-// written.
-constexpr int kResolve = 2;            // iterations from compute to resolution
-constexpr int kDefer = kResolve + 1;   // iterations from compute to write-out
-constexpr int kValBufs = kDefer + 2;   // LDS value buffers (ring)
+// aggregates at about the same time, so a tile is resolved kResolve
+// iterations later, when its predecessors have published their aggregates and
+// most of them their prefixes: the look-back then mostly reads one window and
+// rarely waits.  The scan wave's work of iteration i only has to be done
+// before barrier i + 1, so it does not hold the compute waves up while it
+// waits on memory.  Tickets: before barrier i the scan wave stores
+// T(i + kAhead + 1) in the ticket ring; the compute waves look it up right
+// after barrier i and start its loads in iteration i + 1.  The last tile
+// stores the new *count; the first tile of each tensor stores the tensor's
+// segment start.  Both loops run while any tile is still to be computed,
+// resolved or written.
+#ifndef PULSE_RESOLVE
+#define PULSE_RESOLVE 4
+#endif
+constexpr int kResolve = PULSE_RESOLVE;  // iterations from compute to resolution
+constexpr int kDefer = kResolve + 1;     // iterations from compute to write-out
+// ring of per-wave exclusive prefixes: filled at i, read at i + kDefer
+constexpr int kWexclRing = kDefer + 1 <= 4 ? 4 : 8;
+static_assert(kChunk <= kDefer, "a chunk's tiles must all be computed before the first resolves");
+// LDS value buffers (ring).  Each compute thread reads back only the values
+// it staged itself: tile T(i) is staged in slot i mod kValBufs after the
+// write-out of T(i - kDefer) has emptied that slot, so kDefer buffers suffice.
+constexpr int kValBufs = kDefer;
 
 struct ScanState {
   Ticket tk;
@@ -324,15 +400,19 @@ struct ScanState {
 
 template <int U, int NW, typename Params>
 __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot2,
-                               uint32_t* s_wexcl4, uint64_t* s_excl2) {
+                               uint32_t* s_wexcl, uint64_t* s_excl2) {
   const int lane = lane_id();
   // tiles come in chunks of kChunk consecutive tiles, one atomic per chunk;
-  // next_tile / left: the unused part of the block's current chunk
-  uint64_t g0 = 0;
+  // next_tile / left: the unused part of the block's current chunk.  The next
+  // chunk is always drawn one chunk ahead (`pre`, lane 0), so the atomic's
+  // round trip overlaps a whole chunk of iterations instead of delaying the
+  // ticket store that the compute waves wait for at the barrier.
+  uint64_t g0 = 0, pre = 0;
   uint32_t next_tile = 0, left = 0;
   auto take = [&]() -> uint64_t {  // lane 0 only
     if (left == 0) {
-      const uint64_t c = draw_ticket(p.ws);
+      const uint64_t c = pre;
+      pre = draw_ticket(p.ws);
       g0 = c >> kTicketBits;
       next_tile = (uint32_t)(c & kTicketMask) * kChunk;
       left = kChunk;
@@ -341,41 +421,46 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
     return make_ticket(g0, next_tile++, p.ntiles);
   };
   if (lane == 0) {
-    s_tk[0] = take();
-    s_tk[1] = take();
+    pre = draw_ticket(p.ws);
+    bool more = true;
+    for (int q = 0; q <= kAhead; ++q) {
+      s_tk[q] = more ? take() : kNoTicket;
+      more = decode_ticket(s_tk[q]).tile < p.ntiles;
+    }
   }
-  __syncthreads();  // first two tickets
+  __syncthreads();  // T(0) .. T(kAhead)
   // g0 (lane 0 only) comes from the counter itself: a ticket slot may hold
   // kNoTicket when the block's first chunk lies past the last tile, and the
   // sequence base must never move backwards
   uint64_t count_in = 0;
+  const uint32_t lane_begin = owner_lane_begin(p);
   ScanState hist[kDefer];  // hist[d]: T(i - 1 - d)
 #pragma unroll
   for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
   for (int it = 0;; ++it) {
-    const Ticket cur = decode_ticket(s_tk[it % 3]);
+    const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
     bool pending = have_cur;
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) break;
-    const bool have_next = decode_ticket(s_tk[(it + 1) % 3]).tile < p.ntiles;
-    if (lane == 0) s_tk[(it + 2) % 3] = have_next ? take() : kNoTicket;
+    const bool have_last = ticket_at(s_tk, it + kAhead).tile < p.ntiles;
+    if (lane == 0) s_tk[(it + kAhead + 1) & (kTkRing - 1)] = have_last ? take() : kNoTicket;
     // first look-back window of T(i - kResolve), overlapping the compute of T(i)
     const ScanState res = hist[kResolve - 1];
     LookWindow<PULSE_LOOKBACK_K> win;
     const bool walk = res.valid && res.tk.tile != 0;
     if (walk) look_back_issue<PULSE_LOOKBACK_K>(p.ws, res.tk, (int64_t)res.tk.tile - 1, win);
-    __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + 2) is in s_tk
+    __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + kAhead + 1) in s_tk
     ScanState now;
     now.valid = have_cur;
     if (have_cur) {
       const uint32_t v = lane < U * NW ? s_wtot2[(it & 1) * U * NW + lane] : 0u;
       const uint32_t incl = wave_incl_scan(v);
-      if (lane < U * NW) s_wexcl4[(it & 3) * U * NW + lane] = incl - v;
+      if (lane < U * NW) s_wexcl[(it & (kWexclRing - 1)) * U * NW + lane] = incl - v;
       now.tk = cur;
       now.agg = __shfl(incl, 63, 64);
-      now.k = find_owner(p.tile_begin, p.ntensors, cur.tile);
+      now.k = owner_of(lane_begin, cur.tile);
       if (cur.tile == 0) {
         count_in = *p.count;  // append position, written by an earlier call
         if (lane == 0) status_publish(p.ws, cur.seq, kFlagPrefix, count_in + now.agg);
@@ -445,14 +530,31 @@ __device__ __forceinline__ uint32_t get_u32(const uint4& v, int i) {
 
 
 // Blocks of `kernel` (launched with `block` threads) that fit on the current
-// device at once: the grid of a persistent launch.  Cached per device.
+// device at once: the grid of a persistent launch.  The occupancy query is
+// made once per (device, kernel) and remembered.
 inline int persistent_grid(const void* kernel, int block) {
+  struct Entry {
+    const void* kernel;
+    int dev, block, grid;
+  };
+  static Entry cache[64];
+  static int used = 0;
+  static std::mutex mu;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
+  {
+    std::lock_guard<std::mutex> g(mu);
+    for (int i = 0; i < used; ++i)
+      if (cache[i].kernel == kernel && cache[i].dev == dev && cache[i].block == block)
+        return cache[i].grid;
+  }
   int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, 0) != hipSuccess) return 0;
-  return cus * (per_cu > 0 ? per_cu : 1);
+  const int grid = cus * (per_cu > 0 ? per_cu : 1);
+  std::lock_guard<std::mutex> g(mu);
+  if (used < 64) cache[used++] = Entry{kernel, dev, block, grid};
+  return grid;
 }
 
 }  // namespace pulse

@@ -12,15 +12,15 @@
 //
 // Block = NW compute waves + 1 scan wave, persistent over tiles drawn by
 // ticket (device_common.hpp).  Iteration i of the compute waves turns tile
-// T(i), already in registers, into masks and BF16 values (staged in an LDS
-// ring), refilling each group's registers with T(i + 1)'s loads as soon as it
-// is consumed; it then publishes per-wave counts and meets the scan wave at
-// the one barrier of the iteration.  The scan wave meanwhile publishes T(i)'s
-// aggregate and resolves the exclusive prefix of T(i - 2) by look-back, so the
-// compute waves write T(i - 3)'s changed entries at their final positions one
-// iteration after its prefix is known.  Neither the look-back nor the ticket
-// atomic sits between a tile's loads and the next: the memory pipe holds one
-// tile per block at all times.
+// T(i), already in registers, into masks and BF16 values, refilling each
+// group's registers with T(i + kAhead)'s loads as soon as it is consumed, so
+// kAhead tiles' loads are always in flight; it then publishes per-wave counts
+// and meets the scan wave at the one barrier of the iteration.  The scan wave
+// meanwhile publishes T(i)'s aggregate and resolves the exclusive prefix of
+// T(i - kResolve) by look-back, and after the barrier the compute waves write
+// the changed entries of T(i - kDefer) at their final positions, reading the
+// values back from an LDS ring.  Neither the look-back nor the ticket atomic
+// sits between a tile's loads and the next.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -37,9 +37,10 @@ struct TileCtx {
   uint32_t tile_in_tensor;
 };
 
-__device__ __forceinline__ TileCtx locate(const EncodeParams& p, uint32_t tile, uint32_t tile_elems) {
+__device__ __forceinline__ TileCtx locate(const EncodeParams& p, uint32_t lane_begin, uint32_t tile,
+                                          uint32_t tile_elems) {
   TileCtx c;
-  c.k = find_owner(p.tile_begin, p.ntensors, tile);
+  c.k = owner_of(lane_begin, tile);
   c.tile_in_tensor = tile - p.tile_begin[c.k];
   c.e0 = (uint64_t)c.tile_in_tensor * tile_elems;
   c.n = p.t[c.k].n;
@@ -82,14 +83,28 @@ __device__ __forceinline__ void load_group(TileRegs<TBC, U>& r, int u, const Til
 
 }  // namespace
 
-template <int NW, int U>
+// What the write-out of a tile needs kDefer iterations after its compute:
+// where it lies (wave-uniform) and, per lane, the change masks (8 bits per
+// group) and lane prefixes (16 bits per group).
+template <int U>
+struct Deferred {
+  uint64_t e0;
+  int k;
+  bool valid;
+  uint32_t mask;
+  uint32_t excl[(U + 1) / 2];
+};
+
+// REFRESH: some tensor of the launch has an inference copy to refresh in the
+// same pass (a separate instantiation, so the plain encode carries no test).
+template <int NW, int U, bool REFRESH>
 __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   constexpr int TBC = NW * 64;
   constexpr uint32_t TILE = TBC * U * 8;
-  __shared__ uint64_t s_tk[3];
+  __shared__ uint64_t s_tk[kTkRing];
   __shared__ uint64_t s_excl[2];
   __shared__ uint32_t s_wtot[2 * U * NW];
-  __shared__ uint32_t s_wexcl[4 * U * NW];
+  __shared__ uint32_t s_wexcl[kWexclRing * U * NW];
   __shared__ uint4 s_vals[kValBufs][U * TBC];
   static_assert(U * NW <= 64, "block scan runs on one wave");
   static_assert(U <= 4, "masks of all groups are packed into one register");
@@ -103,64 +118,77 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
     return;
   }
 
-  // ---------------- compute waves.  Iteration `it` computes tile `cur` (its
-  // data already in registers) group by group, refilling each group's
-  // registers with the next tile's loads as soon as they are consumed, then
-  // writes the entries of the tile computed kDefer iterations earlier (`old`),
-  // whose prefix the scan wave has just resolved.  Staged values live in a
-  // ring of kValBufs LDS buffers (filled at it, written out at it + kDefer,
-  // and one of slack for a slower wave).
-  __syncthreads();  // first two tickets
-  TileRegs<TBC, U> r;
-  TileCtx cc;
-  {
-    const Ticket t0 = decode_ticket(s_tk[0]);
-    if (t0.tile < p.ntiles) {
-      cc = locate(p, t0.tile, TILE);
-      const bool full = cc.e0 + TILE <= cc.n;
+  // ---------------- compute waves.  Register set q holds tile T(i) for
+  // i = q mod kAhead.  Iteration i computes T(i) group by group, refilling
+  // each group's registers with the loads of T(i + kAhead) as soon as they are
+  // consumed, then writes the entries of T(i - kDefer), whose prefix the scan
+  // wave resolved in the previous iteration.  Staged values live in a ring of
+  // kValBufs LDS buffers private to each thread; a tile's values wait in
+  // registers over the barrier and take the slot its write-out just freed.
+  __syncthreads();  // T(0) .. T(kAhead) are in s_tk
+  static_assert(kAhead == 1 || kAhead == 2, "one or two register sets");
+  const uint32_t lane_begin = owner_lane_begin(p);
+  TileRegs<TBC, U> r0, r1;
+  uint64_t e0_0 = 0, e0_1 = 0;  // first element of the tile in each register set
+  int k_0 = 0, k_1 = 0;          // and its tensor
 #pragma unroll
-      for (int u = 0; u < U; ++u) load_group<TBC, U>(r, u, cc, tid, full);
+  for (int q = 0; q < kAhead; ++q) {
+    const Ticket t = ticket_at(s_tk, q);
+    if (t.tile < p.ntiles) {
+      const TileCtx c = locate(p, lane_begin, t.tile, TILE);
+      const bool full = c.e0 + TILE <= c.n;
+#pragma unroll
+      for (int u = 0; u < U; ++u) load_group<TBC, U>(q == 0 ? r0 : r1, u, c, tid, full);
+      (q == 0 ? e0_0 : e0_1) = c.e0;
+      (q == 0 ? k_0 : k_1) = c.k;
     }
   }
-  // per deferred tile: context, masks (8 bits per group) and lane prefixes
-  // (16 bits per group), packed to keep the register count down
-  TileCtx hctx[kDefer];
-  uint32_t hmask[kDefer], hexcl[kDefer][(U + 1) / 2];
-  bool hvalid[kDefer];
+  // The next tile to load, T(i + kAhead), is looked up one iteration early,
+  // right after the barrier that publishes its ticket, so the lookup overlaps
+  // the write-out instead of delaying the loads.
+  TileCtx cn;
+  bool have_next = false, next_full = false;
+  auto look_up_next = [&](int i) {
+    const Ticket t = ticket_at(s_tk, i + kAhead);
+    have_next = t.tile < p.ntiles;
+    if (have_next) {
+      cn = locate(p, lane_begin, t.tile, TILE);
+      next_full = cn.e0 + TILE <= cn.n;
+    }
+  };
+  look_up_next(0);
+  Deferred<U> hist[kDefer];
 #pragma unroll
-  for (int d = 0; d < kDefer; ++d) hvalid[d] = false;
-  for (int it = 0;; ++it) {
-    const Ticket cur = decode_ticket(s_tk[it % 3]);
-    const Ticket nxt = decode_ticket(s_tk[(it + 1) % 3]);
+  for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
+
+  // One iteration on register set `rg`, whose tile starts at element ce0 of
+  // tensor ck; false when the block has nothing left to compute, resolve or
+  // write.
+  auto step = [&](const int it, TileRegs<TBC, U>& rg, uint64_t& ce0, int& ck) -> bool {
+    const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
     bool pending = have_cur;
 #pragma unroll
-    for (int d = 0; d < kDefer; ++d) pending |= hvalid[d];
-    if (!pending) break;
-    const bool have_next = nxt.tile < p.ntiles;
-    const TileCtx cn = have_next ? locate(p, nxt.tile, TILE) : cc;
-    const bool next_full = cn.e0 + TILE <= cn.n;
+    for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
+    if (!pending) return false;
     uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
+    uint4 hv[U];  // BF16 values of T(i), staged after the write-out
     if (have_cur) {
       uint32_t cnt[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        uint32_t m = 0, b16[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t wbits = i < 4 ? get_u32(r.a[u], i) : get_u32(r.b[u], i - 4);
-          const uint32_t sw = get_u32(r.c[u], i >> 1);
-          const uint32_t sv = (i & 1) ? (sw >> 16) : (sw & 0xFFFFu);
-          b16[i] = bf16_rne_bits(wbits);
-          m |= (uint32_t)(b16[i] != sv) << i;
-        }
+        // BF16 pairs (elements 2j, 2j + 1) against the snapshot's words
+        const uint32_t h0 = bf16x2_rne(rg.a[u].x, rg.a[u].y);
+        const uint32_t h1 = bf16x2_rne(rg.a[u].z, rg.a[u].w);
+        const uint32_t h2 = bf16x2_rne(rg.b[u].x, rg.b[u].y);
+        const uint32_t h3 = bf16x2_rne(rg.b[u].z, rg.b[u].w);
+        const uint32_t m = diff2(h0, rg.c[u].x) | (diff2(h1, rg.c[u].y) << 2) |
+                           (diff2(h2, rg.c[u].z) << 4) | (diff2(h3, rg.c[u].w) << 6);
         mask_packed |= m << (8 * u);
         cnt[u] = __builtin_popcount(m);
-        s_vals[it % kValBufs][u * TBC + tid] =
-            make_uint4(b16[0] | (b16[1] << 16), b16[2] | (b16[3] << 16), b16[4] | (b16[5] << 16),
-                       b16[6] | (b16[7] << 16));
-        // this group's registers are free: start the next tile's loads into them
-        if (have_next) load_group<TBC, U>(r, u, cn, tid, next_full);
+        hv[u] = make_uint4(h0, h1, h2, h3);
+        // this group's registers are free: start T(i + kAhead)'s loads into them
+        if (have_next) load_group<TBC, U>(rg, u, cn, tid, next_full);
       }
       // lane-exclusive prefix of each group's counts (two groups per 32-bit scan)
 #pragma unroll
@@ -174,24 +202,24 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
         }
       }
     }
-    __syncthreads();  // wave totals of `cur` published; prefix of `old` resolved
+    __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
-    if (hvalid[kDefer - 1]) {
-      const TileCtx& oc = hctx[kDefer - 1];
-      const int oi = it - kDefer;  // iteration that computed `old`
+    const Deferred<U>& od = hist[kDefer - 1];
+    if (od.valid) {
+      const int oi = it - kDefer;  // iteration that computed the tile
       const uint64_t tile_excl = s_excl[oi & 1];
       const uint64_t cap = p.capacity;
-      const uint32_t base = p.t[oc.k].index_base;
-      uint16_t* __restrict__ refresh = p.t[oc.k].refresh;
+      const uint32_t base = p.t[od.k].index_base;
+      uint16_t* __restrict__ refresh = REFRESH ? p.t[od.k].refresh : nullptr;
       const uint16_t* vals16 = reinterpret_cast<const uint16_t*>(s_vals[oi % kValBufs]);
-      const uint32_t* wexcl = s_wexcl + (oi & 3) * U * NW;
+      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * U * NW;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        uint32_t m = (hmask[kDefer - 1] >> (8 * u)) & 0xFFu;
+        uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
         if (m == 0) continue;
         uint64_t pos = tile_excl + wexcl[u * NW + wid] +
-                       ((hexcl[kDefer - 1][u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-        const uint64_t e = oc.e0 + (uint64_t)(u * TBC + tid) * 8;
+                       ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
         while (m) {
           const int i = __builtin_ctz(m);
           m &= m - 1;
@@ -205,20 +233,29 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
         }
       }
     }
+    if (have_cur) {
 #pragma unroll
-    for (int d = kDefer - 1; d > 0; --d) {
-      hctx[d] = hctx[d - 1];
-      hmask[d] = hmask[d - 1];
-      hvalid[d] = hvalid[d - 1];
-#pragma unroll
-      for (int q = 0; q < (U + 1) / 2; ++q) hexcl[d][q] = hexcl[d - 1][q];
+      for (int u = 0; u < U; ++u) s_vals[it % kValBufs][u * TBC + tid] = hv[u];
     }
-    hctx[0] = cc;
-    hmask[0] = mask_packed;
-    hvalid[0] = have_cur;
 #pragma unroll
-    for (int q = 0; q < (U + 1) / 2; ++q) hexcl[0][q] = excl_packed[q];
-    cc = cn;
+    for (int d = kDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
+    hist[0].e0 = ce0;
+    hist[0].k = ck;
+    hist[0].valid = have_cur;
+    hist[0].mask = mask_packed;
+#pragma unroll
+    for (int q = 0; q < (U + 1) / 2; ++q) hist[0].excl[q] = excl_packed[q];
+    if (have_next) {
+      ce0 = cn.e0;
+      ck = cn.k;
+    }
+    look_up_next(it + 1);  // its ticket was stored before this iteration's barrier
+    return true;
+  };
+
+  for (int it = 0;; it += kAhead) {
+    if (!step(it, r0, e0_0, k_0)) return;
+    if (kAhead == 2 && !step(it + 1, r1, e0_1, k_1)) return;
   }
 }
 
@@ -239,12 +276,19 @@ hipError_t launch_encode(EncodeParams& p, hipStream_t stream) {
                        (const uint64_t*)p.count, p.seg_begin, (uint32_t)p.ntensors);
     return hipGetLastError();
   }
-  const int grid_cap = persistent_grid((const void*)encode_kernel<kEncodeNW, kEncodeU>,
-                                       (kEncodeNW + 1) * 64);
+  bool refresh = false;
+  for (int k = 0; k < p.ntensors; ++k) refresh |= p.t[k].refresh != nullptr;
+  const void* fn = refresh ? (const void*)encode_kernel<kEncodeNW, kEncodeU, true>
+                           : (const void*)encode_kernel<kEncodeNW, kEncodeU, false>;
+  const int grid_cap = persistent_grid(fn, (kEncodeNW + 1) * 64);
   if (grid_cap <= 0) return hipErrorInvalidConfiguration;
   const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
-  hipLaunchKernelGGL((encode_kernel<kEncodeNW, kEncodeU>), dim3(grid), dim3((kEncodeNW + 1) * 64),
-                     0, stream, p);
+  if (refresh)
+    hipLaunchKernelGGL((encode_kernel<kEncodeNW, kEncodeU, true>), dim3(grid),
+                       dim3((kEncodeNW + 1) * 64), 0, stream, p);
+  else
+    hipLaunchKernelGGL((encode_kernel<kEncodeNW, kEncodeU, false>), dim3(grid),
+                       dim3((kEncodeNW + 1) * 64), 0, stream, p);
   return hipGetLastError();
 }
 

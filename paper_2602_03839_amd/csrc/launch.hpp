@@ -10,6 +10,7 @@
 namespace pulse {
 
 constexpr int kMaxBatch = 64;  // tensors per launch; larger batches are split
+static_assert(kMaxBatch <= 64, "the tile -> tensor lookup keeps one tensor per lane");
 
 // Tile shapes: compute threads per block (a multiple of 64; one more wave is
 // added for the scan) and 8-element groups per thread.  The defaults give

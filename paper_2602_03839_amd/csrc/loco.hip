@@ -5,8 +5,8 @@
 // (0 where sent, s elsewhere) -- one pass over Delta and e.
 //
 // Same persistent, pipelined tile structure and ordered compaction as
-// encode.hip (NW compute waves + 1 scan wave; the next tile's loads are in
-// flight while the scan wave walks back).  The residual of a tile is stored
+// encode.hip (NW compute waves + 1 scan wave; the loads of the next kAhead
+// tiles are in flight while the scan wave walks back).  The residual of a tile is stored
 // densely right after the selection; the rare selected-but-beyond-capacity
 // entries are patched back to s in the write phase (same lane, same address,
 // so program order keeps the later store).
@@ -27,9 +27,10 @@ struct LocoCtx {
   uint32_t tile_in_tensor;
 };
 
-__device__ __forceinline__ LocoCtx locate(const LocoParams& p, uint32_t tile, uint32_t tile_elems) {
+__device__ __forceinline__ LocoCtx locate(const LocoParams& p, uint32_t lane_begin, uint32_t tile,
+                                          uint32_t tile_elems) {
   LocoCtx c;
-  c.k = find_owner(p.tile_begin, p.ntensors, tile);
+  c.k = owner_of(lane_begin, tile);
   c.tile_in_tensor = tile - p.tile_begin[c.k];
   c.e0 = (uint64_t)c.tile_in_tensor * tile_elems;
   c.n = p.t[c.k].n;
@@ -84,14 +85,24 @@ __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const Lo
 
 }  // namespace
 
+// What the write-out of a tile needs kDefer iterations after its compute.
+template <int U>
+struct LocoDeferred {
+  uint64_t e0;
+  int k;
+  bool valid;
+  uint32_t mask;
+  uint32_t excl[(U + 1) / 2];
+};
+
 template <int NW, int U, bool GATE>
 __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
   constexpr int TBC = NW * 64;
   constexpr uint32_t TILE = TBC * U * 8;
-  __shared__ uint64_t s_tk[3];
+  __shared__ uint64_t s_tk[kTkRing];
   __shared__ uint64_t s_excl[2];
   __shared__ uint32_t s_wtot[2 * U * NW];
-  __shared__ uint32_t s_wexcl[4 * U * NW];
+  __shared__ uint32_t s_wexcl[kWexclRing * U * NW];
   __shared__ uint4 s_vals[kValBufs][U * TBC * 2];
   static_assert(U * NW <= 64, "block scan runs on one wave");
   static_assert(U <= 4, "masks of all groups are packed into one register");
@@ -106,46 +117,62 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
     return;
   }
 
-  // ---------------- compute waves (same schedule as encode_kernel: compute
-  // `cur` group by group while refilling the registers with the next tile,
-  // then write the entries of the tile computed kDefer iterations earlier)
-  __syncthreads();  // first two tickets
-  LocoRegs<U, GATE> g;
-  LocoCtx cc;
-  {
-    const Ticket t0 = decode_ticket(s_tk[0]);
-    if (t0.tile < p.ntiles) {
-      cc = locate(p, t0.tile, TILE);
-      const bool full = cc.e0 + TILE <= cc.n;
+  // ---------------- compute waves (same schedule as encode_kernel: register
+  // set i mod kAhead holds T(i); compute it group by group while refilling the
+  // registers with T(i + kAhead), then write the entries of T(i - kDefer))
+  __syncthreads();  // T(0) .. T(kAhead) are in s_tk
+  static_assert(kAhead == 1 || kAhead == 2, "one or two register sets");
+  const uint32_t lane_begin = owner_lane_begin(p);
+  LocoRegs<U, GATE> g0, g1;
+  uint64_t e0_0 = 0, e0_1 = 0;
+  int k_0 = 0, k_1 = 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) load_group<TBC, U, GATE>(g, u, cc, tid, full);
+  for (int q = 0; q < kAhead; ++q) {
+    const Ticket t = ticket_at(s_tk, q);
+    if (t.tile < p.ntiles) {
+      const LocoCtx c = locate(p, lane_begin, t.tile, TILE);
+      const bool full = c.e0 + TILE <= c.n;
+#pragma unroll
+      for (int u = 0; u < U; ++u) load_group<TBC, U, GATE>(q == 0 ? g0 : g1, u, c, tid, full);
+      (q == 0 ? e0_0 : e0_1) = c.e0;
+      (q == 0 ? k_0 : k_1) = c.k;
     }
   }
-  LocoCtx hctx[kDefer];
-  uint32_t hmask[kDefer], hexcl[kDefer][(U + 1) / 2];
-  bool hvalid[kDefer];
+  // T(i + kAhead) is looked up right after the barrier that publishes it
+  LocoCtx cn;
+  bool have_next = false, next_full = false;
+  auto look_up_next = [&](int i) {
+    const Ticket t = ticket_at(s_tk, i + kAhead);
+    have_next = t.tile < p.ntiles;
+    if (have_next) {
+      cn = locate(p, lane_begin, t.tile, TILE);
+      next_full = cn.e0 + TILE <= cn.n;
+    }
+  };
+  look_up_next(0);
+  LocoDeferred<U> hist[kDefer];
 #pragma unroll
-  for (int d = 0; d < kDefer; ++d) hvalid[d] = false;
-  for (int it = 0;; ++it) {
-    const Ticket cur = decode_ticket(s_tk[it % 3]);
-    const Ticket nxt = decode_ticket(s_tk[(it + 1) % 3]);
+  for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
+
+  auto step = [&](const int it, LocoRegs<U, GATE>& g, uint64_t& ce0, int& ck) -> bool {
+    const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
     bool pending = have_cur;
 #pragma unroll
-    for (int d = 0; d < kDefer; ++d) pending |= hvalid[d];
-    if (!pending) break;
-    const bool have_next = nxt.tile < p.ntiles;
-    const LocoCtx cn = have_next ? locate(p, nxt.tile, TILE) : cc;
-    const bool next_full = cn.e0 + TILE <= cn.n;
+    for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
+    if (!pending) return false;
     uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
+    uint4 av[2 * U];  // a = Delta + e of T(i), staged after the write-out
     if (have_cur) {
       uint32_t cnt[U];
-      const bool full = cc.e0 + TILE <= cc.n;
-      const bool gate = GATE && cc.th != nullptr;
+      const uint64_t cn_n = p.t[ck].n;
+      float* const cres = p.t[ck].residual;
+      const bool full = ce0 + TILE <= cn_n;
+      const bool gate = GATE && p.t[ck].theta != nullptr;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const uint64_t e = cc.e0 + (uint64_t)(u * TBC + tid) * 8;
-        const bool vec = full || e + 8 <= cc.n;
+        const uint64_t e = ce0 + (uint64_t)(u * TBC + tid) * 8;
+        const bool vec = full || e + 8 <= cn_n;
         uint32_t m = 0;
         float a[8], nr[8];
 #pragma unroll
@@ -153,38 +180,47 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           const float dv = __uint_as_float(i < 4 ? get_u32(g.d0[u], i) : get_u32(g.d1[u], i - 4));
           const float rv = __uint_as_float(i < 4 ? get_u32(g.r0[u], i) : get_u32(g.r1[u], i - 4));
           a[i] = dv + rv;
-          bool sel;
-          if (gate) {
-            const float tv = __uint_as_float(i < 4 ? get_u32(g.t0[GATE ? u : 0], i)
-                                                   : get_u32(g.t1[GATE ? u : 0], i - 4));
-            const float after = tv - a[i];
-            sel = bf16_rne_bits(__float_as_uint(tv)) != bf16_rne_bits(__float_as_uint(after));
-          } else {
-            sel = fabsf(a[i]) >= tau;
-          }
-          if (!vec && !(e + i < cc.n)) sel = false;
-          m |= (uint32_t)sel << i;
-          nr[i] = sel ? 0.0f : a[i];
         }
+        if (gate) {
+          // selected iff bf16(theta) != bf16(theta - a), pairwise on the cvt unit
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint4& tq = j < 2 ? g.t0[GATE ? u : 0] : g.t1[GATE ? u : 0];
+            const uint32_t t_lo = get_u32(tq, (2 * j) & 3), t_hi = get_u32(tq, (2 * j + 1) & 3);
+            const float after_lo = __uint_as_float(t_lo) - a[2 * j];
+            const float after_hi = __uint_as_float(t_hi) - a[2 * j + 1];
+            m |= diff2(bf16x2_rne(t_lo, t_hi),
+                       bf16x2_rne(__float_as_uint(after_lo), __float_as_uint(after_hi)))
+                 << (2 * j);
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) m |= (uint32_t)(fabsf(a[i]) >= tau) << i;
+        }
+        if (!vec) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i)
+            if (!(e + i < cn_n)) m &= ~(1u << i);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) nr[i] = ((m >> i) & 1u) ? 0.0f : a[i];
         if (vec) {
-          store16_stream(cc.r + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
+          store16_stream(cres + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
                                               __float_as_uint(nr[2]), __float_as_uint(nr[3])));
-          store16_stream(cc.r + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
+          store16_stream(cres + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
                                                   __float_as_uint(nr[6]), __float_as_uint(nr[7])));
         } else {
 #pragma unroll
           for (int i = 0; i < 8; ++i)
-            if (e + i < cc.n) cc.r[e + i] = nr[i];
+            if (e + i < cn_n) cres[e + i] = nr[i];
         }
         mask_packed |= m << (8 * u);
         cnt[u] = __builtin_popcount(m);
-        s_vals[it % kValBufs][(u * TBC + tid) * 2] =
-            make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
-                       __float_as_uint(a[3]));
-        s_vals[it % kValBufs][(u * TBC + tid) * 2 + 1] =
-            make_uint4(__float_as_uint(a[4]), __float_as_uint(a[5]), __float_as_uint(a[6]),
-                       __float_as_uint(a[7]));
-        // this group's registers are free: start the next tile's loads into them
+        av[2 * u] = make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
+                               __float_as_uint(a[3]));
+        av[2 * u + 1] = make_uint4(__float_as_uint(a[4]), __float_as_uint(a[5]),
+                                   __float_as_uint(a[6]), __float_as_uint(a[7]));
+        // this group's registers are free: start T(i + kAhead)'s loads into them
         if (have_next) load_group<TBC, U, GATE>(g, u, cn, tid, next_full);
       }
 #pragma unroll
@@ -198,23 +234,24 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
         }
       }
     }
-    __syncthreads();  // wave totals of `cur` published; prefix of `old` resolved
+    __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
-    if (hvalid[kDefer - 1]) {
-      const LocoCtx& oc = hctx[kDefer - 1];
+    const LocoDeferred<U>& od = hist[kDefer - 1];
+    if (od.valid) {
       const int oi = it - kDefer;
       const uint64_t tile_excl = s_excl[oi & 1];
       const uint64_t cap = p.capacity;
-      const uint32_t base = p.t[oc.k].index_base;
+      const uint32_t base = p.t[od.k].index_base;
+      float* const ores = p.t[od.k].residual;
       const float* vals = reinterpret_cast<const float*>(s_vals[oi % kValBufs]);
-      const uint32_t* wexcl = s_wexcl + (oi & 3) * U * NW;
+      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * U * NW;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        uint32_t m = (hmask[kDefer - 1] >> (8 * u)) & 0xFFu;
+        uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
         if (m == 0) continue;
         uint64_t pos = tile_excl + wexcl[u * NW + wid] +
-                       ((hexcl[kDefer - 1][u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-        const uint64_t e = oc.e0 + (uint64_t)(u * TBC + tid) * 8;
+                       ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
         while (m) {
           const int i = __builtin_ctz(m);
           m &= m - 1;
@@ -223,26 +260,38 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
             p.idx[pos] = base + (uint32_t)(e + i);
             p.val[pos] = v;
           } else {
-            oc.r[e + i] = v;  // selected but not sent: error feedback keeps it
+            ores[e + i] = v;  // selected but not sent: error feedback keeps it
           }
           ++pos;
         }
       }
     }
+    if (have_cur) {
 #pragma unroll
-    for (int d = kDefer - 1; d > 0; --d) {
-      hctx[d] = hctx[d - 1];
-      hmask[d] = hmask[d - 1];
-      hvalid[d] = hvalid[d - 1];
-#pragma unroll
-      for (int q = 0; q < (U + 1) / 2; ++q) hexcl[d][q] = hexcl[d - 1][q];
+      for (int u = 0; u < U; ++u) {
+        s_vals[it % kValBufs][(u * TBC + tid) * 2] = av[2 * u];
+        s_vals[it % kValBufs][(u * TBC + tid) * 2 + 1] = av[2 * u + 1];
+      }
     }
-    hctx[0] = cc;
-    hmask[0] = mask_packed;
-    hvalid[0] = have_cur;
 #pragma unroll
-    for (int q = 0; q < (U + 1) / 2; ++q) hexcl[0][q] = excl_packed[q];
-    cc = cn;
+    for (int d = kDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
+    hist[0].e0 = ce0;
+    hist[0].k = ck;
+    hist[0].valid = have_cur;
+    hist[0].mask = mask_packed;
+#pragma unroll
+    for (int q = 0; q < (U + 1) / 2; ++q) hist[0].excl[q] = excl_packed[q];
+    if (have_next) {
+      ce0 = cn.e0;
+      ck = cn.k;
+    }
+    look_up_next(it + 1);  // its ticket was stored before this iteration's barrier
+    return true;
+  };
+
+  for (int it = 0;; it += kAhead) {
+    if (!step(it, g0, e0_0, k_0)) return;
+    if (kAhead == 2 && !step(it + 1, g1, e0_1, k_1)) return;
   }
 }
 

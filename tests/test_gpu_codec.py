@@ -211,8 +211,8 @@ def test_workspace_sequence_base_only_grows():
         run_encode(w_new, s_or, s_d, ws)
         seen.append(int(ws.view(torch.int64)[0].item()) >> 24)
     assert all(b > a for a, b in zip(seen, seen[1:])), seen
-    assert int(ws.view(torch.int64)[1].item()) == 0  # no look-back gave up
-    assert int(ws.view(torch.int64)[2].item()) == 0  # every launch finished
+    assert int(ws.view(torch.int64)[16].item()) == 0  # no look-back gave up
+    assert int(ws.view(torch.int64)[32].item()) == 0  # every launch finished
 
 
 def test_encode_workspace_ring_wraps(ws):
@@ -238,7 +238,7 @@ def test_encode_workspace_ring_wraps(ws):
             np.testing.assert_array_equal(got, np.flatnonzero(flip.cpu().numpy()).astype(np.uint32))
         else:
             np.testing.assert_array_equal(got, first)
-    assert int(ws.view(torch.int64)[1].item()) == 0  # no look-back ever gave up
+    assert int(ws.view(torch.int64)[16].item()) == 0  # no look-back ever gave up
 
 
 # --------------------------------------------------------------------------- batch
