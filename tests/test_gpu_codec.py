@@ -2,7 +2,7 @@
 
 Every case runs through the C ABI (ctypes binding) on the GPU and through the
 CPU oracle on the same seeded inputs; each side computes its own snapshot.
-Sizes span several 16384-element encode tiles with ragged tails; edge cases
+Sizes span several 15360-element encode tiles with ragged tails; edge cases
 cover empty and one-element tensors, 0% and 100% density, first/last element
 changes, append offsets, index bases, capacity overflow, refresh (separate
 and in place), special values, and the workspace ring wrapping around.

@@ -1,0 +1,312 @@
+"""Full-size parameter sets, run in the launch configuration the benchmark
+times: batches of <= 64 tensors, a patch buffer sized for 5% of the set (10%
+for the sparsifier), one workspace for every launch.
+
+* c2 (0.5B-shaped, 494,005,120 params, flat uint32 indices) is compared with
+  the oracle in full, element by element, including the fused refresh.
+* c3 (7B-shaped, 20-step chains at lr 3e-7, 1e-6, 3e-6), c4 (32B-shaped, one
+  fused step at lr 1e-6) and c5 (7B-shaped PULSELoCo, 10 rounds) are too large
+  for the oracle in test time.  They are checked
+    (a) at full size against the definition, computed on the GPU with torch's
+        own BF16 cast, comparison, nonzero and FP32 add (no kernel of this
+        library takes part), and
+    (b) on sampled windows, element by element, against the oracle.
+
+Snapshots come from torch's BF16 cast of the masters, so no input of either
+side is produced by the library under test.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_03839_amd import pulse
+from paper_2602_03839_amd import workloads as wl
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+CHUNK = 64
+CFG = {"0.5b": 2, "7b": 3, "32b": 4}
+WINDOW = 1 << 20
+
+
+def chunks(n, k=CHUNK):
+    return [(a, min(a + k, n)) for a in range(0, n, k)]
+
+
+def bf16_bits(t: torch.Tensor) -> torch.Tensor:
+    """torch's own RNE cast, as int16 bit patterns (no NaN in these workloads)."""
+    return t.to(torch.bfloat16).view(torch.int16)
+
+
+class ModelSet:
+    """FP32 masters of a model-shaped set in one flat buffer, with per-tensor views."""
+
+    def __init__(self, key: str):
+        self.key, self.cfg = key, CFG[key]
+        self.specs = wl.SHAPES[key].tensors()
+        self.sizes = [s.numel for s in self.specs]
+        self.offs = [0]
+        for n in self.sizes:
+            self.offs.append(self.offs[-1] + n)
+        self.N = self.offs[-1]
+        self.T = len(self.sizes)
+        self.flat = self.N < (1 << 32)
+
+    def view(self, buf, i):
+        return buf[self.offs[i]:self.offs[i + 1]]
+
+    def base(self, i):
+        return self.offs[i] if self.flat else 0
+
+    def init(self, w, S):
+        for i, spec in enumerate(self.specs):
+            wv = self.view(w, i)
+            wl.init_weights_(wv, spec, self.cfg, 0, i)
+            self.view(S, i).copy_(bf16_bits(wv))
+
+    def step(self, w, lr, t):
+        for i in range(self.T):
+            wl.adam_step_(self.view(w, i), lr, self.cfg, t, i)
+
+    def windows(self, rng):
+        """(tensor, begin, end): first and last tensor ends, the largest tensor, two random."""
+        big = int(np.argmax(self.sizes))
+        last = self.T - 1
+        out = [(0, 0, min(WINDOW, self.sizes[0])),
+               (last, max(0, self.sizes[last] - WINDOW - 3), self.sizes[last]),
+               (big, self.sizes[big] // 2 - 77, self.sizes[big] // 2 - 77 + WINDOW)]
+        for i in rng.choice(self.T, 2, replace=False):
+            n = self.sizes[i]
+            a = int(rng.integers(0, max(1, n - WINDOW)))
+            out.append((int(i), a, min(n, a + WINDOW)))
+        return out
+
+
+def encode_set(ms, w, S, R, idx, val, count, seg, ws):
+    count.zero_()
+    for a, b in chunks(ms.T):
+        pulse.EncodeBatch([pulse.EncodeTensor(ms.view(w, i), ms.view(S, i),
+                                              None if R is None else ms.view(R, i), ms.base(i))
+                           for i in range(a, b)])(idx, val, count, ws, seg_begin=seg[a:])
+
+
+def segments(seg, count):
+    return seg.cpu().tolist() + [int(count.item())]
+
+
+def check_encode_definition(ms, w, S, idx, val, segs):
+    """Every tensor's segment is exactly the changed positions of bf16(w) vs S, with their values."""
+    for i in range(ms.T):
+        b16 = bf16_bits(ms.view(w, i))
+        nz = torch.nonzero(b16 != ms.view(S, i)).flatten()
+        lo, hi = segs[i], segs[i + 1]
+        assert hi - lo == nz.numel(), (i, hi - lo, nz.numel())
+        got = idx[lo:hi].to(torch.int64) & 0xFFFFFFFF
+        assert torch.equal(got, nz + ms.base(i)), i
+        assert torch.equal(val[lo:hi], b16[nz]), i
+
+
+def host_windows(ms, wins, *bufs):
+    return [[ms.view(b, i)[a:e].cpu().numpy() for b in bufs] for i, a, e in wins]
+
+
+def gpu_entries(ms, idx, val, segs, i, a, e):
+    """The patch entries of tensor i whose index lies in [a, e) (host arrays)."""
+    lo, hi = segs[i], segs[i + 1]
+    gi = idx[lo:hi].cpu().numpy().view(np.uint32)
+    gv = val[lo:hi].cpu().numpy()
+    base = ms.base(i)
+    p, q = np.searchsorted(gi, base + a), np.searchsorted(gi, base + e)
+    return gi[p:q], gv[p:q]
+
+
+@pytest.fixture
+def fresh_memory():
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def test_c2_full_oracle_parity(fresh_memory):
+    """0.5B-shaped set, one fused step at lr 1e-6: patch, segments and refreshed copy
+    equal the oracle's for all 494,005,120 parameters."""
+    oracle.build()
+    ms = ModelSet("0.5b")
+    w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
+    S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
+    ms.init(w, S)
+    ms.step(w, 1e-6, 1)
+    R = S.clone()
+    cap = ms.N // 20
+    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    val = torch.empty(cap, dtype=torch.int16, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
+    ws = pulse.workspace()
+    encode_set(ms, w, S, R, idx, val, count, seg, ws)
+    torch.cuda.synchronize()
+    segs = segments(seg, count)
+    nnz = segs[-1]
+    assert 0.007 < nnz / ms.N < 0.012
+    h_w, h_s = w.cpu().numpy(), S.cpu().numpy().view(np.uint16)
+    h_idx = idx[:nnz].cpu().numpy().view(np.uint32)
+    h_val = val[:nnz].cpu().numpy().view(np.uint16)
+    h_r = R.cpu().numpy().view(np.uint16)
+    o_idx = np.zeros(nnz, np.uint32)
+    o_val = np.zeros(nnz, np.uint16)
+    o_r = h_s.copy()
+    c = 0
+    for i in range(ms.T):
+        a, b = ms.offs[i], ms.offs[i + 1]
+        assert segs[i] == c, i
+        c, _, _ = oracle.encode(h_w[a:b], h_s[a:b], index_base=ms.base(i), capacity=nnz, count_in=c,
+                                idx_out=o_idx, val_out=o_val, refresh=o_r[a:b])
+    assert c == nnz
+    np.testing.assert_array_equal(h_idx, o_idx)
+    np.testing.assert_array_equal(h_val, o_val)
+    np.testing.assert_array_equal(h_r, o_r)
+
+
+@pytest.mark.parametrize("lr", [3e-7, 1e-6, 3e-6])
+def test_c3_twenty_step_chain(fresh_memory, lr):
+    """7B-shaped set, 20 consecutive steps; each step's snapshot is the copy the
+    previous patches refreshed.  The standalone apply keeps a second copy."""
+    oracle.build()
+    ms = ModelSet("7b")
+    rng = np.random.default_rng(int(lr * 1e9))
+    w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
+    S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
+    ms.init(w, S)
+    R = S.clone()  # refreshed by the fused encode
+    Q = S.clone()  # written by the standalone apply
+    cap = ms.N // 20
+    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    val = torch.empty(cap, dtype=torch.int16, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
+    ws = pulse.workspace()
+    apply = pulse.ApplyBatch([pulse.ApplyTensor(ms.view(Q, i), ms.base(i)) for i in range(ms.T)])
+    rejected = torch.zeros(1, dtype=torch.int64, device="cuda")
+    dens = []
+    for t in range(1, 21):
+        ms.step(w, lr, t)
+        sample = t in (1, 20)
+        if sample:
+            wins = ms.windows(rng)
+            hw = host_windows(ms, wins, w, S)
+        encode_set(ms, w, S, R, idx, val, count, seg, ws)
+        apply(idx, val, seg, count, rejected=rejected)
+        segs = segments(seg, count)
+        assert segs[-1] <= cap
+        dens.append(segs[-1] / ms.N)
+        check_encode_definition(ms, w, S, idx, val, segs)
+        if sample:
+            for (i, a, e), (ww, ss) in zip(wins, hw):
+                ss = ss.view(np.uint16)
+                r = ss.copy()
+                cnt, oi, ov = oracle.encode(ww, ss, index_base=ms.base(i) + a, refresh=r)
+                gi, gv = gpu_entries(ms, idx, val, segs, i, a, e)
+                np.testing.assert_array_equal(gi, oi[:cnt])
+                np.testing.assert_array_equal(gv.view(np.uint16), ov[:cnt])
+                np.testing.assert_array_equal(ms.view(R, i)[a:e].cpu().numpy().view(np.uint16), r)
+        S.copy_(R)  # the next snapshot is the patched copy
+    assert int(rejected.item()) == 0
+    for i in range(ms.T):
+        want = bf16_bits(ms.view(w, i))
+        assert torch.equal(ms.view(R, i), want), i
+        assert torch.equal(ms.view(Q, i), want), i
+    lo, hi = {3e-7: (0.002, 0.005), 1e-6: (0.007, 0.012), 3e-6: (0.018, 0.03)}[lr]
+    assert lo < dens[0] < hi, dens[0]
+
+
+def test_c4_single_fused_step_32b(fresh_memory):
+    """32B-shaped set resident on one GPU: one fused encode+refresh step at lr 1e-6."""
+    oracle.build()
+    ms = ModelSet("32b")
+    rng = np.random.default_rng(4)
+    w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
+    S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
+    ms.init(w, S)
+    ms.step(w, 1e-6, 1)
+    R = S.clone()
+    cap = ms.N // 20
+    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    val = torch.empty(cap, dtype=torch.int16, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
+    ws = pulse.workspace()
+    wins = ms.windows(rng)
+    hw = host_windows(ms, wins, w, S)
+    encode_set(ms, w, S, R, idx, val, count, seg, ws)
+    segs = segments(seg, count)
+    assert 0.007 < segs[-1] / ms.N < 0.012 and segs[-1] <= cap
+    check_encode_definition(ms, w, S, idx, val, segs)
+    for i in range(ms.T):
+        assert torch.equal(ms.view(R, i), bf16_bits(ms.view(w, i))), i
+    for (i, a, e), (ww, ss) in zip(wins, hw):
+        ss = ss.view(np.uint16)
+        r = ss.copy()
+        cnt, oi, ov = oracle.encode(ww, ss, index_base=a, refresh=r)
+        gi, gv = gpu_entries(ms, idx, val, segs, i, a, e)
+        np.testing.assert_array_equal(gi, oi[:cnt])
+        np.testing.assert_array_equal(gv.view(np.uint16), ov[:cnt])
+        np.testing.assert_array_equal(ms.view(R, i)[a:e].cpu().numpy().view(np.uint16), r)
+
+
+def test_c5_loco_ten_rounds_7b(fresh_memory):
+    """PULSELoCo on the 7B-shaped set: 10 rounds at a fixed tau, residual carried
+    in FP32; every round's patch and residual are bit-exact."""
+    oracle.build()
+    ms = ModelSet("7b")
+    rng = np.random.default_rng(5)
+    tau = wl.loco_tau()
+    d = torch.empty(ms.N, dtype=torch.float32, device="cuda")
+    e = torch.zeros(ms.N, dtype=torch.float32, device="cuda")
+    e_old = torch.empty_like(e)
+    cap = ms.N // 10
+    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    val = torch.empty(cap, dtype=torch.float32, device="cuda")
+    count = torch.zeros(1, dtype=torch.int64, device="cuda")
+    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
+    ws = pulse.workspace()
+    batches = [pulse.LocoBatch([pulse.LocoTensor(ms.view(d, i), ms.view(e, i), None, 0)
+                                for i in range(a, b)]) for a, b in chunks(ms.T)]
+    tau32 = float(np.float32(tau))
+    dens = []
+    for r in range(10):
+        for i in range(ms.T):
+            wl.loco_delta_(ms.view(d, i), 5, r, i)
+        e_old.copy_(e)
+        sample = r in (0, 9)
+        if sample:
+            wins = ms.windows(rng)
+            hw = host_windows(ms, wins, d, e_old)
+        count.zero_()
+        for (a, _b), b in zip(chunks(ms.T), batches):
+            b(tau, idx, val, count, ws, seg_begin=seg[a:])
+        segs = segments(seg, count)
+        assert segs[-1] <= cap
+        dens.append(segs[-1] / ms.N)
+        for i in range(ms.T):
+            s = ms.view(d, i) + ms.view(e_old, i)
+            sel = s.abs() >= tau32
+            nz = torch.nonzero(sel).flatten()
+            lo, hi = segs[i], segs[i + 1]
+            assert hi - lo == nz.numel(), (r, i)
+            assert torch.equal(idx[lo:hi].to(torch.int64) & 0xFFFFFFFF, nz), (r, i)
+            assert torch.equal(val[lo:hi].view(torch.int32), s[nz].view(torch.int32)), (r, i)
+            want = torch.where(sel, torch.zeros_like(s), s)
+            assert torch.equal(ms.view(e, i).view(torch.int32), want.view(torch.int32)), (r, i)
+        if sample:
+            for (i, a, ee), (dd, eo) in zip(wins, hw):
+                res = eo.copy()
+                cnt, oi, ov = oracle.loco(dd, res, tau, index_base=a)
+                gi, gv = gpu_entries(ms, idx, val, segs, i, a, ee)
+                np.testing.assert_array_equal(gi, oi[:cnt])
+                np.testing.assert_array_equal(gv.view(np.uint32), ov[:cnt].view(np.uint32))
+                np.testing.assert_array_equal(ms.view(e, i)[a:ee].cpu().numpy().view(np.uint32),
+                                              res.view(np.uint32))
+    assert abs(dens[0] - 0.02) < 0.002 and dens[-1] > 0.035
