@@ -103,6 +103,22 @@ int pulse_encode(const float *w_new, const uint16_t *snap, uint64_t n,
                  uint32_t index_base, uint16_t *refresh,
                  void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Flags of a batched encode tensor.
+ *
+ * PULSE_REFRESH_MIRRORS_SNAP: the caller guarantees that refresh[i] == snap[i]
+ * (same bits) at every position i that this call does not select, which holds
+ * when `refresh` is W_{t-1}, the copy Alg. 1 Decode starts from
+ * (W_t <- W_{t-1}; W_t[I] <- V).  The result is then the same as without the
+ * flag, but the kernel may rewrite unselected elements with their own value:
+ * it writes whole aligned 128-byte runs of `refresh` that contain an emitted
+ * change, instead of one 2-byte write per change.  `refresh` must then be
+ * 16-byte aligned (else PULSE_EALIGN).  A refresh that IS the snapshot
+ * (refresh == snap) is treated this way without the flag.  If the guarantee
+ * does not hold, unselected elements of such runs take snap's value.
+ */
+#define PULSE_REFRESH_MIRRORS_SNAP 1u
+
 /* One tensor of a batched encode (fields as in pulse_encode). */
 typedef struct pulse_encode_tensor {
     const float *w_new;
@@ -110,6 +126,7 @@ typedef struct pulse_encode_tensor {
     uint16_t *refresh; /* may be NULL */
     uint64_t n;
     uint32_t index_base;
+    uint32_t flags;    /* 0 or PULSE_REFRESH_MIRRORS_SNAP */
 } pulse_encode_tensor;
 
 /*

@@ -2,7 +2,7 @@
 // App. H.5, Alg. 4): dst[idx[k] - index_base] = val[k].  A pure copy of bit
 // patterns into the receiver's BF16 copy in place; the destination is never
 // read, so the kernel streams the patch once and issues one 2-byte store per
-// entry.  The entry range comes from device memory (encode's running count),
+// entry (loads and stores non-temporal: nothing here is touched twice).  The entry range comes from device memory (encode's running count),
 // so the grid is fixed and strides over it.
 #include "device_common.hpp"
 #include "launch.hpp"
@@ -37,12 +37,12 @@ __global__ __launch_bounds__(TB) void apply_kernel(ApplyParams p) {
   int t = 0;
   for (uint64_t k = lo + (uint64_t)blockIdx.x * TB + tid; k < hi; k += stride) {
     while (t + 1 < nt && s_seg[t + 1] <= k) ++t;
-    const uint32_t id = p.idx[k];
-    const uint16_t v = p.val[k];
+    const uint32_t id = load_nt(p.idx + k);
+    const uint16_t v = load_nt(p.val + k);
     const uint32_t base = s_t[t].index_base;
     const uint64_t j = (uint64_t)(id - base);
     if (id >= base && j < s_t[t].n) {
-      s_t[t].dst[j] = v;
+      store_nt(s_t[t].dst + j, v);
     } else {
       ++rejected;
     }

@@ -106,15 +106,18 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   __shared__ uint32_t s_wtot[2 * U * NW];
   __shared__ uint32_t s_wexcl[kWexclRing * U * NW];
   __shared__ uint4 s_vals[kValBufs][U * TBC];
+  __shared__ uint32_t s_tcnt[2];
+  __shared__ uint32_t s_stage[2][kStageCap];  // (offset in tile << 16) | bf16 value
   static_assert(U * NW <= 64, "block scan runs on one wave");
   static_assert(U <= 4, "masks of all groups are packed into one register");
+  static_assert(TILE <= 65536, "offsets within a tile are staged in 16 bits");
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid >> 6;
 
   if (wid == NW) {
-    scan_wave_loop<U, NW>(p, s_tk, s_wtot, s_wexcl, s_excl);
+    scan_wave_loop<U, NW, true>(p, s_tk, s_wtot, s_wexcl, s_excl, s_tcnt);
     return;
   }
 
@@ -160,6 +163,16 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   Deferred<U> hist[kDefer];
 #pragma unroll
   for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
+  // the tile written out in the previous iteration, whose staged entries this
+  // iteration copies to the patch (block-uniform)
+  struct {
+    uint64_t excl, e0;
+    uint32_t count;
+    int k;
+    bool valid, staged;
+  } cp;
+  cp.valid = false;
+  cp.staged = false;
 
   // One iteration on register set `rg`, whose tile starts at element ce0 of
   // tensor ck; false when the block has nothing left to compute, resolve or
@@ -167,7 +180,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   auto step = [&](const int it, TileRegs<TBC, U>& rg, uint64_t& ce0, int& ck) -> bool {
     const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
-    bool pending = have_cur;
+    bool pending = have_cur || cp.valid;
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) return false;
@@ -204,34 +217,79 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
     }
     __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
+    // copy-out of the tile staged in the previous iteration: entry j of the
+    // tile goes to patch position excl + j, consecutive threads, consecutive j
+    if (cp.staged) {
+      const uint32_t* st = s_stage[(it - 1) & 1];
+      const uint32_t base = p.t[cp.k].index_base + (uint32_t)cp.e0;
+      const uint64_t cap = p.capacity;
+      for (uint32_t j = tid; j < cp.count; j += TBC) {
+        const uint64_t pos = cp.excl + j;
+        if (pos < cap) {
+          const uint32_t x = st[j];
+          store_nt(p.idx + pos, base + (x >> 16));
+          store_nt(p.val + pos, (uint16_t)x);
+        }
+      }
+    }
+
     const Deferred<U>& od = hist[kDefer - 1];
+    cp.valid = od.valid;
+    cp.staged = false;
     if (od.valid) {
       const int oi = it - kDefer;  // iteration that computed the tile
       const uint64_t tile_excl = s_excl[oi & 1];
+      const uint32_t tile_cnt = s_tcnt[oi & 1];
+      const bool staged = tile_cnt <= kStageCap;
+      uint32_t* st = s_stage[it & 1];
       const uint64_t cap = p.capacity;
       const uint32_t base = p.t[od.k].index_base;
       uint16_t* __restrict__ refresh = REFRESH ? p.t[od.k].refresh : nullptr;
-      const uint16_t* vals16 = reinterpret_cast<const uint16_t*>(s_vals[oi % kValBufs]);
+      const uint4* vals = s_vals[oi % kValBufs];
+      const uint16_t* vals16 = reinterpret_cast<const uint16_t*>(vals);
       const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * U * NW;
+      // Whole-run refresh (the inference copy equals the snapshot wherever
+      // nothing changed): every lane of a run of kSectorLanes lanes that holds
+      // a change stores its eight BF16 values as one 16-byte write, so the
+      // run's bytes are rewritten whole -- unchanged values equal the
+      // snapshot's -- in one request instead of one partial write per change.
+      // All lanes are active here (od is block-uniform).
+      const bool sector = REFRESH && refresh != nullptr && p.t[od.k].mirror != 0u;
+      const uint32_t run_mask = REFRESH ? or_across_lanes<kSectorLanes>(od.mask) : 0u;
+      const uint64_t tn = p.t[od.k].n;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
-        if (m == 0) continue;
-        uint64_t pos = tile_excl + wexcl[u * NW + wid] +
-                       ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-        const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
+        const bool run_any = sector && ((run_mask >> (8 * u)) & 0xFFu) != 0u;
+        if (m == 0 && !run_any) continue;
+        const uint32_t rank0 = wexcl[u * NW + wid] + ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        uint64_t pos = tile_excl + rank0;
+        const uint32_t le = (uint32_t)(u * TBC + tid) * 8;  // offset of slot 0 in the tile
+        const uint64_t e = od.e0 + le;
+        // a whole run is written only when every change of the lane is emitted
+        const bool whole = run_any && e + 8 <= tn && pos + __builtin_popcount(m) <= cap;
+        if (whole) store16_stream(refresh + e, vals[u * TBC + tid]);
+        uint32_t r = rank0;
         while (m) {
           const int i = __builtin_ctz(m);
           m &= m - 1;
-          const uint16_t v = vals16[(u * TBC + tid) * 8 + i];
-          if (pos < cap) {
-            p.idx[pos] = base + (uint32_t)(e + i);
-            p.val[pos] = v;
-            if (refresh) refresh[e + i] = v;
+          const uint16_t v = vals16[le + i];
+          if (staged) {
+            st[r] = ((le + i) << 16) | v;
+          } else if (pos < cap) {
+            store_nt(p.idx + pos, base + (uint32_t)(e + i));
+            store_nt(p.val + pos, v);
           }
+          if (REFRESH && refresh && !whole && pos < cap) store_nt(refresh + e + i, v);
           ++pos;
+          ++r;
         }
       }
+      cp.staged = staged && tile_cnt > 0;
+      cp.excl = tile_excl;
+      cp.count = tile_cnt;
+      cp.e0 = od.e0;
+      cp.k = od.k;
     }
     if (have_cur) {
 #pragma unroll

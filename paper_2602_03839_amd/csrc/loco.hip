@@ -113,7 +113,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
   const float tau = p.tau;
 
   if (wid == NW) {
-    scan_wave_loop<U, NW>(p, s_tk, s_wtot, s_wexcl, s_excl);
+    scan_wave_loop<U, NW, false>(p, s_tk, s_wtot, s_wexcl, s_excl, nullptr);
     return;
   }
 

@@ -50,6 +50,15 @@ int check_range(uint64_t n, uint32_t index_base, const char* who, uint32_t t) {
   return PULSE_OK;
 }
 
+// The refresh target holds the snapshot's bits on entry: it is the snapshot
+// itself, or the caller says it is kept in step with it.
+bool refresh_mirrors(const pulse_encode_tensor& d) {
+#ifdef PULSE_FORCE_MIRROR
+  return true;
+#endif
+  return d.refresh == d.snap || (d.flags & PULSE_REFRESH_MIRRORS_SNAP) != 0;
+}
+
 uint32_t tiles_for(uint64_t n, uint32_t tile) { return (uint32_t)((n + tile - 1) / tile); }
 
 }  // namespace
@@ -98,6 +107,10 @@ int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, ui
       return fail(PULSE_EALIGN, "encode tensor %u: w_new/snap not 16-byte aligned", t);
     if (d.refresh && !aligned(d.refresh, 2))
       return fail(PULSE_EALIGN, "encode tensor %u: refresh misaligned", t);
+    if (d.flags & ~(uint32_t)PULSE_REFRESH_MIRRORS_SNAP)
+      return fail(PULSE_EINVAL, "encode tensor %u: unknown flags 0x%x", t, d.flags);
+    if (d.refresh && refresh_mirrors(d) && !aligned16(d.refresh))
+      return fail(PULSE_EALIGN, "encode tensor %u: mirrored refresh not 16-byte aligned", t);
     if (int rc = check_range(d.n, d.index_base, "encode", t)) return rc;
   }
 
@@ -124,6 +137,7 @@ int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, ui
       p.t[k].refresh = d.refresh;
       p.t[k].n = d.n;
       p.t[k].index_base = d.index_base;
+      p.t[k].mirror = d.refresh && refresh_mirrors(d) ? 1u : 0u;
       tiles += nt;
       ++k;
     }
@@ -146,6 +160,7 @@ int pulse_encode(const float* w_new, const uint16_t* snap, uint64_t n, uint32_t*
   d.refresh = refresh;
   d.n = n;
   d.index_base = index_base;
+  d.flags = 0;
   return pulse_encode_batch(&d, 1, idx, val, capacity, count, nullptr, workspace,
                             workspace_bytes, stream);
 }

@@ -34,7 +34,10 @@ class PulseError(RuntimeError):
 class _EncodeTensor(ctypes.Structure):
     _fields_ = [("w_new", ctypes.c_void_p), ("snap", ctypes.c_void_p),
                 ("refresh", ctypes.c_void_p), ("n", ctypes.c_uint64),
-                ("index_base", ctypes.c_uint32)]
+                ("index_base", ctypes.c_uint32), ("flags", ctypes.c_uint32)]
+
+
+REFRESH_MIRRORS_SNAP = 1  # PULSE_REFRESH_MIRRORS_SNAP
 
 
 class _ApplyTensor(ctypes.Structure):
@@ -152,6 +155,7 @@ class EncodeTensor:
     snap: torch.Tensor
     refresh: Optional[torch.Tensor] = None
     index_base: int = 0
+    mirrors_snap: bool = False  # refresh holds snap's bits on entry (PULSE_REFRESH_MIRRORS_SNAP)
 
 
 class EncodeBatch:
@@ -164,7 +168,7 @@ class EncodeBatch:
             assert t.w_new.dtype == torch.float32 and _is16(t.snap)
             assert t.w_new.numel() == t.snap.numel()
             arr[i] = _EncodeTensor(_p(t.w_new), _p(t.snap), _p(t.refresh), t.w_new.numel(),
-                                   t.index_base)
+                                   t.index_base, REFRESH_MIRRORS_SNAP if t.mirrors_snap else 0)
         self.arr = arr
         self.keep = list(tensors)
 

@@ -301,6 +301,65 @@ def test_encode_apply_batch_ragged_with_empty_tensors(ws):
         np.testing.assert_array_equal(h16(a.dst), r)
 
 
+@pytest.mark.parametrize("cap_frac", [1.0, 0.5, 0.0])
+def test_encode_mirrored_refresh_batch(ws, cap_frac):
+    """PULSE_REFRESH_MIRRORS_SNAP: the inference copy starts equal to the snapshot
+    and is refreshed in whole 128-byte runs; it must end bit-identical to the
+    oracle's per-entry refresh, also when the patch overflows (only emitted
+    entries refresh) and across ragged tails, 0% and 100% density."""
+    rng = np.random.default_rng(13)
+    sizes = [5, TILE, 3 * TILE + 11, 1, 40_000, 2 * TILE - 1, 17, 8 * TILE + 8, 100_003]
+    dens = [0.5, 0.02, 0.01, 1.0, 0.0, 1.0, 0.3, 0.005, 0.02]
+    count_in = 13
+    tensors_or, descs, refs_d = [], [], []
+    base = 0
+    for n, d in zip(sizes, dens):
+        w_new = special_mix(rng, n)
+        flip = rng.random(n) < d
+        s_or, s_d = snapshots(w_new, flip)
+        r_d = s_d.clone()
+        tensors_or.append((w_new, s_or, base))
+        descs.append(pulse.EncodeTensor(dev(w_new), s_d, r_d, base, mirrors_snap=True))
+        refs_d.append(r_d)
+        base += n
+    nnz = sum(int((oracle.cast(w) != s).sum()) for w, s, _ in tensors_or)
+    cap = count_in + int(nnz * cap_frac)
+    o_idx = np.zeros(max(cap, 1), np.uint32)
+    o_val = np.zeros(max(cap, 1), np.uint16)
+    o_refs, o_seg = [], []
+    cnt = count_in
+    for w_new, s_or, b in tensors_or:
+        o_seg.append(cnt)
+        r = s_or.copy()
+        cnt, _, _ = oracle.encode(w_new, s_or, index_base=b, capacity=cap, count_in=cnt,
+                                  idx_out=o_idx, val_out=o_val, refresh=r)
+        o_refs.append(r)
+    g_idx = torch.zeros(max(cap, 1), dtype=torch.int32, device="cuda")
+    g_val = torch.zeros(max(cap, 1), dtype=torch.int16, device="cuda")
+    g_cnt = counter(count_in)
+    g_seg = torch.full((len(sizes),), -1, dtype=torch.int64, device="cuda")
+    pulse.EncodeBatch(descs)(g_idx, g_val, g_cnt, ws, seg_begin=g_seg, capacity=cap)
+    torch.cuda.synchronize()
+    assert read_count(g_cnt) == cnt
+    np.testing.assert_array_equal(g_seg.cpu().numpy(), np.array(o_seg, np.int64))
+    m = min(cnt, cap)
+    np.testing.assert_array_equal(h32(g_idx)[count_in:m], o_idx[count_in:m])
+    np.testing.assert_array_equal(h16(g_val)[count_in:m], o_val[count_in:m])
+    for r_d, r in zip(refs_d, o_refs):
+        np.testing.assert_array_equal(h16(r_d), r)
+
+
+def test_encode_mirrored_refresh_rejects_misaligned(ws):
+    w = torch.zeros(64, dtype=torch.float32, device="cuda")
+    s = torch.zeros(64, dtype=torch.int16, device="cuda")
+    r = torch.zeros(72, dtype=torch.int16, device="cuda")
+    idx = torch.zeros(64, dtype=torch.int32, device="cuda")
+    val = torch.zeros(64, dtype=torch.int16, device="cuda")
+    b = pulse.EncodeBatch([pulse.EncodeTensor(w, s, r[1:65], 0, mirrors_snap=True)])
+    with pytest.raises(pulse.PulseError, match="EALIGN"):
+        b(idx, val, counter(0), ws)
+
+
 def test_apply_rejects_out_of_range():
     rng = np.random.default_rng(10)
     n = 50_000
