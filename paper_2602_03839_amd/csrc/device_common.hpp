@@ -181,7 +181,7 @@ constexpr uint64_t kNoTicket = kTicketMask;
 
 // Tiles per ticket.  A chunk's tiles are processed in consecutive iterations,
 // so the chunk's last aggregate appears kChunk - 1 iterations after its first;
-// with kChunk <= kDefer later tiles never wait for it at resolution time.
+// with kChunk <= RES + 1 later tiles never wait for it at resolution time.
 #ifndef PULSE_CHUNK
 #define PULSE_CHUNK 4
 #endif
@@ -366,76 +366,56 @@ __device__ __forceinline__ int owner_of(uint32_t lane_begin, uint32_t t) {
 //   iteration i            compute waves publish its wave totals
 //                          (s_wtot[i & 1]); after the barrier the scan wave
 //                          combines them (group-major) into s_wexcl (ring
-//                          of kWexclRing)
+//                          of wexcl_ring(RES))
 //                          and publishes the tile aggregate (tile 0 of the
 //                          launch publishes its inclusive prefix, folding in
 //                          the append position *count);
-//   iteration i + kResolve the scan wave resolves the tile: the first
+//   iteration i + RES      the scan wave resolves the tile: the first
 //                          look-back window is read before the barrier,
 //                          overlapping the compute, and is consumed after it;
 //                          it publishes the inclusive prefix and stores the
 //                          exclusive prefix in s_excl[i & 1];
-//   iteration i + kDefer   after the barrier the compute waves write its
-//                          entries (into an LDS staging buffer, in patch
-//                          order, when they fit);
-//   iteration i + kDefer + 1  the block copies the staged entries to the
-//                          patch, consecutive threads writing consecutive
-//                          entries.
-// Tiles computed in the same iteration by different blocks publish their
-// aggregates at about the same time, so a tile is resolved kResolve
-// iterations later, when its predecessors have published their aggregates and
-// most of them their prefixes: the look-back then mostly reads one window and
-// rarely waits.  The scan wave's work of iteration i only has to be done
-// before barrier i + 1, so it does not hold the compute waves up while it
-// waits on memory.  Tickets: before barrier i the scan wave stores
-// T(i + kAhead + 1) in the ticket ring; the compute waves look it up right
-// after barrier i and start its loads in iteration i + 1.  The last tile
-// stores the new *count; the first tile of each tensor stores the tensor's
-// segment start.  Both loops run while any tile is still to be computed,
-// resolved or written.
-#ifndef PULSE_RESOLVE
-#define PULSE_RESOLVE 4
-#endif
-constexpr int kResolve = PULSE_RESOLVE;  // iterations from compute to resolution
-constexpr int kDefer = kResolve + 1;     // iterations from compute to write-out
-// ring of per-wave exclusive prefixes: filled at i, read at i + kDefer
-constexpr int kWexclRing = kDefer + 1 <= 4 ? 4 : 8;
-static_assert(kChunk <= kDefer, "a chunk's tiles must all be computed before the first resolves");
-// LDS value buffers (ring).  Each compute thread reads back only the values
-// it staged itself: tile T(i) is staged in slot i mod kValBufs after the
-// write-out of T(i - kDefer) has emptied that slot, so kDefer buffers suffice.
-constexpr int kValBufs = kDefer;
-
-// Patch write-out through LDS (encode).  Written straight from the lanes that
-// found them, a tile's few entries (about 1% of its elements) reach memory as
-// dozens of small partial-line writes, one per wave and group.  Instead the
-// compute waves put a tile's entries, once its prefix is known, into an LDS
-// buffer at their rank within the tile, and in the next iteration the whole
-// block copies the buffer out: thread t writes entry t, so the patch is
-// written in contiguous runs (0.6 ms less per step on the 32B-shaped set).
-// A tile with more entries than a buffer holds (above ~7% density) is written
-// straight from the lanes.  Two buffers alternate; an entry is stored as its
-// element's offset within the tile (16 bits) and its value.  The sparsifier
-// writes from the lanes: its tiles are half as long, and staging measured
-// slower there.
-#ifndef PULSE_STAGE_CAP
-#define PULSE_STAGE_CAP 1024
-#endif
-constexpr uint32_t kStageCap = PULSE_STAGE_CAP;
+//   iteration i + RES + 1  after the barrier the compute waves write its
+//                          entries to the patch.
+// Iterations from a tile's compute to its resolution (RES) and to its
+// write-out (RES + 1), per kernel; a deeper lag finds more predecessors
+// already resolved and costs LDS for what waits to be written.
+// Ring of per-wave exclusive prefixes: filled at i, read at i + RES + 1.
+constexpr int wexcl_ring(int res) {
+  return res + 2 <= 4 ? 4 : res + 2 <= 8 ? 8 : res + 2 <= 16 ? 16 : 32;
+}
 
 struct ScanState {
   Ticket tk;
   uint64_t agg;
   int k;
   bool valid;
+  bool ovf;  // some wave-group of the tile found more than seg_cap entries
 };
 
-// STAGED: the compute waves copy each tile's staged entries out one iteration
-// after its write-out (encode); the scan wave then also publishes tile counts
-// in s_cnt2 and runs one iteration longer with them.
-template <int U, int NW, bool STAGED, typename Params>
+// Optional outputs for encode (all null for the sparsifier):
+//   s_cnt2 / s_ovf2: on resolving a tile the scan wave also stores its entry
+//     count and whether one of its wave-groups found more than seg_cap entries
+//     (the compaction segments overflowed);
+//   s_known: the latest tile this block has resolved and its inclusive prefix,
+//     two slots, slot i & 1 written in iteration i (and read by the compute
+//     waves in iteration i + 2).  Entries of any later tile t lie below
+//     incl + (t - tile) * tile_elems.  Before the first resolution it holds
+//     (kNoTile, *count).
+struct KnownPrefix {
+  uint64_t incl;
+  uint32_t tile;
+};
+constexpr uint32_t kNoTile = 0xFFFFFFFFu;
+
+template <int U, int NW, int RES, typename Params>
 __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot2,
-                               uint32_t* s_wexcl, uint64_t* s_excl2, uint32_t* s_cnt2) {
+                               uint32_t* s_wexcl, uint64_t* s_excl2, uint32_t* s_cnt2,
+                               uint32_t* s_ovf2, uint32_t seg_cap, KnownPrefix* s_known) {
+  constexpr int kResolve = RES;
+  constexpr int kDefer = RES + 1;
+  constexpr int kWexclRing = wexcl_ring(RES);
+  static_assert(kChunk <= kDefer, "a chunk's tiles must all be computed before the first resolves");
   const int lane = lane_id();
   // tiles come in chunks of kChunk consecutive tiles, one atomic per chunk;
   // next_tile / left: the unused part of the block's current chunk.  The next
@@ -456,6 +436,11 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
     return make_ticket(g0, next_tile++, p.ntiles);
   };
   if (lane == 0) {
+    if (s_known) {
+      const uint64_t c0 = __hip_atomic_load(p.count, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_known[0] = KnownPrefix{c0, kNoTile};
+      s_known[1] = KnownPrefix{c0, kNoTile};
+    }
     pre = draw_ticket(p.ws);
     bool more = true;
     for (int q = 0; q <= kAhead; ++q) {
@@ -472,13 +457,10 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
   ScanState hist[kDefer];  // hist[d]: T(i - 1 - d)
 #pragma unroll
   for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
-  // the tile the compute waves wrote out in the previous iteration; they copy
-  // its staged entries to the patch in this one, so the loop runs on for it
-  bool drained = false;
   for (int it = 0;; ++it) {
     const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
-    bool pending = have_cur || (STAGED && drained);
+    bool pending = have_cur;
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) break;
@@ -498,6 +480,7 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
       if (lane < U * NW) s_wexcl[(it & (kWexclRing - 1)) * U * NW + lane] = incl - v;
       now.tk = cur;
       now.agg = __shfl(incl, 63, 64);
+      now.ovf = __ballot(lane < U * NW && v > seg_cap) != 0;
       now.k = owner_of(lane_begin, cur.tile);
       if (cur.tile == 0) {
         count_in = *p.count;  // append position, written by an earlier call
@@ -516,7 +499,9 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
       }
       if (lane == 0) {
         s_excl2[(it - kResolve) & 1] = excl;
-        if (STAGED) s_cnt2[(it - kResolve) & 1] = (uint32_t)res.agg;
+        if (s_cnt2) s_cnt2[(it - kResolve) & 1] = (uint32_t)res.agg;
+        if (s_ovf2) s_ovf2[(it - kResolve) & 1] = res.ovf ? 1u : 0u;
+        if (s_known) s_known[it & 1] = KnownPrefix{excl + res.agg, res.tk.tile};
         if (res.tk.tile == p.ntiles - 1) *p.count = excl + res.agg;
         if (p.seg_begin) {
           // segment starts of this tensor and of the empty tensors just before it
@@ -531,7 +516,7 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
         }
       }
     }
-    drained = hist[kDefer - 1].valid;
+    if (s_known && !res.valid && lane == 0) s_known[it & 1] = s_known[(it - 1) & 1];
 #pragma unroll
     for (int d = kDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
     hist[0] = now;

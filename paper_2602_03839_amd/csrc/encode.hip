@@ -12,15 +12,22 @@
 //
 // Block = NW compute waves + 1 scan wave, persistent over tiles drawn by
 // ticket (device_common.hpp).  Iteration i of the compute waves turns tile
-// T(i), already in registers, into masks and BF16 values, refilling each
-// group's registers with T(i + kAhead)'s loads as soon as it is consumed, so
-// kAhead tiles' loads are always in flight; it then publishes per-wave counts
-// and meets the scan wave at the one barrier of the iteration.  The scan wave
-// meanwhile publishes T(i)'s aggregate and resolves the exclusive prefix of
-// T(i - kResolve) by look-back, and after the barrier the compute waves write
-// the changed entries of T(i - kDefer) at their final positions, reading the
-// values back from an LDS ring.  Neither the look-back nor the ticket atomic
-// sits between a tile's loads and the next.
+// T(i), already in registers, into change masks and BF16 values, refilling
+// each group's registers with T(i + kAhead)'s loads as soon as it is consumed,
+// so kAhead tiles' loads are always in flight.  Each wave compacts its changed
+// entries at once into a small LDS segment per (group, wave) at their rank
+// within the wave, publishes its counts, and meets the scan wave at the one
+// barrier of the iteration.  The scan wave meanwhile publishes T(i)'s
+// aggregate and resolves the exclusive prefix of T(i - kResolve) by look-back,
+// and after the barrier the whole block copies the entries of T(i - kDefer)
+// from the segments to the patch, thread j writing the tile's entry j, so the
+// patch is written in contiguous runs.  Neither the look-back nor the ticket
+// atomic sits between a tile's loads and the next.
+//
+// The segments hold kSegCap entries per (group, wave): enough for the ~1-5%
+// densities of the method at every tile (a wave-group covers 512 elements).
+// A tile where some wave-group found more is written from the lanes instead,
+// each reloading its changed FP32 masters to recover the BF16 values.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -83,17 +90,45 @@ __device__ __forceinline__ void load_group(TileRegs<TBC, U>& r, int u, const Til
 
 }  // namespace
 
+// Compaction segments: kSegCap entries per (group, wave) and tile, in
+// kDefer + 2 slots.  A tile's slot is filled in its compute iteration i,
+// before barrier i, and read by every wave in the write-out of iteration
+// i + kDefer, after barrier i + kDefer.  Waves leave that write-out and start
+// computing iteration i + kDefer + 1 at different times, so the slot may be
+// refilled only from iteration i + kDefer + 2 on, after the next barrier.
+#ifndef PULSE_SEG_CAP
+#define PULSE_SEG_CAP 64
+#endif
+constexpr uint32_t kSegCap = PULSE_SEG_CAP;
+// Iterations from a tile's compute to its resolution and to its write-out.
+#ifndef PULSE_ENCODE_RESOLVE
+#define PULSE_ENCODE_RESOLVE 4
+#endif
+constexpr int kResolve = PULSE_ENCODE_RESOLVE;
+constexpr int kDefer = kResolve + 1;
+constexpr int kWexclRing = wexcl_ring(kResolve);
+constexpr int kSegSlots = kDefer + 2;
+
 // What the write-out of a tile needs kDefer iterations after its compute:
 // where it lies (wave-uniform) and, per lane, the change masks (8 bits per
-// group) and lane prefixes (16 bits per group).
+// group) and lane prefixes (16 bits per group), used only when the tile's
+// segments overflowed.
 template <int U>
 struct Deferred {
   uint64_t e0;
   int k;
   bool valid;
+  bool refreshed;  // the refresh was written at compute time
   uint32_t mask;
   uint32_t excl[(U + 1) / 2];
 };
+
+// BF16 value of slot i (0..7) of a lane's group, from its four BF16 pairs.
+__device__ __forceinline__ uint16_t bf16_slot(uint32_t h0, uint32_t h1, uint32_t h2, uint32_t h3,
+                                              int i) {
+  const uint32_t w = i < 2 ? h0 : i < 4 ? h1 : i < 6 ? h2 : h3;
+  return (uint16_t)(w >> (16 * (i & 1)));
+}
 
 // REFRESH: some tensor of the launch has an inference copy to refresh in the
 // same pass (a separate instantiation, so the plain encode carries no test).
@@ -101,33 +136,36 @@ template <int NW, int U, bool REFRESH>
 __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   constexpr int TBC = NW * 64;
   constexpr uint32_t TILE = TBC * U * 8;
+  constexpr int NSEG = U * NW;  // wave-groups per tile, group-major
   __shared__ uint64_t s_tk[kTkRing];
   __shared__ uint64_t s_excl[2];
-  __shared__ uint32_t s_wtot[2 * U * NW];
-  __shared__ uint32_t s_wexcl[kWexclRing * U * NW];
-  __shared__ uint4 s_vals[kValBufs][U * TBC];
   __shared__ uint32_t s_tcnt[2];
-  __shared__ uint32_t s_stage[2][kStageCap];  // (offset in tile << 16) | bf16 value
-  static_assert(U * NW <= 64, "block scan runs on one wave");
+  __shared__ uint32_t s_tovf[2];
+  __shared__ uint32_t s_wtot[2 * NSEG];
+  __shared__ uint32_t s_wexcl[kWexclRing * NSEG];
+  __shared__ uint32_t s_seg[kSegSlots][NSEG][kSegCap];  // (offset in tile << 16) | bf16 value
+  __shared__ KnownPrefix s_known[2];
+  static_assert(NSEG <= 64, "block scan runs on one wave");
   static_assert(U <= 4, "masks of all groups are packed into one register");
-  static_assert(TILE <= 65536, "offsets within a tile are staged in 16 bits");
+  static_assert(TILE <= 65536, "offsets within a tile are stored in 16 bits");
+  static_assert(kWexclRing >= kDefer + 1, "wave prefixes must outlive the write-out");
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid >> 6;
 
   if (wid == NW) {
-    scan_wave_loop<U, NW, true>(p, s_tk, s_wtot, s_wexcl, s_excl, s_tcnt);
+    scan_wave_loop<U, NW, kResolve>(p, s_tk, s_wtot, s_wexcl, s_excl, s_tcnt, s_tovf, kSegCap,
+                                     s_known);
     return;
   }
 
   // ---------------- compute waves.  Register set q holds tile T(i) for
   // i = q mod kAhead.  Iteration i computes T(i) group by group, refilling
   // each group's registers with the loads of T(i + kAhead) as soon as they are
-  // consumed, then writes the entries of T(i - kDefer), whose prefix the scan
-  // wave resolved in the previous iteration.  Staged values live in a ring of
-  // kValBufs LDS buffers private to each thread; a tile's values wait in
-  // registers over the barrier and take the slot its write-out just freed.
+  // consumed, compacts its entries into the segments, and after the barrier
+  // writes the entries of T(i - kDefer), whose prefix the scan wave resolved
+  // in the previous iteration.
   __syncthreads();  // T(0) .. T(kAhead) are in s_tk
   static_assert(kAhead == 1 || kAhead == 2, "one or two register sets");
   const uint32_t lane_begin = owner_lane_begin(p);
@@ -163,16 +201,6 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   Deferred<U> hist[kDefer];
 #pragma unroll
   for (int d = 0; d < kDefer; ++d) hist[d].valid = false;
-  // the tile written out in the previous iteration, whose staged entries this
-  // iteration copies to the patch (block-uniform)
-  struct {
-    uint64_t excl, e0;
-    uint32_t count;
-    int k;
-    bool valid, staged;
-  } cp;
-  cp.valid = false;
-  cp.staged = false;
 
   // One iteration on register set `rg`, whose tile starts at element ce0 of
   // tensor ck; false when the block has nothing left to compute, resolve or
@@ -180,26 +208,26 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
   auto step = [&](const int it, TileRegs<TBC, U>& rg, uint64_t& ce0, int& ck) -> bool {
     const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
-    bool pending = have_cur || cp.valid;
+    bool pending = have_cur;
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) return false;
     uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
-    uint4 hv[U];  // BF16 values of T(i), staged after the write-out
+    bool refreshed = false;
     if (have_cur) {
       uint32_t cnt[U];
+      uint32_t hb[U][4];  // BF16 pairs of each group
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         // BF16 pairs (elements 2j, 2j + 1) against the snapshot's words
-        const uint32_t h0 = bf16x2_rne(rg.a[u].x, rg.a[u].y);
-        const uint32_t h1 = bf16x2_rne(rg.a[u].z, rg.a[u].w);
-        const uint32_t h2 = bf16x2_rne(rg.b[u].x, rg.b[u].y);
-        const uint32_t h3 = bf16x2_rne(rg.b[u].z, rg.b[u].w);
-        const uint32_t m = diff2(h0, rg.c[u].x) | (diff2(h1, rg.c[u].y) << 2) |
-                           (diff2(h2, rg.c[u].z) << 4) | (diff2(h3, rg.c[u].w) << 6);
+        hb[u][0] = bf16x2_rne(rg.a[u].x, rg.a[u].y);
+        hb[u][1] = bf16x2_rne(rg.a[u].z, rg.a[u].w);
+        hb[u][2] = bf16x2_rne(rg.b[u].x, rg.b[u].y);
+        hb[u][3] = bf16x2_rne(rg.b[u].z, rg.b[u].w);
+        const uint32_t m = diff2(hb[u][0], rg.c[u].x) | (diff2(hb[u][1], rg.c[u].y) << 2) |
+                           (diff2(hb[u][2], rg.c[u].z) << 4) | (diff2(hb[u][3], rg.c[u].w) << 6);
         mask_packed |= m << (8 * u);
         cnt[u] = __builtin_popcount(m);
-        hv[u] = make_uint4(h0, h1, h2, h3);
         // this group's registers are free: start T(i + kAhead)'s loads into them
         if (have_next) load_group<TBC, U>(rg, u, cn, tid, next_full);
       }
@@ -210,96 +238,123 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_kernel(EncodeParams p) {
         const uint32_t incl = wave_incl_scan(packed);
         excl_packed[u >> 1] = incl - packed;
         if (lane == 63) {
-          s_wtot[(it & 1) * U * NW + u * NW + wid] = incl & 0xFFFFu;
-          if (u + 1 < U) s_wtot[(it & 1) * U * NW + (u + 1) * NW + wid] = incl >> 16;
+          s_wtot[(it & 1) * NSEG + u * NW + wid] = incl & 0xFFFFu;
+          if (u + 1 < U) s_wtot[(it & 1) * NSEG + (u + 1) * NW + wid] = incl >> 16;
+        }
+      }
+      // compaction: each changed entry at its rank within the wave-group
+      uint32_t(*seg)[kSegCap] = s_seg[it % kSegSlots];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        uint32_t m = (mask_packed >> (8 * u)) & 0xFFu;
+        uint32_t r = (excl_packed[u >> 1] >> (16 * (u & 1))) & 0xFFFFu;
+        const uint32_t le = (uint32_t)(u * TBC + tid) * 8;  // offset of slot 0 in the tile
+        while (m) {
+          const int i = __builtin_ctz(m);
+          m &= m - 1;
+          if (r < kSegCap)
+            seg[u * NW + wid][r] =
+                ((le + i) << 16) | bf16_slot(hb[u][0], hb[u][1], hb[u][2], hb[u][3], i);
+          ++r;
+        }
+      }
+      // Refresh at compute time, while the values are in registers, when every
+      // entry of T(i) will be emitted: its entries lie below the inclusive
+      // prefix of the latest tile this block resolved plus TILE for each tile
+      // in between (the scan wave's slot from two iterations ago).
+      uint16_t* __restrict__ refresh = REFRESH ? p.t[ck].refresh : nullptr;
+      const KnownPrefix kp = s_known[it & 1];
+      const uint64_t span = kp.tile == kNoTile ? (uint64_t)cur.tile + 1 : (uint64_t)(cur.tile - kp.tile);
+      refreshed = REFRESH && refresh != nullptr && kp.incl <= p.capacity &&
+                  span <= (p.capacity - kp.incl) / TILE;
+      if (refreshed) {
+        const uint64_t tn = p.t[ck].n;
+        // Whole-run refresh (the inference copy equals the snapshot wherever
+        // nothing changed): every lane of a run of kSectorLanes lanes that
+        // holds a change stores its eight BF16 values as one 16-byte write,
+        // so the run's bytes are rewritten whole -- unchanged values equal the
+        // snapshot's -- in one request instead of one partial write per
+        // change.  All lanes are active here (have_cur is block-uniform).
+        const bool sector = p.t[ck].mirror != 0u;
+        const uint32_t run_mask = or_across_lanes<kSectorLanes>(mask_packed);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          uint32_t m = (mask_packed >> (8 * u)) & 0xFFu;
+          const uint64_t e = ce0 + (uint64_t)(u * TBC + tid) * 8;
+          if (sector && ((run_mask >> (8 * u)) & 0xFFu) != 0u && e + 8 <= tn) {
+            store16_stream(refresh + e, make_uint4(hb[u][0], hb[u][1], hb[u][2], hb[u][3]));
+            continue;
+          }
+          while (m) {
+            const int i = __builtin_ctz(m);
+            m &= m - 1;
+            store_nt(refresh + e + i, bf16_slot(hb[u][0], hb[u][1], hb[u][2], hb[u][3], i));
+          }
         }
       }
     }
     __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
-    // copy-out of the tile staged in the previous iteration: entry j of the
-    // tile goes to patch position excl + j, consecutive threads, consecutive j
-    if (cp.staged) {
-      const uint32_t* st = s_stage[(it - 1) & 1];
-      const uint32_t base = p.t[cp.k].index_base + (uint32_t)cp.e0;
-      const uint64_t cap = p.capacity;
-      for (uint32_t j = tid; j < cp.count; j += TBC) {
-        const uint64_t pos = cp.excl + j;
-        if (pos < cap) {
-          const uint32_t x = st[j];
-          store_nt(p.idx + pos, base + (x >> 16));
-          store_nt(p.val + pos, (uint16_t)x);
-        }
-      }
-    }
-
     const Deferred<U>& od = hist[kDefer - 1];
-    cp.valid = od.valid;
-    cp.staged = false;
     if (od.valid) {
       const int oi = it - kDefer;  // iteration that computed the tile
       const uint64_t tile_excl = s_excl[oi & 1];
       const uint32_t tile_cnt = s_tcnt[oi & 1];
-      const bool staged = tile_cnt <= kStageCap;
-      uint32_t* st = s_stage[it & 1];
+      const bool overflowed = s_tovf[oi & 1] != 0u;
       const uint64_t cap = p.capacity;
       const uint32_t base = p.t[od.k].index_base;
-      uint16_t* __restrict__ refresh = REFRESH ? p.t[od.k].refresh : nullptr;
-      const uint4* vals = s_vals[oi % kValBufs];
-      const uint16_t* vals16 = reinterpret_cast<const uint16_t*>(vals);
-      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * U * NW;
-      // Whole-run refresh (the inference copy equals the snapshot wherever
-      // nothing changed): every lane of a run of kSectorLanes lanes that holds
-      // a change stores its eight BF16 values as one 16-byte write, so the
-      // run's bytes are rewritten whole -- unchanged values equal the
-      // snapshot's -- in one request instead of one partial write per change.
-      // All lanes are active here (od is block-uniform).
-      const bool sector = REFRESH && refresh != nullptr && p.t[od.k].mirror != 0u;
-      const uint32_t run_mask = REFRESH ? or_across_lanes<kSectorLanes>(od.mask) : 0u;
-      const uint64_t tn = p.t[od.k].n;
+      // refresh not written at compute time: only emitted entries, here
+      uint16_t* __restrict__ late_refresh =
+          (REFRESH && !od.refreshed) ? p.t[od.k].refresh : nullptr;
+      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * NSEG;
+      if (!overflowed) {
+        // entry j of the tile lies in the last wave-group q whose prefix is <= j
+        const uint32_t(*seg)[kSegCap] = s_seg[oi % kSegSlots];
+        const uint32_t tbase = base + (uint32_t)od.e0;
+        for (uint32_t j = tid; j < tile_cnt; j += TBC) {
+          int q = 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
-        const bool run_any = sector && ((run_mask >> (8 * u)) & 0xFFu) != 0u;
-        if (m == 0 && !run_any) continue;
-        const uint32_t rank0 = wexcl[u * NW + wid] + ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-        uint64_t pos = tile_excl + rank0;
-        const uint32_t le = (uint32_t)(u * TBC + tid) * 8;  // offset of slot 0 in the tile
-        const uint64_t e = od.e0 + le;
-        // a whole run is written only when every change of the lane is emitted
-        const bool whole = run_any && e + 8 <= tn && pos + __builtin_popcount(m) <= cap;
-        if (whole) store16_stream(refresh + e, vals[u * TBC + tid]);
-        uint32_t r = rank0;
-        while (m) {
-          const int i = __builtin_ctz(m);
-          m &= m - 1;
-          const uint16_t v = vals16[le + i];
-          if (staged) {
-            st[r] = ((le + i) << 16) | v;
-          } else if (pos < cap) {
-            store_nt(p.idx + pos, base + (uint32_t)(e + i));
-            store_nt(p.val + pos, v);
+          for (int step = 32; step > 0; step >>= 1)
+            if (q + step < NSEG && wexcl[q + step] <= j) q += step;
+          const uint64_t pos = tile_excl + j;
+          if (pos < cap) {
+            const uint32_t x = seg[q][j - wexcl[q]];
+            store_nt(p.idx + pos, tbase + (x >> 16));
+            store_nt(p.val + pos, (uint16_t)x);
+            if (late_refresh) store_nt(late_refresh + od.e0 + (x >> 16), (uint16_t)x);
           }
-          if (REFRESH && refresh && !whole && pos < cap) store_nt(refresh + e + i, v);
-          ++pos;
-          ++r;
+        }
+      } else {
+        // a wave-group found more entries than its segment holds: every lane
+        // writes its own entries, recovering the values from the FP32 masters
+        const float* w = p.t[od.k].w_new;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
+          uint64_t pos = tile_excl + wexcl[u * NW + wid] +
+                         ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+          const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
+          while (m) {
+            const int i = __builtin_ctz(m);
+            m &= m - 1;
+            if (pos < cap) {
+              const uint32_t b = __float_as_uint(w[e + i]);
+              const uint16_t v = (uint16_t)bf16x2_rne(b, b);
+              store_nt(p.idx + pos, base + (uint32_t)(e + i));
+              store_nt(p.val + pos, v);
+              if (late_refresh) store_nt(late_refresh + e + i, v);
+            }
+            ++pos;
+          }
         }
       }
-      cp.staged = staged && tile_cnt > 0;
-      cp.excl = tile_excl;
-      cp.count = tile_cnt;
-      cp.e0 = od.e0;
-      cp.k = od.k;
-    }
-    if (have_cur) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) s_vals[it % kValBufs][u * TBC + tid] = hv[u];
     }
 #pragma unroll
     for (int d = kDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
     hist[0].e0 = ce0;
     hist[0].k = ck;
     hist[0].valid = have_cur;
+    hist[0].refreshed = refreshed;
     hist[0].mask = mask_packed;
 #pragma unroll
     for (int q = 0; q < (U + 1) / 2; ++q) hist[0].excl[q] = excl_packed[q];

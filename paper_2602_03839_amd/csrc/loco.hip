@@ -85,6 +85,18 @@ __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const Lo
 
 }  // namespace
 
+// Iterations from a tile's compute to its resolution and to its write-out.
+#ifndef PULSE_LOCO_RESOLVE
+#define PULSE_LOCO_RESOLVE 4
+#endif
+constexpr int kResolve = PULSE_LOCO_RESOLVE;
+constexpr int kDefer = kResolve + 1;
+constexpr int kWexclRing = wexcl_ring(kResolve);
+// LDS value buffers (ring).  Each compute thread reads back only the values
+// it staged itself: tile T(i) is staged in slot i mod kValBufs after the
+// write-out of T(i - kDefer) has emptied that slot, so kDefer buffers suffice.
+constexpr int kValBufs = kDefer;
+
 // What the write-out of a tile needs kDefer iterations after its compute.
 template <int U>
 struct LocoDeferred {
@@ -113,7 +125,8 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
   const float tau = p.tau;
 
   if (wid == NW) {
-    scan_wave_loop<U, NW, false>(p, s_tk, s_wtot, s_wexcl, s_excl, nullptr);
+    scan_wave_loop<U, NW, kResolve>(p, s_tk, s_wtot, s_wexcl, s_excl, nullptr, nullptr, 0u,
+                                     nullptr);
     return;
   }
 

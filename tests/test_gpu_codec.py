@@ -349,6 +349,39 @@ def test_encode_mirrored_refresh_batch(ws, cap_frac):
         np.testing.assert_array_equal(h16(r_d), r)
 
 
+def test_encode_many_tiles_per_block_exact(ws):
+    """Long runs of tiles per block (2^27 elements, ~34 tiles per block) at the
+    method's low densities, several times over: every index and value exact.
+    Exercises the reuse of the per-tile LDS slots across many iterations, where
+    waves drift apart between barriers."""
+    n = 1 << 27
+    g = torch.Generator(device="cuda").manual_seed(5)
+    w = torch.empty(n, dtype=torch.float32, device="cuda").normal_(0, 0.1, generator=g)
+    for dens in (0.003, 0.01, 0.05):
+        s = pulse.cast_bf16(w)
+        flip = torch.rand(n, device="cuda", generator=g) < dens
+        s ^= flip.to(torch.int16)
+        want = torch.nonzero(flip).flatten()
+        b16 = pulse.cast_bf16(w)
+        # a patch buffer with room for every element lets the refresh be written
+        # at compute time; a tight one defers it to the write-out
+        idx = torch.empty(n, dtype=torch.int32, device="cuda")
+        val = torch.empty(n, dtype=torch.int16, device="cuda")
+        refs = [s.clone(), s.clone()]
+        for rep in range(4):
+            cnt = counter(0)
+            r = refs[rep - 2] if rep >= 2 else None
+            b = pulse.EncodeBatch([pulse.EncodeTensor(w, s, r, 0, mirrors_snap=True)])
+            b(idx, val, cnt, ws, capacity=n if rep == 3 else want.numel() + 16)
+            torch.cuda.synchronize()
+            assert read_count(cnt) == want.numel()
+            got = idx[: want.numel()].to(torch.int64) & 0xFFFFFFFF
+            assert torch.equal(got, want), (dens, rep)
+            assert torch.equal(val[: want.numel()], b16[want]), (dens, rep)
+        for r in refs:
+            assert torch.equal(r, b16), dens
+
+
 def test_encode_mirrored_refresh_rejects_misaligned(ws):
     w = torch.zeros(64, dtype=torch.float32, device="cuda")
     s = torch.zeros(64, dtype=torch.int16, device="cuda")
