@@ -324,14 +324,26 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
       look_back_issue<LK>(ws, tk, j, win);
       continue;
     }
-    uint64_t v = 0;
+    // Every word before the nearest prefix is a tile aggregate (a count of at
+    // most one tile, so 64 * LK of them fit 32 bits): sum them with the DPP
+    // scan instead of 64-bit lane shuffles, and take the one prefix value
+    // from its lane.
+    uint32_t a = 0;
 #pragma unroll
     for (int m = 0; m < LK; ++m) {
-      const bool take = m < first_m || (m == first_m && lane <= first_l);
-      if (take) v += win.w[m] & kValueMask;
+      const bool take = m < first_m || (m == first_m && lane < first_l);
+      if (take) a += (uint32_t)(win.w[m] & kValueMask);
     }
-    excl += wave_sum_u64(v);
-    if (first_m < LK) return excl;
+    excl += __builtin_amdgcn_readlane(wave_incl_scan(a), 63);
+    if (first_m < LK) {
+      uint64_t pw = 0;
+#pragma unroll
+      for (int m = 0; m < LK; ++m)
+        if (m == first_m) pw = win.w[m] & kValueMask;
+      const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)pw, first_l);
+      const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(pw >> 32), first_l);
+      return excl + (((uint64_t)hi << 32) | lo);
+    }
     j -= 64 * LK;
     look_back_issue<LK>(ws, tk, j, win);
   }
