@@ -13,6 +13,7 @@ and marshals numpy arrays into it with ctypes.
     encode(w_new, snap, ...)         Sec. 4.2 Alg. 1 Encode, App. H.5 Alg. 3
     apply(dst, idx, val, ...)        Sec. 4.2 Alg. 1 Decode, App. H.5 Alg. 4
     loco(delta, residual, tau, ...)  Sec. 4.3 Alg. 2 (s = Delta + e, selection, error feedback)
+    outer_step(theta, m, lists, ...) Sec. 4.3 Alg. 2 (SparseSync average, outer Nesterov step)
 """
 from __future__ import annotations
 
@@ -59,6 +60,8 @@ def _load():
             lib.oracle_apply.restype = u64
             lib.oracle_loco.argtypes = [vp, vp, u64, f32, vp, u32, vp, vp, u64, u64]
             lib.oracle_loco.restype = u64
+            lib.oracle_outer_step.argtypes = [vp, vp, u64, u32, u32, vp, vp, vp, f32, f32]
+            lib.oracle_outer_step.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -175,3 +178,28 @@ def loco(delta, residual: np.ndarray, tau: float, theta=None, index_base: int = 
                                 _ptr(theta), index_base, _ptr(idx_out), _ptr(val_out),
                                 capacity, count_in)
     return int(count), idx_out, val_out
+
+
+def outer_step(theta: np.ndarray, momentum: np.ndarray, lists, mu: float = 0.9,
+               alpha: float = 0.7, index_base: int = 0) -> None:
+    """Alg. 2's SparseSync average and outer Nesterov step, in place on theta and momentum.
+
+    ``lists`` is a sequence of (idx, val) pairs, one per worker, in worker order:
+    uint32 indices (index_base + i) and FP32 values.
+    """
+    assert theta.dtype == np.float32 and momentum.dtype == np.float32
+    assert theta.flags["C_CONTIGUOUS"] and momentum.flags["C_CONTIGUOUS"]
+    assert theta.size == momentum.size
+    keep = [(np.ascontiguousarray(i, dtype=np.uint32), _f32(v).ravel()) for i, v in lists]
+    for i, v in keep:
+        assert i.size == v.size
+    R = len(keep)
+    idx_p = (ctypes.c_void_p * max(R, 1))(*[i.ctypes.data for i, _ in keep])
+    val_p = (ctypes.c_void_p * max(R, 1))(*[v.ctypes.data for _, v in keep])
+    cnt = np.array([i.size for i, _ in keep] or [0], dtype=np.uint64)
+    rc = _load().oracle_outer_step(_ptr(theta), _ptr(momentum), theta.size, index_base, R,
+                                   ctypes.cast(idx_p, ctypes.c_void_p),
+                                   ctypes.cast(val_p, ctypes.c_void_p), _ptr(cnt),
+                                   float(np.float32(mu)), float(np.float32(alpha)))
+    if rc != 0:
+        raise MemoryError("oracle_outer_step could not allocate its scratch vector")

@@ -19,6 +19,9 @@
  *                        Alg. 4 (direct value assignment, no FP arithmetic).
  *   oracle_loco          Sec. 4.3, Alg. 2: s = Delta + e, the selection, and the
  *                        error-feedback update e[I] <- 0, e[not I] <- s.
+ *   oracle_outer_step    Sec. 4.3, Alg. 2: SparseSync's union-average of the
+ *                        workers' selected values, then the outer Nesterov step
+ *                        m <- mu m + g, theta <- theta - alpha (mu m + g).
  *
  * Readings where the paper is silent (all listed in the design notes):
  *   - A NaN input casts to a quiet NaN that keeps the sign and the leading
@@ -37,6 +40,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 static float float_from_bits(uint32_t u)
@@ -181,4 +185,55 @@ uint64_t oracle_loco(const float *delta, float *residual, uint64_t n, float tau,
             count++;
     }
     return count;
+}
+
+/*
+ * PULSELoCo outer step (Sec. 4.3, Alg. 2: the SparseSync line and the two
+ * outer-optimizer lines after it).
+ *
+ * SparseSync returns the union of the R workers' selected sets, each value the
+ * average over all R workers of what they sent, a worker that did not send an
+ * index counting as zero:
+ *   g_i = (v_0[i] + v_1[i] + ... + v_{R-1}[i]) / R,  summed left to right in
+ *         worker order, starting from +0, with v_r[i] = 0 where worker r sent
+ *         nothing; g_i = +0 when R == 0.
+ * Then the outer Sutskever-form Nesterov step with momentum mu, step alpha:
+ *   m_i     <- mu * m_i + g_i
+ *   theta_i <- theta_i - alpha * (mu * m_i + g_i)      (m_i the new momentum)
+ * Each operation is rounded to FP32 on its own (no fused multiply-add).
+ *
+ * Worker r's list is entries [0, count[r]) of idx[r] / val[r], indices of the
+ * form index_base + i; an index outside [index_base, index_base + n) is
+ * ignored.  Indices within one list are distinct.  Returns 0, or -1 if the
+ * scratch vector cannot be allocated.
+ */
+int oracle_outer_step(float *theta, float *momentum, uint64_t n, uint32_t index_base,
+                      uint32_t nlists, const uint32_t *const *idx, const float *const *val,
+                      const uint64_t *count, float mu, float alpha)
+{
+    float *g = (float *)calloc(n ? n : 1, sizeof(float)); /* all +0 */
+    if (!g)
+        return -1;
+    for (uint32_t r = 0; r < nlists; r++) {
+        for (uint64_t k = 0; k < count[r]; k++) {
+            uint32_t j = idx[r][k];
+            if (j < index_base || (uint64_t)(j - index_base) >= n)
+                continue;
+            g[j - index_base] = g[j - index_base] + val[r][k];
+        }
+    }
+    for (uint64_t i = 0; i < n; i++) {
+        float gi = g[i];
+        if (nlists > 0)
+            gi = gi / (float)nlists;
+        float m = mu * momentum[i];
+        m = m + gi;
+        momentum[i] = m;
+        float t = mu * m;
+        t = t + gi;
+        float step = alpha * t;
+        theta[i] = theta[i] - step;
+    }
+    free(g);
+    return 0;
 }
