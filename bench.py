@@ -11,8 +11,8 @@ pass.  That step is the headline.
 
 Also measured, outside the headline: the unfused form (encode, then the
 standalone scatter apply of the patch into the inference copy) and the
-PULSELoCo error-feedback sparsification over the 7B-shaped set (10 rounds,
-fixed threshold).  All inputs are generated on the GPU before timing and stay
+PULSELoCo rounds over the 7B-shaped set (10 rounds, fixed threshold): the
+error-feedback sparsification and the outer step that consumes its patch.  All inputs are generated on the GPU before timing and stay
 resident in HBM.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
@@ -298,7 +298,9 @@ def main():
 
 
 def loco_leg(args, device, stream):
-    """PULSELoCo sparsification with error feedback over the 7B-shaped set, fixed threshold."""
+    """PULSELoCo rounds over the 7B-shaped set at a fixed threshold: the error-feedback
+    sparsification (Alg. 2, one worker) and the outer step that consumes its patch
+    (SparseSync average over R = 1 worker, outer Nesterov, mu 0.9, alpha 0.7)."""
     import numpy as np
     import torch
     from paper_2602_03839_amd import pulse
@@ -308,33 +310,50 @@ def loco_leg(args, device, stream):
     sizes = [s.numel for s in specs]
     offs = np.concatenate([[0], np.cumsum(sizes)]).tolist()
     N = offs[-1]
+    T = len(sizes)
     tau = wl.loco_tau()
     delta = torch.empty(N, dtype=torch.float32, device=device)
     resid = torch.zeros(N, dtype=torch.float32, device=device)
+    theta = torch.empty(N, dtype=torch.float32, device=device).normal_(0.0, 0.02 ** 0.5)
+    mom = torch.zeros(N, dtype=torch.float32, device=device)
     cap = N // 10
     idx = torch.empty(cap, dtype=torch.int32, device=device)
     val = torch.empty(cap, dtype=torch.float32, device=device)
     count = torch.zeros(1, dtype=torch.int64, device=device)
+    seg = torch.zeros(T, dtype=torch.int64, device=device)
     ws = pulse.workspace(device)
-    parts = chunks(len(sizes), CHUNK)
-    batches = [pulse.LocoBatch([pulse.LocoTensor(delta[offs[i]:offs[i + 1]], resid[offs[i]:offs[i + 1]],
-                                                 None, 0) for i in range(a, b)]) for a, b in parts]
-    ms, dens = [], []
+    parts = chunks(T, CHUNK)
+    view = lambda b, i: b[offs[i]:offs[i + 1]]
+    batches = [pulse.LocoBatch([pulse.LocoTensor(view(delta, i), view(resid, i), None, 0)
+                                for i in range(a, b)]) for a, b in parts]
+    outer = pulse.OuterBatch([pulse.OuterTensor(view(theta, i), view(mom, i), 0) for i in range(T)])
+    lists = [pulse.SparseList(idx, val, seg, count, capacity=cap)]
+    ms, ms_outer, dens = [], [], []
     for r in range(args.loco_rounds):
-        for i in range(len(sizes)):
-            wl.loco_delta_(delta[offs[i]:offs[i + 1]], 5, r, i)
+        for i in range(T):
+            wl.loco_delta_(view(delta, i), 5, r, i)
         count.zero_()
         torch.cuda.synchronize()
         a, e = event_pair()
+        c, d = event_pair()
         a.record(stream)
-        for b in batches:
-            b(tau, idx, val, count, ws)
+        for (t0, _t1), b in zip(parts, batches):
+            b(tau, idx, val, count, ws, seg_begin=seg[t0:])
         e.record(stream)
-        e.synchronize()
+        c.record(stream)
+        outer(lists, mu=0.9, alpha=0.7)
+        d.record(stream)
+        d.synchronize()
         ms.append(a.elapsed_time(e))
+        ms_outer.append(c.elapsed_time(d))
         dens.append(int(count.item()) / N)
-    med = float(np.median(ms[1:] if len(ms) > 1 else ms))
-    log(f"[bench] loco 7b: median {med:.3f} ms/round ({12.0 * N / med / 1e6:.0f} GB/s at 12 B/param); "
+    skip = 1 if len(ms) > 1 else 0
+    med = float(np.median(ms[skip:]))
+    med_outer = float(np.median(ms_outer[skip:]))
+    nnz_mean = float(np.mean(dens[skip:])) * N
+    outer_bytes = 16.0 * N + 8.0 * nnz_mean
+    log(f"[bench] loco 7b: sparsify median {med:.3f} ms/round ({12.0 * N / med / 1e6:.0f} GB/s at 12 B/param); "
+        f"outer step median {med_outer:.3f} ms ({outer_bytes / med_outer / 1e6:.0f} GB/s); "
         f"density {dens[0]:.4%} -> {dens[-1]:.4%}")
     return {
         "params": N,
@@ -344,6 +363,14 @@ def loco_leg(args, device, stream):
         "GBps_12B_per_param": round(12.0 * N / med / 1e6, 2),
         "kernel": "loco_kernel (threshold form)",
         "density_first_last": [round(dens[0], 6), round(dens[-1], 6)],
+        "outer_step": {
+            "kernel": "outer_kernel (SparseSync average over 1 worker + outer Nesterov)",
+            "ms_per_round_median": round(med_outer, 4),
+            "GBps_algorithmic": round(outer_bytes / med_outer / 1e6, 2),
+            "hbm_frac_of_peak": round(outer_bytes / med_outer / 1e6 / HBM_PEAK_GBS, 4),
+            "bytes_per_round": outer_bytes,
+        },
+        "round_ms_median": round(med + med_outer, 4),
     }
 
 

@@ -7,6 +7,7 @@
  *   - the sparse value patch of PULSESync: encode (Sec. 4.2, Alg. 1 Encode;
  *     App. H.5, Alg. 3) and apply (Alg. 1 Decode; App. H.5, Alg. 4),
  *   - PULSELoCo's error-feedback sparsification of FP32 pseudo-gradients
+ *     and its outer step, SparseSync's average plus outer Nesterov momentum
  *     (Sec. 4.3, Alg. 2).
  *
  * Conventions for every entry point:
@@ -210,6 +211,56 @@ int pulse_loco_sparsify_batch(const pulse_loco_tensor *tensors, uint32_t ntensor
                               uint32_t *idx, float *val, uint64_t capacity, uint64_t *count,
                               uint64_t *seg_begin, void *workspace, size_t workspace_bytes,
                               void *stream);
+
+/*
+ * One worker's sparse FP32 list for the outer step, as pulse_loco_sparsify
+ * writes it: entries in strictly ascending index order within each tensor,
+ * indices of the form index_base + i.
+ *   idx, val    device arrays; entries at positions >= capacity are ignored.
+ *   seg_begin   device uint64 [ntensors]: position of each tensor's first entry.
+ *   end         device uint64: one past the last tensor's last entry (e.g.
+ *               the sparsifier's count).
+ */
+typedef struct pulse_sparse_list {
+    const uint32_t *idx;
+    const float *val;
+    uint64_t capacity;
+    const uint64_t *seg_begin;
+    const uint64_t *end;
+} pulse_sparse_list;
+
+#define PULSE_MAX_LISTS 8 /* workers per call */
+
+/* One tensor of the outer step. */
+typedef struct pulse_outer_tensor {
+    float *theta;    /* FP32 [n], in/out, 16-byte aligned */
+    float *momentum; /* FP32 [n], in/out, 16-byte aligned (zero before the first round) */
+    uint64_t n;
+    uint32_t index_base;
+} pulse_outer_tensor;
+
+/*
+ * pulse_outer_step_batch -- PULSELoCo's outer update (Sec. 4.3, Alg. 2: the
+ * SparseSync line and the two lines after it), per tensor:
+ *   g_i = (sum over workers r, in list order, of r's value at index i) / R,
+ *         a worker without an entry at i counting as zero; g = 0 if R == 0;
+ *   m_i     <- mu * m_i + g_i
+ *   theta_i <- theta_i - alpha * (mu * m_i + g_i)    (m_i the new momentum)
+ * every operation rounded to FP32 on its own (no fused multiply-add).  The
+ * paper uses mu = 0.9, alpha = 0.7.  g is formed on the fly from the sorted
+ * lists; nothing is allocated.  Entries whose index lies outside the tensor
+ * are ignored; unsorted lists give an undefined result.
+ *   tensors   HOST array [ntensors]; lists HOST array [nlists], nlists <= PULSE_MAX_LISTS.
+ */
+int pulse_outer_step_batch(const pulse_outer_tensor *tensors, uint32_t ntensors,
+                           const pulse_sparse_list *lists, uint32_t nlists,
+                           float mu, float alpha, void *stream);
+
+/* pulse_outer_step_batch for one tensor; each list's seg_begin points to the
+ * position of the tensor's first entry and `end` one past its last. */
+int pulse_outer_step(float *theta, float *momentum, uint64_t n, uint32_t index_base,
+                     const pulse_sparse_list *lists, uint32_t nlists,
+                     float mu, float alpha, void *stream);
 
 #ifdef __cplusplus
 }

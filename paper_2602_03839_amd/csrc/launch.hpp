@@ -105,7 +105,36 @@ struct ApplyParams {
   ApplyTensorDesc t[kMaxBatch];
 };
 
+constexpr int kMaxLists = 8;  // workers' lists per outer-step launch
+
+struct OuterTensorDesc {
+  float* theta;
+  float* momentum;
+  uint64_t n;
+  uint32_t index_base;
+};
+
+struct OuterListDesc {
+  const uint32_t* idx;
+  const float* val;
+  uint64_t capacity;
+  const uint64_t* seg_begin;  // device [ntensors], offset to this launch's first tensor
+  const uint64_t* end;        // device: end of this launch's last tensor's entries
+};
+
+struct OuterParams {
+  uint32_t nunits;
+  int ntensors;
+  int nlists;
+  float mu;
+  float alpha;
+  uint32_t tile_begin[kMaxBatch + 1];  // first work unit of each tensor
+  OuterTensorDesc t[kMaxBatch];
+  OuterListDesc l[kMaxLists];
+};
+
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
+static_assert(sizeof(OuterParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(ApplyParams) < 4096, "kernel argument block too large");
 
@@ -115,5 +144,7 @@ hipError_t launch_encode(EncodeParams& p, hipStream_t stream);
 hipError_t launch_loco(LocoParams& p, hipStream_t stream);
 hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);
 hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream);
+uint64_t outer_unit_elems();
+hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
 
 }  // namespace pulse

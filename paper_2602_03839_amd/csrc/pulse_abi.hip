@@ -287,4 +287,80 @@ int pulse_loco_sparsify(const float* delta, float* residual, uint64_t n, float t
                                    workspace_bytes, stream);
 }
 
+int pulse_outer_step_batch(const pulse_outer_tensor* tensors, uint32_t ntensors,
+                           const pulse_sparse_list* lists, uint32_t nlists, float mu, float alpha,
+                           void* stream) {
+  if (ntensors == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "outer: tensors is NULL");
+  if (nlists > (uint32_t)pulse::kMaxLists)
+    return fail(PULSE_EINVAL, "outer: %u lists, at most %d", nlists, pulse::kMaxLists);
+  if (nlists > 0 && !lists) return fail(PULSE_EINVAL, "outer: lists is NULL");
+  for (uint32_t r = 0; r < nlists; ++r) {
+    const pulse_sparse_list& L = lists[r];
+    if (!L.seg_begin || !L.end) return fail(PULSE_EINVAL, "outer list %u: seg_begin/end is NULL", r);
+    if (L.capacity > 0 && (!L.idx || !L.val))
+      return fail(PULSE_EINVAL, "outer list %u: idx/val NULL with capacity > 0", r);
+    if (!aligned(L.seg_begin, 8) || !aligned(L.end, 8))
+      return fail(PULSE_EALIGN, "outer list %u: counters not 8-byte aligned", r);
+    if ((L.idx && !aligned(L.idx, 4)) || (L.val && !aligned(L.val, 4)))
+      return fail(PULSE_EALIGN, "outer list %u: idx/val misaligned", r);
+  }
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_outer_tensor& d = tensors[t];
+    if (d.n == 0) continue;
+    if (!d.theta || !d.momentum) return fail(PULSE_EINVAL, "outer tensor %u: NULL theta/momentum", t);
+    if (!aligned16(d.theta) || !aligned16(d.momentum))
+      return fail(PULSE_EALIGN, "outer tensor %u: theta/momentum not 16-byte aligned", t);
+    if (int rc = check_range(d.n, d.index_base, "outer", t)) return rc;
+  }
+  const uint64_t unit = pulse::outer_unit_elems();
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::OuterParams p;
+    memset(&p, 0, sizeof p);
+    p.mu = mu;
+    p.alpha = alpha;
+    p.nlists = (int)nlists;
+    uint64_t units = 0;
+    int k = 0;
+    while (t0 + k < ntensors && k < pulse::kMaxBatch) {
+      const pulse_outer_tensor& d = tensors[t0 + k];
+      const uint64_t nu = (d.n + unit - 1) / unit;
+      if (k > 0 && units + nu > 0xFFFFFFFFull) break;
+      p.tile_begin[k] = (uint32_t)units;
+      p.t[k].theta = d.theta;
+      p.t[k].momentum = d.momentum;
+      p.t[k].n = d.n;
+      p.t[k].index_base = d.index_base;
+      units += nu;
+      ++k;
+    }
+    p.tile_begin[k] = (uint32_t)units;
+    p.ntensors = k;
+    p.nunits = (uint32_t)units;
+    for (uint32_t r = 0; r < nlists; ++r) {
+      p.l[r].idx = lists[r].idx;
+      p.l[r].val = lists[r].val;
+      p.l[r].capacity = lists[r].capacity;
+      p.l[r].seg_begin = lists[r].seg_begin + t0;
+      p.l[r].end = (t0 + k < ntensors) ? lists[r].seg_begin + t0 + k : lists[r].end;
+    }
+    if (int rc = hip_status(pulse::launch_outer(p, (hipStream_t)stream), "outer launch")) return rc;
+    t0 += k;
+  }
+  return ok();
+}
+
+int pulse_outer_step(float* theta, float* momentum, uint64_t n, uint32_t index_base,
+                     const pulse_sparse_list* lists, uint32_t nlists, float mu, float alpha,
+                     void* stream) {
+  if (n == 0) return ok();
+  pulse_outer_tensor d;
+  d.theta = theta;
+  d.momentum = momentum;
+  d.n = n;
+  d.index_base = index_base;
+  return pulse_outer_step_batch(&d, 1, lists, nlists, mu, alpha, stream);
+}
+
 }  // extern "C"

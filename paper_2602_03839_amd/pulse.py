@@ -51,9 +51,22 @@ class _LocoTensor(ctypes.Structure):
                 ("index_base", ctypes.c_uint32)]
 
 
+class _OuterTensor(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_void_p), ("momentum", ctypes.c_void_p),
+                ("n", ctypes.c_uint64), ("index_base", ctypes.c_uint32)]
+
+
+class _SparseList(ctypes.Structure):
+    _fields_ = [("idx", ctypes.c_void_p), ("val", ctypes.c_void_p), ("capacity", ctypes.c_uint64),
+                ("seg_begin", ctypes.c_void_p), ("end", ctypes.c_void_p)]
+
+
+MAX_LISTS = 8  # PULSE_MAX_LISTS
+
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
            "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
-           "pulse_loco_sparsify", "pulse_loco_sparsify_batch")
+           "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
+           "pulse_outer_step", "pulse_outer_step_batch")
 
 
 def lib():
@@ -80,6 +93,8 @@ def lib():
             L.pulse_apply_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, vp]
             L.pulse_loco_sparsify.argtypes = [vp, vp, u64, f32, vp, vp, vp, u64, vp, u32, vp, sz, vp]
             L.pulse_loco_sparsify_batch.argtypes = [vp, u32, f32, vp, vp, u64, vp, vp, vp, sz, vp]
+            L.pulse_outer_step.argtypes = [vp, vp, u64, u32, vp, u32, f32, f32, vp]
+            L.pulse_outer_step_batch.argtypes = [vp, u32, vp, u32, f32, f32, vp]
             for name in EXPORTS[3:]:
                 getattr(L, name).restype = i32
             _lib = L
@@ -249,3 +264,68 @@ class LocoBatch:
         _check(lib().pulse_loco_sparsify_batch(self.arr, self.n, float(tau), _p(idx), _p(val),
                                                cap, _p(count), _p(seg_begin), _p(ws), ws.numel(),
                                                _stream(stream)), "pulse_loco_sparsify_batch")
+
+
+@dataclass
+class SparseList:
+    """One worker's sorted FP32 list (as the sparsifier writes it) for the outer step.
+
+    ``seg_begin``: device int64 [ntensors] (the position of each tensor's first
+    entry); ``end``: device int64 [1] one past the last tensor's last entry.
+    """
+    idx: torch.Tensor
+    val: torch.Tensor
+    seg_begin: torch.Tensor
+    end: torch.Tensor
+    capacity: Optional[int] = None
+
+
+def _lists(lists: Sequence[SparseList]):
+    if len(lists) > MAX_LISTS:
+        raise PulseError(f"at most {MAX_LISTS} lists per call")
+    arr = (_SparseList * max(1, len(lists)))()
+    for r, L in enumerate(lists):
+        assert L.idx.element_size() == 4 and L.val.dtype == torch.float32
+        assert L.seg_begin.element_size() == 8 and L.end.element_size() == 8
+        arr[r] = _SparseList(_p(L.idx), _p(L.val), _capacity(L.idx, L.val, L.capacity),
+                             _p(L.seg_begin), _p(L.end))
+    return arr
+
+
+def outer_step(theta: torch.Tensor, momentum: torch.Tensor, lists: Sequence[SparseList],
+               mu: float = 0.9, alpha: float = 0.7, index_base: int = 0, stream=None) -> None:
+    """PULSELoCo's outer update of one tensor (pulse_outer_step)."""
+    assert theta.dtype == torch.float32 and momentum.dtype == torch.float32
+    assert theta.numel() == momentum.numel()
+    arr = _lists(lists)
+    _check(lib().pulse_outer_step(_p(theta), _p(momentum), theta.numel(), index_base, arr,
+                                  len(lists), float(mu), float(alpha), _stream(stream)),
+           "pulse_outer_step")
+
+
+@dataclass
+class OuterTensor:
+    theta: torch.Tensor
+    momentum: torch.Tensor
+    index_base: int = 0
+
+
+class OuterBatch:
+    """Descriptor array for pulse_outer_step_batch, built once and reused."""
+
+    def __init__(self, tensors: Sequence[OuterTensor]):
+        self.n = len(tensors)
+        arr = (_OuterTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert t.theta.dtype == torch.float32 and t.momentum.dtype == torch.float32
+            assert t.theta.numel() == t.momentum.numel()
+            arr[i] = _OuterTensor(_p(t.theta), _p(t.momentum), t.theta.numel(), t.index_base)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, lists: Sequence[SparseList], mu: float = 0.9, alpha: float = 0.7,
+                 stream=None):
+        arr = _lists(lists)
+        _check(lib().pulse_outer_step_batch(self.arr, self.n, arr, len(lists), float(mu),
+                                            float(alpha), _stream(stream)),
+               "pulse_outer_step_batch")

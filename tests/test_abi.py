@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name
@@ -104,3 +104,24 @@ def test_cast_validation(L):
     assert L.pulse_cast_bf16(None, None, 0, None) == OK
     assert L.pulse_cast_bf16(None, A, 5, None) == EINVAL
     assert L.pulse_cast_bf16(A + 4, A, 5, None) == EALIGN
+
+
+def test_outer_step_validation(L):
+    import ctypes
+    step = L.pulse_outer_step
+    lst = (pulse._SparseList * 9)()
+    for r in range(9):
+        lst[r] = pulse._SparseList(A, A, 10, A, A)
+    assert step(None, None, 0, 0, None, 0, 0.9, 0.7, None) == OK  # n == 0
+    assert step(None, A, 10, 0, lst, 1, 0.9, 0.7, None) == EINVAL
+    assert step(A + 4, A, 10, 0, lst, 1, 0.9, 0.7, None) == EALIGN
+    assert step(A, A, 10, 0, lst, 9, 0.9, 0.7, None) == EINVAL  # more than PULSE_MAX_LISTS
+    assert b"lists" in L.pulse_last_error()
+    assert step(A, A, 10, (1 << 32) - 5, lst, 1, 0.9, 0.7, None) == ERANGE
+    bad = (pulse._SparseList * 1)()
+    bad[0] = pulse._SparseList(A, A, 10, None, A)
+    assert step(A, A, 10, 0, bad, 1, 0.9, 0.7, None) == EINVAL
+    bad[0] = pulse._SparseList(None, A, 10, A, A)
+    assert step(A, A, 10, 0, bad, 1, 0.9, 0.7, None) == EINVAL
+    bad[0] = pulse._SparseList(A + 2, A, 10, A, A)
+    assert step(A, A, 10, 0, bad, 1, 0.9, 0.7, None) == EALIGN
