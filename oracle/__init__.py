@@ -14,6 +14,8 @@ and marshals numpy arrays into it with ctypes.
     apply(dst, idx, val, ...)        Sec. 4.2 Alg. 1 Decode, App. H.5 Alg. 4
     loco(delta, residual, tau, ...)  Sec. 4.3 Alg. 2 (s = Delta + e, selection, error feedback)
     outer_step(theta, m, lists, ...) Sec. 4.3 Alg. 2 (SparseSync average, outer Nesterov step)
+    varint_encode(idx) / varint_decode(stream)
+                                     App. H.2 / App. F.3 delta-varint index stream
 """
 from __future__ import annotations
 
@@ -62,6 +64,10 @@ def _load():
             lib.oracle_loco.restype = u64
             lib.oracle_outer_step.argtypes = [vp, vp, u64, u32, u32, vp, vp, vp, f32, f32]
             lib.oracle_outer_step.restype = ctypes.c_int
+            lib.oracle_varint_encode.argtypes = [vp, u64, vp, u64]
+            lib.oracle_varint_encode.restype = u64
+            lib.oracle_varint_decode.argtypes = [vp, u64, vp, u64]
+            lib.oracle_varint_decode.restype = ctypes.c_int64
             _lib = lib
     return _lib
 
@@ -203,3 +209,25 @@ def outer_step(theta: np.ndarray, momentum: np.ndarray, lists, mu: float = 0.9,
                                    float(np.float32(mu)), float(np.float32(alpha)))
     if rc != 0:
         raise MemoryError("oracle_outer_step could not allocate its scratch vector")
+
+
+def varint_encode(idx) -> np.ndarray:
+    """Delta-varint byte stream (uint8) of one sorted index list."""
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    L = _load()
+    n = int(L.oracle_varint_encode(_ptr(idx), idx.size, None, 0))
+    out = np.zeros(max(n, 1), dtype=np.uint8)
+    assert int(L.oracle_varint_encode(_ptr(idx), idx.size, _ptr(out), n)) == n
+    return out[:n]
+
+
+def varint_decode(stream) -> np.ndarray:
+    """Indices (uint32) of a delta-varint byte stream."""
+    stream = np.ascontiguousarray(stream, dtype=np.uint8)
+    L = _load()
+    n = int(L.oracle_varint_decode(_ptr(stream), stream.size, None, 0))
+    if n < 0:
+        raise ValueError("the stream ends inside a number")
+    out = np.zeros(max(n, 1), dtype=np.uint32)
+    L.oracle_varint_decode(_ptr(stream), stream.size, _ptr(out), n)
+    return out[:n]

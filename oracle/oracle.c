@@ -22,6 +22,9 @@
  *   oracle_outer_step    Sec. 4.3, Alg. 2: SparseSync's union-average of the
  *                        workers' selected values, then the outer Nesterov step
  *                        m <- mu m + g, theta <- theta - alpha (mu m + g).
+ *   oracle_varint_encode App. H.2 (index encoding: sorted, first index as-is,
+ *   oracle_varint_decode then differences) and App. F.3 (PULSELoCo's sparse
+ *                        stream: delta-encoded, varint-packed indices).
  *
  * Readings where the paper is silent (all listed in the design notes):
  *   - A NaN input casts to a quiet NaN that keeps the sign and the leading
@@ -236,4 +239,66 @@ int oracle_outer_step(float *theta, float *momentum, uint64_t n, uint32_t index_
     }
     free(g);
     return 0;
+}
+
+/*
+ * Index stream of one sorted list (App. H.2 "Index Encoding"; App. F.3 "Sparse
+ * stream format": indices delta-encoded and varint-packed).
+ *
+ * The first index is stored as it is and every later one as its difference
+ * from the previous index, d_0 = idx[0], d_k = idx[k] - idx[k-1] (indices
+ * strictly ascending, so d_k >= 1 for k >= 1).  Each d_k is written as an
+ * unsigned varint: 7-bit groups, least significant first, every byte but the
+ * last of a number carrying 0x80.
+ *
+ * oracle_varint_encode writes bytes [0, out_capacity) of the stream and returns
+ * its full length (the caller detects overflow as length > out_capacity).
+ * oracle_varint_decode reads `nbytes` bytes and writes up to `max_out`
+ * indices; it returns the number of indices in the stream, or -1 if the stream
+ * ends inside a number.
+ */
+uint64_t oracle_varint_encode(const uint32_t *idx, uint64_t count, uint8_t *out,
+                              uint64_t out_capacity)
+{
+    uint64_t pos = 0;
+    for (uint64_t k = 0; k < count; k++) {
+        uint32_t d = k == 0 ? idx[0] : idx[k] - idx[k - 1];
+        for (;;) {
+            uint8_t byte = (uint8_t)(d & 0x7F);
+            d >>= 7;
+            if (d != 0)
+                byte |= 0x80;
+            if (pos < out_capacity)
+                out[pos] = byte;
+            pos++;
+            if (d == 0)
+                break;
+        }
+    }
+    return pos;
+}
+
+int64_t oracle_varint_decode(const uint8_t *in, uint64_t nbytes, uint32_t *out, uint64_t max_out)
+{
+    uint64_t count = 0, pos = 0;
+    uint32_t prev = 0;
+    while (pos < nbytes) {
+        uint64_t d = 0;
+        int shift = 0;
+        for (;;) {
+            if (pos >= nbytes)
+                return -1;
+            uint8_t byte = in[pos++];
+            d |= (uint64_t)(byte & 0x7F) << shift;
+            shift += 7;
+            if (!(byte & 0x80))
+                break;
+        }
+        uint32_t v = count == 0 ? (uint32_t)d : prev + (uint32_t)d;
+        if (count < max_out)
+            out[count] = v;
+        prev = v;
+        count++;
+    }
+    return (int64_t)count;
 }
