@@ -124,6 +124,7 @@ def main():
                          "the snapshot (mirror), or one 2-byte write per change (sparse)")
     ap.add_argument("--no-loco", action="store_true", help="skip the PULSELoCo leg")
     ap.add_argument("--loco-rounds", type=int, default=10)
+    ap.add_argument("--no-varint", action="store_true", help="skip the wire-format (delta-varint) leg")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -237,11 +238,14 @@ def main():
     assert torch.equal(check, ps.R[: check.numel()]), "inference copy differs from bf16(w')"
     del check, idx_head, val_head
 
+    # ---- the patch's wire format: delta-varint index stream, encoded and decoded
+    varint = None if args.no_varint else varint_leg(args, ps, idx, count, seg, sent, ws, stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(ps, args.cpu_sample, idx, val, seg, nnz, cap)
 
-    from paper_2602_03839_amd.traffic import read_summary
+    from paper_2602_03839_amd.traffic import read_summary  # noqa: E402
     traffic = read_summary(TRAFFIC_FILE) if args.workload == "32b" else None
     out = {
         "metric": METRIC,
@@ -281,6 +285,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "legs": {
+            "varint_patch": varint,
             "encode_then_apply": {
                 "ms_per_step": round(unf_ms, 4),
                 "GBps_scanned": round(6.0 * ps.N / (unf_ms * 1e-3) / 1e9, 2),
@@ -295,6 +300,60 @@ def main():
     if not args.no_loco:
         out["legs"]["loco_7b"] = loco_leg(args, device, stream)
     print(json.dumps(out), flush=True)
+
+
+def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
+    """The patch's index stream in the paper's wire format (App. H.2 / F.3): the
+    per-tensor segments of the last encode pass, delta-varint encoded and decoded."""
+    import numpy as np
+    import torch
+    from paper_2602_03839_amd import pulse
+
+    # App. F.3 bound per segment: nnz + (N - nnz)/127 bytes; N = tensor length
+    segs = seg.cpu().numpy().tolist() + [sent]
+    bound = sum((segs[i + 1] - segs[i]) + (n - (segs[i + 1] - segs[i])) // 127
+                for i, n in enumerate(ps.sizes))
+    out = torch.empty(bound + 64, dtype=torch.uint8, device=idx.device)
+    total = torch.zeros(1, dtype=torch.int64, device=idx.device)
+    back = torch.empty(sent + 1, dtype=torch.int32, device=idx.device)
+    got = torch.zeros(1, dtype=torch.int64, device=idx.device)
+    end = torch.tensor([sent], dtype=torch.int64, device=idx.device)
+    reps = max(3, args.steps)
+    te, td = [], []
+    for r in range(reps + 1):
+        a, b = event_pair()
+        c, d = event_pair()
+        a.record(stream)
+        pulse.varint_encode(idx, end, out, total, ws, seg_begin=seg, capacity=sent)
+        b.record(stream)
+        c.record(stream)
+        pulse.varint_decode(out, total, back, got, ws, seg_begin=seg)
+        d.record(stream)
+        d.synchronize()
+        if r:
+            te.append(a.elapsed_time(b))
+            td.append(c.elapsed_time(d))
+    nbytes = int(total.item())
+    assert nbytes <= bound, (nbytes, bound)
+    assert int(got.item()) == sent
+    assert torch.equal(back[:sent], idx[:sent]), "varint round trip differs from the patch"
+    enc_ms, dec_ms = float(np.median(te)), float(np.median(td))
+    enc_bytes = 4.0 * sent + nbytes          # indices read, stream written
+    dec_bytes = nbytes + 4.0 * sent * 3      # stream read, differences written, re-read, indices written
+    log(f"[bench] varint: {sent:,} indices -> {nbytes / 1e6:.1f} MB ({nbytes / sent:.3f} B/index, "
+        f"bound {bound / 1e6:.1f} MB); encode {enc_ms:.3f} ms, decode {dec_ms:.3f} ms")
+    del out, back
+    return {
+        "entries": sent,
+        "stream_bytes": nbytes,
+        "bytes_per_index": round(nbytes / max(sent, 1), 4),
+        "paper_bound_bytes": bound,
+        "encode_ms": round(enc_ms, 4),
+        "decode_ms": round(dec_ms, 4),
+        "encode_GBps_algorithmic": round(enc_bytes / enc_ms / 1e6, 2),
+        "decode_GBps_algorithmic": round(dec_bytes / dec_ms / 1e6, 2),
+        "kernels": "varint_encode_kernel; varint_gaps_kernel + varint_sums_kernel",
+    }
 
 
 def loco_leg(args, device, stream):

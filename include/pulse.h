@@ -262,6 +262,53 @@ int pulse_outer_step(float *theta, float *momentum, uint64_t n, uint32_t index_b
                      const pulse_sparse_list *lists, uint32_t nlists,
                      float mu, float alpha, void *stream);
 
+/*
+ * pulse_varint_encode -- the delta-varint index stream of a sorted patch
+ * (App. H.2 "Index Encoding": sort, first index as it is, then differences;
+ * App. F.3 "Sparse stream format": indices delta-encoded and varint-packed).
+ * Per segment (one per tensor) the first index is written as it is and every
+ * later one as its difference from the previous, each as an unsigned varint
+ * (7-bit groups, least significant first, 0x80 on every byte but the last of
+ * a number).  Segments follow each other in order; values are not part of the
+ * stream (they stay in the patch's value array).
+ *   idx         device uint32 [capacity], indices ascending within each segment.
+ *   end         device uint64: the number of entries (e.g. encode's count);
+ *               only entries below min(*end, capacity) are read.
+ *   seg_begin   NULL (one segment) or device uint64 [nseg], non-decreasing:
+ *               the entry where each segment starts (encode's seg_begin).
+ *               Entry 0 always starts a segment.
+ *   out         device bytes, `out_capacity` of them; bytes past it are not
+ *               written, *total_bytes still receives the full length.
+ *   seg_bytes   NULL or device uint64 [nseg]: the byte where each segment's
+ *               numbers start (an empty segment: where the next one starts).
+ *   total_bytes device uint64: the stream's length.
+ *   workspace   the encode/sparsify workspace (same rules; may be shared on
+ *               one stream).
+ * The stream is at most nnz + (N - nnz)/127 bytes for nnz entries out of N
+ * positions (App. F.3 accounting).
+ */
+int pulse_varint_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end,
+                        const uint64_t *seg_begin, uint32_t nseg,
+                        uint8_t *out, uint64_t out_capacity,
+                        uint64_t *seg_bytes, uint64_t *total_bytes,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * pulse_varint_decode -- indices back from a delta-varint stream (Alg. 1
+ * Decode's DeltaDecode step).
+ *   in          device bytes [in_capacity]; *nbytes (device uint64) of them
+ *               form the stream.  A stream cut inside a number drops it.
+ *   seg_begin   NULL (one segment) or device uint64 [nseg]: the entry where
+ *               each segment starts (container metadata sent with the stream).
+ *   idx         device uint32 [capacity] receiving the indices; entries past
+ *               capacity are not written.
+ *   count       device uint64: the number of entries in the stream.
+ */
+int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t *nbytes,
+                        const uint64_t *seg_begin, uint32_t nseg,
+                        uint32_t *idx, uint64_t capacity, uint64_t *count,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -133,6 +133,34 @@ struct OuterParams {
   OuterListDesc l[kMaxLists];
 };
 
+struct VarintEncParams {
+  uint64_t* ws;
+  const uint32_t* idx;
+  uint64_t capacity;           // entries readable in idx
+  const uint64_t* end;         // device: entries in the list
+  const uint64_t* seg_begin;   // device [nseg], may be null (one segment)
+  uint32_t nseg;
+  uint8_t* out;
+  uint64_t out_capacity;
+  uint64_t* seg_bytes;         // device [nseg], may be null
+  uint64_t* total;             // device
+  uint32_t ntiles;
+};
+
+struct VarintDecParams {
+  uint64_t* ws;
+  const uint8_t* in;
+  uint64_t in_capacity;
+  const uint64_t* nbytes;      // device: bytes in the stream
+  const uint64_t* seg_begin;   // device [nseg], may be null (one segment)
+  uint32_t nseg;
+  uint32_t* idx;
+  uint64_t capacity;           // entries writable in idx
+  uint64_t* count;             // device: entries decoded
+  uint32_t ntiles;             // byte tiles
+  uint32_t ntiles2;            // entry tiles
+};
+
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(OuterParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
@@ -145,6 +173,10 @@ hipError_t launch_loco(LocoParams& p, hipStream_t stream);
 hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);
 hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream);
 uint64_t outer_unit_elems();
+uint32_t varint_entry_tile();
+uint32_t varint_byte_tile();
+hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
+hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
 
 }  // namespace pulse

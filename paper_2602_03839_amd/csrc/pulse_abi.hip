@@ -363,4 +363,68 @@ int pulse_outer_step(float* theta, float* momentum, uint64_t n, uint32_t index_b
   return pulse_outer_step_batch(&d, 1, lists, nlists, mu, alpha, stream);
 }
 
+int pulse_varint_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end,
+                        const uint64_t* seg_begin, uint32_t nseg, uint8_t* out,
+                        uint64_t out_capacity, uint64_t* seg_bytes, uint64_t* total_bytes,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (!end || !total_bytes) return fail(PULSE_EINVAL, "varint encode: end/total_bytes is NULL");
+  if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "varint encode: idx is NULL");
+  if (out_capacity > 0 && !out) return fail(PULSE_EINVAL, "varint encode: out is NULL");
+  if (nseg > 0 && !seg_begin) return fail(PULSE_EINVAL, "varint encode: seg_begin is NULL");
+  if (!aligned(end, 8) || !aligned(total_bytes, 8) || (seg_begin && !aligned(seg_begin, 8)) ||
+      (seg_bytes && !aligned(seg_bytes, 8)))
+    return fail(PULSE_EALIGN, "varint encode: counters not 8-byte aligned");
+  if (idx && !aligned(idx, 4)) return fail(PULSE_EALIGN, "varint encode: idx misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  const uint64_t tile = pulse::varint_entry_tile();
+  const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
+  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "varint encode: capacity too large");
+  pulse::VarintEncParams p;
+  memset(&p, 0, sizeof p);
+  p.ws = (uint64_t*)workspace;
+  p.idx = idx;
+  p.capacity = capacity;
+  p.end = end;
+  p.seg_begin = nseg ? seg_begin : nullptr;
+  p.nseg = nseg;
+  p.out = out;
+  p.out_capacity = out_capacity;
+  p.seg_bytes = nseg ? seg_bytes : nullptr;
+  p.total = total_bytes;
+  p.ntiles = (uint32_t)nt;
+  return hip_status(pulse::launch_varint_encode(p, (hipStream_t)stream), "varint encode launch");
+}
+
+int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t* nbytes,
+                        const uint64_t* seg_begin, uint32_t nseg, uint32_t* idx, uint64_t capacity,
+                        uint64_t* count, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!nbytes || !count) return fail(PULSE_EINVAL, "varint decode: nbytes/count is NULL");
+  if (in_capacity > 0 && !in) return fail(PULSE_EINVAL, "varint decode: in is NULL");
+  if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "varint decode: idx is NULL");
+  if (nseg > 0 && !seg_begin) return fail(PULSE_EINVAL, "varint decode: seg_begin is NULL");
+  if (!aligned(nbytes, 8) || !aligned(count, 8) || (seg_begin && !aligned(seg_begin, 8)))
+    return fail(PULSE_EALIGN, "varint decode: counters not 8-byte aligned");
+  if (idx && !aligned(idx, 4)) return fail(PULSE_EALIGN, "varint decode: idx misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  const uint64_t bt = pulse::varint_byte_tile(), et = pulse::varint_entry_tile();
+  const uint64_t nt = in_capacity == 0 ? 1 : (in_capacity + bt - 1) / bt;
+  const uint64_t nt2 = capacity == 0 ? 1 : (capacity + et - 1) / et;
+  if (nt > pulse::kMaxTilesPerLaunch || nt2 > pulse::kMaxTilesPerLaunch)
+    return fail(PULSE_EINVAL, "varint decode: capacity too large");
+  pulse::VarintDecParams p;
+  memset(&p, 0, sizeof p);
+  p.ws = (uint64_t*)workspace;
+  p.in = in;
+  p.in_capacity = in_capacity;
+  p.nbytes = nbytes;
+  p.seg_begin = nseg ? seg_begin : nullptr;
+  p.nseg = nseg;
+  p.idx = idx;
+  p.capacity = capacity;
+  p.count = count;
+  p.ntiles = (uint32_t)nt;
+  p.ntiles2 = (uint32_t)nt2;
+  return hip_status(pulse::launch_varint_decode(p, (hipStream_t)stream), "varint decode launch");
+}
+
 }  // extern "C"

@@ -1,0 +1,437 @@
+// varint.hip -- the delta-varint index stream of a sorted patch on gfx950
+// (App. H.2 "Index Encoding": first index as it is, then differences; App. F.3
+// "Sparse stream format": delta-encoded, varint-packed indices).  Each number
+// is an unsigned varint: 7-bit groups, least significant first, every byte but
+// the last carrying 0x80.  A patch of several tensors is a list of segments
+// (one per tensor); every segment restarts with its first index as it is.
+//
+// All three kernels are persistent chained scans over tiles drawn by ticket,
+// with the same workspace ticket counter and status ring (and the same
+// decoupled look-back) as encode and sparsify, so they may share a workspace
+// with them on one stream:
+//   varint_encode_kernel   entries -> bytes: per-entry varint lengths, their
+//                          ordered exclusive sum gives each entry's bytes.
+//   varint_gaps_kernel     bytes -> differences at entry positions: the
+//                          ordered count of terminating bytes numbers the
+//                          entries.
+//   varint_sums_kernel     differences -> indices: a segmented running sum,
+//                          restarting at every segment's first entry; a tile
+//                          that holds a restart knows its inclusive sum by
+//                          itself and publishes it as a prefix at once.
+// Each tile is staged in LDS so global loads and stores stay contiguous.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace pulse {
+
+namespace {
+
+constexpr int kVT = 256;                  // threads per block
+constexpr int kVPer = 16;                 // entries per thread
+constexpr uint32_t kVTile = kVT * kVPer;  // 4096 entries per tile
+constexpr uint32_t kBTile = 8192;         // bytes per decode tile (32 per thread)
+constexpr int kVWaves = kVT / 64;
+
+__device__ __forceinline__ uint32_t varint_len(uint32_t d) {
+  return d < (1u << 7) ? 1u : d < (1u << 14) ? 2u : d < (1u << 21) ? 3u : d < (1u << 28) ? 4u : 5u;
+}
+
+// Block-wide exclusive sum of one value per thread (any order-preserving
+// block of kVT threads); *total receives the block's sum.
+__device__ uint32_t block_excl_sum(uint32_t v, uint32_t* s_w, uint32_t* total) {
+  const int lane = lane_id(), wid = threadIdx.x >> 6;
+  const uint32_t incl = wave_incl_scan(v);
+  if (lane == 63) s_w[wid] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kVWaves; ++w) {
+    const uint32_t x = s_w[w];
+    if (w < wid) before += x;
+    all += x;
+  }
+  __syncthreads();  // s_w may be reused
+  *total = all;
+  return before + incl - v;
+}
+
+// First position in [0, n) with a[pos] >= key (a non-decreasing), whole wave.
+__device__ uint32_t wave_lower_bound64(const uint64_t* a, uint32_t n, uint64_t key) {
+  const int lane = lane_id();
+  uint32_t lo = 0, hi = n;
+  while (hi - lo > 64) {
+    const uint32_t span = hi - lo;
+    const uint32_t p = lo + (uint32_t)((uint64_t)span * (uint32_t)(lane + 1) / 65u);
+    const uint64_t ge = __ballot(a[p] >= key);
+    if (ge == 0) {
+      lo = (uint32_t)__shfl((int)p, 63, 64) + 1;
+    } else {
+      const int f = __builtin_ctzll(ge);
+      const uint32_t pf = (uint32_t)__shfl((int)p, f, 64);
+      lo = f > 0 ? (uint32_t)__shfl((int)p, f - 1, 64) + 1 : lo;
+      hi = pf;
+    }
+  }
+  const uint32_t q = lo + (uint32_t)lane;
+  const uint64_t ge = __ballot(q < hi && a[q] >= key);
+  return ge == 0 ? hi : lo + (uint32_t)__builtin_ctzll(ge);
+}
+
+// Persistent ticket loop shared by the three kernels.  fn(tk) processes tile
+// tk.tile; every thread of the block calls it.  One tile per ticket: a block
+// publishes a tile's aggregate only when it reaches the tile, so with several
+// tiles per ticket the first tile of the next block's draw would wait for
+// this block's later tiles, each behind its own look-back -- a chain through
+// every block.  (The encode and sparsify kernels draw four at a time because
+// they publish aggregates iterations ahead of resolving.)
+template <typename Fn>
+__device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
+  __shared__ uint64_t s_tk;
+  uint64_t g0 = 0;  // thread 0 only
+  for (;;) {
+    if (threadIdx.x == 0) {
+      const uint64_t c = draw_ticket(ws);
+      g0 = c >> kTicketBits;
+      s_tk = make_ticket(g0, (uint32_t)(c & kTicketMask), ntiles);
+    }
+    __syncthreads();
+    const Ticket tk = decode_ticket(s_tk);
+    __syncthreads();  // s_tk is read by every thread before it is overwritten
+    if (tk.tile >= ntiles) break;
+    fn(tk);
+  }
+  if (threadIdx.x == 0) finish_launch(ws, g0, ntiles, gridDim.x);
+}
+
+// Exclusive prefix of the tile's `agg` over the earlier tiles of the launch
+// (block-uniform result).  With `restart`, the tile's inclusive value is
+// `incl_known` whatever came before (a segment starts in it), published as a
+// prefix at once; the tile still looks back for its own entries before the
+// restart.
+__device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg, bool restart,
+                                    uint64_t incl_known, uint64_t* s_b) {
+  if (threadIdx.x < 64) {
+    const int lane = lane_id();
+    uint64_t excl = 0;
+    if (tk.tile == 0) {
+      if (lane == 0) status_publish(ws, tk.seq, kFlagPrefix, restart ? incl_known : agg);
+    } else {
+      if (lane == 0)
+        status_publish(ws, tk.seq, restart ? kFlagPrefix : kFlagAggregate, restart ? incl_known : agg);
+      LookWindow<1> win;
+      look_back_issue<1>(ws, tk, (int64_t)tk.tile - 1, win);
+      excl = look_back<1>(ws, tk, win);
+      if (lane == 0 && !restart) status_publish(ws, tk.seq, kFlagPrefix, excl + agg);
+    }
+    if (lane == 0) *s_b = excl;
+  }
+  __syncthreads();
+  const uint64_t r = *s_b;
+  __syncthreads();  // s_b may be rewritten by the next tile
+  return r;
+}
+
+// Marks the segment starts that fall in [k0, k1) in the LDS bitmap (bit
+// i - k0) and returns (through LDS) the range [lo, hi) of segments starting
+// there.  Entry 0 always starts a segment.  Wave 0 only.
+__device__ void mark_starts(const uint64_t* seg_begin, uint32_t nseg, uint64_t k0, uint64_t k1,
+                            uint32_t* s_flags, uint32_t* s_range) {
+  const int lane = lane_id();
+  uint32_t lo = 0, hi = 0;
+  if (seg_begin && nseg > 0) {
+    lo = wave_lower_bound64(seg_begin, nseg, k0);
+    hi = lo;
+    for (uint32_t s = lo + (uint32_t)lane;; s += 64) {
+      const bool in = s < nseg && seg_begin[s] < k1;
+      if (in) {
+        const uint32_t i = (uint32_t)(seg_begin[s] - k0);
+        atomicOr(&s_flags[i >> 5], 1u << (i & 31));
+      }
+      const uint64_t b = __ballot(in);
+      hi += (uint32_t)__builtin_popcountll(b);
+      if (b != ~0ull) break;
+    }
+  }
+  if (lane == 0) {
+    if (k0 == 0 && k1 > 0) atomicOr(&s_flags[0], 1u);
+    s_range[0] = lo;
+    s_range[1] = hi;
+  }
+}
+
+__device__ __forceinline__ bool flag_at(const uint32_t* s_flags, uint32_t i) {
+  return (s_flags[i >> 5] >> (i & 31)) & 1u;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- encode
+
+__global__ __launch_bounds__(kVT) void varint_encode_kernel(VarintEncParams p) {
+  __shared__ uint32_t s_idx[kVTile + 1];   // [0] = the entry before the tile
+  __shared__ uint16_t s_off[kVTile];       // byte offset of each entry in the tile
+  __shared__ uint8_t s_bytes[kVTile * 5];
+  __shared__ uint32_t s_flags[kVTile / 32];
+  __shared__ uint32_t s_w[kVWaves];
+  __shared__ uint32_t s_range[2];
+  __shared__ uint64_t s_b;
+  const int tid = threadIdx.x;
+  const uint64_t end = *p.end;
+  const uint64_t nent = end < p.capacity ? end : p.capacity;
+  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t k0 = (uint64_t)tk.tile * kVTile;
+    const uint64_t k1 = k0 + kVTile < nent ? k0 + kVTile : (k0 < nent ? nent : k0);
+    const uint32_t cnt = (uint32_t)(k1 - k0);
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_flags[w] = 0;
+    // entries, staged contiguously; the entry before the tile as well
+    for (uint32_t i = tid; i < cnt; i += kVT) s_idx[1 + i] = p.idx[k0 + i];
+    if (tid == 0) s_idx[0] = k0 > 0 && k0 <= nent ? p.idx[k0 - 1] : 0u;
+    __syncthreads();
+    if (tid < 64) mark_starts(p.seg_begin, p.nseg, k0, k1, s_flags, s_range);
+    __syncthreads();
+    // this thread's entries t*16 .. t*16+15: lengths and local offsets
+    uint32_t d[kVPer], len[kVPer], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kVPer + j;
+      d[j] = 0;
+      len[j] = 0;
+      if (i < cnt) {
+        const uint32_t cur = s_idx[1 + i];
+        d[j] = flag_at(s_flags, i) ? cur : cur - s_idx[i];
+        len[j] = varint_len(d[j]);
+      }
+      sum += len[j];
+    }
+    uint32_t agg32;
+    const uint32_t texcl = block_excl_sum(sum, s_w, &agg32);
+    const uint64_t agg = agg32;
+    const uint64_t excl = chain_exclusive(p.ws, tk, agg, false, 0, &s_b);
+    // bytes into LDS
+    uint32_t o = texcl;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kVPer + j;
+      if (i < cnt) {
+        s_off[i] = (uint16_t)o;
+        uint32_t v = d[j];
+        for (uint32_t q = 0; q < len[j]; ++q) {
+          s_bytes[o + q] = (uint8_t)((v & 0x7Fu) | (q + 1 < len[j] ? 0x80u : 0u));
+          v >>= 7;
+        }
+        o += len[j];
+      }
+    }
+    __syncthreads();
+    // contiguous copy-out (consecutive threads, consecutive bytes)
+    for (uint32_t b = tid; b < agg32; b += kVT) {
+      const uint64_t pos = excl + b;
+      if (pos < p.out_capacity) p.out[pos] = s_bytes[b];
+    }
+    // byte offset of each segment that starts in this tile
+    if (p.seg_bytes && tid < 64) {
+      for (uint32_t s = s_range[0] + (uint32_t)lane_id(); s < s_range[1]; s += 64)
+        p.seg_bytes[s] = excl + s_off[(uint32_t)(p.seg_begin[s] - k0)];
+    }
+    // the tile holding the last entry (tile 0 for an empty list) ends the stream
+    const bool last = nent == 0 ? tk.tile == 0 : (k0 <= nent - 1 && nent - 1 < k0 + kVTile);
+    if (last && tid < 64) {
+      const uint64_t total = excl + agg;
+      if (tid == 0) *p.total = total;
+      if (p.seg_bytes && p.nseg > 0) {
+        const uint32_t from = wave_lower_bound64(p.seg_begin, p.nseg, nent);
+        for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) p.seg_bytes[s] = total;
+      }
+    }
+    __syncthreads();
+  });
+}
+
+// ---------------------------------------------------------------- decode, pass 1
+
+__global__ __launch_bounds__(kVT) void varint_gaps_kernel(VarintDecParams p) {
+  __shared__ uint8_t s_in[4 + kBTile];      // 4 bytes before the tile, then the tile
+  __shared__ uint32_t s_gap[kBTile];        // values, in entry order
+  __shared__ uint32_t s_w[kVWaves];
+  __shared__ uint64_t s_b;
+  constexpr int kPer = kBTile / kVT;        // bytes per thread
+  const int tid = threadIdx.x;
+  const uint64_t nb0 = *p.nbytes;
+  const uint64_t nbytes = nb0 < p.in_capacity ? nb0 : p.in_capacity;
+  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t b0 = (uint64_t)tk.tile * kBTile;
+    const uint64_t b1 = b0 + kBTile < nbytes ? b0 + kBTile : (b0 < nbytes ? nbytes : b0);
+    const uint32_t cnt = (uint32_t)(b1 - b0);
+    for (uint32_t i = tid; i < cnt; i += kVT) s_in[4 + i] = p.in[b0 + i];
+    if (tid < 4) s_in[tid] = b0 >= 4 - (uint64_t)tid ? p.in[b0 - 4 + tid] : 0u;  // 0: a terminator
+    __syncthreads();
+    // terminating bytes of this thread's run
+    uint32_t nterm = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kPer + j;
+      nterm += (i < cnt && !(s_in[4 + i] & 0x80u)) ? 1u : 0u;
+    }
+    uint32_t agg32;
+    const uint32_t texcl = block_excl_sum(nterm, s_w, &agg32);
+    const uint64_t excl = chain_exclusive(p.ws, tk, agg32, false, 0, &s_b);
+    // the value of each number that ends in this tile (it starts at most 4
+    // bytes earlier, possibly in the previous tile)
+    uint32_t e = texcl;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kPer + j;
+      if (i < cnt && !(s_in[4 + i] & 0x80u)) {
+        int st = (int)i;
+        while (st > (int)i - 4 && (s_in[4 + st - 1] & 0x80u) && (b0 + (uint64_t)st) > 0) --st;
+        uint32_t v = 0;
+        for (int q = st; q <= (int)i; ++q) v |= (uint32_t)(s_in[4 + q] & 0x7Fu) << (7 * (q - st));
+        s_gap[e] = v;
+        ++e;
+      }
+    }
+    __syncthreads();
+    for (uint32_t q = tid; q < agg32; q += kVT) {
+      const uint64_t pos = excl + q;
+      if (pos < p.capacity) p.idx[pos] = s_gap[q];
+    }
+    const bool last = nbytes == 0 ? tk.tile == 0 : (b0 <= nbytes - 1 && nbytes - 1 < b0 + kBTile);
+    if (last && tid == 0) *p.count = excl + agg32;
+    __syncthreads();
+  });
+}
+
+// ---------------------------------------------------------------- decode, pass 2
+
+__global__ __launch_bounds__(kVT) void varint_sums_kernel(VarintDecParams p) {
+  __shared__ uint32_t s_v[kVTile];
+  __shared__ uint32_t s_flags[kVTile / 32];
+  __shared__ uint32_t s_range[2];
+  __shared__ uint32_t s_tsum[kVT];     // per thread: sum since its last restart
+  __shared__ uint32_t s_trst[kVT];     // per thread: has a restart
+  __shared__ uint64_t s_b;
+  __shared__ uint32_t s_tail[2];       // the tile's (has restart, sum after the last one)
+  const int tid = threadIdx.x;
+  const uint64_t c0 = *p.count;
+  const uint64_t nent = c0 < p.capacity ? c0 : p.capacity;
+  for_each_ticket(p.ws, p.ntiles2, [&](const Ticket& tk) {
+    const uint64_t k0 = (uint64_t)tk.tile * kVTile;
+    const uint64_t k1 = k0 + kVTile < nent ? k0 + kVTile : (k0 < nent ? nent : k0);
+    const uint32_t cnt = (uint32_t)(k1 - k0);
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_flags[w] = 0;
+    for (uint32_t i = tid; i < cnt; i += kVT) s_v[i] = p.idx[k0 + i];
+    __syncthreads();
+    if (tid < 64) mark_starts(p.seg_begin, p.nseg, k0, k1, s_flags, s_range);
+    __syncthreads();
+    // this thread's run: sum since its last restart
+    uint32_t run = 0;
+    bool rst = false;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kVPer + j;
+      if (i < cnt) {
+        if (flag_at(s_flags, i)) {
+          run = 0;
+          rst = true;
+        }
+        run += s_v[i];
+      }
+    }
+    s_tsum[tid] = run;
+    s_trst[tid] = rst ? 1u : 0u;
+    __syncthreads();
+    // carry into each thread from the threads before it, within the tile
+    // (the segmented sum of the runs, walked by one wave with 4 runs per lane)
+    if (tid < 64) {
+      uint32_t c = 0;
+      bool r = false;
+      uint32_t vals[4];
+      bool rs[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        vals[q] = s_tsum[tid * 4 + q];
+        rs[q] = s_trst[tid * 4 + q] != 0u;
+        c = rs[q] ? vals[q] : c + vals[q];
+        r = r || rs[q];
+      }
+      // inclusive segmented scan of the lanes' (r, c) pairs
+      uint32_t ic = c;
+      bool ir = r;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t oc = (uint32_t)__shfl_up((int)ic, d, 64);
+        const int orr = __shfl_up(ir ? 1 : 0, d, 64);
+        if (lane_id() >= d && !ir) {
+          ic = oc + ic;
+          ir = orr != 0;
+        }
+      }
+      // exclusive value for each of the lane's 4 threads
+      uint32_t ec = (uint32_t)__shfl_up((int)ic, 1, 64);
+      bool er = __shfl_up(ir ? 1 : 0, 1, 64) != 0;
+      if (lane_id() == 0) {
+        ec = 0;
+        er = false;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        s_tsum[tid * 4 + q] = ec;            // carry from earlier threads of the tile
+        s_trst[tid * 4 + q] = er ? 1u : 0u;  // ... which started after a restart
+        ec = rs[q] ? vals[q] : ec + vals[q];
+        er = er || rs[q];
+      }
+      if (tid == 63) {
+        s_tail[0] = ir ? 1u : 0u;
+        s_tail[1] = ic;
+      }
+    }
+    __syncthreads();
+    const bool tile_rst = s_tail[0] != 0u;
+    const uint32_t tile_sum = s_tail[1];
+    const uint64_t carry = chain_exclusive(p.ws, tk, tile_sum, tile_rst, tile_sum, &s_b);
+    // indices: before any restart in the tile the carry from earlier tiles applies
+    uint32_t acc = s_tsum[tid] + (s_trst[tid] ? 0u : (uint32_t)carry);
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = (uint32_t)tid * kVPer + j;
+      if (i < cnt) {
+        if (flag_at(s_flags, i)) acc = 0;
+        acc += s_v[i];
+        s_v[i] = acc;
+      }
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < cnt; i += kVT) p.idx[k0 + i] = s_v[i];
+    __syncthreads();
+  });
+}
+
+uint32_t varint_entry_tile() { return kVTile; }
+uint32_t varint_byte_tile() { return kBTile; }
+
+static uint32_t varint_grid(uint32_t ntiles) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  const uint32_t cap = (uint32_t)(cus > 0 ? cus : 1) * 2u;
+  return ntiles < cap ? ntiles : cap;
+}
+
+hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream) {
+  const uint32_t grid = varint_grid(p.ntiles);
+  if (grid == 0) return hipErrorInvalidDevice;
+  hipLaunchKernelGGL(varint_encode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream) {
+  uint32_t grid = varint_grid(p.ntiles);
+  if (grid == 0) return hipErrorInvalidDevice;
+  hipLaunchKernelGGL(varint_gaps_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  grid = varint_grid(p.ntiles2);
+  hipLaunchKernelGGL(varint_sums_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace pulse

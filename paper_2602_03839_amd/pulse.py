@@ -66,7 +66,8 @@ MAX_LISTS = 8  # PULSE_MAX_LISTS
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
            "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
-           "pulse_outer_step", "pulse_outer_step_batch")
+           "pulse_outer_step", "pulse_outer_step_batch",
+           "pulse_varint_encode", "pulse_varint_decode")
 
 
 def lib():
@@ -95,6 +96,8 @@ def lib():
             L.pulse_loco_sparsify_batch.argtypes = [vp, u32, f32, vp, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_outer_step.argtypes = [vp, vp, u64, u32, vp, u32, f32, f32, vp]
             L.pulse_outer_step_batch.argtypes = [vp, u32, vp, u32, f32, f32, vp]
+            L.pulse_varint_encode.argtypes = [vp, u64, vp, vp, u32, vp, u64, vp, vp, vp, sz, vp]
+            L.pulse_varint_decode.argtypes = [vp, u64, vp, vp, u32, vp, u64, vp, vp, sz, vp]
             for name in EXPORTS[3:]:
                 getattr(L, name).restype = i32
             _lib = L
@@ -329,3 +332,32 @@ class OuterBatch:
         _check(lib().pulse_outer_step_batch(self.arr, self.n, arr, len(lists), float(mu),
                                             float(alpha), _stream(stream)),
                "pulse_outer_step_batch")
+
+
+def varint_encode(idx: torch.Tensor, end: torch.Tensor, out: torch.Tensor, total: torch.Tensor,
+                  ws: torch.Tensor, seg_begin: Optional[torch.Tensor] = None,
+                  seg_bytes: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
+                  stream=None) -> None:
+    """Delta-varint stream of a sorted patch's indices (pulse_varint_encode)."""
+    assert idx.element_size() == 4 and out.element_size() == 1
+    assert end.element_size() == 8 and total.element_size() == 8
+    cap = idx.numel() if capacity is None else capacity
+    assert 0 <= cap <= idx.numel()
+    nseg = 0 if seg_begin is None else seg_begin.numel()
+    if seg_bytes is not None:
+        assert seg_begin is not None and seg_bytes.numel() >= nseg
+    _check(lib().pulse_varint_encode(_p(idx), cap, _p(end), _p(seg_begin), nseg, _p(out),
+                                     out.numel(), _p(seg_bytes), _p(total), _p(ws), ws.numel(),
+                                     _stream(stream)), "pulse_varint_encode")
+
+
+def varint_decode(stream_bytes: torch.Tensor, nbytes: torch.Tensor, idx: torch.Tensor,
+                  count: torch.Tensor, ws: torch.Tensor, seg_begin: Optional[torch.Tensor] = None,
+                  stream=None) -> None:
+    """Indices back from a delta-varint stream (pulse_varint_decode)."""
+    assert stream_bytes.element_size() == 1 and idx.element_size() == 4
+    assert nbytes.element_size() == 8 and count.element_size() == 8
+    nseg = 0 if seg_begin is None else seg_begin.numel()
+    _check(lib().pulse_varint_decode(_p(stream_bytes), stream_bytes.numel(), _p(nbytes),
+                                     _p(seg_begin), nseg, _p(idx), idx.numel(), _p(count), _p(ws),
+                                     ws.numel(), _stream(stream)), "pulse_varint_decode")
