@@ -16,6 +16,10 @@ and marshals numpy arrays into it with ctypes.
     outer_step(theta, m, lists, ...) Sec. 4.3 Alg. 2 (SparseSync average, outer Nesterov step)
     varint_encode(idx) / varint_decode(stream)
                                      App. H.2 / App. F.3 delta-varint index stream
+    sha256(msg)                      FIPS 180-4 SHA-256 (the primitive of App. J.4's hash)
+    leaf_hashes(stream) / merkle_root(digests) / tree_hash(tensors)
+                                     App. J.4 weight hash, read as an RFC 6962 tree
+                                     over 16 KiB chunks of the BF16 byte stream
 """
 from __future__ import annotations
 
@@ -68,6 +72,12 @@ def _load():
             lib.oracle_varint_encode.restype = u64
             lib.oracle_varint_decode.argtypes = [vp, u64, vp, u64]
             lib.oracle_varint_decode.restype = ctypes.c_int64
+            lib.oracle_sha256.argtypes = [vp, u64, vp]
+            lib.oracle_sha256.restype = None
+            lib.oracle_leaf_hashes.argtypes = [vp, u64, u64, vp]
+            lib.oracle_leaf_hashes.restype = None
+            lib.oracle_merkle_root.argtypes = [vp, u64, vp]
+            lib.oracle_merkle_root.restype = None
             _lib = lib
     return _lib
 
@@ -231,3 +241,55 @@ def varint_decode(stream) -> np.ndarray:
     out = np.zeros(max(n, 1), dtype=np.uint32)
     L.oracle_varint_decode(_ptr(stream), stream.size, _ptr(out), n)
     return out[:n]
+
+
+LEAF_BYTES = 16384
+"""Chunk size of the weight hash: 16 KiB of the BF16 byte stream (8192 values)."""
+
+
+def _bytes(a) -> np.ndarray:
+    if isinstance(a, (bytes, bytearray, memoryview)):
+        return np.frombuffer(bytes(a), dtype=np.uint8)
+    a = np.ascontiguousarray(a)
+    return a.reshape(-1).view(np.uint8)
+
+
+def sha256(msg) -> bytes:
+    """SHA-256 digest (32 bytes) of a byte string or of an array's raw bytes."""
+    m = _bytes(msg)
+    out = np.zeros(32, dtype=np.uint8)
+    _load().oracle_sha256(_ptr(m) if m.size else None, m.size, _ptr(out))
+    return out.tobytes()
+
+
+def leaf_hashes(stream, leaf_bytes: int = LEAF_BYTES) -> np.ndarray:
+    """Leaf digests, shape (nleaves, 32) uint8, of the chunks of a byte stream."""
+    m = _bytes(stream)
+    assert leaf_bytes >= 1
+    n = (m.size + leaf_bytes - 1) // leaf_bytes
+    out = np.zeros((max(n, 1), 32), dtype=np.uint8)
+    if n:
+        _load().oracle_leaf_hashes(_ptr(m), m.size, leaf_bytes, _ptr(out))
+    return out[:n]
+
+
+def merkle_root(digests) -> bytes:
+    """RFC 6962 tree root over leaf digests given as an (n, 32) uint8 array."""
+    d = np.ascontiguousarray(digests, dtype=np.uint8).reshape(-1, 32)
+    out = np.zeros(32, dtype=np.uint8)
+    _load().oracle_merkle_root(_ptr(d) if d.size else None, d.shape[0], _ptr(out))
+    return out.tobytes()
+
+
+def tree_hash(tensors, leaf_bytes: int = LEAF_BYTES):
+    """Weight hash of BF16 tensors (uint16 arrays) concatenated in the given order.
+
+    Returns (root: bytes, leaf digests: (nleaves, 32) uint8).
+    """
+    if isinstance(tensors, np.ndarray):
+        tensors = [tensors]
+    parts = [_u16(t).ravel() for t in tensors]
+    stream = np.concatenate(parts) if parts else np.zeros(0, dtype=np.uint16)
+    stream = stream.astype("<u2", copy=False)
+    d = leaf_hashes(stream.view(np.uint8), leaf_bytes)
+    return merkle_root(d), d

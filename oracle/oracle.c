@@ -25,6 +25,10 @@
  *   oracle_varint_encode App. H.2 (index encoding: sorted, first index as-is,
  *   oracle_varint_decode then differences) and App. F.3 (PULSELoCo's sparse
  *                        stream: delta-encoded, varint-packed indices).
+ *   oracle_sha256        App. J.4 (weight-level integrity hash): SHA-256 as
+ *   oracle_leaf_hashes   FIPS 180-4 defines it, applied as a tree (RFC 6962
+ *   oracle_merkle_root   Merkle Tree Hash) over fixed-size chunks of the
+ *                        concatenated BF16 bytes.
  *
  * Readings where the paper is silent (all listed in the design notes):
  *   - A NaN input casts to a quiet NaN that keeps the sign and the leading
@@ -32,6 +36,8 @@
  *   - Overflow rounds to +-inf exactly as IEEE RNE with an unbounded exponent.
  *   - Subnormals are rounded like any other value (no flush to zero).
  *   - Equality of BF16 values is bitwise, so +0 and -0 differ (Sec. 3 metric).
+ *   - The weight hash is a tree of SHA-256 over 16 KiB chunks of the BF16 byte
+ *     stream (low byte of each value first), not one SHA-256 over the stream.
  *   - Output entries beyond `capacity` are not written; the returned count is
  *     still the true total.  `refresh` is written only for emitted entries.  In
  *     the sparsifier an entry that was selected but not emitted stays in the
@@ -301,4 +307,192 @@ int64_t oracle_varint_decode(const uint8_t *in, uint64_t nbytes, uint32_t *out, 
         count++;
     }
     return (int64_t)count;
+}
+
+/* ------------------------------------------------------------------------
+ * Weight-level integrity hash (App. J.4, "Weight-level integrity" and
+ * "Deterministic hashing"; the hash h of Alg. 3 and of the sync protocol).
+ *
+ * The paper hashes the raw BF16 bit patterns of all parameters, concatenated
+ * in a fixed order, with SHA-256.  The message here is that concatenation
+ * as it sits in memory: each BF16 value as its two bytes, low byte first.
+ *
+ * A single SHA-256 over the whole stream is one long chain of compressions
+ * and cannot be split, so the checksum is read as a tree of SHA-256 (the
+ * design notes give the reasons): the stream is cut into chunks of
+ * `leaf_bytes` bytes (the last one may be shorter) and combined with the
+ * Merkle Tree Hash of RFC 6962, Sec. 2.1:
+ *     MTH({})      = SHA-256()                        (empty stream)
+ *     MTH({c})     = SHA-256(0x00 || c)               (one chunk: leaf hash)
+ *     MTH(D[0:n])  = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])),
+ *                    k = the largest power of two smaller than n.
+ *
+ * SHA-256 itself follows FIPS 180-4: padding (5.1.1), parsing into 512-bit
+ * blocks (5.2.1), the initial hash value (5.3.3) and the computation (6.2.2).
+ * Its constants are taken from their definitions rather than typed in: the
+ * first 32 bits of the fractional parts of the square roots (initial hash
+ * value) and cube roots (round constants) of the first primes, found here
+ * with exact integer roots.
+ * ------------------------------------------------------------------------ */
+
+typedef struct {
+    uint32_t k[64];
+    uint32_t h0[8];
+} sha_consts;
+
+/* largest y with y^e <= v, by binary search over the bits of y (e = 2 or 3) */
+static uint64_t iroot128(unsigned __int128 v, int e)
+{
+    uint64_t y = 0;
+    for (int bit = 40; bit >= 0; bit--) {
+        uint64_t t = y | ((uint64_t)1 << bit);
+        unsigned __int128 p = (unsigned __int128)t * t;
+        if (e == 3)
+            p *= t;
+        if (p <= v)
+            y = t;
+    }
+    return y;
+}
+
+static void sha_make_consts(sha_consts *c)
+{
+    int found = 0;
+    for (uint64_t p = 2; found < 64; p++) {
+        int prime = 1;
+        for (uint64_t d = 2; d * d <= p; d++)
+            if (p % d == 0) {
+                prime = 0;
+                break;
+            }
+        if (!prime)
+            continue;
+        /* frac(cbrt(p)) * 2^32 = cbrt(p * 2^96) mod 2^32; likewise for sqrt */
+        c->k[found] = (uint32_t)iroot128((unsigned __int128)p << 96, 3);
+        if (found < 8)
+            c->h0[found] = (uint32_t)iroot128((unsigned __int128)p << 64, 2);
+        found++;
+    }
+}
+
+static uint32_t rotr32(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
+
+static void sha256_with(const sha_consts *c, const uint8_t *msg, uint64_t len, uint8_t out[32])
+{
+    /* 5.1.1: append the bit 1, zeros up to 448 mod 512 bits, and the 64-bit length */
+    uint64_t padded = ((len + 8) / 64 + 1) * 64;
+    uint8_t *m = calloc(padded, 1);
+    if (len)
+        memcpy(m, msg, len);
+    m[len] = 0x80;
+    uint64_t bits = len * 8;
+    for (int i = 0; i < 8; i++)
+        m[padded - 1 - i] = (uint8_t)(bits >> (8 * i));
+
+    uint32_t H[8];
+    memcpy(H, c->h0, sizeof H);
+    for (uint64_t blk = 0; blk < padded / 64; blk++) {
+        const uint8_t *M = m + 64 * blk;
+        uint32_t W[64];
+        for (int t = 0; t < 16; t++)
+            W[t] = (uint32_t)M[4 * t] << 24 | (uint32_t)M[4 * t + 1] << 16 |
+                   (uint32_t)M[4 * t + 2] << 8 | (uint32_t)M[4 * t + 3];
+        for (int t = 16; t < 64; t++) {
+            uint32_t s0 = rotr32(W[t - 15], 7) ^ rotr32(W[t - 15], 18) ^ (W[t - 15] >> 3);
+            uint32_t s1 = rotr32(W[t - 2], 17) ^ rotr32(W[t - 2], 19) ^ (W[t - 2] >> 10);
+            W[t] = s1 + W[t - 7] + s0 + W[t - 16];
+        }
+        uint32_t a = H[0], b = H[1], cc = H[2], d = H[3];
+        uint32_t e = H[4], f = H[5], g = H[6], h = H[7];
+        for (int t = 0; t < 64; t++) {
+            uint32_t S1 = rotr32(e, 6) ^ rotr32(e, 11) ^ rotr32(e, 25);
+            uint32_t ch = (e & f) ^ (~e & g);
+            uint32_t T1 = h + S1 + ch + c->k[t] + W[t];
+            uint32_t S0 = rotr32(a, 2) ^ rotr32(a, 13) ^ rotr32(a, 22);
+            uint32_t maj = (a & b) ^ (a & cc) ^ (b & cc);
+            uint32_t T2 = S0 + maj;
+            h = g;
+            g = f;
+            f = e;
+            e = d + T1;
+            d = cc;
+            cc = b;
+            b = a;
+            a = T1 + T2;
+        }
+        H[0] += a;
+        H[1] += b;
+        H[2] += cc;
+        H[3] += d;
+        H[4] += e;
+        H[5] += f;
+        H[6] += g;
+        H[7] += h;
+    }
+    free(m);
+    for (int i = 0; i < 8; i++)
+        for (int j = 0; j < 4; j++)
+            out[4 * i + j] = (uint8_t)(H[i] >> (24 - 8 * j));
+}
+
+void oracle_sha256(const uint8_t *msg, uint64_t len, uint8_t out[32])
+{
+    sha_consts c;
+    sha_make_consts(&c);
+    sha256_with(&c, msg, len, out);
+}
+
+/* leaf hash of RFC 6962: SHA-256 over the byte 0x00 followed by the chunk */
+static void leaf_hash(const sha_consts *c, const uint8_t *chunk, uint64_t len, uint8_t out[32])
+{
+    uint8_t *buf = malloc(len + 1);
+    buf[0] = 0x00;
+    if (len)
+        memcpy(buf + 1, chunk, len);
+    sha256_with(c, buf, len + 1, out);
+    free(buf);
+}
+
+/* digests[i] = leaf hash of bytes [i*leaf_bytes, min((i+1)*leaf_bytes, nbytes)) */
+void oracle_leaf_hashes(const uint8_t *stream, uint64_t nbytes, uint64_t leaf_bytes,
+                        uint8_t *digests)
+{
+    sha_consts c;
+    sha_make_consts(&c);
+    uint64_t nleaves = (nbytes + leaf_bytes - 1) / leaf_bytes;
+    for (uint64_t i = 0; i < nleaves; i++) {
+        uint64_t lo = i * leaf_bytes;
+        uint64_t len = nbytes - lo < leaf_bytes ? nbytes - lo : leaf_bytes;
+        leaf_hash(&c, stream + lo, len, digests + 32 * i);
+    }
+}
+
+/* MTH over the leaf digests d[lo, hi), hi - lo >= 1 */
+static void mth(const sha_consts *c, const uint8_t *d, uint64_t lo, uint64_t hi, uint8_t out[32])
+{
+    uint64_t n = hi - lo;
+    if (n == 1) {
+        memcpy(out, d + 32 * lo, 32);
+        return;
+    }
+    uint64_t k = 1;
+    while (k * 2 < n)
+        k *= 2;
+    uint8_t node[65];
+    node[0] = 0x01;
+    mth(c, d, lo, lo + k, node + 1);
+    mth(c, d, lo + k, hi, node + 33);
+    sha256_with(c, node, sizeof node, out);
+}
+
+/* root of the tree over `nleaves` leaf digests (32 bytes each); no leaves:
+ * the hash of the empty message */
+void oracle_merkle_root(const uint8_t *digests, uint64_t nleaves, uint8_t root[32])
+{
+    sha_consts c;
+    sha_make_consts(&c);
+    if (nleaves == 0)
+        sha256_with(&c, NULL, 0, root);
+    else
+        mth(&c, digests, 0, nleaves, root);
 }
