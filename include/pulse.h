@@ -8,7 +8,9 @@
  *     App. H.5, Alg. 3) and apply (Alg. 1 Decode; App. H.5, Alg. 4),
  *   - PULSELoCo's error-feedback sparsification of FP32 pseudo-gradients
  *     and its outer step, SparseSync's average plus outer Nesterov momentum
- *     (Sec. 4.3, Alg. 2).
+ *     (Sec. 4.3, Alg. 2),
+ *   - the delta-varint index stream (App. H.2, App. F.3) and the weight hash
+ *     a receiver checks after applying a patch (App. J.4).
  *
  * Conventions for every entry point:
  *   - Pointers are DEVICE pointers (HIP device memory of the current device)
@@ -308,6 +310,55 @@ int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t 
                         const uint64_t *seg_begin, uint32_t nseg,
                         uint32_t *idx, uint64_t capacity, uint64_t *count,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Weight hash (App. J.4 "Weight-level integrity", "Deterministic hashing"):
+ * a SHA-256 digest of the BF16 bit patterns of all tensors, concatenated in
+ * the order given, that the sender publishes with each patch and the receiver
+ * recomputes over the weights it rebuilt.
+ *
+ * The message is the tensors' bytes as they sit in memory (each value's two
+ * bytes, low byte first).  One SHA-256 over it cannot be split across a GPU,
+ * so the digest is a tree of SHA-256 (FIPS 180-4): the message is cut into
+ * leaves of PULSE_HASH_LEAF_BYTES bytes (the last may be shorter) and the
+ * leaves are combined by the Merkle Tree Hash of RFC 6962, Sec. 2.1:
+ *   leaf digest  SHA-256(0x00 || leaf bytes)
+ *   node digest  SHA-256(0x01 || left digest || right digest), the left
+ *                subtree holding the largest power of two of leaves below the
+ *                count;
+ *   no leaves    SHA-256 of the empty message.
+ * The digest depends only on the concatenated bytes, not on how they are
+ * split into tensors.  A message of at most one leaf hashes to
+ * SHA-256(0x00 || message).
+ */
+#define PULSE_HASH_LEAF_BYTES 16384
+
+typedef struct pulse_hash_tensor {
+    const uint16_t *data; /* device; 4-byte aligned; may be NULL when n == 0 */
+    uint64_t n;           /* BF16 values */
+} pulse_hash_tensor;
+
+/* Number of leaves of a message of `total_values` BF16 values. */
+uint64_t pulse_hash_leaf_count(uint64_t total_values);
+
+/* Workspace bytes pulse_hash_tree needs for `ntensors` tensors holding
+ * `total_values` values together (not the encode workspace; it needs no
+ * zero-filling). */
+size_t pulse_hash_workspace_bytes(uint32_t ntensors, uint64_t total_values);
+
+/*
+ * pulse_hash_tree -- the weight hash of `ntensors` tensors (host array).
+ *   leaf_digests  device, 32 * pulse_hash_leaf_count(total) bytes, 4-byte
+ *                 aligned: every leaf's digest (FIPS byte order), kept so that
+ *                 a mismatch can be narrowed to 16 KiB chunks. May be NULL
+ *                 only when there are no values.
+ *   root          device, 32 bytes, 4-byte aligned: the digest.
+ *   workspace     device, 256-byte aligned, pulse_hash_workspace_bytes() bytes.
+ * Errors: EINVAL (NULL pointer, workspace too small), EALIGN, EHIP.
+ */
+int pulse_hash_tree(const pulse_hash_tensor *tensors, uint32_t ntensors,
+                    uint8_t *leaf_digests, uint8_t *root,
+                    void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

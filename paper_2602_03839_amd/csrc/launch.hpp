@@ -161,6 +161,56 @@ struct VarintDecParams {
   uint32_t ntiles2;            // entry tiles
 };
 
+// Weight hash: a tree of SHA-256 over 16 KiB chunks ("leaves") of the
+// concatenated BF16 bytes.  The tensors' pointers and stream offsets go to a
+// device table in the caller's workspace, written by small setup launches
+// that also gather the leaves which do not lie inside one tensor (a boundary
+// between tensors falls inside them) into one 16 KiB scratch slot each.
+constexpr uint64_t kHashLeafElems = 8192;
+constexpr uint64_t kHashLeafBytes = 2 * kHashLeafElems;
+constexpr int kHashSetupBatch = 64;
+constexpr uint32_t kHashTreeFan = 512;  // digests reduced by one tree block
+
+struct HashEntry {
+  const uint16_t* ptr;
+  uint64_t off;  // stream offset (elements) of the tensor's first value
+};
+
+struct HashCopyJob {
+  const uint16_t* src;
+  uint64_t dst;    // byte offset in the scratch slots
+  uint64_t count;  // values
+};
+
+struct HashSetupParams {
+  HashEntry* table;
+  uint8_t* scratch;
+  uint32_t first_entry;
+  uint32_t nentries;
+  uint32_t njobs;
+  HashEntry entries[kHashSetupBatch];
+  HashCopyJob jobs[kHashSetupBatch];
+};
+
+struct HashLeafParams {
+  const HashEntry* table;  // ntensors entries + one whose off is the stream length
+  uint32_t ntensors;
+  const uint8_t* scratch;  // slot t: the leaf that starts inside tensor t, if gathered
+  uint8_t* digests;        // out: nleaves x 32 bytes
+  uint64_t nleaves;
+  uint64_t total;          // stream length in values
+};
+
+// A leaf [x, x + le) that starts inside the tensor [off, end) is read in place
+// when it ends inside that tensor and its last aligned 4-byte word does too
+// (the kernel reads whole words; the tensor's base is 4-byte aligned).
+__host__ __device__ inline bool hash_leaf_in_place(uint64_t x, uint64_t le, uint64_t off,
+                                                   uint64_t end) {
+  const uint64_t lend = x + le;
+  return lend <= end && (((lend - off) & 1) == 0 || lend < end);
+}
+
+static_assert(sizeof(HashSetupParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(OuterParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
@@ -178,5 +228,8 @@ uint32_t varint_byte_tile();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
+hipError_t launch_hash_setup(const HashSetupParams& p, hipStream_t stream);
+hipError_t launch_hash_leaves(const HashLeafParams& p, hipStream_t stream);
+hipError_t launch_hash_tree(const uint8_t* in, uint64_t n_in, uint8_t* out, hipStream_t stream);
 
 }  // namespace pulse

@@ -5,6 +5,9 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "../../include/pulse.h"
 #include "device_common.hpp"
 #include "launch.hpp"
@@ -60,6 +63,29 @@ bool refresh_mirrors(const pulse_encode_tensor& d) {
 }
 
 uint32_t tiles_for(uint64_t n, uint32_t tile) { return (uint32_t)((n + tile - 1) / tile); }
+
+// Workspace of the weight hash: the tensor table (one entry per tensor plus
+// the end of the stream), one 16 KiB scratch slot per tensor, and two buffers
+// for the tree levels above the leaves (level 1 and level 2; later levels
+// reuse them alternately, each smaller than the one before).
+struct HashLayout {
+  size_t table, scratch, lv1, lv2, total;
+};
+
+size_t round256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+HashLayout hash_layout(uint32_t ntensors, uint64_t total_values) {
+  const uint64_t leaves = (total_values + pulse::kHashLeafElems - 1) / pulse::kHashLeafElems;
+  const uint64_t n1 = (leaves + pulse::kHashTreeFan - 1) / pulse::kHashTreeFan;
+  const uint64_t n2 = (n1 + pulse::kHashTreeFan - 1) / pulse::kHashTreeFan;
+  HashLayout L;
+  L.table = 0;
+  L.scratch = L.table + round256(((size_t)ntensors + 1) * sizeof(pulse::HashEntry));
+  L.lv1 = L.scratch + (size_t)ntensors * pulse::kHashLeafBytes;
+  L.lv2 = L.lv1 + round256((size_t)n1 * 32);
+  L.total = L.lv2 + round256((size_t)n2 * 32);
+  return L;
+}
 
 }  // namespace
 
@@ -425,6 +451,114 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   p.ntiles = (uint32_t)nt;
   p.ntiles2 = (uint32_t)nt2;
   return hip_status(pulse::launch_varint_decode(p, (hipStream_t)stream), "varint decode launch");
+}
+
+uint64_t pulse_hash_leaf_count(uint64_t total_values) {
+  return (total_values + pulse::kHashLeafElems - 1) / pulse::kHashLeafElems;
+}
+
+size_t pulse_hash_workspace_bytes(uint32_t ntensors, uint64_t total_values) {
+  return hash_layout(ntensors, total_values).total;
+}
+
+int pulse_hash_tree(const pulse_hash_tensor* tensors, uint32_t ntensors, uint8_t* leaf_digests,
+                    uint8_t* root, void* workspace, size_t workspace_bytes, void* stream) {
+  using pulse::HashEntry;
+  using pulse::kHashLeafElems;
+  if (ntensors > 0 && !tensors) return fail(PULSE_EINVAL, "hash: tensors is NULL");
+  if (!root) return fail(PULSE_EINVAL, "hash: root is NULL");
+  if (!aligned(root, 4)) return fail(PULSE_EALIGN, "hash: root not 4-byte aligned");
+  // The stream: the non-empty tensors in order.
+  std::vector<HashEntry> ent;
+  ent.reserve((size_t)ntensors + 1);
+  uint64_t total = 0;
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_hash_tensor& d = tensors[t];
+    if (d.n == 0) continue;
+    if (!d.data) return fail(PULSE_EINVAL, "hash tensor %u: data is NULL", t);
+    if (!aligned(d.data, 4)) return fail(PULSE_EALIGN, "hash tensor %u: data not 4-byte aligned", t);
+    ent.push_back(HashEntry{d.data, total});
+    total += d.n;
+  }
+  const uint32_t nt = (uint32_t)ent.size();
+  ent.push_back(HashEntry{nullptr, total});
+  const uint64_t nleaves = pulse_hash_leaf_count(total);
+  if (nleaves > 0 && !leaf_digests) return fail(PULSE_EINVAL, "hash: leaf_digests is NULL");
+  if (leaf_digests && !aligned(leaf_digests, 4))
+    return fail(PULSE_EALIGN, "hash: leaf_digests not 4-byte aligned");
+  if ((nleaves + 255) / 256 > 0x7FFFFFFFull) return fail(PULSE_EINVAL, "hash: too many leaves");
+  if (!workspace) return fail(PULSE_EINVAL, "hash: workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(PULSE_EALIGN, "hash: workspace not 256-byte aligned");
+  const HashLayout L = hash_layout(nt, total);
+  if (workspace_bytes < L.total)
+    return fail(PULSE_EINVAL, "hash: workspace has %zu bytes, needs %zu", workspace_bytes, L.total);
+  uint8_t* ws = (uint8_t*)workspace;
+  hipStream_t s = (hipStream_t)stream;
+
+  // Leaves that do not lie inside one tensor are gathered into the scratch
+  // slot of the tensor they start in.  Only a tensor's first and last leaf
+  // can be such a leaf; one copy job per (tensor, leaf) pair.
+  std::vector<pulse::HashCopyJob> jobs;
+  auto owner = [&](uint64_t x) {  // the tensor holding stream value x
+    auto it = std::upper_bound(ent.begin(), ent.begin() + nt, x,
+                               [](uint64_t v, const HashEntry& e) { return v < e.off; });
+    return (uint32_t)(it - ent.begin()) - 1;
+  };
+  for (uint32_t p = 0; p < nt; ++p) {
+    const uint64_t off = ent[p].off, end = ent[p + 1].off;
+    const uint64_t lf = off / kHashLeafElems, ll = (end - 1) / kHashLeafElems;
+    const uint64_t ends[2] = {lf, ll};
+    for (int i = 0; i < (ll == lf ? 1 : 2); ++i) {
+      const uint64_t x = ends[i] * kHashLeafElems;
+      const uint64_t le = std::min<uint64_t>(kHashLeafElems, total - x);
+      const uint32_t q = x >= off ? p : owner(x);
+      if (pulse::hash_leaf_in_place(x, le, ent[q].off, ent[q + 1].off)) continue;
+      const uint64_t a = std::max(x, off), b = std::min(x + le, end);
+      jobs.push_back(pulse::HashCopyJob{ent[p].ptr + (a - off),
+                                        (uint64_t)q * pulse::kHashLeafBytes + 2 * (a - x), b - a});
+    }
+  }
+
+  // Setup launches: the table and the gathers, 64 of each per launch.
+  const size_t E = ent.size(), J = jobs.size();
+  const size_t nsetup = std::max((E + pulse::kHashSetupBatch - 1) / pulse::kHashSetupBatch,
+                                 (J + pulse::kHashSetupBatch - 1) / pulse::kHashSetupBatch);
+  for (size_t i = 0; i < nsetup; ++i) {
+    pulse::HashSetupParams p;
+    memset(&p, 0, sizeof p);
+    p.table = (HashEntry*)(ws + L.table);
+    p.scratch = ws + L.scratch;
+    const size_t e0 = i * pulse::kHashSetupBatch, j0 = e0;
+    p.first_entry = (uint32_t)e0;
+    p.nentries = e0 < E ? (uint32_t)std::min<size_t>(pulse::kHashSetupBatch, E - e0) : 0;
+    p.njobs = j0 < J ? (uint32_t)std::min<size_t>(pulse::kHashSetupBatch, J - j0) : 0;
+    for (uint32_t k = 0; k < p.nentries; ++k) p.entries[k] = ent[e0 + k];
+    for (uint32_t k = 0; k < p.njobs; ++k) p.jobs[k] = jobs[j0 + k];
+    if (int rc = hip_status(pulse::launch_hash_setup(p, s), "hash setup launch")) return rc;
+  }
+
+  pulse::HashLeafParams lp;
+  lp.table = (const HashEntry*)(ws + L.table);
+  lp.ntensors = nt;
+  lp.scratch = ws + L.scratch;
+  lp.digests = leaf_digests;
+  lp.nleaves = nleaves;
+  lp.total = total;
+  if (int rc = hip_status(pulse::launch_hash_leaves(lp, s), "hash leaf launch")) return rc;
+
+  // Tree levels, 9 per launch, until one digest is left (written to root).
+  const uint8_t* in = leaf_digests;
+  uint64_t n = nleaves;
+  int level = 0;
+  do {
+    const uint64_t n_out = n <= 1 ? 1 : (n + pulse::kHashTreeFan - 1) / pulse::kHashTreeFan;
+    uint8_t* out = n_out == 1 ? root : ws + (level % 2 == 0 ? L.lv1 : L.lv2);
+    if (int rc = hip_status(pulse::launch_hash_tree(in, n, out, s), "hash tree launch")) return rc;
+    in = out;
+    n = n_out;
+    ++level;
+  } while (in != root);
+  return ok();
 }
 
 }  // extern "C"

@@ -63,11 +63,19 @@ class _SparseList(ctypes.Structure):
 
 MAX_LISTS = 8  # PULSE_MAX_LISTS
 
+
+class _HashTensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n", ctypes.c_uint64)]
+
+
+HASH_LEAF_BYTES = 16384  # PULSE_HASH_LEAF_BYTES
+
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
            "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
            "pulse_outer_step", "pulse_outer_step_batch",
-           "pulse_varint_encode", "pulse_varint_decode")
+           "pulse_varint_encode", "pulse_varint_decode",
+           "pulse_hash_leaf_count", "pulse_hash_workspace_bytes", "pulse_hash_tree")
 
 
 def lib():
@@ -98,8 +106,14 @@ def lib():
             L.pulse_outer_step_batch.argtypes = [vp, u32, vp, u32, f32, f32, vp]
             L.pulse_varint_encode.argtypes = [vp, u64, vp, vp, u32, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_varint_decode.argtypes = [vp, u64, vp, vp, u32, vp, u64, vp, vp, sz, vp]
+            L.pulse_hash_leaf_count.argtypes = [u64]
+            L.pulse_hash_leaf_count.restype = u64
+            L.pulse_hash_workspace_bytes.argtypes = [u32, u64]
+            L.pulse_hash_workspace_bytes.restype = sz
+            L.pulse_hash_tree.argtypes = [vp, u32, vp, vp, vp, sz, vp]
             for name in EXPORTS[3:]:
-                getattr(L, name).restype = i32
+                if name not in ("pulse_hash_leaf_count", "pulse_hash_workspace_bytes"):
+                    getattr(L, name).restype = i32
             _lib = L
     return _lib
 
@@ -361,3 +375,48 @@ def varint_decode(stream_bytes: torch.Tensor, nbytes: torch.Tensor, idx: torch.T
     _check(lib().pulse_varint_decode(_p(stream_bytes), stream_bytes.numel(), _p(nbytes),
                                      _p(seg_begin), nseg, _p(idx), idx.numel(), _p(count), _p(ws),
                                      ws.numel(), _stream(stream)), "pulse_varint_decode")
+
+
+def hash_leaf_count(total_values: int) -> int:
+    return int(lib().pulse_hash_leaf_count(int(total_values)))
+
+
+class HashBatch:
+    """Weight hash (pulse_hash_tree) of 2-byte tensors, concatenated in order.
+
+    Owns the descriptor array, the workspace, the leaf digests (nleaves x 32
+    uint8) and the root (32 uint8); build it once per set of tensors and call
+    it after each update of their values.
+    """
+
+    def __init__(self, tensors: Sequence[torch.Tensor], device=None):
+        self.n = len(tensors)
+        arr = (_HashTensor * max(1, self.n))()
+        total = 0
+        for i, t in enumerate(tensors):
+            assert _is16(t) and t.is_contiguous()
+            arr[i] = _HashTensor(_p(t) if t.numel() else None, t.numel())
+            total += t.numel()
+        dev = device or (tensors[0].device if tensors else "cuda")
+        self.arr = arr
+        self.keep = list(tensors)
+        self.total = total
+        self.nleaves = hash_leaf_count(total)
+        nonempty = sum(1 for t in tensors if t.numel())
+        self.ws = torch.empty(int(lib().pulse_hash_workspace_bytes(nonempty, total)),
+                              dtype=torch.uint8, device=dev)
+        self.leaves = torch.empty((max(self.nleaves, 1), 32), dtype=torch.uint8, device=dev)
+        self.root = torch.empty(32, dtype=torch.uint8, device=dev)
+
+    def __call__(self, stream=None) -> torch.Tensor:
+        _check(lib().pulse_hash_tree(self.arr, self.n, _p(self.leaves), _p(self.root),
+                                     _p(self.ws), self.ws.numel(), _stream(stream)),
+               "pulse_hash_tree")
+        return self.root
+
+
+def hash_tree(tensors: Sequence[torch.Tensor], stream=None):
+    """Weight hash of the tensors: (root [32] uint8, leaf digests [nleaves, 32] uint8)."""
+    b = HashBatch(tensors)
+    b(stream)
+    return b.root, b.leaves[:b.nleaves]

@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 17, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name
@@ -125,3 +125,30 @@ def test_outer_step_validation(L):
     assert step(A, A, 10, 0, bad, 1, 0.9, 0.7, None) == EINVAL
     bad[0] = pulse._SparseList(A + 2, A, 10, A, A)
     assert step(A, A, 10, 0, bad, 1, 0.9, 0.7, None) == EALIGN
+
+
+def test_hash_sizes_and_validation(L):
+    assert L.pulse_hash_leaf_count(0) == 0
+    assert L.pulse_hash_leaf_count(1) == 1
+    assert L.pulse_hash_leaf_count(8192) == 1
+    assert L.pulse_hash_leaf_count(8193) == 2
+    assert L.pulse_hash_leaf_count(32_763_417_600) == 3_999_441
+    # table + one 16 KiB scratch slot per tensor + two tree-level buffers
+    assert L.pulse_hash_workspace_bytes(3, 3 * 8192) >= 3 * 16384
+    wsb = L.pulse_hash_workspace_bytes(2, 200)
+    ws = A * 8
+    arr = (pulse._HashTensor * 2)()
+    arr[0] = pulse._HashTensor(A, 100)
+    arr[1] = pulse._HashTensor(A + 2, 100)
+    h = L.pulse_hash_tree
+    assert h(arr, 2, A, A, ws, wsb, None) == EALIGN
+    assert b"tensor 1" in L.pulse_last_error()
+    arr[1] = pulse._HashTensor(None, 100)
+    assert h(arr, 2, A, A, ws, wsb, None) == EINVAL
+    arr[1] = pulse._HashTensor(A + 4, 100)
+    assert h(arr, 2, A, None, ws, wsb, None) == EINVAL          # root
+    assert h(arr, 2, None, A, ws, wsb, None) == EINVAL          # leaf digests
+    assert h(arr, 2, A, A, None, wsb, None) == EINVAL           # workspace
+    assert h(arr, 2, A, A, ws + 4, wsb, None) == EALIGN
+    assert h(arr, 2, A, A, ws, wsb - 1, None) == EINVAL
+    assert h(None, 2, A, A, ws, wsb, None) == EINVAL
