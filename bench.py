@@ -12,8 +12,10 @@ pass.  That step is the headline.
 Also measured, outside the headline: the unfused form (encode, then the
 standalone scatter apply of the patch into the inference copy) and the
 PULSELoCo rounds over the 7B-shaped set (10 rounds, fixed threshold): the
-error-feedback sparsification and the outer step that consumes its patch.  All inputs are generated on the GPU before timing and stay
-resident in HBM.
+error-feedback sparsification and the outer step that consumes its patch;
+the patch's delta-varint index stream; and the weight hash (a SHA-256 tree)
+of the refreshed inference copy that a receiver checks.  All inputs are
+generated on the GPU before timing and stay resident in HBM.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
@@ -38,6 +40,14 @@ WORKLOAD_IDS = {"0.5b": 2, "7b": 3, "32b": 4}
 CHUNK = 64  # tensors per launch (the library's batch limit)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "encode_fused_32b_traffic.txt")
 CALIB_WORDS = 1 << 28  # int32 words of the plain copy kernel run for counter calibration
+# Vector-ALU peak for 32-bit integer work: 256 CUs x 4 SIMDs x 16 lanes, one
+# operation per lane per clock, at 2.4 GHz (lane-operations per second).
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+# VALU instructions of one SHA-256 compression in the leaf kernel: per round 6
+# rotates, 4 three-input bitwise ops (two XOR3, Ch, Maj) and 4 adds; per
+# schedule step 4 rotates, 2 shifts, 2 XOR3 and 2 adds; 8 adds into the state;
+# 16 byte permutes assembling the message words; 3 of loop control.
+SHA_VALU_PER_BLOCK = 64 * 14 + 48 * 10 + 8 + 16 + 3
 
 
 def log(*a):
@@ -125,6 +135,7 @@ def main():
     ap.add_argument("--no-loco", action="store_true", help="skip the PULSELoCo leg")
     ap.add_argument("--loco-rounds", type=int, default=10)
     ap.add_argument("--no-varint", action="store_true", help="skip the wire-format (delta-varint) leg")
+    ap.add_argument("--no-hash", action="store_true", help="skip the weight-hash leg")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -241,6 +252,9 @@ def main():
     # ---- the patch's wire format: delta-varint index stream, encoded and decoded
     varint = None if args.no_varint else varint_leg(args, ps, idx, count, seg, sent, ws, stream)
 
+    # ---- the weight hash a receiver checks after applying the patch
+    whash = None if args.no_hash else hash_leg(args, ps, stream)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(ps, args.cpu_sample, idx, val, seg, nnz, cap)
@@ -286,6 +300,7 @@ def main():
         "cpu_baseline": cpu,
         "legs": {
             "varint_patch": varint,
+            "weight_hash": whash,
             "encode_then_apply": {
                 "ms_per_step": round(unf_ms, 4),
                 "GBps_scanned": round(6.0 * ps.N / (unf_ms * 1e-3) / 1e9, 2),
@@ -353,6 +368,46 @@ def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
         "encode_GBps_algorithmic": round(enc_bytes / enc_ms / 1e6, 2),
         "decode_GBps_algorithmic": round(dec_bytes / dec_ms / 1e6, 2),
         "kernels": "varint_encode_kernel; varint_gaps_kernel + varint_sums_kernel",
+    }
+
+
+def hash_leg(args, ps, stream):
+    """Weight hash (App. J.4) of the refreshed BF16 inference copy: a SHA-256 tree
+    over 16 KiB chunks of its bytes, the check a receiver runs after a patch."""
+    import numpy as np
+    import torch
+    from paper_2602_03839_amd import pulse
+
+    batch = pulse.HashBatch([ps.view(ps.R, i) for i in range(len(ps.specs))])
+    reps = max(3, args.steps)
+    times, roots = [], set()
+    for r in range(reps + 1):
+        a, b = event_pair()
+        a.record(stream)
+        batch(stream)
+        b.record(stream)
+        b.synchronize()
+        roots.add(bytes(batch.root.cpu().numpy()))
+        if r:
+            times.append(a.elapsed_time(b))
+    assert len(roots) == 1, "the weight hash changed between calls on unchanged weights"
+    ms = float(np.median(times))
+    blocks = batch.nleaves * ((pulse.HASH_LEAF_BYTES + 1 + 1 + 8 + 63) // 64)
+    tops = blocks * SHA_VALU_PER_BLOCK / (ms * 1e-3) / 1e12
+    log(f"[bench] weight hash: {batch.nleaves:,} leaves of 16 KiB in {ms:.3f} ms "
+        f"({2.0 * ps.N / ms / 1e6:.0f} GB/s of BF16; {tops:.1f} T lane-ops/s = "
+        f"{tops / ALU_PEAK_TOPS:.1%} of the vector-ALU peak)")
+    nleaves = batch.nleaves
+    del batch
+    return {
+        "leaves": nleaves,
+        "root": roots.pop().hex(),
+        "ms": round(ms, 4),
+        "GBps_bf16_hashed": round(2.0 * ps.N / ms / 1e6, 2),
+        "roofline": {"bound": "alu", "achieved": round(tops, 3), "peak": round(ALU_PEAK_TOPS, 3),
+                     "unit": "T lane-ops/s", "frac": round(tops / ALU_PEAK_TOPS, 4),
+                     "valu_per_64B_block": SHA_VALU_PER_BLOCK},
+        "kernels": "hash_setup_kernel + hash_leaf_kernel + hash_tree_kernel (whole call timed)",
     }
 
 
