@@ -16,6 +16,10 @@ and marshals numpy arrays into it with ctypes.
     outer_step(theta, m, lists, ...) Sec. 4.3 Alg. 2 (SparseSync average, outer Nesterov step)
     varint_encode(idx) / varint_decode(stream)
                                      App. H.2 / App. F.3 delta-varint index stream
+    fp8_e4m3(y) / cast_fp8 / cast_mxfp4
+                                     App. D compute views cast_D for FP8 E4M3 and MXFP4
+    encode_fp8 / encode_mxfp4 / apply_fp8 / apply_mxfp4 / loco_gate_lp
+                                     Alg. 1 and Alg. 2's gate for receivers computing in D
     sha256(msg)                      FIPS 180-4 SHA-256 (the primitive of App. J.4's hash)
     leaf_hashes(stream) / merkle_root(digests) / tree_hash(tensors)
                                      App. J.4 weight hash, read as an RFC 6962 tree
@@ -72,6 +76,25 @@ def _load():
             lib.oracle_varint_encode.restype = u64
             lib.oracle_varint_decode.argtypes = [vp, u64, vp, u64]
             lib.oracle_varint_decode.restype = ctypes.c_int64
+            lib.oracle_fp8_e4m3.argtypes = [f32]
+            lib.oracle_fp8_e4m3.restype = ctypes.c_uint8
+            lib.oracle_fp8_value.argtypes = [ctypes.c_uint8]
+            lib.oracle_fp8_value.restype = ctypes.c_double
+            lib.oracle_cast_fp8.argtypes = [vp, vp, u64, f32]
+            lib.oracle_cast_fp8.restype = None
+            lib.oracle_cast_mxfp4.argtypes = [vp, u64, vp, vp]
+            lib.oracle_cast_mxfp4.restype = None
+            lib.oracle_encode_fp8.argtypes = [vp, vp, u64, f32, u32, vp, vp, u64, u64]
+            lib.oracle_encode_fp8.restype = u64
+            lib.oracle_encode_mxfp4.argtypes = [vp, vp, vp, u64, u32, vp, vp, u64, u64]
+            lib.oracle_encode_mxfp4.restype = u64
+            lib.oracle_apply_fp8.argtypes = [vp, u64, vp, vp, u64, u64, u32]
+            lib.oracle_apply_fp8.restype = u64
+            lib.oracle_apply_mxfp4.argtypes = [vp, vp, u64, vp, vp, u64, u64, u32]
+            lib.oracle_apply_mxfp4.restype = u64
+            lib.oracle_loco_gate_lp.argtypes = [ctypes.c_int, f32, vp, vp, u64, vp, u32, vp, vp,
+                                                u64, u64]
+            lib.oracle_loco_gate_lp.restype = u64
             lib.oracle_sha256.argtypes = [vp, u64, vp]
             lib.oracle_sha256.restype = None
             lib.oracle_leaf_hashes.argtypes = [vp, u64, u64, vp]
@@ -241,6 +264,118 @@ def varint_decode(stream) -> np.ndarray:
     out = np.zeros(max(n, 1), dtype=np.uint32)
     L.oracle_varint_decode(_ptr(stream), stream.size, _ptr(out), n)
     return out[:n]
+
+
+FP8, MXFP4 = 1, 2  # receiver compute dtypes of App. D
+
+
+def fp8_e4m3(y: float) -> int:
+    """E4M3 code of one FP32 value (nearest, ties to even code, saturating)."""
+    return int(_load().oracle_fp8_e4m3(float(np.float32(y))))
+
+
+def fp8_value(c: int) -> float:
+    return float(_load().oracle_fp8_value(int(c) & 0xFF))
+
+
+def cast_fp8(x, inv_scale: float = 1.0) -> np.ndarray:
+    """FP8 E4M3 codes (uint8) of fl32(x * inv_scale)."""
+    x = _f32(x).ravel()
+    out = np.zeros(x.size, dtype=np.uint8)
+    _load().oracle_cast_fp8(_ptr(x), _ptr(out), x.size, float(np.float32(inv_scale)))
+    return out
+
+
+def cast_mxfp4(x):
+    """MXFP4 view of one tensor: (packed codes uint8[(n+1)//2], scales uint8[(n+31)//32])."""
+    x = _f32(x).ravel()
+    n = x.size
+    codes = np.zeros(max((n + 1) // 2, 1), dtype=np.uint8)
+    scales = np.zeros(max((n + 31) // 32, 1), dtype=np.uint8)
+    _load().oracle_cast_mxfp4(_ptr(x), n, _ptr(codes), _ptr(scales))
+    return codes[:(n + 1) // 2], scales[:(n + 31) // 32]
+
+
+def mx_codes(packed: np.ndarray, n: int) -> np.ndarray:
+    """Unpack MXFP4 codes: one uint8 (0..15) per value."""
+    p = np.asarray(packed, dtype=np.uint8)
+    out = np.empty(2 * p.size, dtype=np.uint8)
+    out[0::2] = p & 0xF
+    out[1::2] = p >> 4
+    return out[:n]
+
+
+def encode_fp8(w_new, snap, inv_scale: float = 1.0, index_base: int = 0,
+               capacity: int | None = None, count_in: int = 0):
+    """Alg. 1 Encode for an FP8 receiver: (count, idx uint32, val uint8)."""
+    w_new = _f32(w_new).ravel()
+    snap = np.ascontiguousarray(snap, dtype=np.uint8).ravel()
+    n = w_new.size
+    assert snap.size == n
+    if capacity is None:
+        capacity = count_in + n
+    idx = np.zeros(max(capacity, 1), dtype=np.uint32)
+    val = np.zeros(max(capacity, 1), dtype=np.uint8)
+    cnt = _load().oracle_encode_fp8(_ptr(w_new), _ptr(snap), n, float(np.float32(inv_scale)),
+                                    index_base, _ptr(idx), _ptr(val), capacity, count_in)
+    return int(cnt), idx, val
+
+
+def encode_mxfp4(w_new, snap_codes, snap_scales, index_base: int = 0,
+                 capacity: int | None = None, count_in: int = 0):
+    """Alg. 1 Encode for an MXFP4 receiver: (count, idx uint32, val uint16 = scale << 8 | code)."""
+    w_new = _f32(w_new).ravel()
+    n = w_new.size
+    sc = np.ascontiguousarray(snap_codes, dtype=np.uint8)
+    ss = np.ascontiguousarray(snap_scales, dtype=np.uint8)
+    assert sc.size >= (n + 1) // 2 and ss.size >= (n + 31) // 32
+    if capacity is None:
+        capacity = count_in + n
+    idx = np.zeros(max(capacity, 1), dtype=np.uint32)
+    val = np.zeros(max(capacity, 1), dtype=np.uint16)
+    cnt = _load().oracle_encode_mxfp4(_ptr(w_new), _ptr(sc) if sc.size else None,
+                                      _ptr(ss) if ss.size else None, n, index_base, _ptr(idx),
+                                      _ptr(val), capacity, count_in)
+    return int(cnt), idx, val
+
+
+def apply_fp8(dst: np.ndarray, idx, val, begin: int = 0, end: int | None = None,
+              index_base: int = 0) -> int:
+    assert dst.dtype == np.uint8 and dst.flags["C_CONTIGUOUS"]
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    val = np.ascontiguousarray(val, dtype=np.uint8)
+    end = idx.size if end is None else end
+    return int(_load().oracle_apply_fp8(_ptr(dst), dst.size, _ptr(idx), _ptr(val), begin, end,
+                                        index_base))
+
+
+def apply_mxfp4(codes: np.ndarray, scales: np.ndarray, n: int, idx, val, begin: int = 0,
+                end: int | None = None, index_base: int = 0) -> int:
+    assert codes.dtype == np.uint8 and scales.dtype == np.uint8
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    val = np.ascontiguousarray(val, dtype=np.uint16)
+    end = idx.size if end is None else end
+    return int(_load().oracle_apply_mxfp4(_ptr(codes), _ptr(scales), n, _ptr(idx), _ptr(val),
+                                          begin, end, index_base))
+
+
+def loco_gate_lp(dtype: int, delta, residual: np.ndarray, theta, inv_scale: float = 1.0,
+                 index_base: int = 0, capacity: int | None = None, count_in: int = 0):
+    """Alg. 2 selection by the gate of a receiver computing in D (FP8 or MXFP4);
+    ``residual`` is updated in place.  Returns (count, idx, val)."""
+    delta = _f32(delta).ravel()
+    theta = _f32(theta).ravel()
+    assert residual.dtype == np.float32 and residual.flags["C_CONTIGUOUS"]
+    n = delta.size
+    assert residual.size == n and theta.size == n and dtype in (FP8, MXFP4)
+    if capacity is None:
+        capacity = count_in + n
+    idx = np.zeros(max(capacity, 1), dtype=np.uint32)
+    val = np.zeros(max(capacity, 1), dtype=np.float32)
+    cnt = _load().oracle_loco_gate_lp(dtype, float(np.float32(inv_scale)), _ptr(delta),
+                                      _ptr(residual), n, _ptr(theta), index_base, _ptr(idx),
+                                      _ptr(val), capacity, count_in)
+    return int(cnt), idx, val
 
 
 LEAF_BYTES = 16384

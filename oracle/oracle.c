@@ -25,6 +25,11 @@
  *   oracle_varint_encode App. H.2 (index encoding: sorted, first index as-is,
  *   oracle_varint_decode then differences) and App. F.3 (PULSELoCo's sparse
  *                        stream: delta-encoded, varint-packed indices).
+ *   oracle_fp8_e4m3,     App. D (lower-precision receivers): the compute view
+ *   oracle_cast_fp8,     cast_D for D = FP8 E4M3 and MXFP4, Alg. 1's encode and
+ *   oracle_cast_mxfp4,   apply on D-values, and the gate G_D of Alg. 2 for a
+ *   oracle_encode_fp8/_mxfp4, oracle_apply_fp8/_mxfp4, oracle_loco_gate_lp
+ *                        receiver that computes in D.
  *   oracle_sha256        App. J.4 (weight-level integrity hash): SHA-256 as
  *   oracle_leaf_hashes   FIPS 180-4 defines it, applied as a tree (RFC 6962
  *   oracle_merkle_root   Merkle Tree Hash) over fixed-size chunks of the
@@ -495,4 +500,261 @@ void oracle_merkle_root(const uint8_t *digests, uint64_t nleaves, uint8_t root[3
         sha256_with(&c, NULL, 0, root);
     else
         mth(&c, digests, 0, nleaves, root);
+}
+
+/* ------------------------------------------------------------------------
+ * Lower-precision receivers (App. D): the compute view cast_D for
+ * D = FP8 E4M3 and D = MXFP4, the patch of changed D-values, its apply, and
+ * the compute-visibility gate G_D(theta, s) = {i : cast_D(theta_i) !=
+ * cast_D(theta_i - s_i)} (App. D, its opening definition).
+ *
+ * Formats (OCP 8-bit floating point and OCP Microscaling v1.0, which App. D
+ * names): FP8 E4M3 has bias 7, 3 mantissa bits, subnormals, no infinity,
+ * NaN = S.1111.111, largest finite 448.  MXFP4 holds blocks of 32 consecutive
+ * values of a tensor (the last block of a tensor may be shorter) as one E8M0
+ * scale 2^E (byte E + 127) and 32 E2M1 codes (sign, 2 exponent bits, 1
+ * mantissa bit: magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6), two codes per byte,
+ * the even-indexed value in the low nibble.
+ *
+ * Readings (listed in the design notes):
+ *   - FP8 values carry a per-tensor FP32 scale: the receiver computes with
+ *     y = fl32(x * inv_scale) cast to E4M3, rounded to nearest with ties to
+ *     the even code, saturating to +-448 (also for +-inf); NaN -> 0x7F with
+ *     the sign kept; the sign of a value rounding to zero is kept.
+ *   - MXFP4: E = clamp(exponent field of the block's largest |x| - 129,
+ *     -127, 127), i.e. floor(log2(amax)) - 2 for a normal amax (2 = the
+ *     exponent of E2M1's largest value); zero and subnormal amax give -127,
+ *     an infinite one 126.  A block holding a NaN gets scale byte 0xFF and
+ *     all codes 0.  Each code is x / 2^E rounded to the nearest E2M1 value,
+ *     ties to the even code, saturating to +-6, sign kept.
+ *   - Compute view of an MXFP4 value = (its block's scale byte, its code);
+ *     a patch entry carries both as (scale << 8) | code.
+ * ------------------------------------------------------------------------ */
+
+static double fp8_value(int c) /* c in 0..0x7E, magnitude */
+{
+    int e = c >> 3, m = c & 7;
+    return e == 0 ? ldexp((double)m, -9) : ldexp((double)(8 + m), e - 10);
+}
+
+uint8_t oracle_fp8_e4m3(float y)
+{
+    if (isnan(y))
+        return (uint8_t)(0x7F | (signbit(y) ? 0x80 : 0));
+    if (isinf(y)) /* saturating: the largest finite code */
+        return (uint8_t)(0x7E | (signbit(y) ? 0x80 : 0));
+    double a = fabs((double)y);
+    int best = 0;
+    double bd = a; /* distance to code 0 */
+    for (int c = 1; c <= 0x7E; c++) {
+        double d = fabs(a - fp8_value(c));
+        if (d < bd || (d == bd && (c & 1) == 0)) {
+            bd = d;
+            best = c;
+        }
+    }
+    return (uint8_t)(best | (signbit(y) ? 0x80 : 0));
+}
+
+double oracle_fp8_value(uint8_t c)
+{
+    if ((c & 0x7F) == 0x7F)
+        return NAN;
+    double v = fp8_value(c & 0x7F);
+    return (c & 0x80) ? -v : v;
+}
+
+void oracle_cast_fp8(const float *x, uint8_t *out, uint64_t n, float inv_scale)
+{
+    for (uint64_t i = 0; i < n; i++) {
+        float y = x[i] * inv_scale;
+        out[i] = oracle_fp8_e4m3(y);
+    }
+}
+
+static const double e2m1_mag[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
+
+static uint8_t e2m1_code(double q) /* q finite or infinite, not NaN */
+{
+    if (isinf(q)) /* saturating: the largest magnitude, 6 */
+        return (uint8_t)(7 | (signbit(q) ? 8 : 0));
+    double a = fabs(q);
+    int best = 0;
+    double bd = a;
+    for (int c = 1; c < 8; c++) {
+        double d = fabs(a - e2m1_mag[c]);
+        if (d < bd || (d == bd && (c & 1) == 0)) {
+            bd = d;
+            best = c;
+        }
+    }
+    return (uint8_t)(best | (signbit(q) ? 8 : 0));
+}
+
+/* scale byte and codes of the block x[0..len) */
+static uint8_t mx_block(const float *x, uint64_t len, uint8_t *codes)
+{
+    float amax = 0.0f;
+    for (uint64_t i = 0; i < len; i++) {
+        if (isnan(x[i])) {
+            for (uint64_t j = 0; j < len; j++)
+                codes[j] = 0;
+            return 0xFF;
+        }
+        if (fabsf(x[i]) > amax)
+            amax = fabsf(x[i]);
+    }
+    int ef = (int)((bits_from_float(amax) >> 23) & 0xFF);
+    int E = ef - 129;
+    if (E < -127)
+        E = -127;
+    if (E > 127)
+        E = 127;
+    for (uint64_t i = 0; i < len; i++)
+        codes[i] = e2m1_code(ldexp((double)x[i], -E)); /* exact in double */
+    return (uint8_t)(E + 127);
+}
+
+/* codes: (n + 1) / 2 bytes, scales: (n + 31) / 32 bytes */
+void oracle_cast_mxfp4(const float *x, uint64_t n, uint8_t *codes, uint8_t *scales)
+{
+    uint8_t c[32];
+    memset(codes, 0, (n + 1) / 2);
+    for (uint64_t b = 0; b * 32 < n; b++) {
+        uint64_t len = n - b * 32 < 32 ? n - b * 32 : 32;
+        scales[b] = mx_block(x + b * 32, len, c);
+        for (uint64_t i = 0; i < len; i++) {
+            uint64_t k = b * 32 + i;
+            codes[k / 2] |= (uint8_t)(c[i] << (4 * (k & 1)));
+        }
+    }
+}
+
+static uint8_t nibble(const uint8_t *codes, uint64_t k) { return (codes[k / 2] >> (4 * (k & 1))) & 0xF; }
+
+/* Encode for an FP8 receiver: emit (index_base + i, code) wherever the code of
+ * fl32(w_new * inv_scale) differs from snap[i]; capacity/count as oracle_encode. */
+uint64_t oracle_encode_fp8(const float *w_new, const uint8_t *snap, uint64_t n, float inv_scale,
+                           uint32_t index_base, uint32_t *idx, uint8_t *val, uint64_t capacity,
+                           uint64_t count_in)
+{
+    uint64_t count = count_in;
+    for (uint64_t i = 0; i < n; i++) {
+        uint8_t c = oracle_fp8_e4m3(w_new[i] * inv_scale);
+        if (c != snap[i]) {
+            if (count < capacity) {
+                idx[count] = index_base + (uint32_t)i;
+                val[count] = c;
+            }
+            count++;
+        }
+    }
+    return count;
+}
+
+/* Encode for an MXFP4 receiver: emit (index_base + i, (scale << 8) | code)
+ * wherever the value's block scale or code differs from the snapshot's. */
+uint64_t oracle_encode_mxfp4(const float *w_new, const uint8_t *snap_codes,
+                             const uint8_t *snap_scales, uint64_t n, uint32_t index_base,
+                             uint32_t *idx, uint16_t *val, uint64_t capacity, uint64_t count_in)
+{
+    uint64_t count = count_in;
+    uint8_t c[32];
+    for (uint64_t b = 0; b * 32 < n; b++) {
+        uint64_t len = n - b * 32 < 32 ? n - b * 32 : 32;
+        uint8_t s = mx_block(w_new + b * 32, len, c);
+        for (uint64_t i = 0; i < len; i++) {
+            uint64_t k = b * 32 + i;
+            if (s != snap_scales[b] || c[i] != nibble(snap_codes, k)) {
+                if (count < capacity) {
+                    idx[count] = index_base + (uint32_t)k;
+                    val[count] = (uint16_t)((s << 8) | c[i]);
+                }
+                count++;
+            }
+        }
+    }
+    return count;
+}
+
+/* Apply for an FP8 receiver: dst[idx[k] - index_base] = val[k], k in [begin, end);
+ * returns the number of entries outside dst. */
+uint64_t oracle_apply_fp8(uint8_t *dst, uint64_t n, const uint32_t *idx, const uint8_t *val,
+                          uint64_t begin, uint64_t end, uint32_t index_base)
+{
+    uint64_t rejected = 0;
+    for (uint64_t k = begin; k < end; k++) {
+        uint64_t j = (uint64_t)idx[k] - index_base;
+        if (idx[k] < index_base || j >= n) {
+            rejected++;
+            continue;
+        }
+        dst[j] = val[k];
+    }
+    return rejected;
+}
+
+/* Apply for an MXFP4 receiver: the entry's code into its nibble and its scale
+ * into its block's scale byte. */
+uint64_t oracle_apply_mxfp4(uint8_t *codes, uint8_t *scales, uint64_t n, const uint32_t *idx,
+                            const uint16_t *val, uint64_t begin, uint64_t end, uint32_t index_base)
+{
+    uint64_t rejected = 0;
+    for (uint64_t k = begin; k < end; k++) {
+        uint64_t j = (uint64_t)idx[k] - index_base;
+        if (idx[k] < index_base || j >= n) {
+            rejected++;
+            continue;
+        }
+        int sh = 4 * (int)(j & 1);
+        codes[j / 2] = (uint8_t)((codes[j / 2] & ~(0xF << sh)) | ((val[k] & 0xF) << sh));
+        scales[j / 32] = (uint8_t)(val[k] >> 8);
+    }
+    return rejected;
+}
+
+/* The PULSELoCo gate for a receiver computing in D (dtype 1 = FP8 E4M3 with
+ * inv_scale, 2 = MXFP4): a = fl32(delta + e); keep i iff cast_D(theta)_i !=
+ * cast_D(theta - a)_i (for MXFP4 the (scale, code) pairs, each vector with its
+ * own block scales); emission, capacity and residual exactly as oracle_loco. */
+uint64_t oracle_loco_gate_lp(int dtype, float inv_scale, const float *delta, float *residual,
+                             uint64_t n, const float *theta, uint32_t index_base, uint32_t *idx,
+                             float *val, uint64_t capacity, uint64_t count_in)
+{
+    float *a = malloc((n ? n : 1) * sizeof(float));
+    float *after = malloc((n ? n : 1) * sizeof(float));
+    uint8_t *keep = malloc(n ? n : 1);
+    for (uint64_t i = 0; i < n; i++) {
+        a[i] = delta[i] + residual[i];
+        after[i] = theta[i] - a[i];
+    }
+    if (dtype == 1) {
+        for (uint64_t i = 0; i < n; i++)
+            keep[i] = oracle_fp8_e4m3(theta[i] * inv_scale) != oracle_fp8_e4m3(after[i] * inv_scale);
+    } else {
+        uint8_t c0[32], c1[32];
+        for (uint64_t b = 0; b * 32 < n; b++) {
+            uint64_t len = n - b * 32 < 32 ? n - b * 32 : 32;
+            uint8_t s0 = mx_block(theta + b * 32, len, c0);
+            uint8_t s1 = mx_block(after + b * 32, len, c1);
+            for (uint64_t i = 0; i < len; i++)
+                keep[b * 32 + i] = s0 != s1 || c0[i] != c1[i];
+        }
+    }
+    uint64_t count = count_in;
+    for (uint64_t i = 0; i < n; i++) {
+        if (keep[i] && count < capacity) {
+            idx[count] = index_base + (uint32_t)i;
+            val[count] = a[i];
+            residual[i] = 0.0f;
+        } else {
+            residual[i] = a[i];
+        }
+        if (keep[i])
+            count++;
+    }
+    free(a);
+    free(after);
+    free(keep);
+    return count;
 }
