@@ -312,6 +312,96 @@ int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t 
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Receivers that compute in a precision below BF16 (App. D): the compute view
+ * cast_D of the FP32 masters, the patch of the values whose view changes
+ * (Alg. 1 with D in place of BF16), and its apply on the receiver's D copy.
+ *   PULSE_DTYPE_FP8_E4M3  OCP FP8 E4M3 (bias 7, no infinity, largest 448).
+ *       A tensor carries an FP32 scale: the receiver computes with
+ *       fl32(w * inv_scale), rounded to the nearest code (ties to the even
+ *       code), saturating to +-448 (also for +-inf); NaN -> 0x7F with its sign.
+ *       One uint8 code per value.
+ *   PULSE_DTYPE_MXFP4     OCP MXFP4: blocks of 32 consecutive values of a
+ *       tensor (the last may be shorter) share one E8M0 scale byte E + 127,
+ *       E = clamp(exponent field of the block's largest |w| - 129, -127, 127)
+ *       (= floor(log2 max|w|) - 2 for a normal maximum); each value is the
+ *       E2M1 code (sign, 2 exponent bits, 1 mantissa bit) of w / 2^E, nearest
+ *       with ties to the even code, saturating to +-6.  A block holding a NaN
+ *       gets scale 0xFF and codes 0.  Codes are packed two per byte, the
+ *       even-indexed value in the low nibble: (n + 1) / 2 code bytes and
+ *       (n + 31) / 32 scale bytes per tensor.  A value's compute view is the
+ *       pair (its block's scale, its code); a patch entry's value is
+ *       (scale << 8) | code as uint16, so a scale change re-sends its block.
+ */
+#define PULSE_DTYPE_FP8_E4M3 1
+#define PULSE_DTYPE_MXFP4 2
+
+/* Dense D view of one tensor: FP8 codes[n] (8-byte aligned), or MXFP4 packed
+ * codes (4-byte aligned) and scales. `src` 16-byte aligned; inv_scale is
+ * used by FP8 only; scales may be NULL for FP8. */
+int pulse_cast_lowp(int dtype, const float *src, uint64_t n, float inv_scale,
+                    uint8_t *codes, uint8_t *scales, void *stream);
+
+typedef struct pulse_lowp_tensor {
+    const float *w_new;          /* FP32 masters, 16-byte aligned */
+    const uint8_t *snap;         /* the receiver's D view: FP8 codes (8-byte aligned) or
+                                    MXFP4 packed codes (4-byte aligned) */
+    const uint8_t *snap_scales;  /* MXFP4 scale bytes; unused for FP8 */
+    uint64_t n;
+    uint32_t index_base;
+    float inv_scale;             /* FP8 only */
+} pulse_lowp_tensor;
+
+/*
+ * pulse_encode_lowp_batch -- Alg. 1 Encode for a receiver computing in D:
+ * every value whose D view differs bitwise from the snapshot's is emitted as
+ * (index_base + i, value) in index order, tensors in the order given; value =
+ * the FP8 code (val: uint8[capacity]) or (scale << 8) | code (val:
+ * uint16[capacity], 2-byte aligned).  idx, count, seg_begin, capacity and
+ * the workspace follow pulse_encode_batch.  The snapshot is not refreshed:
+ * the receiver's copy is brought up to date by pulse_apply_lowp_batch.
+ */
+int pulse_encode_lowp_batch(int dtype, const pulse_lowp_tensor *tensors, uint32_t ntensors,
+                            uint32_t *idx, void *val, uint64_t capacity, uint64_t *count,
+                            uint64_t *seg_begin, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
+typedef struct pulse_lowp_apply_tensor {
+    uint8_t *codes;   /* FP8 codes or MXFP4 packed codes */
+    uint8_t *scales;  /* MXFP4 scale bytes; unused for FP8 */
+    uint64_t n;
+    uint32_t index_base;
+} pulse_lowp_apply_tensor;
+
+/*
+ * pulse_apply_lowp_batch -- Alg. 1 Decode on a D copy: entry k of tensor t's
+ * segment [seg_begin[t], next start or *end) writes its code to value
+ * idx[k] - index_base (MXFP4: its nibble, and its scale to the value's
+ * block).  Indices must be unique and ascending within a segment (as encode
+ * writes them); entries outside the tensor are counted in *rejected.
+ */
+int pulse_apply_lowp_batch(int dtype, const pulse_lowp_apply_tensor *tensors, uint32_t ntensors,
+                           const uint32_t *idx, const void *val, uint64_t capacity,
+                           const uint64_t *seg_begin, const uint64_t *end,
+                           uint64_t *rejected, void *stream);
+
+/*
+ * pulse_loco_sparsify_lowp_batch -- Alg. 2's selection with the gate of a
+ * receiver that computes in D (App. D: G_D(theta, s) = {i : cast_D(theta_i) !=
+ * cast_D(theta_i - s_i)}): a = fl32(delta + e) is selected iff
+ * cast_D(theta) and cast_D(fl32(theta - a)) differ at i -- for FP8 the codes
+ * of fl32(theta * inv_scales[t]) and fl32((theta - a) * inv_scales[t]), for
+ * MXFP4 the (block scale, code) pairs, each vector's blocks scaled by their
+ * own maximum.  Every tensor needs theta; inv_scales (host array, one per
+ * tensor) is read for FP8 only.  Emission, capacity, residual, counts and the
+ * workspace are those of pulse_loco_sparsify_batch.
+ */
+int pulse_loco_sparsify_lowp_batch(int dtype, const pulse_loco_tensor *tensors,
+                                   const float *inv_scales, uint32_t ntensors,
+                                   uint32_t *idx, float *val, uint64_t capacity, uint64_t *count,
+                                   uint64_t *seg_begin, void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
+/*
  * Weight hash (App. J.4 "Weight-level integrity", "Deterministic hashing"):
  * a SHA-256 digest of the BF16 bit patterns of all tensors, concatenated in
  * the order given, that the sender publishes with each patch and the receiver

@@ -66,12 +66,17 @@ struct EncodeParams {
   EncodeTensorDesc t[kMaxBatch];
 };
 
+// Receivers that compute in a lower precision than BF16 (App. D).
+constexpr int kDtypeFp8 = 1;    // OCP FP8 E4M3, per-tensor FP32 scale
+constexpr int kDtypeMxfp4 = 2;  // OCP MXFP4: E8M0 scale per 32 values, E2M1 codes
+
 struct LocoTensorDesc {
   const float* delta;
   float* residual;
   const float* theta;
   uint64_t n;
   uint32_t index_base;
+  float inv_scale;  // FP8 gate: the receiver's per-tensor scale
 };
 
 struct LocoParams {
@@ -82,6 +87,7 @@ struct LocoParams {
   uint64_t* count;
   uint64_t* seg_begin;
   float tau;
+  int gate_dtype;  // with theta: 0 = BF16 gate, kDtypeFp8 / kDtypeMxfp4 = that receiver's gate
   uint32_t ntiles;
   int ntensors;
   uint32_t tile_begin[kMaxBatch + 1];
@@ -161,6 +167,53 @@ struct VarintDecParams {
   uint32_t ntiles2;            // entry tiles
 };
 
+// Receivers that compute in a lower precision D (App. D); kDtypeFp8 and
+// kDtypeMxfp4 are defined above LocoParams.
+
+struct LowpTensorDesc {
+  const float* w_new;
+  const uint8_t* snap;         // FP8: n codes; MXFP4: (n + 1) / 2 bytes of packed codes
+  const uint8_t* snap_scales;  // MXFP4: (n + 31) / 32 scale bytes
+  uint64_t n;
+  uint32_t index_base;
+  float inv_scale;             // FP8: the receiver computes with fl32(w * inv_scale)
+};
+
+struct LowpParams {
+  uint64_t* ws;
+  uint32_t* idx;
+  void* val;  // FP8: uint8 codes; MXFP4: uint16 (scale << 8) | code
+  uint64_t capacity;
+  uint64_t* count;
+  uint64_t* seg_begin;
+  uint32_t ntiles;
+  int ntensors;
+  uint32_t tile_begin[kMaxBatch + 1];
+  LowpTensorDesc t[kMaxBatch];
+};
+
+struct LowpApplyTensorDesc {
+  uint8_t* codes;
+  uint8_t* scales;  // MXFP4 only
+  uint64_t n;
+  uint32_t index_base;
+};
+
+struct LowpApplyParams {
+  const uint32_t* idx;
+  const void* val;
+  uint64_t capacity;
+  const uint64_t* seg_begin;
+  const uint64_t* end;
+  uint64_t* rejected;
+  int ntensors;
+  int dtype;
+  LowpApplyTensorDesc t[kMaxBatch];
+};
+
+static_assert(sizeof(LowpParams) < 4096, "kernel argument block too large");
+static_assert(sizeof(LowpApplyParams) < 4096, "kernel argument block too large");
+
 // Weight hash: a tree of SHA-256 over 16 KiB chunks ("leaves") of the
 // concatenated BF16 bytes.  The tensors' pointers and stream offsets go to a
 // device table in the caller's workspace, written by small setup launches
@@ -228,6 +281,11 @@ uint32_t varint_byte_tile();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
+uint32_t lowp_tile_elems();
+hipError_t launch_encode_lowp(int dtype, LowpParams& p, hipStream_t stream);
+hipError_t launch_apply_lowp(const LowpApplyParams& p, hipStream_t stream);
+hipError_t launch_cast_lowp(int dtype, const float* src, uint64_t n, float inv_scale,
+                            uint8_t* codes, uint8_t* scales, hipStream_t stream);
 hipError_t launch_hash_setup(const HashSetupParams& p, hipStream_t stream);
 hipError_t launch_hash_leaves(const HashLeafParams& p, hipStream_t stream);
 hipError_t launch_hash_tree(const uint8_t* in, uint64_t n_in, uint8_t* out, hipStream_t stream);

@@ -2,7 +2,9 @@
 // Alg. 2): s = Delta + e in FP32, select by threshold |s| >= tau or by the
 // compute-visibility gate bf16(theta) != bf16(theta - s) (Sec. 4.1), emit the
 // selected (index, FP32 value) pairs in index order, and rewrite the residual
-// (0 where sent, s elsewhere) -- one pass over Delta and e.
+// (0 where sent, s elsewhere) -- one pass over Delta and e.  The gate may
+// also be that of a receiver computing in FP8 E4M3 or MXFP4 (App. D):
+// cast_D(theta) != cast_D(theta - s), for MXFP4 on (block scale, code) pairs.
 //
 // Same persistent, pipelined tile structure and ordered compaction as
 // encode.hip (NW compute waves + 1 scan wave; the loads of the next kAhead
@@ -12,6 +14,7 @@
 // so program order keeps the later store).
 #include "device_common.hpp"
 #include "launch.hpp"
+#include "lowp_cast.hpp"
 
 namespace pulse {
 
@@ -107,8 +110,11 @@ struct LocoDeferred {
   uint32_t excl[(U + 1) / 2];
 };
 
-template <int NW, int U, bool GATE>
+// GM: 0 = threshold only, 1 = BF16 gate, 2 = FP8 gate, 3 = MXFP4 gate
+// (tensors without theta use the threshold in every mode).
+template <int NW, int U, int GM>
 __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
+  constexpr bool GATE = GM != 0;
   constexpr int TBC = NW * 64;
   constexpr uint32_t TILE = TBC * U * 8;
   __shared__ uint64_t s_tk[kTkRing];
@@ -194,7 +200,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           const float rv = __uint_as_float(i < 4 ? get_u32(g.r0[u], i) : get_u32(g.r1[u], i - 4));
           a[i] = dv + rv;
         }
-        if (gate) {
+        if (gate && GM == 1) {
           // selected iff bf16(theta) != bf16(theta - a), pairwise on the cvt unit
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -205,6 +211,26 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
             m |= diff2(bf16x2_rne(t_lo, t_hi),
                        bf16x2_rne(__float_as_uint(after_lo), __float_as_uint(after_hi)))
                  << (2 * j);
+          }
+        } else if (gate) {
+          float th[8], af[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint4& tq = i < 4 ? g.t0[GATE ? u : 0] : g.t1[GATE ? u : 0];
+            th[i] = __uint_as_float(get_u32(tq, i & 3));
+            af[i] = th[i] - a[i];
+          }
+          if (GM == 2) {
+            // selected iff fp8(theta * s) != fp8((theta - a) * s)
+            const float is = p.t[ck].inv_scale;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) m |= (uint32_t)(fp8_code(th[i] * is) != fp8_code(af[i] * is)) << i;
+          } else {
+            // selected iff (scale, code) of theta's block != that of theta - a
+            uint32_t c0[8], c1[8];
+            const uint32_t s0 = mx_view8(th, c0), s1 = mx_view8(af, c1);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) m |= (uint32_t)(s0 != s1 || c0[i] != c1[i]) << i;
           }
         } else {
 #pragma unroll
@@ -327,17 +353,21 @@ hipError_t launch_loco(LocoParams& p, hipStream_t stream) {
   }
   bool gate = false;
   for (int k = 0; k < p.ntensors; ++k) gate |= p.t[k].theta != nullptr;
-  const void* fn = gate ? (const void*)loco_kernel<kLocoNW, kLocoU, true>
-                        : (const void*)loco_kernel<kLocoNW, kLocoU, false>;
-  const int grid_cap = persistent_grid(fn, (kLocoNW + 1) * 64);
+  const int gm = !gate ? 0 : p.gate_dtype == kDtypeFp8 ? 2 : p.gate_dtype == kDtypeMxfp4 ? 3 : 1;
+  const void* fns[4] = {(const void*)loco_kernel<kLocoNW, kLocoU, 0>,
+                        (const void*)loco_kernel<kLocoNW, kLocoU, 1>,
+                        (const void*)loco_kernel<kLocoNW, kLocoU, 2>,
+                        (const void*)loco_kernel<kLocoNW, kLocoU, 3>};
+  const int grid_cap = persistent_grid(fns[gm], (kLocoNW + 1) * 64);
   if (grid_cap <= 0) return hipErrorInvalidConfiguration;
   const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
-  if (gate)
-    hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, true>), dim3(grid), dim3((kLocoNW + 1) * 64),
-                       0, stream, p);
-  else
-    hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, false>), dim3(grid),
-                       dim3((kLocoNW + 1) * 64), 0, stream, p);
+  const dim3 block((kLocoNW + 1) * 64);
+  switch (gm) {
+    case 0: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 0>), dim3(grid), block, 0, stream, p); break;
+    case 1: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 1>), dim3(grid), block, 0, stream, p); break;
+    case 2: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 2>), dim3(grid), block, 0, stream, p); break;
+    default: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 3>), dim3(grid), block, 0, stream, p); break;
+  }
   return hipGetLastError();
 }
 

@@ -241,10 +241,14 @@ int pulse_apply(uint16_t* dst, uint64_t n, const uint32_t* idx, const uint16_t* 
   return pulse_apply_batch(&d, 1, idx, val, capacity, begin, end, rejected, stream);
 }
 
-int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensors, float tau,
-                              uint32_t* idx, float* val, uint64_t capacity, uint64_t* count,
-                              uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
-                              void* stream) {
+namespace {
+
+// Shared by the threshold/BF16-gate sparsifier and the lower-precision gate:
+// the per-tensor inv_scale array may be null (no FP8 gate).
+int loco_batch(const pulse_loco_tensor* tensors, const float* inv_scales, uint32_t ntensors,
+               float tau, int gate_dtype, uint32_t* idx, float* val, uint64_t capacity,
+               uint64_t* count, uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
+               void* stream) {
   if (ntensors == 0) return ok();
   if (!tensors) return fail(PULSE_EINVAL, "loco: tensors is NULL");
   if (!count) return fail(PULSE_EINVAL, "loco: count is NULL");
@@ -258,6 +262,7 @@ int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensor
     const pulse_loco_tensor& d = tensors[t];
     if (d.n == 0) continue;
     if (!d.delta || !d.residual) return fail(PULSE_EINVAL, "loco tensor %u: NULL delta/residual", t);
+    if (gate_dtype != 0 && !d.theta) return fail(PULSE_EINVAL, "loco tensor %u: theta is NULL", t);
     if (!aligned16(d.delta) || !aligned16(d.residual) || (d.theta && !aligned16(d.theta)))
       return fail(PULSE_EALIGN, "loco tensor %u: delta/residual/theta not 16-byte aligned", t);
     if (int rc = check_range(d.n, d.index_base, "loco", t)) return rc;
@@ -274,6 +279,7 @@ int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensor
     p.count = count;
     p.seg_begin = seg_begin ? seg_begin + t0 : nullptr;
     p.tau = tau;
+    p.gate_dtype = gate_dtype;
     uint32_t tiles = 0;
     int k = 0;
     while (t0 + k < ntensors && k < pulse::kMaxBatch) {
@@ -286,6 +292,7 @@ int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensor
       p.t[k].theta = d.theta;
       p.t[k].n = d.n;
       p.t[k].index_base = d.index_base;
+      p.t[k].inv_scale = inv_scales ? inv_scales[t0 + k] : 1.0f;
       tiles += nt;
       ++k;
     }
@@ -296,6 +303,29 @@ int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensor
     t0 += k;
   }
   return ok();
+}
+
+}  // namespace
+
+int pulse_loco_sparsify_batch(const pulse_loco_tensor* tensors, uint32_t ntensors, float tau,
+                              uint32_t* idx, float* val, uint64_t capacity, uint64_t* count,
+                              uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  return loco_batch(tensors, nullptr, ntensors, tau, 0, idx, val, capacity, count, seg_begin,
+                    workspace, workspace_bytes, stream);
+}
+
+int pulse_loco_sparsify_lowp_batch(int dtype, const pulse_loco_tensor* tensors,
+                                   const float* inv_scales, uint32_t ntensors, uint32_t* idx,
+                                   float* val, uint64_t capacity, uint64_t* count,
+                                   uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)
+    return fail(PULSE_EINVAL, "loco_lowp: unknown dtype %d", dtype);
+  if (dtype == PULSE_DTYPE_FP8_E4M3 && ntensors > 0 && !inv_scales)
+    return fail(PULSE_EINVAL, "loco_lowp: inv_scales is NULL");
+  return loco_batch(tensors, inv_scales, ntensors, 0.0f, dtype, idx, val, capacity, count,
+                    seg_begin, workspace, workspace_bytes, stream);
 }
 
 int pulse_loco_sparsify(const float* delta, float* residual, uint64_t n, float tau,
@@ -451,6 +481,131 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   p.ntiles = (uint32_t)nt;
   p.ntiles2 = (uint32_t)nt2;
   return hip_status(pulse::launch_varint_decode(p, (hipStream_t)stream), "varint decode launch");
+}
+
+int pulse_cast_lowp(int dtype, const float* src, uint64_t n, float inv_scale, uint8_t* codes,
+                    uint8_t* scales, void* stream) {
+  if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)
+    return fail(PULSE_EINVAL, "cast_lowp: unknown dtype %d", dtype);
+  if (n == 0) return ok();
+  if (!src || !codes || (dtype == PULSE_DTYPE_MXFP4 && !scales))
+    return fail(PULSE_EINVAL, "cast_lowp: NULL pointer");
+  if (!aligned16(src) || !aligned(codes, dtype == PULSE_DTYPE_FP8_E4M3 ? 8 : 4))
+    return fail(PULSE_EALIGN, "cast_lowp: src/codes misaligned");
+  return hip_status(pulse::launch_cast_lowp(dtype, src, n, inv_scale, codes, scales,
+                                            (hipStream_t)stream),
+                    "cast_lowp launch");
+}
+
+int pulse_encode_lowp_batch(int dtype, const pulse_lowp_tensor* tensors, uint32_t ntensors,
+                            uint32_t* idx, void* val, uint64_t capacity, uint64_t* count,
+                            uint64_t* seg_begin, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)
+    return fail(PULSE_EINVAL, "encode_lowp: unknown dtype %d", dtype);
+  if (ntensors == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "encode_lowp: tensors is NULL");
+  if (!count) return fail(PULSE_EINVAL, "encode_lowp: count is NULL");
+  if (capacity > 0 && (!idx || !val))
+    return fail(PULSE_EINVAL, "encode_lowp: idx/val NULL with capacity > 0");
+  if (!aligned(count, 8) || (seg_begin && !aligned(seg_begin, 8)))
+    return fail(PULSE_EALIGN, "encode_lowp: count/seg_begin not 8-byte aligned");
+  if ((idx && !aligned(idx, 4)) || (val && dtype == PULSE_DTYPE_MXFP4 && !aligned(val, 2)))
+    return fail(PULSE_EALIGN, "encode_lowp: idx/val misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  const uintptr_t snap_align = dtype == PULSE_DTYPE_FP8_E4M3 ? 8 : 4;
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_lowp_tensor& d = tensors[t];
+    if (d.n == 0) continue;
+    if (!d.w_new || !d.snap || (dtype == PULSE_DTYPE_MXFP4 && !d.snap_scales))
+      return fail(PULSE_EINVAL, "encode_lowp tensor %u: NULL pointer", t);
+    if (!aligned16(d.w_new) || !aligned(d.snap, snap_align))
+      return fail(PULSE_EALIGN, "encode_lowp tensor %u: w_new/snap misaligned", t);
+    if (int rc = check_range(d.n, d.index_base, "encode_lowp", t)) return rc;
+  }
+  const uint32_t tile = pulse::lowp_tile_elems();
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::LowpParams p;
+    memset(&p, 0, sizeof p);
+    p.ws = (uint64_t*)workspace;
+    p.idx = idx;
+    p.val = val;
+    p.capacity = capacity;
+    p.count = count;
+    p.seg_begin = seg_begin ? seg_begin + t0 : nullptr;
+    uint32_t tiles = 0;
+    int k = 0;
+    while (t0 + k < ntensors && k < pulse::kMaxBatch) {
+      const pulse_lowp_tensor& d = tensors[t0 + k];
+      const uint32_t nt = tiles_for(d.n, tile);
+      if (k > 0 && (uint64_t)tiles + nt > pulse::kMaxTilesPerLaunch) break;
+      p.tile_begin[k] = tiles;
+      p.t[k].w_new = d.w_new;
+      p.t[k].snap = d.snap;
+      p.t[k].snap_scales = d.snap_scales;
+      p.t[k].n = d.n;
+      p.t[k].index_base = d.index_base;
+      p.t[k].inv_scale = d.inv_scale;
+      tiles += nt;
+      ++k;
+    }
+    p.tile_begin[k] = tiles;
+    p.ntensors = k;
+    p.ntiles = tiles;
+    if (int rc = hip_status(pulse::launch_encode_lowp(dtype, p, (hipStream_t)stream),
+                            "encode_lowp launch"))
+      return rc;
+    t0 += k;
+  }
+  return ok();
+}
+
+int pulse_apply_lowp_batch(int dtype, const pulse_lowp_apply_tensor* tensors, uint32_t ntensors,
+                           const uint32_t* idx, const void* val, uint64_t capacity,
+                           const uint64_t* seg_begin, const uint64_t* end, uint64_t* rejected,
+                           void* stream) {
+  if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)
+    return fail(PULSE_EINVAL, "apply_lowp: unknown dtype %d", dtype);
+  if (ntensors == 0 || capacity == 0) return ok();
+  if (!tensors) return fail(PULSE_EINVAL, "apply_lowp: tensors is NULL");
+  if (!idx || !val) return fail(PULSE_EINVAL, "apply_lowp: idx/val is NULL");
+  if (!seg_begin || !end) return fail(PULSE_EINVAL, "apply_lowp: seg_begin/end is NULL");
+  if (!aligned(seg_begin, 8) || !aligned(end, 8) || (rejected && !aligned(rejected, 8)))
+    return fail(PULSE_EALIGN, "apply_lowp: counters not 8-byte aligned");
+  if (!aligned(idx, 4) || (dtype == PULSE_DTYPE_MXFP4 && !aligned(val, 2)))
+    return fail(PULSE_EALIGN, "apply_lowp: idx/val misaligned");
+  for (uint32_t t = 0; t < ntensors; ++t) {
+    const pulse_lowp_apply_tensor& d = tensors[t];
+    if (d.n > 0 && (!d.codes || (dtype == PULSE_DTYPE_MXFP4 && !d.scales)))
+      return fail(PULSE_EINVAL, "apply_lowp tensor %u: NULL codes/scales", t);
+    if (int rc = check_range(d.n, d.index_base, "apply_lowp", t)) return rc;
+  }
+  uint32_t t0 = 0;
+  while (t0 < ntensors) {
+    pulse::LowpApplyParams p;
+    memset(&p, 0, sizeof p);
+    const uint32_t k = (ntensors - t0) < (uint32_t)pulse::kMaxBatch ? (ntensors - t0)
+                                                                     : (uint32_t)pulse::kMaxBatch;
+    p.idx = idx;
+    p.val = val;
+    p.capacity = capacity;
+    p.seg_begin = seg_begin + t0;
+    p.end = (t0 + k < ntensors) ? seg_begin + t0 + k : end;
+    p.rejected = rejected;
+    p.ntensors = (int)k;
+    p.dtype = dtype;
+    for (uint32_t i = 0; i < k; ++i) {
+      p.t[i].codes = tensors[t0 + i].codes;
+      p.t[i].scales = tensors[t0 + i].scales;
+      p.t[i].n = tensors[t0 + i].n;
+      p.t[i].index_base = tensors[t0 + i].index_base;
+    }
+    if (int rc = hip_status(pulse::launch_apply_lowp(p, (hipStream_t)stream), "apply_lowp launch"))
+      return rc;
+    t0 += k;
+  }
+  return ok();
 }
 
 uint64_t pulse_hash_leaf_count(uint64_t total_values) {

@@ -64,6 +64,20 @@ class _SparseList(ctypes.Structure):
 MAX_LISTS = 8  # PULSE_MAX_LISTS
 
 
+class _LowpTensor(ctypes.Structure):
+    _fields_ = [("w_new", ctypes.c_void_p), ("snap", ctypes.c_void_p),
+                ("snap_scales", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("index_base", ctypes.c_uint32), ("inv_scale", ctypes.c_float)]
+
+
+class _LowpApplyTensor(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("n", ctypes.c_uint64),
+                ("index_base", ctypes.c_uint32)]
+
+
+FP8_E4M3, MXFP4 = 1, 2  # PULSE_DTYPE_FP8_E4M3, PULSE_DTYPE_MXFP4
+
+
 class _HashTensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("n", ctypes.c_uint64)]
 
@@ -75,7 +89,9 @@ EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
            "pulse_outer_step", "pulse_outer_step_batch",
            "pulse_varint_encode", "pulse_varint_decode",
-           "pulse_hash_leaf_count", "pulse_hash_workspace_bytes", "pulse_hash_tree")
+           "pulse_hash_leaf_count", "pulse_hash_workspace_bytes", "pulse_hash_tree",
+           "pulse_cast_lowp", "pulse_encode_lowp_batch", "pulse_apply_lowp_batch",
+           "pulse_loco_sparsify_lowp_batch")
 
 
 def lib():
@@ -111,6 +127,11 @@ def lib():
             L.pulse_hash_workspace_bytes.argtypes = [u32, u64]
             L.pulse_hash_workspace_bytes.restype = sz
             L.pulse_hash_tree.argtypes = [vp, u32, vp, vp, vp, sz, vp]
+            L.pulse_cast_lowp.argtypes = [i32, vp, u64, f32, vp, vp, vp]
+            L.pulse_encode_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
+            L.pulse_apply_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, vp]
+            L.pulse_loco_sparsify_lowp_batch.argtypes = [i32, vp, vp, u32, vp, vp, u64, vp, vp, vp,
+                                                         sz, vp]
             for name in EXPORTS[3:]:
                 if name not in ("pulse_hash_leaf_count", "pulse_hash_workspace_bytes"):
                     getattr(L, name).restype = i32
@@ -375,6 +396,104 @@ def varint_decode(stream_bytes: torch.Tensor, nbytes: torch.Tensor, idx: torch.T
     _check(lib().pulse_varint_decode(_p(stream_bytes), stream_bytes.numel(), _p(nbytes),
                                      _p(seg_begin), nseg, _p(idx), idx.numel(), _p(count), _p(ws),
                                      ws.numel(), _stream(stream)), "pulse_varint_decode")
+
+
+def lowp_sizes(dtype: int, n: int):
+    """(code bytes, scale bytes) of one tensor's D view."""
+    if dtype == FP8_E4M3:
+        return n, 0
+    return (n + 1) // 2, (n + 31) // 32
+
+
+def cast_lowp(dtype: int, src: torch.Tensor, inv_scale: float = 1.0, codes=None, scales=None,
+              stream=None):
+    """Dense D view of an FP32 tensor: (codes uint8, scales uint8 or None)."""
+    assert src.dtype == torch.float32 and src.is_contiguous()
+    nc, ns = lowp_sizes(dtype, src.numel())
+    if codes is None:
+        codes = torch.empty(max(nc, 1), dtype=torch.uint8, device=src.device)
+    if scales is None and dtype == MXFP4:
+        scales = torch.empty(max(ns, 1), dtype=torch.uint8, device=src.device)
+    _check(lib().pulse_cast_lowp(dtype, _p(src), src.numel(), float(inv_scale), _p(codes),
+                                 _p(scales), _stream(stream)), "pulse_cast_lowp")
+    return codes, scales
+
+
+@dataclass
+class LowpTensor:
+    w_new: torch.Tensor
+    snap: torch.Tensor                      # FP8 codes or MXFP4 packed codes (uint8)
+    snap_scales: Optional[torch.Tensor] = None
+    index_base: int = 0
+    inv_scale: float = 1.0
+
+
+class EncodeLowpBatch:
+    """Descriptor array for pulse_encode_lowp_batch (val: uint8 for FP8, int16 for MXFP4)."""
+
+    def __init__(self, dtype: int, tensors: Sequence[LowpTensor]):
+        self.dtype, self.n = dtype, len(tensors)
+        arr = (_LowpTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert t.w_new.dtype == torch.float32 and t.snap.element_size() == 1
+            arr[i] = _LowpTensor(_p(t.w_new), _p(t.snap), _p(t.snap_scales), t.w_new.numel(),
+                                 t.index_base, float(t.inv_scale))
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_encode_lowp_batch(self.dtype, self.arr, self.n, _p(idx), _p(val), cap,
+                                             _p(count), _p(seg_begin), _p(ws), ws.numel(),
+                                             _stream(stream)), "pulse_encode_lowp_batch")
+
+
+@dataclass
+class LowpApplyTensor:
+    codes: torch.Tensor
+    scales: Optional[torch.Tensor] = None
+    n: int = 0
+    index_base: int = 0
+
+
+class ApplyLowpBatch:
+    def __init__(self, dtype: int, tensors: Sequence[LowpApplyTensor]):
+        self.dtype, self.n = dtype, len(tensors)
+        arr = (_LowpApplyTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            arr[i] = _LowpApplyTensor(_p(t.codes), _p(t.scales), t.n, t.index_base)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, idx, val, seg_begin, end, rejected=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_apply_lowp_batch(self.dtype, self.arr, self.n, _p(idx), _p(val), cap,
+                                            _p(seg_begin), _p(end), _p(rejected),
+                                            _stream(stream)), "pulse_apply_lowp_batch")
+
+
+class LocoLowpBatch:
+    """pulse_loco_sparsify_lowp_batch: Alg. 2's selection by an FP8/MXFP4 receiver's gate."""
+
+    def __init__(self, dtype: int, tensors: Sequence[LocoTensor], inv_scales=None):
+        self.dtype, self.n = dtype, len(tensors)
+        arr = (_LocoTensor * max(1, self.n))()
+        for i, t in enumerate(tensors):
+            assert t.theta is not None
+            arr[i] = _LocoTensor(_p(t.delta), _p(t.residual), _p(t.theta), t.delta.numel(),
+                                 t.index_base)
+        sc = list(inv_scales) if inv_scales is not None else [1.0] * self.n
+        self.scales = (ctypes.c_float * max(1, self.n))(*sc)
+        self.arr = arr
+        self.keep = list(tensors)
+
+    def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
+        cap = _capacity(idx, val, capacity)
+        _check(lib().pulse_loco_sparsify_lowp_batch(self.dtype, self.arr, self.scales, self.n,
+                                                    _p(idx), _p(val), cap, _p(count),
+                                                    _p(seg_begin), _p(ws), ws.numel(),
+                                                    _stream(stream)),
+               "pulse_loco_sparsify_lowp_batch")
 
 
 def hash_leaf_count(total_values: int) -> int:
