@@ -136,6 +136,8 @@ def main():
     ap.add_argument("--loco-rounds", type=int, default=10)
     ap.add_argument("--no-varint", action="store_true", help="skip the wire-format (delta-varint) leg")
     ap.add_argument("--no-hash", action="store_true", help="skip the weight-hash leg")
+    ap.add_argument("--no-receivers", action="store_true",
+                    help="skip the FP8/MXFP4-receiver and k-step legs (7B set)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -314,6 +316,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_loco:
         out["legs"]["loco_7b"] = loco_leg(args, device, stream)
+    if not args.no_receivers:
+        out["legs"]["receivers_7b"] = receivers_leg(args, device, stream)
     print(json.dumps(out), flush=True)
 
 
@@ -486,6 +490,142 @@ def loco_leg(args, device, stream):
         },
         "round_ms_median": round(med + med_outer, 4),
     }
+
+
+def receivers_leg(args, device, stream):
+    """Receivers below BF16 (App. D) and k-step patches (App. A.1) on the 7B-shaped set.
+
+    From w_0 (the workload's init) the leg keeps the BF16 snapshot, the FP8 E4M3
+    view (per-tensor scale 448 / max|w_0|) and the MXFP4 view.  After one Adam
+    step at the bench lr it times the FP8 and MXFP4 encode against their views
+    and the apply of each patch into a receiver copy; then it continues the
+    chain and reports the k-step BF16 density against w_0's snapshot for
+    k = 1, 8, 16, 32 (the same encode, an older snapshot).
+    """
+    import numpy as np
+    import torch
+    from paper_2602_03839_amd import pulse
+    from paper_2602_03839_amd import workloads as wl
+
+    specs = wl.SHAPES["7b"].tensors()
+    sizes = [s.numel for s in specs]
+    offs = np.concatenate([[0], np.cumsum(sizes)]).tolist()
+    N, T = offs[-1], len(sizes)
+    cfg = WORKLOAD_IDS["7b"]
+    view = lambda b, i: b[offs[i]:offs[i + 1]]
+    mx_offs = [0]
+    for n in sizes:  # each tensor's packed codes start 16-byte aligned
+        mx_offs.append(mx_offs[-1] + ((n + 1) // 2 + 15) // 16 * 16)
+    sc_offs = [0]
+    for n in sizes:
+        sc_offs.append(sc_offs[-1] + (n + 31) // 32)
+    w = torch.empty(N, dtype=torch.float32, device=device)
+    S0 = torch.empty(N, dtype=torch.int16, device=device)
+    F0 = torch.empty(N, dtype=torch.uint8, device=device)
+    Mc = torch.empty(mx_offs[-1], dtype=torch.uint8, device=device)
+    Ms = torch.empty(sc_offs[-1], dtype=torch.uint8, device=device)
+    inv = []
+    for i, spec in enumerate(specs):
+        wv = view(w, i)
+        wl.init_weights_(wv, spec, cfg, 0, i)
+        pulse.cast_bf16(wv, out=view(S0, i))
+        inv.append(float(448.0 / float(wv.abs().max().item())))
+        pulse.cast_lowp(pulse.FP8_E4M3, wv, inv[i], codes=view(F0, i))
+        pulse.cast_lowp(pulse.MXFP4, wv, codes=Mc[mx_offs[i]:mx_offs[i + 1]],
+                        scales=Ms[sc_offs[i]:sc_offs[i + 1]])
+    for i in range(T):
+        wl.adam_step_(view(w, i), args.lr, cfg, 1, i)
+    cap = N // 10
+    idx = torch.empty(cap, dtype=torch.int32, device=device)
+    val8 = torch.empty(cap, dtype=torch.uint8, device=device)
+    val16 = torch.empty(cap, dtype=torch.int16, device=device)
+    count = torch.zeros(1, dtype=torch.int64, device=device)
+    seg = torch.zeros(T, dtype=torch.int64, device=device)
+    ws = pulse.workspace(device)
+    parts = chunks(T, CHUNK)
+    mcv = lambda i: Mc[mx_offs[i]:mx_offs[i + 1]]
+    msv = lambda i: Ms[sc_offs[i]:sc_offs[i + 1]]
+    enc = {
+        "fp8_e4m3": [pulse.EncodeLowpBatch(pulse.FP8_E4M3, [
+            pulse.LowpTensor(view(w, i), view(F0, i), None, 0, inv[i]) for i in range(a, b)])
+            for a, b in parts],
+        "mxfp4": [pulse.EncodeLowpBatch(pulse.MXFP4, [
+            pulse.LowpTensor(view(w, i), mcv(i), msv(i), 0) for i in range(a, b)])
+            for a, b in parts],
+    }
+    F1, Mc1, Ms1 = F0.clone(), Mc.clone(), Ms.clone()
+    app = {
+        "fp8_e4m3": pulse.ApplyLowpBatch(pulse.FP8_E4M3, [
+            pulse.LowpApplyTensor(view(F1, i), None, sizes[i], 0) for i in range(T)]),
+        "mxfp4": pulse.ApplyLowpBatch(pulse.MXFP4, [
+            pulse.LowpApplyTensor(Mc1[mx_offs[i]:mx_offs[i + 1]], Ms1[sc_offs[i]:sc_offs[i + 1]],
+                                  sizes[i], 0) for i in range(T)]),
+    }
+    per_param = {"fp8_e4m3": 5.0, "mxfp4": 4.5 + 1.0 / 32}
+    per_entry = {"fp8_e4m3": 5.0, "mxfp4": 6.0}
+    out = {"params": N, "lr": args.lr, "scale": "fp8: 448 / max|w_0| per tensor"}
+    reps = max(3, args.steps)
+    for name, batches in enc.items():
+        val = val8 if name == "fp8_e4m3" else val16
+        te, ta = [], []
+        for r in range(reps + 1):
+            count.zero_()
+            a, e = event_pair()
+            c, d = event_pair()
+            a.record(stream)
+            for (t0, _t1), b in zip(parts, batches):
+                b(idx, val, count, ws, seg_begin=seg[t0:])
+            e.record(stream)
+            c.record(stream)
+            app[name](idx, val, seg, count)
+            d.record(stream)
+            d.synchronize()
+            if r:
+                te.append(a.elapsed_time(e))
+                ta.append(c.elapsed_time(d))
+        nnz = int(count.item())
+        assert nnz <= cap, f"{name} patch overflow"
+        ms_e, ms_a = float(np.median(te)), float(np.median(ta))
+        gbs = (per_param[name] * N + per_entry[name] * nnz) / ms_e / 1e6
+        log(f"[bench] {name} receiver 7b: encode {ms_e:.3f} ms ({gbs:.0f} GB/s, "
+            f"{gbs / HBM_PEAK_GBS:.1%} of HBM), apply {ms_a:.3f} ms, density {nnz / N:.5%}")
+        out[name] = {"encode_ms": round(ms_e, 4), "apply_ms": round(ms_a, 4), "nnz": nnz,
+                     "density": round(nnz / N, 7), "encode_GBps_algorithmic": round(gbs, 2),
+                     "encode_hbm_frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+                     "bytes_per_param": per_param[name], "bytes_per_entry": per_entry[name]}
+    # the receiver copies now hold cast_D(w_1)
+    chk = torch.empty(sizes[0], dtype=torch.uint8, device=device)
+    pulse.cast_lowp(pulse.FP8_E4M3, view(w, 0), inv[0], codes=chk)
+    assert torch.equal(chk, view(F1, 0)), "FP8 receiver copy differs from the cast"
+    del F1, Mc1, Ms1, chk, enc, app
+
+    # k-step: BF16 patches against w_0's snapshot
+    plain = [pulse.EncodeBatch([pulse.EncodeTensor(view(w, i), view(S0, i), None, 0)
+                                for i in range(a, b)]) for a, b in parts]
+    dens, kms = {}, None
+    for t in range(1, 33):
+        if t > 1:
+            for i in range(T):
+                wl.adam_step_(view(w, i), args.lr, cfg, t, i)
+        if t in (1, 8, 16, 32):
+            times = []
+            for r in range(3 if t == 32 else 1):
+                count.zero_()
+                a, e = event_pair()
+                a.record(stream)
+                for (t0, _t1), b in zip(parts, plain):
+                    b(idx, val16, count, ws, seg_begin=seg[t0:])
+                e.record(stream)
+                e.synchronize()
+                times.append(a.elapsed_time(e))
+            dens[t] = int(count.item()) / N
+            kms = float(np.median(times))
+    log(f"[bench] k-step BF16 density vs w_0 (7b): " +
+        ", ".join(f"k={k}: {d:.4%}" for k, d in dens.items()) + f"; k=32 encode {kms:.3f} ms")
+    out["kstep_bf16"] = {"density": {str(k): round(d, 6) for k, d in dens.items()},
+                         "sparsity": {str(k): round(1 - d, 6) for k, d in dens.items()},
+                         "encode_ms_k32": round(kms, 4)}
+    return out
 
 
 def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):

@@ -61,7 +61,7 @@ def gpu_encode(w_new: np.ndarray, snap: np.ndarray, capacity=None, index_base=0,
     patch.count.fill_(count_in)
     w_d, s_d = dev(w_new), dev(snap)
     ref_d = None
-    if refresh == "alias":
+    if isinstance(refresh, str) and refresh == "alias":
         ref_d = s_d
     elif refresh is not None:
         ref_d = dev(refresh)

@@ -152,3 +152,45 @@ def test_hash_sizes_and_validation(L):
     assert h(arr, 2, A, A, ws + 4, wsb, None) == EALIGN
     assert h(arr, 2, A, A, ws, wsb - 1, None) == EINVAL
     assert h(None, 2, A, A, ws, wsb, None) == EINVAL
+
+
+def test_lowp_validation(L):
+    ws, wsb = ws_args(L)
+    FP8, MX = pulse.FP8_E4M3, pulse.MXFP4
+    # cast
+    assert L.pulse_cast_lowp(3, A, 10, 1.0, A, A, None) == EINVAL
+    assert L.pulse_cast_lowp(FP8, A, 0, 1.0, None, None, None) == OK
+    assert L.pulse_cast_lowp(MX, A, 10, 1.0, A, None, None) == EINVAL      # scales
+    assert L.pulse_cast_lowp(FP8, A + 4, 10, 1.0, A, None, None) == EALIGN
+    assert L.pulse_cast_lowp(FP8, A, 10, 1.0, A + 4, None, None) == EALIGN  # 8-byte codes
+    # encode
+    arr = (pulse._LowpTensor * 2)()
+    arr[0] = pulse._LowpTensor(A, A, A, 100, 0, 1.0)
+    arr[1] = pulse._LowpTensor(A, A + 4, None, 100, 0, 1.0)
+    enc = L.pulse_encode_lowp_batch
+    assert enc(0, arr, 2, A, A, 10, A, None, ws, wsb, None) == EINVAL
+    assert enc(FP8, arr, 2, A, A, 10, A, None, ws, wsb, None) == EALIGN    # FP8 snap 8-byte
+    assert b"tensor 1" in L.pulse_last_error()
+    assert enc(MX, arr, 2, A, A, 10, A, None, ws, wsb, None) == EINVAL     # MXFP4 scales
+    arr[1] = pulse._LowpTensor(A, A + 4, A, 100, 0, 1.0)
+    assert enc(MX, arr, 2, A, A + 1, 10, A, None, ws, wsb, None) == EALIGN  # uint16 val
+    assert enc(MX, arr, 2, A, A, 10, None, None, ws, wsb, None) == EINVAL   # count
+    arr[1] = pulse._LowpTensor(A, A + 4, A, 100, (1 << 32) - 5, 1.0)
+    assert enc(MX, arr, 2, A, A, 10, A, None, ws, wsb, None) == ERANGE
+    # apply
+    at = (pulse._LowpApplyTensor * 1)()
+    at[0] = pulse._LowpApplyTensor(A, None, 100, 0)
+    ap = L.pulse_apply_lowp_batch
+    assert ap(MX, at, 1, A, A, 10, A, A, None, None) == EINVAL             # scales
+    assert ap(FP8, at, 1, A, A, 10, A + 4, A, None, None) == EALIGN
+    assert ap(FP8, at, 1, None, A, 10, A, A, None, None) == EINVAL
+    # sparsifier gate
+    lt = (pulse._LocoTensor * 1)()
+    lt[0] = pulse._LocoTensor(A, A, None, 100, 0)
+    sc = (ctypes.c_float * 1)(1.0)
+    lo = L.pulse_loco_sparsify_lowp_batch
+    assert lo(MX, lt, None, 1, A, A, 10, A, None, ws, wsb, None) == EINVAL   # theta
+    lt[0] = pulse._LocoTensor(A, A, A, 100, 0)
+    assert lo(FP8, lt, None, 1, A, A, 10, A, None, ws, wsb, None) == EINVAL  # inv_scales
+    assert lo(7, lt, sc, 1, A, A, 10, A, None, ws, wsb, None) == EINVAL
+    assert lo(FP8, lt, sc, 1, A, A, 10, A, None, ws + 8, wsb, None) == EALIGN
