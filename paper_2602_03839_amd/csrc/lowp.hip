@@ -147,32 +147,40 @@ __device__ __forceinline__ void lowp_load(LowpRegs& g, const LowpCtx& c, uint64_
 #ifndef PULSE_LOWP_TB
 #define PULSE_LOWP_TB 960
 #endif
+#ifndef PULSE_LOWP_U
+#define PULSE_LOWP_U 2
+#endif
 constexpr int kLowpNW = PULSE_LOWP_TB / 64;
+constexpr int kLowpU = PULSE_LOWP_U;
 constexpr int kLowpResolve = 4;
 constexpr int kLowpDefer = kLowpResolve + 1;
 constexpr int kLowpWexclRing = wexcl_ring(kLowpResolve);
 constexpr int kLowpValBufs = kLowpDefer;
 
+template <int U>
 struct LowpDeferred {
   uint64_t e0;
   int k;
   bool valid;
-  uint32_t mask;
-  uint32_t excl;  // entries before this lane's in its wave
+  uint32_t mask;                // 8 bits per group
+  uint32_t excl[(U + 1) / 2];   // entries before this lane's in its wave, 16 bits per group
 };
 
-// One group of 8 values per lane per tile (U = 1).
-template <int NW, int DT>
+// U groups of 8 values per lane per tile; group u of lane tid covers values
+// e0 + (u * TBC + tid) * 8 ...  The new D values of a group are staged in LDS
+// as 8 bytes (FP8: the codes; MXFP4: the packed codes and the scale byte)
+// until the tile's write-out, kDefer iterations later.
+template <int NW, int U, int DT>
 __global__ __launch_bounds__((NW + 1) * 64) void encode_lowp_kernel(LowpParams p) {
   constexpr int TBC = NW * 64;
-  constexpr uint32_t TILE = TBC * 8;
-  constexpr int U = 1;
+  constexpr uint32_t TILE = TBC * U * 8;
   __shared__ uint64_t s_tk[kTkRing];
   __shared__ uint64_t s_excl[2];
   __shared__ uint32_t s_wtot[2 * U * NW];
   __shared__ uint32_t s_wexcl[kLowpWexclRing * U * NW];
-  // staged new values of each group: FP8 8 codes (uint2); MXFP4 8 x uint16 (uint4)
-  __shared__ uint4 s_vals[kLowpValBufs][DT == kDtypeFp8 ? TBC / 2 : TBC];
+  __shared__ uint2 s_vals[kLowpValBufs][U * TBC];
+  static_assert(U * NW <= 64, "block scan runs on one wave");
+  static_assert(U <= 4, "masks of all groups are packed into one register");
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -187,7 +195,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_lowp_kernel(LowpParams p
   __syncthreads();  // T(0) .. T(kAhead) are in s_tk
   static_assert(kAhead == 1 || kAhead == 2, "one or two register sets");
   const uint32_t lane_begin = owner_lane_begin(p);
-  LowpRegs g0, g1;
+  LowpRegs g0[U], g1[U];
   uint64_t e0_0 = 0, e0_1 = 0;
   int k_0 = 0, k_1 = 0;
 #pragma unroll
@@ -196,7 +204,9 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_lowp_kernel(LowpParams p
     if (t.tile < p.ntiles) {
       const LowpCtx c = lowp_locate(p, lane_begin, t.tile, TILE);
       const bool full = c.e0 + TILE <= c.n;
-      lowp_load<DT>(q == 0 ? g0 : g1, c, c.e0 + (uint64_t)tid * 8, full);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        lowp_load<DT>((q == 0 ? g0 : g1)[u], c, c.e0 + (uint64_t)(u * TBC + tid) * 8, full);
       (q == 0 ? e0_0 : e0_1) = c.e0;
       (q == 0 ? k_0 : k_1) = c.k;
     }
@@ -212,115 +222,121 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_lowp_kernel(LowpParams p
     }
   };
   look_up_next(0);
-  LowpDeferred hist[kLowpDefer];
+  LowpDeferred<U> hist[kLowpDefer];
 #pragma unroll
   for (int d = 0; d < kLowpDefer; ++d) hist[d].valid = false;
 
-  auto step = [&](const int it, LowpRegs& g, uint64_t& ce0, int& ck) -> bool {
+  auto step = [&](const int it, LowpRegs (&g)[U], uint64_t& ce0, int& ck) -> bool {
     const Ticket cur = ticket_at(s_tk, it);
     const bool have_cur = cur.tile < p.ntiles;
     bool pending = have_cur;
 #pragma unroll
     for (int d = 0; d < kLowpDefer; ++d) pending |= hist[d].valid;
     if (!pending) return false;
-    uint32_t m = 0, excl = 0;
-    uint4 staged = make_uint4(0, 0, 0, 0);
+    uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
+    uint2 staged[U];
     if (have_cur) {
       const uint64_t cn_n = p.t[ck].n;
-      const uint64_t e = ce0 + (uint64_t)tid * 8;
-      float x[8];
+      const bool full = ce0 + TILE <= cn_n;
+      uint32_t cnt[U];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[i] = __uint_as_float(get_u32(g.w0, i));
-        x[i + 4] = __uint_as_float(get_u32(g.w1, i));
-      }
-      if (DT == kDtypeFp8) {
-        const float is = p.t[ck].inv_scale;
-        uint32_t lo = 0, hi = 0;
+      for (int u = 0; u < U; ++u) {
+        const uint64_t e = ce0 + (uint64_t)(u * TBC + tid) * 8;
+        float x[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t c = fp8_code(x[i] * is);
-          const uint32_t old = ((i < 4 ? g.s.x : g.s.y) >> (8 * (i & 3))) & 0xFFu;
-          m |= (uint32_t)(c != old) << i;
-          (i < 4 ? lo : hi) |= c << (8 * (i & 3));
+        for (int i = 0; i < 4; ++i) {
+          x[i] = __uint_as_float(get_u32(g[u].w0, i));
+          x[i + 4] = __uint_as_float(get_u32(g[u].w1, i));
         }
-        staged = make_uint4(lo, hi, 0, 0);
-      } else {
-        uint32_t c[8];
-        const uint32_t sc = mx_view8(x, c);
-        const bool scale_moved = sc != g.s.y;
-        uint32_t v[4];
+        uint32_t m = 0;
+        if (DT == kDtypeFp8) {
+          const float is = p.t[ck].inv_scale;
+          uint32_t lo = 0, hi = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t old = (g.s.x >> (4 * i)) & 0xFu;
-          m |= (uint32_t)(scale_moved || c[i] != old) << i;
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t c = fp8_code(x[i] * is);
+            const uint32_t old = ((i < 4 ? g[u].s.x : g[u].s.y) >> (8 * (i & 3))) & 0xFFu;
+            m |= (uint32_t)(c != old) << i;
+            (i < 4 ? lo : hi) |= c << (8 * (i & 3));
+          }
+          staged[u] = make_uint2(lo, hi);
+        } else {
+          uint32_t c[8];
+          const uint32_t sc = mx_view8(x, c);
+          const bool scale_moved = sc != g[u].s.y;
+          uint32_t packed = 0;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t old = (g[u].s.x >> (4 * i)) & 0xFu;
+            m |= (uint32_t)(scale_moved || c[i] != old) << i;
+            packed |= c[i] << (4 * i);
+          }
+          staged[u] = make_uint2(packed, sc);
         }
+        if (!full && !(e + 8 <= cn_n)) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = ((sc << 8) | c[2 * j]) | (((sc << 8) | c[2 * j + 1]) << 16);
-        staged = make_uint4(v[0], v[1], v[2], v[3]);
+          for (int i = 0; i < 8; ++i)
+            if (!(e + i < cn_n)) m &= ~(1u << i);
+        }
+        mask_packed |= m << (8 * u);
+        cnt[u] = __builtin_popcount(m);
+        // this group's registers are free: start T(i + kAhead)'s loads into them
+        if (have_next) lowp_load<DT>(g[u], cn, cn.e0 + (uint64_t)(u * TBC + tid) * 8, next_full);
       }
-      if (!(ce0 + TILE <= cn_n) && !(e + 8 <= cn_n)) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (!(e + i < cn_n)) m &= ~(1u << i);
+      for (int u = 0; u < U; u += 2) {
+        const uint32_t packed = cnt[u] | (u + 1 < U ? (cnt[u + 1] << 16) : 0u);
+        const uint32_t incl = wave_incl_scan(packed);
+        excl_packed[u >> 1] = incl - packed;
+        if (lane == 63) {
+          s_wtot[(it & 1) * U * NW + u * NW + wid] = incl & 0xFFFFu;
+          if (u + 1 < U) s_wtot[(it & 1) * U * NW + (u + 1) * NW + wid] = incl >> 16;
+        }
       }
-      // this group's registers are free: start T(i + kAhead)'s loads into them
-      if (have_next) lowp_load<DT>(g, cn, cn.e0 + (uint64_t)tid * 8, next_full);
-      const uint32_t cnt = __builtin_popcount(m);
-      const uint32_t incl = wave_incl_scan(cnt);
-      excl = incl - cnt;
-      if (lane == 63) s_wtot[(it & 1) * U * NW + wid] = incl;
     }
     __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
-    const LowpDeferred& od = hist[kLowpDefer - 1];
+    const LowpDeferred<U>& od = hist[kLowpDefer - 1];
     if (od.valid && od.mask) {
       const int oi = it - kLowpDefer;
-      uint64_t pos = s_excl[oi & 1] + s_wexcl[(oi & (kLowpWexclRing - 1)) * U * NW + wid] +
-                     (od.excl);
+      const uint64_t tile_excl = s_excl[oi & 1];
+      const uint32_t* wexcl = s_wexcl + (oi & (kLowpWexclRing - 1)) * U * NW;
       const uint64_t cap = p.capacity;
       const uint32_t base = p.t[od.k].index_base;
-      const uint64_t e = od.e0 + (uint64_t)tid * 8;
-      uint32_t mm = od.mask;
-      if (DT == kDtypeFp8) {
-        const uint2 sv = reinterpret_cast<const uint2*>(s_vals[oi % kLowpValBufs])[tid];
-        uint8_t* val = (uint8_t*)p.val;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        uint32_t mm = (od.mask >> (8 * u)) & 0xFFu;
+        if (mm == 0) continue;
+        uint64_t pos = tile_excl + wexcl[u * NW + wid] +
+                       ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
+        const uint2 sv = s_vals[oi % kLowpValBufs][u * TBC + tid];
         while (mm) {
           const int i = __builtin_ctz(mm);
           mm &= mm - 1;
           if (pos < cap) {
             p.idx[pos] = base + (uint32_t)(e + i);
-            val[pos] = (uint8_t)(((i < 4 ? sv.x : sv.y) >> (8 * (i & 3))) & 0xFFu);
-          }
-          ++pos;
-        }
-      } else {
-        const uint4 sv = s_vals[oi % kLowpValBufs][tid];
-        uint16_t* val = (uint16_t*)p.val;
-        while (mm) {
-          const int i = __builtin_ctz(mm);
-          mm &= mm - 1;
-          if (pos < cap) {
-            p.idx[pos] = base + (uint32_t)(e + i);
-            val[pos] = (uint16_t)((get_u32(sv, i >> 1) >> (16 * (i & 1))) & 0xFFFFu);
+            if (DT == kDtypeFp8)
+              ((uint8_t*)p.val)[pos] = (uint8_t)(((i < 4 ? sv.x : sv.y) >> (8 * (i & 3))) & 0xFFu);
+            else
+              ((uint16_t*)p.val)[pos] = (uint16_t)((sv.y << 8) | ((sv.x >> (4 * i)) & 0xFu));
           }
           ++pos;
         }
       }
     }
     if (have_cur) {
-      if (DT == kDtypeFp8)
-        reinterpret_cast<uint2*>(s_vals[it % kLowpValBufs])[tid] = make_uint2(staged.x, staged.y);
-      else
-        s_vals[it % kLowpValBufs][tid] = staged;
+#pragma unroll
+      for (int u = 0; u < U; ++u) s_vals[it % kLowpValBufs][u * TBC + tid] = staged[u];
     }
 #pragma unroll
     for (int d = kLowpDefer - 1; d > 0; --d) hist[d] = hist[d - 1];
     hist[0].e0 = ce0;
     hist[0].k = ck;
     hist[0].valid = have_cur;
-    hist[0].mask = m;
-    hist[0].excl = excl;
+    hist[0].mask = mask_packed;
+#pragma unroll
+    for (int q = 0; q < (U + 1) / 2; ++q) hist[0].excl[q] = excl_packed[q];
     if (have_next) {
       ce0 = cn.e0;
       ck = cn.k;
@@ -407,7 +423,7 @@ __global__ void lowp_empty_segments_kernel(const uint64_t* count, uint64_t* seg_
   if (i < nseg) seg_begin[i] = *count;
 }
 
-uint32_t lowp_tile_elems() { return kLowpNW * 64 * 8; }
+uint32_t lowp_tile_elems() { return kLowpNW * 64 * kLowpU * 8; }
 
 hipError_t launch_encode_lowp(int dtype, LowpParams& p, hipStream_t stream) {
   if (p.ntiles == 0) {
@@ -416,16 +432,16 @@ hipError_t launch_encode_lowp(int dtype, LowpParams& p, hipStream_t stream) {
                        (const uint64_t*)p.count, p.seg_begin, (uint32_t)p.ntensors);
     return hipGetLastError();
   }
-  const void* fn = dtype == kDtypeFp8 ? (const void*)encode_lowp_kernel<kLowpNW, kDtypeFp8>
-                                      : (const void*)encode_lowp_kernel<kLowpNW, kDtypeMxfp4>;
+  const void* fn = dtype == kDtypeFp8 ? (const void*)encode_lowp_kernel<kLowpNW, kLowpU, kDtypeFp8>
+                                      : (const void*)encode_lowp_kernel<kLowpNW, kLowpU, kDtypeMxfp4>;
   const int grid_cap = persistent_grid(fn, (kLowpNW + 1) * 64);
   if (grid_cap <= 0) return hipErrorInvalidConfiguration;
   const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
   if (dtype == kDtypeFp8)
-    hipLaunchKernelGGL((encode_lowp_kernel<kLowpNW, kDtypeFp8>), dim3(grid),
+    hipLaunchKernelGGL((encode_lowp_kernel<kLowpNW, kLowpU, kDtypeFp8>), dim3(grid),
                        dim3((kLowpNW + 1) * 64), 0, stream, p);
   else
-    hipLaunchKernelGGL((encode_lowp_kernel<kLowpNW, kDtypeMxfp4>), dim3(grid),
+    hipLaunchKernelGGL((encode_lowp_kernel<kLowpNW, kLowpU, kDtypeMxfp4>), dim3(grid),
                        dim3((kLowpNW + 1) * 64), 0, stream, p);
   return hipGetLastError();
 }
