@@ -16,6 +16,9 @@ and marshals numpy arrays into it with ctypes.
     outer_step(theta, m, lists, ...) Sec. 4.3 Alg. 2 (SparseSync average, outer Nesterov step)
     varint_encode(idx) / varint_decode(stream)
                                      App. H.2 / App. F.3 delta-varint index stream
+    coo_encode(idx, seg_begin, cols) / coo_decode(...)
+                                     App. H.2 / H.4.1 2-D COO delta downcast (uint8 row,
+                                     uint16 column fields)
     fp8_e4m3(y) / cast_fp8 / cast_mxfp4
                                      App. D compute views cast_D for FP8 E4M3 and MXFP4
     encode_fp8 / encode_mxfp4 / apply_fp8 / apply_mxfp4 / loco_gate_lp
@@ -95,6 +98,10 @@ def _load():
             lib.oracle_loco_gate_lp.argtypes = [ctypes.c_int, f32, vp, vp, u64, vp, u32, vp, vp,
                                                 u64, u64]
             lib.oracle_loco_gate_lp.restype = u64
+            lib.oracle_coo_encode.argtypes = [vp, u64, vp, u32, vp, vp, vp, vp, u64, vp]
+            lib.oracle_coo_encode.restype = u64
+            lib.oracle_coo_decode.argtypes = [vp, vp, u64, vp, vp, u32, u64, vp, vp, vp]
+            lib.oracle_coo_decode.restype = ctypes.c_int64
             lib.oracle_sha256.argtypes = [vp, u64, vp]
             lib.oracle_sha256.restype = None
             lib.oracle_leaf_hashes.argtypes = [vp, u64, u64, vp]
@@ -264,6 +271,46 @@ def varint_decode(stream) -> np.ndarray:
     out = np.zeros(max(n, 1), dtype=np.uint32)
     L.oracle_varint_decode(_ptr(stream), stream.size, _ptr(out), n)
     return out[:n]
+
+
+def coo_encode(idx, seg_begin, cols, nent: int | None = None):
+    """2-D COO delta downcast of a sorted patch.
+
+    Returns (first uint32[nseg], drow uint8[P], dcol uint16[P], seg_pairs uint64[nseg]).
+    """
+    idx = np.ascontiguousarray(idx, dtype=np.uint32)
+    sb = np.ascontiguousarray(seg_begin, dtype=np.uint64)
+    cols = np.ascontiguousarray(cols, dtype=np.uint32)
+    nseg = sb.size
+    assert cols.size == nseg and nseg >= 1
+    nent = idx.size if nent is None else nent
+    first = np.zeros(nseg, dtype=np.uint32)
+    sp = np.zeros(nseg, dtype=np.uint64)
+    L = _load()
+    P = int(L.oracle_coo_encode(_ptr(idx), nent, _ptr(sb), nseg, _ptr(cols), _ptr(first),
+                                None, None, 0, _ptr(sp)))
+    drow = np.zeros(max(P, 1), dtype=np.uint8)
+    dcol = np.zeros(max(P, 1), dtype=np.uint16)
+    L.oracle_coo_encode(_ptr(idx), nent, _ptr(sb), nseg, _ptr(cols), _ptr(first), _ptr(drow),
+                        _ptr(dcol), P, _ptr(sp))
+    return first, drow[:P], dcol[:P], sp
+
+
+def coo_decode(first, drow, dcol, seg_pairs, seg_begin, cols, nent: int):
+    """Indices back from a 2-D COO delta stream; raises ValueError on a malformed one."""
+    drow = np.ascontiguousarray(drow, dtype=np.uint8)
+    dcol = np.ascontiguousarray(dcol, dtype=np.uint16)
+    sp = np.ascontiguousarray(seg_pairs, dtype=np.uint64)
+    sb = np.ascontiguousarray(seg_begin, dtype=np.uint64)
+    cols = np.ascontiguousarray(cols, dtype=np.uint32)
+    first = np.ascontiguousarray(first, dtype=np.uint32)
+    out = np.zeros(max(nent, 1), dtype=np.uint32)
+    r = _load().oracle_coo_decode(_ptr(drow) if drow.size else None,
+                                  _ptr(dcol) if dcol.size else None, drow.size, _ptr(sp),
+                                  _ptr(sb), sb.size, nent, _ptr(cols), _ptr(first), _ptr(out))
+    if r < 0:
+        raise ValueError("malformed COO stream")
+    return out[:nent]
 
 
 FP8, MXFP4 = 1, 2  # receiver compute dtypes of App. D

@@ -25,6 +25,8 @@
  *   oracle_varint_encode App. H.2 (index encoding: sorted, first index as-is,
  *   oracle_varint_decode then differences) and App. F.3 (PULSELoCo's sparse
  *                        stream: delta-encoded, varint-packed indices).
+ *   oracle_coo_encode    App. H.2 step 4 / App. H.4.1 (type downscaling): the
+ *   oracle_coo_decode    2-D COO delta stream, uint8 row and uint16 column fields.
  *   oracle_fp8_e4m3,     App. D (lower-precision receivers): the compute view
  *   oracle_cast_fp8,     cast_D for D = FP8 E4M3 and MXFP4, Alg. 1's encode and
  *   oracle_cast_mxfp4,   apply on D-values, and the gate G_D of Alg. 2 for a
@@ -757,4 +759,111 @@ uint64_t oracle_loco_gate_lp(int dtype, float inv_scale, const float *delta, flo
     free(after);
     free(keep);
     return count;
+}
+
+/* ------------------------------------------------------------------------
+ * 2-D COO delta downcast of a patch's indices (App. H.2, step 4: downcast the
+ * index types, uint8 row deltas and uint16 column deltas; App. H.4.1 "Type
+ * downscaling"; the delta_coo_downscaled representation of App. H.4).
+ *
+ * A segment (one tensor, `cols` columns, entries ascending) is stored as its
+ * first local index as it is (4 bytes, App. H.2 step 2) followed by one
+ * (uint8 row field, uint16 column field) pair per later entry, row-major:
+ *   same row as the previous entry:   (0, column - previous column)
+ *   a later row, rows ahead = dr:     (dr, column + 1)
+ * A jump of more than 255 rows is sent as (255, 0) escape pairs, each moving
+ * 255 rows down without an entry, then the pair of the remaining 1..255 rows.
+ * No entry yields (255, 0): a same-row pair has row field 0, a new-row pair a
+ * column field >= 1.  Requires 1 <= cols <= 65535.  (The paper notes that
+ * larger jumps are rare but does not say how they are kept lossless; the
+ * escape is this build's reading.)
+ * ------------------------------------------------------------------------ */
+
+/* Pairs of all segments into drow/dcol (positions >= out_capacity are not
+ * written); first[s] = the segment's first index (0 for an empty one),
+ * seg_pairs[s] = where its pairs start.  Segment s holds entries
+ * [seg_begin[s], seg_begin[s + 1]) (the last one up to nent).  Returns the
+ * number of pairs. */
+uint64_t oracle_coo_encode(const uint32_t *idx, uint64_t nent, const uint64_t *seg_begin,
+                           uint32_t nseg, const uint32_t *cols, uint32_t *first, uint8_t *drow,
+                           uint16_t *dcol, uint64_t out_capacity, uint64_t *seg_pairs)
+{
+    uint64_t np = 0;
+    for (uint32_t s = 0; s < nseg; s++) {
+        uint64_t b = seg_begin[s], e = s + 1 < nseg ? seg_begin[s + 1] : nent;
+        uint64_t C = cols[s];
+        seg_pairs[s] = np;
+        first[s] = e > b ? idx[b] : 0;
+        for (uint64_t k = b + 1; k < e; k++) {
+            uint64_t r = idx[k] / C, c = idx[k] % C;
+            uint64_t pr = idx[k - 1] / C, pc = idx[k - 1] % C;
+            uint64_t dr = r - pr;
+            if (dr == 0) {
+                if (np < out_capacity) {
+                    drow[np] = 0;
+                    dcol[np] = (uint16_t)(c - pc);
+                }
+                np++;
+                continue;
+            }
+            while (dr > 255) {
+                if (np < out_capacity) {
+                    drow[np] = 255;
+                    dcol[np] = 0;
+                }
+                np++;
+                dr -= 255;
+            }
+            if (np < out_capacity) {
+                drow[np] = (uint8_t)dr;
+                dcol[np] = (uint16_t)(c + 1);
+            }
+            np++;
+        }
+    }
+    return np;
+}
+
+/* The indices back: entries of segment s go to out[seg_begin[s] ...].
+ * Returns the number of entries, or -1 if a segment's pairs do not give
+ * exactly its entry count or hold a pair no encoder writes. */
+int64_t oracle_coo_decode(const uint8_t *drow, const uint16_t *dcol, uint64_t npairs,
+                          const uint64_t *seg_pairs, const uint64_t *seg_begin, uint32_t nseg,
+                          uint64_t nent, const uint32_t *cols, const uint32_t *first,
+                          uint32_t *out)
+{
+    for (uint32_t s = 0; s < nseg; s++) {
+        uint64_t b = seg_begin[s], e = s + 1 < nseg ? seg_begin[s + 1] : nent;
+        uint64_t p0 = seg_pairs[s], p1 = s + 1 < nseg ? seg_pairs[s + 1] : npairs;
+        uint64_t C = cols[s];
+        if (e == b) {
+            if (p1 != p0)
+                return -1;
+            continue;
+        }
+        uint64_t r = first[s] / C, c = first[s] % C, k = b;
+        out[k++] = first[s];
+        for (uint64_t q = p0; q < p1; q++) {
+            if (drow[q] == 255 && dcol[q] == 0) {
+                r += 255;
+                continue;
+            }
+            if (drow[q] == 0) {
+                if (dcol[q] == 0)
+                    return -1;
+                c += dcol[q];
+            } else {
+                if (dcol[q] == 0)
+                    return -1;
+                r += drow[q];
+                c = dcol[q] - 1u;
+            }
+            if (k >= e)
+                return -1;
+            out[k++] = (uint32_t)(r * C + c);
+        }
+        if (k != e)
+            return -1;
+    }
+    return (int64_t)nent;
 }
