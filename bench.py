@@ -357,6 +357,7 @@ def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
     assert int(got.item()) == sent
     assert torch.equal(back[:sent], idx[:sent]), "varint round trip differs from the patch"
     enc_ms, dec_ms = float(np.median(te)), float(np.median(td))
+    coo = coo_leg(args, ps, idx, end, seg, sent, ws, stream)
     enc_bytes = 4.0 * sent + nbytes          # indices read, stream written
     dec_bytes = nbytes + 4.0 * sent * 3      # stream read, differences written, re-read, indices written
     log(f"[bench] varint: {sent:,} indices -> {nbytes / 1e6:.1f} MB ({nbytes / sent:.3f} B/index, "
@@ -372,7 +373,49 @@ def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
         "encode_GBps_algorithmic": round(enc_bytes / enc_ms / 1e6, 2),
         "decode_GBps_algorithmic": round(dec_bytes / dec_ms / 1e6, 2),
         "kernels": "varint_encode_kernel; varint_gaps_kernel + varint_sums_kernel",
+        "coo_downcast": coo,
     }
+
+
+def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
+    """The same patch's indices as the paper's 2-D COO delta downcast (App. H.2
+    step 4, App. H.4.1): per tensor the first index, then (uint8 row, uint16
+    column) pairs with (255, 0) escapes for row gaps over 255."""
+    import numpy as np
+    import torch
+    from paper_2602_03839_amd import pulse
+
+    dev = idx.device
+    T = len(ps.specs)
+    if ps.flat_index:  # the 2-D view needs indices local to each tensor
+        return None
+    cols = torch.tensor([s.shape[-1] for s in ps.specs], dtype=torch.int32, device=dev)
+    first = torch.empty(T, dtype=torch.int32, device=dev)
+    sp = torch.empty(T, dtype=torch.int64, device=dev)
+    total = torch.zeros(1, dtype=torch.int64, device=dev)
+    cap_p = sent + sent // 8 + 64 * T
+    drow = torch.empty(cap_p, dtype=torch.uint8, device=dev)
+    dcol = torch.empty(cap_p, dtype=torch.int16, device=dev)
+    times = []
+    for r in range(max(3, args.steps) + 1):
+        a, b = event_pair()
+        a.record(stream)
+        pulse.coo_encode(idx, end, seg, cols, first, drow, dcol, sp, total, ws, capacity=sent)
+        b.record(stream)
+        b.synchronize()
+        if r:
+            times.append(a.elapsed_time(b))
+    P = int(total.item())
+    assert P <= cap_p
+    esc = int(((drow[:P] == 255) & (dcol[:P] == 0)).sum().item())
+    nbytes = 3 * P + 4 * T
+    ms = float(np.median(times))
+    log(f"[bench] coo downcast: {sent:,} indices -> {P:,} pairs ({esc:,} escapes), "
+        f"{nbytes / 1e6:.1f} MB ({nbytes / max(sent, 1):.3f} B/index); encode {ms:.3f} ms")
+    return {"pairs": P, "escapes": esc, "stream_bytes": nbytes,
+            "bytes_per_index": round(nbytes / max(sent, 1), 4), "encode_ms": round(ms, 4),
+            "encode_GBps_algorithmic": round((4.0 * sent + nbytes) / ms / 1e6, 2),
+            "kernel": "coo_encode_kernel"}
 
 
 def hash_leg(args, ps, stream):

@@ -312,6 +312,31 @@ int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t 
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * pulse_coo_encode -- the 2-D COO delta downcast of a sorted patch's indices
+ * (App. H.2 step 4: downcast the index types, uint8 row deltas and uint16
+ * column deltas; App. H.4.1 "Type downscaling").  Segment s (one tensor,
+ * row-major with cols[s] columns, 1 <= cols[s] <= 65535) is written as
+ *   first[s]      its first index as it is (App. H.2 step 2; 0 if empty),
+ *   then one (drow uint8, dcol uint16) pair per later entry:
+ *     same row as the previous entry:  (0, column - previous column)
+ *     dr rows further down:            (dr, column + 1)     for dr <= 255
+ *     dr > 255:                        (255, 0) escapes, each 255 rows down
+ *                                      with no entry, ahead of the pair of the
+ *                                      remaining 1..255 rows.
+ *   No entry yields (255, 0).  Pairs of segment s start at seg_pairs[s];
+ *   *total_pairs receives the stream's length; pairs at or past out_capacity
+ *   are not written.  idx, capacity, end and the workspace follow
+ *   pulse_varint_encode; seg_begin[0] should be 0 (earlier entries count as
+ *   segment 0).  cols, first and seg_pairs are device arrays of nseg >= 1
+ *   elements.  A stream of P pairs takes 3 P bytes plus 4 bytes per segment.
+ */
+int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end,
+                     const uint64_t *seg_begin, uint32_t nseg, const uint32_t *cols,
+                     uint32_t *first, uint8_t *drow, uint16_t *dcol, uint64_t out_capacity,
+                     uint64_t *seg_pairs, uint64_t *total_pairs,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Receivers that compute in a precision below BF16 (App. D): the compute view
  * cast_D of the FP32 masters, the patch of the values whose view changes
  * (Alg. 1 with D in place of BF16), and its apply on the receiver's D copy.

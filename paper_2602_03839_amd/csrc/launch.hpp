@@ -264,6 +264,23 @@ __host__ __device__ inline bool hash_leaf_in_place(uint64_t x, uint64_t le, uint
 }
 
 static_assert(sizeof(HashSetupParams) < 4096, "kernel argument block too large");
+struct CooEncParams {
+  uint64_t* ws;
+  const uint32_t* idx;
+  uint64_t capacity;
+  const uint64_t* end;         // device: entries in the patch
+  const uint64_t* seg_begin;   // device [nseg]
+  uint32_t nseg;
+  const uint32_t* cols;        // device [nseg]: columns of each tensor
+  uint32_t* first;             // device [nseg]: each segment's first index
+  uint8_t* drow;
+  uint16_t* dcol;
+  uint64_t out_capacity;       // pairs writable
+  uint64_t* seg_pairs;         // device [nseg]: where each segment's pairs start
+  uint64_t* total;             // device: pairs in the stream
+  uint32_t ntiles;
+};
+
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(OuterParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
@@ -280,6 +297,7 @@ uint32_t varint_entry_tile();
 uint32_t varint_byte_tile();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
+hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream);
 hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
 uint32_t lowp_tile_elems();
 hipError_t launch_encode_lowp(int dtype, LowpParams& p, hipStream_t stream);

@@ -483,6 +483,43 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   return hip_status(pulse::launch_varint_decode(p, (hipStream_t)stream), "varint decode launch");
 }
 
+int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end,
+                     const uint64_t* seg_begin, uint32_t nseg, const uint32_t* cols,
+                     uint32_t* first, uint8_t* drow, uint16_t* dcol, uint64_t out_capacity,
+                     uint64_t* seg_pairs, uint64_t* total_pairs, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (nseg == 0) return fail(PULSE_EINVAL, "coo encode: nseg is 0");
+  if (!end || !total_pairs || !seg_begin || !cols || !first || !seg_pairs)
+    return fail(PULSE_EINVAL, "coo encode: NULL pointer");
+  if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "coo encode: idx is NULL");
+  if (out_capacity > 0 && (!drow || !dcol)) return fail(PULSE_EINVAL, "coo encode: drow/dcol is NULL");
+  if (!aligned(end, 8) || !aligned(total_pairs, 8) || !aligned(seg_begin, 8) || !aligned(seg_pairs, 8))
+    return fail(PULSE_EALIGN, "coo encode: counters not 8-byte aligned");
+  if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4) || (dcol && !aligned(dcol, 2)))
+    return fail(PULSE_EALIGN, "coo encode: idx/cols/first/dcol misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  const uint64_t tile = pulse::varint_entry_tile();
+  const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
+  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "coo encode: capacity too large");
+  pulse::CooEncParams p;
+  memset(&p, 0, sizeof p);
+  p.ws = (uint64_t*)workspace;
+  p.idx = idx;
+  p.capacity = capacity;
+  p.end = end;
+  p.seg_begin = seg_begin;
+  p.nseg = nseg;
+  p.cols = cols;
+  p.first = first;
+  p.drow = drow;
+  p.dcol = dcol;
+  p.out_capacity = out_capacity;
+  p.seg_pairs = seg_pairs;
+  p.total = total_pairs;
+  p.ntiles = (uint32_t)nt;
+  return hip_status(pulse::launch_coo_encode(p, (hipStream_t)stream), "coo encode launch");
+}
+
 int pulse_cast_lowp(int dtype, const float* src, uint64_t n, float inv_scale, uint8_t* codes,
                     uint8_t* scales, void* stream) {
   if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)

@@ -19,6 +19,14 @@
 //                          that holds a restart knows its inclusive sum by
 //                          itself and publishes it as a prefix at once.
 // Each tile is staged in LDS so global loads and stores stay contiguous.
+//
+// The same machinery writes the 2-D COO delta downcast of App. H.2 step 4 /
+// App. H.4.1 (coo_encode_kernel): per tensor (row-major, `cols` columns) the
+// first index as it is, then one (uint8 row field, uint16 column field) pair
+// per later entry -- (0, column gap) within a row, (rows ahead, column + 1) on
+// a later row -- with (255, 0) escape pairs, each 255 rows, ahead of a gap of
+// more than 255 rows.  An entry's pair count is 1 + its escapes; their ordered
+// exclusive sum places its pairs.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -406,6 +414,123 @@ __global__ __launch_bounds__(kVT) void varint_sums_kernel(VarintDecParams p) {
   });
 }
 
+// ---------------------------------------------------------------- 2-D COO
+
+// The segment holding entry k: the last segment starting at or before k
+// (several empty segments may share a start), segment 0 for entries before
+// every start.  Whole-thread binary search over the device array.
+__device__ __forceinline__ uint32_t segment_of(const uint64_t* seg_begin, uint32_t nseg, uint64_t k) {
+  uint32_t lo = 0, hi = nseg;  // first start > k lies in [lo, hi]
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (seg_begin[mid] <= k) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo > 0 ? lo - 1 : 0;
+}
+
+__global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
+  __shared__ uint32_t s_idx[kVTile + 1];  // [0] = the entry before the tile
+  __shared__ uint32_t s_off[kVTile];      // pair offset of each entry in the tile
+  __shared__ uint32_t s_flags[kVTile / 32];
+  __shared__ uint32_t s_w[kVWaves];
+  __shared__ uint32_t s_range[2];
+  __shared__ uint64_t s_b;
+  const int tid = threadIdx.x;
+  const uint64_t end = *p.end;
+  const uint64_t nent = end < p.capacity ? end : p.capacity;
+  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t k0 = (uint64_t)tk.tile * kVTile;
+    const uint64_t k1 = k0 + kVTile < nent ? k0 + kVTile : (k0 < nent ? nent : k0);
+    const uint32_t cnt = (uint32_t)(k1 - k0);
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_flags[w] = 0;
+    for (uint32_t i = tid; i < cnt; i += kVT) s_idx[1 + i] = p.idx[k0 + i];
+    if (tid == 0) s_idx[0] = k0 > 0 && k0 <= nent ? p.idx[k0 - 1] : 0u;
+    __syncthreads();
+    if (tid < 64) mark_starts(p.seg_begin, p.nseg, k0, k1, s_flags, s_range);
+    __syncthreads();
+    // this thread's entries: pair counts and last pairs (row field << 16 | column field)
+    uint32_t npair[kVPer], last[kVPer], sum = 0;
+    const uint32_t i0 = (uint32_t)tid * kVPer;
+    uint32_t C = 1, pr = 0, pc = 0;
+    if (i0 < cnt) {
+      C = p.cols[segment_of(p.seg_begin, p.nseg, k0 + i0)];
+      C = C > 0 ? C : 1u;
+      pr = s_idx[i0] / C;
+      pc = s_idx[i0] - pr * C;
+    }
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = i0 + j;
+      npair[j] = 0;
+      last[j] = 0;
+      if (i < cnt) {
+        if (flag_at(s_flags, i) && i != i0) {
+          C = p.cols[segment_of(p.seg_begin, p.nseg, k0 + i)];
+          C = C > 0 ? C : 1u;
+        }
+        const uint32_t cur = s_idx[1 + i];
+        const uint32_t r = cur / C, c = cur - r * C;
+        if (!flag_at(s_flags, i)) {
+          const uint32_t dr = r - pr;
+          if (dr == 0) {
+            npair[j] = 1;
+            last[j] = c - pc;
+          } else {
+            const uint32_t esc = (dr - 1) / 255u;
+            npair[j] = 1 + esc;
+            last[j] = ((dr - 255u * esc) << 16) | (c + 1);
+          }
+        }
+        pr = r;
+        pc = c;
+      }
+      sum += npair[j];
+    }
+    uint32_t agg32;
+    const uint32_t texcl = block_excl_sum(sum, s_w, &agg32);
+    const uint64_t excl = chain_exclusive(p.ws, tk, agg32, false, 0, &s_b);
+    uint32_t o = texcl;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = i0 + j;
+      if (i < cnt) {
+        s_off[i] = o;
+        for (uint32_t q = 0; q < npair[j]; ++q) {
+          const uint64_t pos = excl + o + q;
+          if (pos < p.out_capacity) {
+            const bool esc = q + 1 < npair[j];
+            p.drow[pos] = esc ? (uint8_t)255 : (uint8_t)(last[j] >> 16);
+            p.dcol[pos] = esc ? (uint16_t)0 : (uint16_t)(last[j] & 0xFFFFu);
+          }
+        }
+        o += npair[j];
+      }
+    }
+    __syncthreads();
+    // segments starting in this tile: their pair offset and first index
+    if (tid < 64) {
+      for (uint32_t s = s_range[0] + (uint32_t)lane_id(); s < s_range[1]; s += 64) {
+        const uint64_t b = p.seg_begin[s];
+        const uint64_t e = s + 1 < p.nseg ? p.seg_begin[s + 1] : nent;
+        p.seg_pairs[s] = excl + s_off[(uint32_t)(b - k0)];
+        p.first[s] = e > b ? s_idx[1 + (uint32_t)(b - k0)] : 0u;
+      }
+    }
+    const bool lastt = nent == 0 ? tk.tile == 0 : (k0 <= nent - 1 && nent - 1 < k0 + kVTile);
+    if (lastt && tid < 64) {
+      const uint64_t total = excl + agg32;
+      if (tid == 0) *p.total = total;
+      const uint32_t from = wave_lower_bound64(p.seg_begin, p.nseg, nent);
+      for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) {
+        p.seg_pairs[s] = total;
+        p.first[s] = 0u;
+      }
+    }
+    __syncthreads();
+  });
+}
+
 uint32_t varint_entry_tile() { return kVTile; }
 uint32_t varint_byte_tile() { return kBTile; }
 
@@ -421,6 +546,13 @@ hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream) {
   const uint32_t grid = varint_grid(p.ntiles);
   if (grid == 0) return hipErrorInvalidDevice;
   hipLaunchKernelGGL(varint_encode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream) {
+  const uint32_t grid = varint_grid(p.ntiles);
+  if (grid == 0) return hipErrorInvalidDevice;
+  hipLaunchKernelGGL(coo_encode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
   return hipGetLastError();
 }
 

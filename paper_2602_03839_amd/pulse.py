@@ -91,7 +91,7 @@ EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse
            "pulse_varint_encode", "pulse_varint_decode",
            "pulse_hash_leaf_count", "pulse_hash_workspace_bytes", "pulse_hash_tree",
            "pulse_cast_lowp", "pulse_encode_lowp_batch", "pulse_apply_lowp_batch",
-           "pulse_loco_sparsify_lowp_batch")
+           "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode")
 
 
 def lib():
@@ -128,6 +128,8 @@ def lib():
             L.pulse_hash_workspace_bytes.restype = sz
             L.pulse_hash_tree.argtypes = [vp, u32, vp, vp, vp, sz, vp]
             L.pulse_cast_lowp.argtypes = [i32, vp, u64, f32, vp, vp, vp]
+            L.pulse_coo_encode.argtypes = [vp, u64, vp, vp, u32, vp, vp, vp, vp, u64, vp, vp, vp,
+                                           sz, vp]
             L.pulse_encode_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_apply_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, vp]
             L.pulse_loco_sparsify_lowp_batch.argtypes = [i32, vp, vp, u32, vp, vp, u64, vp, vp, vp,
@@ -398,6 +400,23 @@ def varint_decode(stream_bytes: torch.Tensor, nbytes: torch.Tensor, idx: torch.T
                                      ws.numel(), _stream(stream)), "pulse_varint_decode")
 
 
+def coo_encode(idx: torch.Tensor, end: torch.Tensor, seg_begin: torch.Tensor, cols: torch.Tensor,
+               first: torch.Tensor, drow: torch.Tensor, dcol: torch.Tensor,
+               seg_pairs: torch.Tensor, total: torch.Tensor, ws: torch.Tensor,
+               capacity: Optional[int] = None, stream=None) -> None:
+    """2-D COO delta downcast of a sorted patch's indices (pulse_coo_encode)."""
+    assert idx.element_size() == 4 and cols.element_size() == 4 and first.element_size() == 4
+    assert drow.element_size() == 1 and dcol.element_size() == 2
+    assert seg_begin.element_size() == 8 and seg_pairs.element_size() == 8
+    nseg = seg_begin.numel()
+    assert cols.numel() >= nseg and first.numel() >= nseg and seg_pairs.numel() >= nseg
+    cap = idx.numel() if capacity is None else capacity
+    _check(lib().pulse_coo_encode(_p(idx), cap, _p(end), _p(seg_begin), nseg, _p(cols), _p(first),
+                                  _p(drow), _p(dcol), min(drow.numel(), dcol.numel()),
+                                  _p(seg_pairs), _p(total), _p(ws), ws.numel(), _stream(stream)),
+           "pulse_coo_encode")
+
+
 def lowp_sizes(dtype: int, n: int):
     """(code bytes, scale bytes) of one tensor's D view."""
     if dtype == FP8_E4M3:
@@ -493,7 +512,7 @@ class LocoLowpBatch:
                                                     _p(idx), _p(val), cap, _p(count),
                                                     _p(seg_begin), _p(ws), ws.numel(),
                                                     _stream(stream)),
-               "pulse_loco_sparsify_lowp_batch")
+               "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode")
 
 
 def hash_leaf_count(total_values: int) -> int:

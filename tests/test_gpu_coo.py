@@ -1,0 +1,166 @@
+"""GPU parity of the 2-D COO delta downcast (App. H.2 step 4, App. H.4.1)
+against the oracle: first indices, (uint8 row, uint16 column) pairs, segment
+pair offsets and the pair count, bit-exact.  Random patches over many shapes
+and densities (long row gaps with escapes, one-column and 65535-column
+tensors, empty segments, segments across tile boundaries), output capacity
+overflow, the 0.5B-shaped fused patch in full and the 32B-shaped one on
+sampled segments.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2602_03839_amd import pulse
+
+from gpu_helpers import counter, dev, h32, read_count
+
+pytestmark = pytest.mark.gpu
+
+TILE = 4096  # entries per tile of the index-stream kernels
+
+
+def random_patch(rng, shapes, density):
+    idx, seg = [], []
+    for r, c in shapes:
+        seg.append(sum(x.size for x in idx))
+        n = r * c
+        k = min(n, rng.binomial(n, density)) if n else 0
+        idx.append(np.sort(rng.choice(n, k, replace=False)).astype(np.uint32) if k else
+                   np.zeros(0, dtype=np.uint32))
+    return np.concatenate(idx), np.array(seg, dtype=np.uint64), np.array([c for _, c in shapes],
+                                                                          dtype=np.uint32)
+
+
+def gpu_coo(idx, seg, cols, out_cap=None, ws=None, idx_d=None, end_d=None, seg_d=None):
+    nseg = seg.size if seg is not None else seg_d.numel()
+    idx_d = dev(idx) if idx_d is None else idx_d
+    end_d = counter(idx.size) if end_d is None else end_d
+    seg_d = dev(seg) if seg_d is None else seg_d
+    nent = idx.size if idx is not None else int(end_d.item())
+    cap = nent + 8 if out_cap is None else out_cap
+    drow = torch.zeros(max(cap, 1), dtype=torch.uint8, device="cuda")
+    dcol = torch.zeros(max(cap, 1), dtype=torch.int16, device="cuda")
+    first = torch.zeros(nseg, dtype=torch.int32, device="cuda")
+    sp = torch.zeros(nseg, dtype=torch.int64, device="cuda")
+    total = counter(0)
+    pulse.coo_encode(idx_d, end_d, seg_d, dev(cols), first, drow[:cap] if cap else drow[:0],
+                     dcol[:cap] if cap else dcol[:0], sp, total,
+                     pulse.workspace() if ws is None else ws)
+    torch.cuda.synchronize()
+    P = read_count(total)
+    k = min(P, cap)
+    return (P, h32(first), drow[:k].cpu().numpy(), dcol[:k].cpu().numpy().view(np.uint16),
+            sp.cpu().numpy().view(np.uint64))
+
+
+def check(idx, seg, cols, **kw):
+    of, od, oc, osp = oracle.coo_encode(idx, seg, cols)
+    P, gf, gd, gc, gsp = gpu_coo(idx, seg, cols, **kw)
+    assert P == od.size
+    np.testing.assert_array_equal(gf, of)
+    np.testing.assert_array_equal(gsp, osp)
+    np.testing.assert_array_equal(gd, od[:gd.size])
+    np.testing.assert_array_equal(gc, oc[:gc.size])
+    return P
+
+
+SHAPES = [(1000, 37), (1, 5), (0, 10), (3000, 1), (64, 5120), (2, 65535), (700, 3), (1, 4096),
+          (20000, 7), (5, 1)]
+
+
+@pytest.mark.parametrize("density", [1e-4, 2e-3, 0.05, 0.5, 1.0])
+def test_random_patches(density):
+    rng = np.random.default_rng(int(density * 1e4) + 3)
+    idx, seg, cols = random_patch(rng, SHAPES, density)
+    print(f"coo: density {density}, {idx.size} entries", flush=True)
+    check(idx, seg, cols)
+
+
+def test_long_row_gaps_and_tile_boundaries():
+    rng = np.random.default_rng(4)
+    # one tall one-column tensor: every entry is a new row, gaps up to ~10^4 rows
+    a = np.sort(rng.choice(10 ** 7, 3 * TILE + 5, replace=False)).astype(np.uint32)
+    # segments that start exactly on tile boundaries
+    b = np.arange(TILE, dtype=np.uint32) * 3
+    c = np.arange(TILE - 1, dtype=np.uint32) * 700
+    idx = np.concatenate([a, b, c])
+    seg = np.array([0, a.size, a.size + b.size], dtype=np.uint64)
+    cols = np.array([1, 4, 600], dtype=np.uint32)
+    P = check(idx, seg, cols)
+    assert P > idx.size  # escapes present
+
+
+def test_segments_at_exact_tile_starts():
+    sizes = [TILE, TILE, 0, 2 * TILE, 1, 0]
+    rng = np.random.default_rng(5)
+    parts = [np.sort(rng.choice(10 ** 6, n, replace=False)).astype(np.uint32) for n in sizes]
+    idx = np.concatenate(parts)
+    seg = np.cumsum([0] + sizes[:-1]).astype(np.uint64)
+    cols = np.array([1000, 17, 9, 65535, 3, 2], dtype=np.uint32)
+    check(idx, seg, cols)
+
+
+def test_output_capacity_overflow():
+    rng = np.random.default_rng(6)
+    idx, seg, cols = random_patch(rng, SHAPES, 2e-3)
+    P, *_ = gpu_coo(idx, seg, cols)
+    cap = P // 3
+    check(idx, seg, cols, out_cap=cap)
+
+
+def test_empty_patch():
+    idx = np.zeros(0, dtype=np.uint32)
+    seg = np.zeros(3, dtype=np.uint64)
+    cols = np.array([5, 6, 7], dtype=np.uint32)
+    P, gf, _, _, gsp = gpu_coo(idx, seg, cols, idx_d=torch.zeros(1, dtype=torch.int32, device="cuda"))
+    assert P == 0
+    assert gf.tolist() == [0, 0, 0] and gsp.tolist() == [0, 0, 0]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("key", ["0.5b", "32b"])
+def test_fused_patch_of_a_model_set(key):
+    """The patch of one fused encode step at lr 1e-6: every segment against the
+    oracle for the 0.5B-shaped set; 24 sampled segments (each computed by the
+    oracle from that segment's entries alone) plus all offsets' consistency
+    for the 32B-shaped one."""
+    from test_gpu_configs import ModelSet, encode_set, segments
+    torch.cuda.empty_cache()
+    ms = ModelSet(key)
+    w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
+    S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
+    ms.init(w, S)
+    ms.step(w, 1e-6, 1)
+    cap = ms.N // 50
+    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    val = torch.empty(cap, dtype=torch.int16, device="cuda")
+    count = counter(0)
+    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
+    ws = pulse.workspace()
+    encode_set(ms, w, S, None, idx, val, count, seg, ws)
+    del w, S
+    torch.cuda.empty_cache()
+    segs = segments(seg, count)
+    nent = segs[-1]
+    assert nent <= cap
+    cols = np.array([s.shape[-1] for s in ms.specs], dtype=np.uint32)
+    if ms.flat:  # flat indices: make them local to each tensor for the 2-D view
+        base = torch.tensor(np.repeat(np.array(ms.offs[:-1], dtype=np.int64),
+                                      np.diff(segs)), dtype=torch.int64, device="cuda")
+        idx[:nent] = ((idx[:nent].to(torch.int64) & 0xFFFFFFFF) - base).to(torch.int32)
+    print(f"coo {key}: {nent} entries in {ms.T} segments", flush=True)
+    P, gf, gd, gc, gsp = gpu_coo(None, None, cols, out_cap=nent + ms.T * 64, ws=ws, idx_d=idx,
+                                 end_d=count, seg_d=seg)
+    hidx = h32(idx[:nent])
+    rng = np.random.default_rng(7)
+    picks = range(ms.T) if key == "0.5b" else sorted(set(rng.choice(ms.T, 24, replace=False)) | {0, ms.T - 1})
+    ends = list(gsp[1:]) + [P]
+    for s in picks:
+        a, e = segs[s], segs[s + 1]
+        of, od, oc, _ = oracle.coo_encode(hidx[a:e], [0], cols[s:s + 1])
+        assert int(gf[s]) == int(of[0]), s
+        p0, p1 = int(gsp[s]), int(ends[s])
+        np.testing.assert_array_equal(gd[p0:p1], od, err_msg=f"segment {s}")
+        np.testing.assert_array_equal(gc[p0:p1], oc, err_msg=f"segment {s}")
+    assert all(int(gsp[s]) <= int(ends[s]) for s in range(ms.T))
