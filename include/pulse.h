@@ -337,6 +337,32 @@ int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end
                      void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * pulse_coo_decode -- the indices back from a 2-D COO delta stream (Alg. 1
+ * Decode's Upcast and DeltaDecode steps for pulse_coo_encode's format).
+ *   drow, dcol    device [pair_capacity]; *npairs (device) of them form the
+ *                 stream.
+ *   seg_begin     device [nseg]: the entry where each segment starts; *nent
+ *                 (device) the number of entries (container metadata sent
+ *                 with the stream, as encode's seg_begin and count).
+ *   seg_pairs, first, cols   as pulse_coo_encode wrote / read them.
+ *   idx           device uint32 [capacity]: entry k of the patch at idx[k];
+ *                 entries at or past capacity are not written.
+ *   scratch       device, 8 * pair_capacity bytes, 8-byte aligned: per-pair
+ *                 state of the first pass.
+ * Two passes: the row and escape count of each pair since its segment's
+ * start (one segmented running sum), then its flat index (a running sum that
+ * restarts at each new-row pair), written at its entry's position.  Requires
+ * fewer than 2^22 escapes per segment (a tensor of at most 2^30 rows).  A
+ * stream that encode did not write decodes to unspecified indices but no
+ * access leaves the buffers.
+ */
+int pulse_coo_decode(const uint8_t *drow, const uint16_t *dcol, uint64_t pair_capacity,
+                     const uint64_t *npairs, const uint64_t *seg_begin, const uint64_t *seg_pairs,
+                     uint32_t nseg, const uint32_t *cols, const uint32_t *first,
+                     const uint64_t *nent, uint32_t *idx, uint64_t capacity, uint64_t *scratch,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Receivers that compute in a precision below BF16 (App. D): the compute view
  * cast_D of the FP32 masters, the patch of the values whose view changes
  * (Alg. 1 with D in place of BF16), and its apply on the receiver's D copy.

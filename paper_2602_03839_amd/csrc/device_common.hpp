@@ -255,7 +255,9 @@ __device__ __forceinline__ void look_back_issue(uint64_t* ws, const Ticket& tk, 
   }
 }
 
-template <int LK>
+// WIDE: the aggregates may exceed 32 bits (a packed multi-field value); they
+// are then summed with 64-bit lane shuffles.
+template <int LK, bool WIDE = false>
 __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win) {
   const int lane = lane_id();
   uint64_t excl = 0;
@@ -328,13 +330,23 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
     // most one tile, so 64 * LK of them fit 32 bits): sum them with the DPP
     // scan instead of 64-bit lane shuffles, and take the one prefix value
     // from its lane.
-    uint32_t a = 0;
+    if (WIDE) {
+      uint64_t a = 0;
 #pragma unroll
-    for (int m = 0; m < LK; ++m) {
-      const bool take = m < first_m || (m == first_m && lane < first_l);
-      if (take) a += (uint32_t)(win.w[m] & kValueMask);
+      for (int m = 0; m < LK; ++m) {
+        const bool take = m < first_m || (m == first_m && lane < first_l);
+        if (take) a += win.w[m] & kValueMask;
+      }
+      excl += wave_sum_u64(a);
+    } else {
+      uint32_t a = 0;
+#pragma unroll
+      for (int m = 0; m < LK; ++m) {
+        const bool take = m < first_m || (m == first_m && lane < first_l);
+        if (take) a += (uint32_t)(win.w[m] & kValueMask);
+      }
+      excl += __builtin_amdgcn_readlane(wave_incl_scan(a), 63);
     }
-    excl += __builtin_amdgcn_readlane(wave_incl_scan(a), 63);
     if (first_m < LK) {
       uint64_t pw = 0;
 #pragma unroll

@@ -281,6 +281,24 @@ struct CooEncParams {
   uint32_t ntiles;
 };
 
+struct CooDecParams {
+  uint64_t* ws;
+  const uint8_t* drow;
+  const uint16_t* dcol;
+  uint64_t pair_capacity;      // pairs readable (and scratch size)
+  const uint64_t* npairs;      // device: pairs in the stream
+  const uint64_t* seg_begin;   // device [nseg]: entry where each segment starts
+  const uint64_t* seg_pairs;   // device [nseg]: pair where each segment starts
+  uint32_t nseg;
+  const uint32_t* cols;        // device [nseg]
+  const uint32_t* first;       // device [nseg]
+  const uint64_t* nent;        // device: entries in the patch
+  uint32_t* idx;
+  uint64_t capacity;
+  uint64_t* scratch;           // device [pair_capacity]: per pair (row, escapes) of pass 1
+  uint32_t ntiles;
+};
+
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(OuterParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
@@ -298,6 +316,7 @@ uint32_t varint_byte_tile();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream);
+hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream);
 hipError_t launch_outer(const OuterParams& p, hipStream_t stream);
 uint32_t lowp_tile_elems();
 hipError_t launch_encode_lowp(int dtype, LowpParams& p, hipStream_t stream);

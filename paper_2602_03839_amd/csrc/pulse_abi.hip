@@ -520,6 +520,46 @@ int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end
   return hip_status(pulse::launch_coo_encode(p, (hipStream_t)stream), "coo encode launch");
 }
 
+int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_capacity,
+                     const uint64_t* npairs, const uint64_t* seg_begin, const uint64_t* seg_pairs,
+                     uint32_t nseg, const uint32_t* cols, const uint32_t* first,
+                     const uint64_t* nent, uint32_t* idx, uint64_t capacity, uint64_t* scratch,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  if (nseg == 0) return fail(PULSE_EINVAL, "coo decode: nseg is 0");
+  if (!npairs || !seg_begin || !seg_pairs || !cols || !first || !nent)
+    return fail(PULSE_EINVAL, "coo decode: NULL pointer");
+  if (pair_capacity > 0 && (!drow || !dcol || !scratch))
+    return fail(PULSE_EINVAL, "coo decode: drow/dcol/scratch is NULL");
+  if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "coo decode: idx is NULL");
+  if (!aligned(npairs, 8) || !aligned(seg_begin, 8) || !aligned(seg_pairs, 8) || !aligned(nent, 8) ||
+      (scratch && !aligned(scratch, 8)))
+    return fail(PULSE_EALIGN, "coo decode: counters/scratch not 8-byte aligned");
+  if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4) || (dcol && !aligned(dcol, 2)))
+    return fail(PULSE_EALIGN, "coo decode: idx/cols/first/dcol misaligned");
+  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  const uint64_t tile = pulse::varint_entry_tile();
+  const uint64_t nt = pair_capacity == 0 ? 1 : (pair_capacity + tile - 1) / tile;
+  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
+  pulse::CooDecParams p;
+  memset(&p, 0, sizeof p);
+  p.ws = (uint64_t*)workspace;
+  p.drow = drow;
+  p.dcol = dcol;
+  p.pair_capacity = pair_capacity;
+  p.npairs = npairs;
+  p.seg_begin = seg_begin;
+  p.seg_pairs = seg_pairs;
+  p.nseg = nseg;
+  p.cols = cols;
+  p.first = first;
+  p.nent = nent;
+  p.idx = idx;
+  p.capacity = capacity;
+  p.scratch = scratch;
+  p.ntiles = (uint32_t)nt;
+  return hip_status(pulse::launch_coo_decode(p, (hipStream_t)stream), "coo decode launch");
+}
+
 int pulse_cast_lowp(int dtype, const float* src, uint64_t n, float inv_scale, uint8_t* codes,
                     uint8_t* scales, void* stream) {
   if (dtype != PULSE_DTYPE_FP8_E4M3 && dtype != PULSE_DTYPE_MXFP4)

@@ -26,7 +26,11 @@
 // per later entry -- (0, column gap) within a row, (rows ahead, column + 1) on
 // a later row -- with (255, 0) escape pairs, each 255 rows, ahead of a gap of
 // more than 255 rows.  An entry's pair count is 1 + its escapes; their ordered
-// exclusive sum places its pairs.
+// exclusive sum places its pairs.  Its decode is two segmented running sums
+// over the pairs: coo_rows_kernel (row and escape count since the segment's
+// start, both restarting at segment starts, packed into one scanned value)
+// and coo_flat_kernel (the flat index, restarting at every new-row pair and
+// segment start, written at the entry's position).
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -116,6 +120,8 @@ __device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
 // `incl_known` whatever came before (a segment starts in it), published as a
 // prefix at once; the tile still looks back for its own entries before the
 // restart.
+// WIDE: aggregates may exceed 32 bits (the look-back then sums in 64 bits).
+template <bool WIDE = false>
 __device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg, bool restart,
                                     uint64_t incl_known, uint64_t* s_b) {
   if (threadIdx.x < 64) {
@@ -128,7 +134,7 @@ __device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg
         status_publish(ws, tk.seq, restart ? kFlagPrefix : kFlagAggregate, restart ? incl_known : agg);
       LookWindow<1> win;
       look_back_issue<1>(ws, tk, (int64_t)tk.tile - 1, win);
-      excl = look_back<1>(ws, tk, win);
+      excl = look_back<1, WIDE>(ws, tk, win);
       if (lane == 0 && !restart) status_publish(ws, tk.seq, kFlagPrefix, excl + agg);
     }
     if (lane == 0) *s_b = excl;
@@ -531,6 +537,248 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
   });
 }
 
+// Segmented inclusive running sum of one 64-bit value per element over a tile
+// staged in s_v (cnt elements), restarting at the elements flagged in s_rf:
+// there the sum is the element's own value.  Elements before the tile's first
+// restart add `carry` from earlier tiles, which chain_exclusive supplies (a
+// tile holding a restart publishes its inclusive tail at once).  s_v ends up
+// holding the sums.  Every thread of the block calls it.
+template <bool WIDE>
+__device__ void tile_segmented_sum(uint64_t* ws, const Ticket& tk, uint64_t* s_v,
+                                   const uint32_t* s_rf, uint32_t cnt, uint64_t* s_tsum,
+                                   uint32_t* s_trst, uint64_t* s_tail, uint64_t* s_b) {
+  const int tid = threadIdx.x;
+  uint64_t run = 0;
+  bool rst = false;
+#pragma unroll
+  for (int j = 0; j < kVPer; ++j) {
+    const uint32_t i = (uint32_t)tid * kVPer + j;
+    if (i < cnt) {
+      if (flag_at(s_rf, i)) {
+        run = 0;
+        rst = true;
+      }
+      run += s_v[i];
+    }
+  }
+  s_tsum[tid] = run;
+  s_trst[tid] = rst ? 1u : 0u;
+  __syncthreads();
+  if (tid < 64) {
+    uint64_t c = 0;
+    bool r = false;
+    uint64_t vals[4];
+    bool rs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      vals[q] = s_tsum[tid * 4 + q];
+      rs[q] = s_trst[tid * 4 + q] != 0u;
+      c = rs[q] ? vals[q] : c + vals[q];
+      r = r || rs[q];
+    }
+    uint64_t ic = c;
+    bool ir = r;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t oc = __shfl_up(ic, d, 64);
+      const int orr = __shfl_up(ir ? 1 : 0, d, 64);
+      if (lane_id() >= d && !ir) {
+        ic = oc + ic;
+        ir = orr != 0;
+      }
+    }
+    uint64_t ec = __shfl_up(ic, 1, 64);
+    bool er = __shfl_up(ir ? 1 : 0, 1, 64) != 0;
+    if (lane_id() == 0) {
+      ec = 0;
+      er = false;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      s_tsum[tid * 4 + q] = ec;
+      s_trst[tid * 4 + q] = er ? 1u : 0u;
+      ec = rs[q] ? vals[q] : ec + vals[q];
+      er = er || rs[q];
+    }
+    if (tid == 63) {
+      s_tail[0] = ir ? 1u : 0u;
+      s_tail[1] = ic;
+    }
+  }
+  __syncthreads();
+  const bool tile_rst = s_tail[0] != 0u;
+  const uint64_t tile_sum = s_tail[1];
+  const uint64_t carry = chain_exclusive<WIDE>(ws, tk, tile_sum, tile_rst, tile_sum, s_b);
+  uint64_t acc = s_tsum[tid] + (s_trst[tid] ? 0u : carry);
+#pragma unroll
+  for (int j = 0; j < kVPer; ++j) {
+    const uint32_t i = (uint32_t)tid * kVPer + j;
+    if (i < cnt) {
+      if (flag_at(s_rf, i)) acc = 0;
+      acc += s_v[i];
+      s_v[i] = acc;
+    }
+  }
+  __syncthreads();
+}
+
+// Pass 1: per pair, (row since the segment's first entry) | (escapes since
+// the segment's start) << 32, inclusive.  The first pair of a segment starts
+// from the row of the segment's first index.
+__global__ __launch_bounds__(kVT) void coo_rows_kernel(CooDecParams p) {
+  __shared__ uint64_t s_v[kVTile];
+  __shared__ uint32_t s_rf[kVTile / 32];
+  __shared__ uint32_t s_range[2];
+  __shared__ uint64_t s_tsum[kVT];
+  __shared__ uint32_t s_trst[kVT];
+  __shared__ uint64_t s_tail[2];
+  __shared__ uint64_t s_b;
+  const int tid = threadIdx.x;
+  const uint64_t n0 = *p.npairs;
+  const uint64_t np = n0 < p.pair_capacity ? n0 : p.pair_capacity;
+  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t q0 = (uint64_t)tk.tile * kVTile;
+    const uint64_t q1 = q0 + kVTile < np ? q0 + kVTile : (q0 < np ? np : q0);
+    const uint32_t cnt = (uint32_t)(q1 - q0);
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_rf[w] = 0;
+    __syncthreads();
+    if (tid < 64) mark_starts(p.seg_pairs, p.nseg, q0, q1, s_rf, s_range);
+    __syncthreads();
+    for (uint32_t i = tid; i < cnt; i += kVT) {
+      const uint32_t dr = p.drow[q0 + i];
+      const bool esc = dr == 255u && p.dcol[q0 + i] == 0;
+      uint64_t v = (uint64_t)dr | ((uint64_t)(esc ? 1u : 0u) << 32);
+      if (flag_at(s_rf, i)) {  // the segment's first pair: start from its first index's row
+        const uint32_t s = segment_of(p.seg_pairs, p.nseg, q0 + i);
+        const uint32_t C = p.cols[s] > 0 ? p.cols[s] : 1u;
+        v += p.first[s] / C;
+      }
+      s_v[i] = v;
+    }
+    __syncthreads();
+    tile_segmented_sum<true>(p.ws, tk, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
+    for (uint32_t i = tid; i < cnt; i += kVT) p.scratch[q0 + i] = s_v[i];
+    __syncthreads();
+  });
+}
+
+// Pass 2: the flat index of every pair's entry, written at
+// seg_begin[s] + 1 + (pairs before it in the segment) - (escapes before it);
+// each segment's first index goes to seg_begin[s].  A thread takes 16
+// consecutive pairs of the tile: it finds its first pair's segment by binary
+// search and moves to the next segment only at a segment start.
+__global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
+  __shared__ uint64_t s_v[kVTile];
+  __shared__ uint32_t s_pair[kVTile];     // drow | dcol << 8
+  __shared__ uint32_t s_rf[kVTile / 32];
+  __shared__ uint32_t s_seg[kVTile / 32];
+  __shared__ uint32_t s_range[2];
+  __shared__ uint64_t s_tsum[kVT];
+  __shared__ uint32_t s_trst[kVT];
+  __shared__ uint64_t s_tail[2];
+  __shared__ uint64_t s_b;
+  const int tid = threadIdx.x;
+  const uint64_t n0 = *p.npairs;
+  const uint64_t np = n0 < p.pair_capacity ? n0 : p.pair_capacity;
+  const uint64_t nent = *p.nent;
+  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t q0 = (uint64_t)tk.tile * kVTile;
+    const uint64_t q1 = q0 + kVTile < np ? q0 + kVTile : (q0 < np ? np : q0);
+    const uint32_t cnt = (uint32_t)(q1 - q0);
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) {
+      s_rf[w] = 0;
+      s_seg[w] = 0;
+    }
+    for (uint32_t i = tid; i < cnt; i += kVT) {
+      s_v[i] = p.scratch[q0 + i];
+      s_pair[i] = (uint32_t)p.drow[q0 + i] | ((uint32_t)p.dcol[q0 + i] << 8);
+    }
+    __syncthreads();
+    if (tid < 64) mark_starts(p.seg_pairs, p.nseg, q0, q1, s_seg, s_range);
+    __syncthreads();
+    // values and restarts of this thread's pairs: a new-row pair restarts at
+    // row * C + column, a segment's first pair at its first index + gap (or,
+    // if it starts a new row, as a new-row pair), a same-row pair adds its
+    // gap, an escape adds nothing (the new-row pair after it restarts)
+    const uint32_t i0 = (uint32_t)tid * kVPer;
+    uint32_t escb[kVPer];
+    uint32_t seg_id = 0, C = 1;
+    uint64_t sp = 0, sb = 0;
+    uint32_t rst_bits = 0, esc_bits = 0;
+    if (i0 < cnt) {
+      seg_id = segment_of(p.seg_pairs, p.nseg, q0 + i0);
+      C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
+      sp = p.seg_pairs[seg_id];
+      sb = p.seg_begin[seg_id];
+    }
+    uint32_t seg_at[kVPer];  // segment of each pair (changes only at starts)
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = i0 + j;
+      escb[j] = 0;
+      seg_at[j] = seg_id;
+      if (i >= cnt) continue;
+      const bool seg_start = flag_at(s_seg, i);
+      if (seg_start && i != i0) {
+        seg_id = segment_of(p.seg_pairs, p.nseg, q0 + i);
+        C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
+        seg_at[j] = seg_id;
+      }
+      const uint32_t pr = s_pair[i];
+      const uint32_t dr = pr & 0xFFu, dc = pr >> 8;
+      const bool esc = dr == 255u && dc == 0;
+      const uint64_t st = s_v[i];
+      escb[j] = (uint32_t)(st >> 32);
+      uint64_t v = esc ? 0 : dc;
+      bool rst = seg_start;
+      if (!esc && dr > 0) {
+        v = (uint64_t)(uint32_t)st * C + dc - 1;
+        rst = true;
+      } else if (seg_start && !esc) {
+        v = (uint64_t)p.first[seg_id] + dc;
+      }
+      if (rst) rst_bits |= 1u << j;
+      if (esc) esc_bits |= 1u << j;
+      s_v[i] = v;
+    }
+    // publish this thread's restart flags (its 16 bits of the tile's bitmap)
+    if (i0 < cnt) atomicOr(&s_rf[i0 >> 5], rst_bits << (i0 & 31));
+    __syncthreads();
+    tile_segmented_sum<true>(p.ws, tk, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
+    // scatter this thread's entries
+    uint32_t cur = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = i0 + j;
+      if (i >= cnt) break;
+      if (seg_at[j] != cur) {
+        cur = seg_at[j];
+        sp = p.seg_pairs[cur];
+        sb = p.seg_begin[cur];
+      }
+      if ((esc_bits >> j) & 1u) continue;
+      const uint64_t pos = sb + 1 + (q0 + i - sp) - escb[j];
+      if (pos < p.capacity) p.idx[pos] = (uint32_t)s_v[i];
+    }
+    // first entries of the segments starting in this tile (and, in the last
+    // tile, of those whose pairs start at the end of the stream)
+    if (tid < 64) {
+      auto put_first = [&](uint32_t s) {
+        const uint64_t b = p.seg_begin[s];
+        const uint64_t e = s + 1 < p.nseg ? p.seg_begin[s + 1] : nent;
+        if (e > b && b < p.capacity) p.idx[b] = p.first[s];
+      };
+      for (uint32_t s = s_range[0] + (uint32_t)lane_id(); s < s_range[1]; s += 64) put_first(s);
+      const bool lastt = np == 0 ? tk.tile == 0 : (q0 <= np - 1 && np - 1 < q0 + kVTile);
+      if (lastt) {
+        const uint32_t from = wave_lower_bound64(p.seg_pairs, p.nseg, np);
+        for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) put_first(s);
+      }
+    }
+    __syncthreads();
+  });
+}
+
 uint32_t varint_entry_tile() { return kVTile; }
 uint32_t varint_byte_tile() { return kBTile; }
 
@@ -553,6 +801,15 @@ hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream) {
   const uint32_t grid = varint_grid(p.ntiles);
   if (grid == 0) return hipErrorInvalidDevice;
   hipLaunchKernelGGL(coo_encode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream) {
+  const uint32_t grid = varint_grid(p.ntiles);
+  if (grid == 0) return hipErrorInvalidDevice;
+  hipLaunchKernelGGL(coo_rows_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(coo_flat_kernel, dim3(grid), dim3(kVT), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -91,7 +91,7 @@ EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse
            "pulse_varint_encode", "pulse_varint_decode",
            "pulse_hash_leaf_count", "pulse_hash_workspace_bytes", "pulse_hash_tree",
            "pulse_cast_lowp", "pulse_encode_lowp_batch", "pulse_apply_lowp_batch",
-           "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode")
+           "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode", "pulse_coo_decode")
 
 
 def lib():
@@ -130,6 +130,8 @@ def lib():
             L.pulse_cast_lowp.argtypes = [i32, vp, u64, f32, vp, vp, vp]
             L.pulse_coo_encode.argtypes = [vp, u64, vp, vp, u32, vp, vp, vp, vp, u64, vp, vp, vp,
                                            sz, vp]
+            L.pulse_coo_decode.argtypes = [vp, vp, u64, vp, vp, vp, u32, vp, vp, vp, vp, u64, vp,
+                                           vp, sz, vp]
             L.pulse_encode_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_apply_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, vp]
             L.pulse_loco_sparsify_lowp_batch.argtypes = [i32, vp, vp, u32, vp, vp, u64, vp, vp, vp,
@@ -417,6 +419,20 @@ def coo_encode(idx: torch.Tensor, end: torch.Tensor, seg_begin: torch.Tensor, co
            "pulse_coo_encode")
 
 
+def coo_decode(drow: torch.Tensor, dcol: torch.Tensor, npairs: torch.Tensor,
+               seg_begin: torch.Tensor, seg_pairs: torch.Tensor, cols: torch.Tensor,
+               first: torch.Tensor, nent: torch.Tensor, idx: torch.Tensor, scratch: torch.Tensor,
+               ws: torch.Tensor, stream=None) -> None:
+    """Indices back from a 2-D COO delta stream (pulse_coo_decode)."""
+    pc = min(drow.numel(), dcol.numel())
+    assert scratch.element_size() == 8 and scratch.numel() >= pc
+    nseg = seg_begin.numel()
+    _check(lib().pulse_coo_decode(_p(drow), _p(dcol), pc, _p(npairs), _p(seg_begin),
+                                  _p(seg_pairs), nseg, _p(cols), _p(first), _p(nent), _p(idx),
+                                  idx.numel(), _p(scratch), _p(ws), ws.numel(), _stream(stream)),
+           "pulse_coo_decode")
+
+
 def lowp_sizes(dtype: int, n: int):
     """(code bytes, scale bytes) of one tensor's D view."""
     if dtype == FP8_E4M3:
@@ -512,7 +528,7 @@ class LocoLowpBatch:
                                                     _p(idx), _p(val), cap, _p(count),
                                                     _p(seg_begin), _p(ws), ws.numel(),
                                                     _stream(stream)),
-               "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode")
+               "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode", "pulse_coo_decode")
 
 
 def hash_leaf_count(total_values: int) -> int:

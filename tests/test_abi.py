@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 22, names
+    assert len(names) == 23, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name

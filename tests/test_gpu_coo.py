@@ -1,6 +1,7 @@
 """GPU parity of the 2-D COO delta downcast (App. H.2 step 4, App. H.4.1)
 against the oracle: first indices, (uint8 row, uint16 column) pairs, segment
-pair offsets and the pair count, bit-exact.  Random patches over many shapes
+pair offsets and the pair count, bit-exact; the GPU decode of the oracle's
+streams and of the GPU's own (round trip) gives the patch back.  Random patches over many shapes
 and densities (long row gaps with escapes, one-column and 65535-column
 tensors, empty segments, segments across tile boundaries), output capacity
 overflow, the 0.5B-shaped fused patch in full and the 32B-shaped one on
@@ -33,6 +34,13 @@ def random_patch(rng, shapes, density):
 
 
 def gpu_coo(idx, seg, cols, out_cap=None, ws=None, idx_d=None, end_d=None, seg_d=None):
+    """GPU encode; without out_cap the pair buffer is sized by a first call's
+    true total (the overflow protocol: *total_pairs is exact even when the
+    buffer was too small)."""
+    if out_cap is None:
+        n = idx.size if idx is not None else int(end_d.item())
+        P = gpu_coo(idx, seg, cols, n + 8, ws, idx_d, end_d, seg_d)[0]
+        out_cap = max(P, n + 8)
     nseg = seg.size if seg is not None else seg_d.numel()
     idx_d = dev(idx) if idx_d is None else idx_d
     end_d = counter(idx.size) if end_d is None else end_d
@@ -164,3 +172,65 @@ def test_fused_patch_of_a_model_set(key):
         np.testing.assert_array_equal(gd[p0:p1], od, err_msg=f"segment {s}")
         np.testing.assert_array_equal(gc[p0:p1], oc, err_msg=f"segment {s}")
     assert all(int(gsp[s]) <= int(ends[s]) for s in range(ms.T))
+    # the GPU's stream decodes on the GPU to the patch
+    back = gpu_decode(gf, gd, gc, gsp, np.array(segs[:-1], dtype=np.uint64), cols, nent, ws=ws)
+    np.testing.assert_array_equal(back, hidx)
+
+
+# ---------------------------------------------------------------- decode
+def gpu_decode(first, drow, dcol, seg_pairs, seg_begin, cols, nent, ws=None, cap=None):
+    nseg = len(seg_begin)
+    P = drow.size
+    d_drow = torch.from_numpy(np.ascontiguousarray(drow, dtype=np.uint8)).cuda() if P else \
+        torch.zeros(1, dtype=torch.uint8, device="cuda")
+    d_dcol = dev(np.ascontiguousarray(dcol, dtype=np.uint16)) if P else \
+        torch.zeros(1, dtype=torch.int16, device="cuda")
+    cap = nent if cap is None else cap
+    idx = torch.full((max(cap, 1),), -1, dtype=torch.int32, device="cuda")
+    scratch = torch.empty(max(P, 1), dtype=torch.int64, device="cuda")
+    pulse.coo_decode(d_drow[:P] if P else d_drow[:0], d_dcol[:P] if P else d_dcol[:0], counter(P),
+                     dev(np.asarray(seg_begin, dtype=np.uint64)),
+                     dev(np.asarray(seg_pairs, dtype=np.uint64)), dev(np.asarray(cols, np.uint32)),
+                     dev(np.asarray(first, np.uint32)), counter(nent), idx[:cap] if cap else idx[:0],
+                     scratch, pulse.workspace() if ws is None else ws)
+    torch.cuda.synchronize()
+    return h32(idx)[:cap]
+
+
+@pytest.mark.parametrize("density", [1e-4, 2e-3, 0.05, 0.5, 1.0])
+def test_decode_oracle_stream(density):
+    """The oracle's stream of a random patch decodes on the GPU to the patch."""
+    rng = np.random.default_rng(int(density * 1e4) + 11)
+    idx, seg, cols = random_patch(rng, SHAPES, density)
+    f, d, c, sp = oracle.coo_encode(idx, seg, cols)
+    np.testing.assert_array_equal(gpu_decode(f, d, c, sp, seg, cols, idx.size), idx)
+
+
+def test_decode_escapes_and_tile_boundaries():
+    rng = np.random.default_rng(12)
+    a = np.sort(rng.choice(10 ** 7, 3 * TILE + 5, replace=False)).astype(np.uint32)
+    b = np.arange(TILE, dtype=np.uint32) * 3
+    e1 = np.array([5], dtype=np.uint32)  # a one-entry segment: no pairs
+    c = np.arange(TILE - 1, dtype=np.uint32) * 700
+    idx = np.concatenate([a, b, e1, c, e1])
+    seg = np.array([0, a.size, a.size + b.size, a.size + b.size, a.size + b.size + 1,
+                    a.size + b.size + 1 + c.size], dtype=np.uint64)
+    cols = np.array([1, 4, 9, 600, 600, 7], dtype=np.uint32)
+    f, d, cc, sp = oracle.coo_encode(idx, seg, cols)
+    assert d.size > idx.size - 6  # escapes present
+    np.testing.assert_array_equal(gpu_decode(f, d, cc, sp, seg, cols, idx.size), idx)
+    # GPU encode -> GPU decode
+    P, gf, gd, gc, gsp = gpu_coo(idx, seg, cols)
+    np.testing.assert_array_equal(gpu_decode(gf, gd, gc, gsp, seg, cols, idx.size), idx)
+
+
+def test_decode_capacity_and_empty():
+    rng = np.random.default_rng(13)
+    idx, seg, cols = random_patch(rng, SHAPES, 2e-3)
+    f, d, c, sp = oracle.coo_encode(idx, seg, cols)
+    cap = idx.size // 2
+    np.testing.assert_array_equal(gpu_decode(f, d, c, sp, seg, cols, idx.size, cap=cap), idx[:cap])
+    z = np.zeros(0, dtype=np.uint32)
+    out = gpu_decode(np.zeros(3, np.uint32), np.zeros(0, np.uint8), np.zeros(0, np.uint16),
+                     np.zeros(3, np.uint64), np.zeros(3, np.uint64), np.array([3, 4, 5], np.uint32), 0)
+    assert out.size == 0 and z.size == 0
