@@ -776,7 +776,7 @@ uint64_t oracle_loco_gate_lp(int dtype, float inv_scale, const float *delta, flo
  * No entry yields (255, 0): a same-row pair has row field 0, a new-row pair a
  * column field >= 1.  Requires 1 <= cols <= 65535.  (The paper notes that
  * larger jumps are rare but does not say how they are kept lossless; the
- * escape is this build's reading.)
+ * escape pair is a reading of that gap.)
  * ------------------------------------------------------------------------ */
 
 /* Pairs of all segments into drow/dcol (positions >= out_capacity are not

@@ -14,8 +14,8 @@
 //
 // The encode kernel has the persistent, ordered single-pass structure of the
 // BF16 encode and the sparsifier (NW compute waves + 1 scan wave; tiles of
-// NW x 64 lanes x 8 values).  An MXFP4 block is 4 neighbouring lanes' 8
-// values, so its largest magnitude is a 4-lane reduction.
+// NW x 64 lanes x U groups x 8 values).  An MXFP4 block is 4 neighbouring
+// lanes' 8 values, so its largest magnitude is a 4-lane reduction.
 #include "device_common.hpp"
 #include "launch.hpp"
 #include "lowp_cast.hpp"
