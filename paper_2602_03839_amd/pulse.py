@@ -528,7 +528,7 @@ class LocoLowpBatch:
                                                     _p(idx), _p(val), cap, _p(count),
                                                     _p(seg_begin), _p(ws), ws.numel(),
                                                     _stream(stream)),
-               "pulse_loco_sparsify_lowp_batch", "pulse_coo_encode", "pulse_coo_decode")
+               "pulse_loco_sparsify_lowp_batch")
 
 
 def hash_leaf_count(total_values: int) -> int:
