@@ -73,3 +73,29 @@ def gpu_encode(w_new: np.ndarray, snap: np.ndarray, capacity=None, index_base=0,
     m = min(c, cap)
     return (c, h32(patch.idx)[:m], h16(patch.val)[:m], h16(s_d),
             h16(ref_d) if ref_d is not None else None)
+
+
+def generated_patch(key: str, density: float, seed: int, device="cuda"):
+    """A patch-shaped index list for a model-shaped set, generated without the
+    codec: in each tensor every position is kept with probability `density`
+    (seeded torch generator on the device), indices local and ascending.
+
+    Returns (idx int32 [cap], seg_begin int64 [T], count int64 [1], segs list
+    of T + 1 entry offsets, specs).
+    """
+    from paper_2602_03839_amd import workloads as wl
+    specs = wl.SHAPES[key].tensors()
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    parts, segs = [], [0]
+    for s in specs:
+        m = torch.rand(s.numel, generator=g, device=device) < density
+        nz = m.nonzero().flatten().to(torch.int32)
+        del m
+        parts.append(nz)
+        segs.append(segs[-1] + nz.numel())
+    idx = torch.cat(parts) if parts else torch.zeros(0, dtype=torch.int32, device=device)
+    del parts
+    seg = torch.tensor(segs[:-1], dtype=torch.int64, device=device)
+    count = torch.tensor([segs[-1]], dtype=torch.int64, device=device)
+    return idx, seg, count, segs, specs

@@ -4,8 +4,8 @@ pair offsets and the pair count, bit-exact; the GPU decode of the oracle's
 streams and of the GPU's own (round trip) gives the patch back.  Random patches over many shapes
 and densities (long row gaps with escapes, one-column and 65535-column
 tensors, empty segments, segments across tile boundaries), output capacity
-overflow, the 0.5B-shaped fused patch in full and the 32B-shaped one on
-sampled segments.
+overflow, a patch-shaped list over the 0.5B-shaped set in full and over the
+32B-shaped one on sampled segments.
 """
 import numpy as np
 import pytest
@@ -14,7 +14,7 @@ import torch
 import oracle
 from paper_2602_03839_amd import pulse
 
-from gpu_helpers import counter, dev, h32, read_count
+from gpu_helpers import counter, dev, generated_patch, h32, read_count
 
 pytestmark = pytest.mark.gpu
 
@@ -128,41 +128,24 @@ def test_empty_patch():
 
 @pytest.mark.slow
 @pytest.mark.parametrize("key", ["0.5b", "32b"])
-def test_fused_patch_of_a_model_set(key):
-    """The patch of one fused encode step at lr 1e-6: every segment against the
-    oracle for the 0.5B-shaped set; 24 sampled segments (each computed by the
-    oracle from that segment's entries alone) plus all offsets' consistency
-    for the 32B-shaped one."""
-    from test_gpu_configs import ModelSet, encode_set, segments
+def test_patch_of_a_model_set(key):
+    """A patch-shaped index list over a model-shaped set (0.94% of positions per
+    tensor, generated without the codec): every segment against the oracle for
+    the 0.5B-shaped set; 24 sampled segments (each computed by the oracle from
+    that segment's entries alone) for the 32B-shaped one; the GPU's stream
+    decodes on the GPU to the list."""
     torch.cuda.empty_cache()
-    ms = ModelSet(key)
-    w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
-    S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
-    ms.init(w, S)
-    ms.step(w, 1e-6, 1)
-    cap = ms.N // 50
-    idx = torch.empty(cap, dtype=torch.int32, device="cuda")
-    val = torch.empty(cap, dtype=torch.int16, device="cuda")
-    count = counter(0)
-    seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
-    ws = pulse.workspace()
-    encode_set(ms, w, S, None, idx, val, count, seg, ws)
-    del w, S
-    torch.cuda.empty_cache()
-    segs = segments(seg, count)
+    idx, seg, count, segs, specs = generated_patch(key, 0.0094, 1234)
     nent = segs[-1]
-    assert nent <= cap
-    cols = np.array([s.shape[-1] for s in ms.specs], dtype=np.uint32)
-    if ms.flat:  # flat indices: make them local to each tensor for the 2-D view
-        base = torch.tensor(np.repeat(np.array(ms.offs[:-1], dtype=np.int64),
-                                      np.diff(segs)), dtype=torch.int64, device="cuda")
-        idx[:nent] = ((idx[:nent].to(torch.int64) & 0xFFFFFFFF) - base).to(torch.int32)
-    print(f"coo {key}: {nent} entries in {ms.T} segments", flush=True)
-    P, gf, gd, gc, gsp = gpu_coo(None, None, cols, out_cap=nent + ms.T * 64, ws=ws, idx_d=idx,
+    T = len(specs)
+    cols = np.array([s.shape[-1] for s in specs], dtype=np.uint32)
+    ws = pulse.workspace()
+    print(f"coo {key}: {nent} entries in {T} segments", flush=True)
+    P, gf, gd, gc, gsp = gpu_coo(None, None, cols, out_cap=nent + T * 64, ws=ws, idx_d=idx,
                                  end_d=count, seg_d=seg)
     hidx = h32(idx[:nent])
     rng = np.random.default_rng(7)
-    picks = range(ms.T) if key == "0.5b" else sorted(set(rng.choice(ms.T, 24, replace=False)) | {0, ms.T - 1})
+    picks = range(T) if key == "0.5b" else sorted(set(rng.choice(T, 24, replace=False)) | {0, T - 1})
     ends = list(gsp[1:]) + [P]
     for s in picks:
         a, e = segs[s], segs[s + 1]
@@ -171,8 +154,7 @@ def test_fused_patch_of_a_model_set(key):
         p0, p1 = int(gsp[s]), int(ends[s])
         np.testing.assert_array_equal(gd[p0:p1], od, err_msg=f"segment {s}")
         np.testing.assert_array_equal(gc[p0:p1], oc, err_msg=f"segment {s}")
-    assert all(int(gsp[s]) <= int(ends[s]) for s in range(ms.T))
-    # the GPU's stream decodes on the GPU to the patch
+    assert all(int(gsp[s]) <= int(ends[s]) for s in range(T))
     back = gpu_decode(gf, gd, gc, gsp, np.array(segs[:-1], dtype=np.uint64), cols, nent, ws=ws)
     np.testing.assert_array_equal(back, hidx)
 
