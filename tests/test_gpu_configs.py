@@ -191,12 +191,14 @@ def test_c3_twenty_step_chain(fresh_memory, lr):
     apply = pulse.ApplyBatch([pulse.ApplyTensor(ms.view(Q, i), ms.base(i)) for i in range(ms.T)])
     rejected = torch.zeros(1, dtype=torch.int64, device="cuda")
     dens = []
+    wins = ms.windows(rng)
     for t in range(1, 21):
-        ms.step(w, lr, t)
         sample = t in (1, 20)
+        if sample:  # the oracle's snapshot: its own cast of w_{t-1} (a generated input)
+            prev = [ww[0] for ww in host_windows(ms, wins, w)]
+        ms.step(w, lr, t)
         if sample:
-            wins = ms.windows(rng)
-            hw = host_windows(ms, wins, w, S)
+            hw = [(ww[0], oracle.cast(p)) for ww, p in zip(host_windows(ms, wins, w), prev)]
         encode_set(ms, w, S, R, idx, val, count, seg, ws)
         apply(idx, val, seg, count, rejected=rejected)
         segs = segments(seg, count)
@@ -205,7 +207,6 @@ def test_c3_twenty_step_chain(fresh_memory, lr):
         check_encode_definition(ms, w, S, idx, val, segs)
         if sample:
             for (i, a, e), (ww, ss) in zip(wins, hw):
-                ss = ss.view(np.uint16)
                 r = ss.copy()
                 cnt, oi, ov = oracle.encode(ww, ss, index_base=ms.base(i) + a, refresh=r)
                 gi, gv = gpu_entries(ms, idx, val, segs, i, a, e)
@@ -276,14 +277,14 @@ def test_c5_loco_ten_rounds_7b(fresh_memory):
                                 for i in range(a, b)]) for a, b in chunks(ms.T)]
     tau32 = float(np.float32(tau))
     dens = []
+    wins = ms.windows(rng)
+    # the oracle carries its own residual in these windows through all rounds
+    o_res = [np.zeros(ee - a, dtype=np.float32) for _i, a, ee in wins]
     for r in range(10):
         for i in range(ms.T):
             wl.loco_delta_(ms.view(d, i), 5, r, i)
         e_old.copy_(e)
-        sample = r in (0, 9)
-        if sample:
-            wins = ms.windows(rng)
-            hw = host_windows(ms, wins, d, e_old)
+        hd = [x[0] for x in host_windows(ms, wins, d)]
         count.zero_()
         for (a, _b), b in zip(chunks(ms.T), batches):
             b(tau, idx, val, count, ws, seg_begin=seg[a:])
@@ -300,13 +301,11 @@ def test_c5_loco_ten_rounds_7b(fresh_memory):
             assert torch.equal(val[lo:hi].view(torch.int32), s[nz].view(torch.int32)), (r, i)
             want = torch.where(sel, torch.zeros_like(s), s)
             assert torch.equal(ms.view(e, i).view(torch.int32), want.view(torch.int32)), (r, i)
-        if sample:
-            for (i, a, ee), (dd, eo) in zip(wins, hw):
-                res = eo.copy()
-                cnt, oi, ov = oracle.loco(dd, res, tau, index_base=a)
-                gi, gv = gpu_entries(ms, idx, val, segs, i, a, ee)
-                np.testing.assert_array_equal(gi, oi[:cnt])
-                np.testing.assert_array_equal(gv.view(np.uint32), ov[:cnt].view(np.uint32))
-                np.testing.assert_array_equal(ms.view(e, i)[a:ee].cpu().numpy().view(np.uint32),
-                                              res.view(np.uint32))
+        for (i, a, ee), dd, res in zip(wins, hd, o_res):
+            cnt, oi, ov = oracle.loco(dd, res, tau, index_base=a)
+            gi, gv = gpu_entries(ms, idx, val, segs, i, a, ee)
+            np.testing.assert_array_equal(gi, oi[:cnt])
+            np.testing.assert_array_equal(gv.view(np.uint32), ov[:cnt].view(np.uint32))
+            np.testing.assert_array_equal(ms.view(e, i)[a:ee].cpu().numpy().view(np.uint32),
+                                          res.view(np.uint32))
     assert abs(dens[0] - 0.02) < 0.002 and dens[-1] > 0.035
