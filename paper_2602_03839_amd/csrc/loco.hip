@@ -223,14 +223,21 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           if (GM == 2) {
             // selected iff fp8(theta * s) != fp8((theta - a) * s)
             const float is = p.t[ck].inv_scale;
+            float y0[8], y1[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) m |= (uint32_t)(fp8_code(th[i] * is) != fp8_code(af[i] * is)) << i;
+            for (int i = 0; i < 8; ++i) {
+              y0[i] = th[i] * is;
+              y1[i] = af[i] * is;
+            }
+            uint32_t lo0, hi0, lo1, hi1;
+            fp8_codes8(y0, lo0, hi0);
+            fp8_codes8(y1, lo1, hi1);
+            m = fp8_change_mask(lo0, hi0, lo1, hi1);
           } else {
             // selected iff (scale, code) of theta's block != that of theta - a
-            uint32_t c0[8], c1[8];
+            uint32_t c0, c1;
             const uint32_t s0 = mx_view8(th, c0), s1 = mx_view8(af, c1);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) m |= (uint32_t)(s0 != s1 || c0[i] != c1[i]) << i;
+            m = s0 != s1 ? 0xFFu : nibble_change_mask(c0, c1);
           }
         } else {
 #pragma unroll

@@ -52,12 +52,11 @@ __global__ __launch_bounds__(kLowpCastTB) void cast_lowp_kernel(const float* __r
       for (int i = 0; i < 8; ++i) x[i] = e + i < n ? src[e + i] : 0.0f;
     }
     if (DT == kDtypeFp8) {
-      uint32_t lo = 0, hi = 0;
+      float y[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        lo |= fp8_code(x[i] * inv_scale) << (8 * i);
-        hi |= fp8_code(x[i + 4] * inv_scale) << (8 * i);
-      }
+      for (int i = 0; i < 8; ++i) y[i] = x[i] * inv_scale;
+      uint32_t lo, hi;
+      fp8_codes8(y, lo, hi);
       if (e + 8 <= n) {
         store_nt((uint64_t*)(codes + e), (uint64_t)lo | ((uint64_t)hi << 32));
       } else {
@@ -65,11 +64,8 @@ __global__ __launch_bounds__(kLowpCastTB) void cast_lowp_kernel(const float* __r
           if (e + i < n) codes[e + i] = (uint8_t)((i < 4 ? lo >> (8 * i) : hi >> (8 * (i - 4))) & 0xFFu);
       }
     } else {
-      uint32_t c[8];
-      const uint32_t sc = mx_view8(x, c);
-      uint32_t packed = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) packed |= c[i] << (4 * i);
+      uint32_t packed;
+      const uint32_t sc = mx_view8(x, packed);
       if (e + 8 <= n) {
         store_nt((uint32_t*)(codes + e / 2), packed);
       } else {
@@ -251,26 +247,17 @@ __global__ __launch_bounds__((NW + 1) * 64) void encode_lowp_kernel(LowpParams p
         uint32_t m = 0;
         if (DT == kDtypeFp8) {
           const float is = p.t[ck].inv_scale;
-          uint32_t lo = 0, hi = 0;
+          float y[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const uint32_t c = fp8_code(x[i] * is);
-            const uint32_t old = ((i < 4 ? g[u].s.x : g[u].s.y) >> (8 * (i & 3))) & 0xFFu;
-            m |= (uint32_t)(c != old) << i;
-            (i < 4 ? lo : hi) |= c << (8 * (i & 3));
-          }
+          for (int i = 0; i < 8; ++i) y[i] = x[i] * is;
+          uint32_t lo, hi;
+          fp8_codes8(y, lo, hi);
+          m = fp8_change_mask(lo, hi, g[u].s.x, g[u].s.y);
           staged[u] = make_uint2(lo, hi);
         } else {
-          uint32_t c[8];
-          const uint32_t sc = mx_view8(x, c);
-          const bool scale_moved = sc != g[u].s.y;
-          uint32_t packed = 0;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const uint32_t old = (g[u].s.x >> (4 * i)) & 0xFu;
-            m |= (uint32_t)(scale_moved || c[i] != old) << i;
-            packed |= c[i] << (4 * i);
-          }
+          uint32_t packed;
+          const uint32_t sc = mx_view8(x, packed);
+          m = sc != g[u].s.y ? 0xFFu : nibble_change_mask(packed, g[u].s.x);
           staged[u] = make_uint2(packed, sc);
         }
         if (!full && !(e + 8 <= cn_n)) {

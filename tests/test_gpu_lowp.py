@@ -95,6 +95,71 @@ def test_mxfp4_cast(n):
     np.testing.assert_array_equal(u8(codes)[: oc.size], oc)
 
 
+def test_mxfp4_cast_every_block_exponent():
+    """Blocks whose largest magnitude has every exponent field 0..255 (E from
+    -127, clamped, to 126, and infinity), the others drawn over a wide range
+    of magnitudes below it, both signs, with some zeros and subnormals."""
+    rng = np.random.default_rng(77)
+    blocks = []
+    for field in range(256):
+        for _ in range(4):
+            top = np.uint32(field << 23) | np.uint32(rng.integers(0, 1 << 23) if field < 255 else 0)
+            mags = rng.integers(0, int(top) + 1, 31, dtype=np.uint64).astype(np.uint32)
+            mags[:3] = (int(top) >> rng.integers(0, 30, 3)).astype(np.uint32)
+            mags[3] = 0
+            b = np.concatenate([[top], mags]).astype(np.uint32)
+            b |= rng.integers(0, 2, 32, dtype=np.uint32) << np.uint32(31)
+            blocks.append(rng.permutation(b))
+    x = np.concatenate(blocks).view(np.float32)
+    codes, scales = pulse.cast_lowp(MX, dev(x))
+    torch.cuda.synchronize()
+    oc, os_ = oracle.cast_mxfp4(x)
+    np.testing.assert_array_equal(u8(scales)[: os_.size], os_)
+    np.testing.assert_array_equal(u8(codes)[: oc.size], oc)
+
+
+@pytest.mark.slow
+def test_mxfp4_cast_every_scaled_value():
+    """Every FP32 value q with |q| < 8, both signs, as E2M1 code: each block of
+    32 holds 31 of them beside an anchor of 8 - 2^-21, which fixes the block
+    exponent at E = 0, so q = x exactly.  Scaled values of a block never reach
+    8 (the largest magnitude is below 2^(E+3)) except for infinity, covered by
+    the cast tests above.  The oracle decides every code."""
+    nmag = 0x41000000                         # magnitudes below 8.0
+    total = 2 * nmag                          # both signs
+    per = 31
+    blocks_per_chunk = 1 << 23
+    chunk = blocks_per_chunk * per
+    anchor = np.uint32(0x40FFFFFF)
+    buf = torch.empty(blocks_per_chunk * 32, dtype=torch.float32, device="cuda")
+    codes = torch.empty(blocks_per_chunk * 16, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(blocks_per_chunk, dtype=torch.uint8, device="cuda")
+    # value j of a chunk starting at c0 (even): magnitude (c0 + j) / 2, negative for odd j
+    k = np.arange(chunk // 2, dtype=np.uint32)
+    step = np.empty(chunk, dtype=np.uint32)
+    step[0::2] = k
+    step[1::2] = k | np.uint32(0x80000000)
+    del k
+    x = np.empty((blocks_per_chunk, 32), dtype=np.uint32)
+    x[:, 0] = anchor
+    for c0 in range(0, total, chunk):
+        print(f"mxfp4 exhaustive: values {c0} / {total}", flush=True)
+        v = step + np.uint32(c0 // 2)
+        if c0 + chunk > total:  # the last chunk: zeros past the end
+            v[total - c0:] = 0
+        x[:, 1:] = v.reshape(-1, per)
+        del v
+        xf = x.reshape(-1).view(np.float32)
+        buf.copy_(torch.from_numpy(xf))
+        pulse.cast_lowp(MX, buf, codes=codes, scales=scales)
+        oc, os_ = oracle.cast_mxfp4(xf)
+        assert (os_ == 127).all()
+        got = codes.cpu().numpy()
+        bad = np.nonzero(got != oc)[0]
+        assert bad.size == 0, (c0, bad[:5].tolist(), xf[2 * bad[:5]].tolist())
+        assert (scales.cpu().numpy() == os_).all()
+
+
 # ---------------------------------------------------------------- encode
 def gpu_encode(dtype, w_new, snap, snap_scales=None, inv_scale=1.0, capacity=None):
     n = w_new.size
