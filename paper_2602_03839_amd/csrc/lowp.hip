@@ -144,7 +144,7 @@ __device__ __forceinline__ void lowp_load(LowpRegs& g, const LowpCtx& c, uint64_
 #define PULSE_LOWP_TB 960
 #endif
 #ifndef PULSE_LOWP_U
-#define PULSE_LOWP_U 2
+#define PULSE_LOWP_U 3
 #endif
 constexpr int kLowpNW = PULSE_LOWP_TB / 64;
 constexpr int kLowpU = PULSE_LOWP_U;

@@ -19,7 +19,7 @@ from gpu_helpers import counter, dev, h32, hf32, read_count
 pytestmark = pytest.mark.gpu
 
 FP8, MX = pulse.FP8_E4M3, pulse.MXFP4
-TILE = 960 * 8  # values per tile of the lower-precision encode (15 waves x 64 lanes x 8)
+TILE = 960 * 8 * 3  # values per tile of the lower-precision encode (15 waves x 64 lanes x 3 groups x 8)
 
 
 def u8(t: torch.Tensor) -> np.ndarray:
