@@ -53,18 +53,21 @@ struct LocoRegs {
 // Loads of group u of a tile for lane `cl`; whole tiles (`full`, uniform
 // across the block) take the straight-line 16-byte path.  In the gate form a
 // tensor without theta loads nothing for it (its selection uses tau).
+// Unlike the read-only encode, this pass rewrites the residual densely: with
+// plain (cached) loads and stores it measured 9% faster on the 7B-shaped set
+// than with the non-temporal hints.
 template <int TBC, int U, bool GATE>
 __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const LocoCtx& c, int cl,
                                            bool full) {
   const uint64_t e = c.e0 + (uint64_t)(u * TBC + cl) * 8;
   if (full) {
-    g.d0[u] = load16_stream(c.d + e);
-    g.d1[u] = load16_stream(c.d + e + 4);
-    g.r0[u] = load16_stream(c.r + e);
-    g.r1[u] = load16_stream(c.r + e + 4);
+    g.d0[u] = load16(c.d + e);
+    g.d1[u] = load16(c.d + e + 4);
+    g.r0[u] = load16(c.r + e);
+    g.r1[u] = load16(c.r + e + 4);
     if (GATE && c.th) {
-      g.t0[u] = load16_stream(c.th + e);
-      g.t1[u] = load16_stream(c.th + e + 4);
+      g.t0[u] = load16(c.th + e);
+      g.t1[u] = load16(c.th + e + 4);
     }
   } else {
     uint32_t dv[8], rv[8], tv[8];
@@ -251,9 +254,9 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) nr[i] = ((m >> i) & 1u) ? 0.0f : a[i];
         if (vec) {
-          store16_stream(cres + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
+          store16(cres + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
                                               __float_as_uint(nr[2]), __float_as_uint(nr[3])));
-          store16_stream(cres + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
+          store16(cres + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
                                                   __float_as_uint(nr[6]), __float_as_uint(nr[7])));
         } else {
 #pragma unroll
