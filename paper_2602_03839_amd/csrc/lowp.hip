@@ -105,11 +105,14 @@ struct LowpRegs {
   uint2 s;       // FP8: 8 codes; MXFP4: .x = 8 packed codes, .y = the block's scale byte
 };
 
+// The FP32 masters take plain loads and the D snapshot non-temporal ones (as
+// in the BF16 encode): 7-9% faster on the 7B-shaped set than non-temporal
+// loads of both.
 template <int DT>
 __device__ __forceinline__ void lowp_load(LowpRegs& g, const LowpCtx& c, uint64_t e, bool full) {
   if (full) {
-    g.w0 = load16_stream(c.w + e);
-    g.w1 = load16_stream(c.w + e + 4);
+    g.w0 = load16(c.w + e);
+    g.w1 = load16(c.w + e + 4);
     if (DT == kDtypeFp8) {
       const uint64_t v = load_nt((const uint64_t*)(c.snap + e));
       g.s = make_uint2((uint32_t)v, (uint32_t)(v >> 32));
