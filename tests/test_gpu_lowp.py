@@ -1,11 +1,12 @@
 """GPU parity of the lower-precision receivers (App. D) against the oracle.
 
 FP8 E4M3 and MXFP4: the dense casts (including every FP32 bit pattern for FP8
-against torch's float8_e4m3fn cast where torch does not overflow), encode
-against the D snapshot (sizes on and around the tile, ragged MXFP4 blocks,
-moved block scales, capacity overflow, batches with empty tensors), apply on
-the receiver's D copy (shared code bytes of neighbouring values, rejected
-entries), and the sparsifier's gate computed in D.  All bit-exact.
+against torch's float8_e4m3fn cast where torch does not overflow, and every
+scaled value |q| < 8 for E2M1), encode against the D snapshot (sizes on and
+around the tile, ragged MXFP4 blocks, moved block scales, special values,
+capacity overflow, batches with empty tensors), apply on the receiver's D
+copy (shared code bytes of neighbouring values, rejected entries), and the
+sparsifier's gate computed in D (with special values too).  All bit-exact.
 """
 import numpy as np
 import pytest
@@ -212,6 +213,41 @@ def test_encode_mxfp4(n, lr):
     np.testing.assert_array_equal(gv, ov[:oc])
 
 
+def plant_specials(rng, x, every):
+    """Special values at a sparse set of positions (one every `every` on
+    average), so that some waves and MXFP4 blocks hold them and most do not."""
+    pos = np.nonzero(rng.random(x.size) < 1.0 / every)[0]
+    sp = specials()
+    x = x.copy()
+    x[pos] = sp[rng.integers(0, sp.size, pos.size)]
+    return x
+
+
+@pytest.mark.parametrize("dtype", [FP8, MX])
+@pytest.mark.parametrize("every", [3, 700])
+def test_encode_special_values(dtype, every):
+    """NaN (both signs), +-inf, values past the FP8 range, ties, subnormals and
+    signed zeros in the old weights (so in the snapshot) and in the new ones,
+    spread over several tiles; for MXFP4 blocks holding a NaN or an infinity."""
+    rng = np.random.default_rng(40 + dtype + every)
+    n = 3 * TILE + 29
+    w = plant_specials(rng, weights(rng, n, 0.05), every)
+    w2 = plant_specials(rng, step(rng, w, 3e-3), every)
+    if dtype == FP8:
+        s = 1000.0
+        snap = oracle.cast_fp8(w, s)
+        oc, oi, ov = oracle.encode_fp8(w2, snap, s)
+        gc, gi, gv = gpu_encode(FP8, w2, snap, inv_scale=s)
+    else:
+        sc, ss = oracle.cast_mxfp4(w)
+        oc, oi, ov = oracle.encode_mxfp4(w2, sc, ss)
+        gc, gi, gv = gpu_encode(MX, w2, sc, ss)
+    assert oc > 0
+    assert gc == oc
+    np.testing.assert_array_equal(gi, oi[:oc])
+    np.testing.assert_array_equal(gv, ov[:oc])
+
+
 @pytest.mark.parametrize("dtype", [FP8, MX])
 def test_encode_capacity_overflow(dtype):
     rng = np.random.default_rng(9)
@@ -334,6 +370,32 @@ def test_loco_gate_lowp(dtype, n):
     pulse.LocoLowpBatch(dtype, [pulse.LocoTensor(dev(delta), gr, dev(theta))], [s])(
         idx, val, count, pulse.workspace())
     torch.cuda.synchronize()
+    assert read_count(count) == oc
+    np.testing.assert_array_equal(h32(idx)[:oc], oi[:oc])
+    np.testing.assert_array_equal(hf32(val)[:oc].view(np.uint32), ov[:oc].view(np.uint32))
+    np.testing.assert_array_equal(hf32(gr).view(np.uint32), res.view(np.uint32))
+
+
+@pytest.mark.parametrize("dtype", [FP8, MX])
+def test_loco_gate_lowp_special_values(dtype):
+    """The gate with special values in theta and in the update: NaN, +-inf,
+    values past the FP8 range, subnormals and signed zeros."""
+    rng = np.random.default_rng(60 + dtype)
+    n = 2 * TILE + 41
+    theta = plant_specials(rng, weights(rng, n, 0.02), 50)
+    delta = plant_specials(rng, (rng.standard_normal(n) * 2e-3).astype(np.float32), 200)
+    e = (rng.standard_normal(n) * 5e-4).astype(np.float32)
+    s = 300.0
+    res = e.copy()
+    oc, oi, ov = oracle.loco_gate_lp(dtype, delta, res, theta, s)
+    gr = dev(e)
+    idx = torch.zeros(n, dtype=torch.int32, device="cuda")
+    val = torch.zeros(n, dtype=torch.float32, device="cuda")
+    count = counter(0)
+    pulse.LocoLowpBatch(dtype, [pulse.LocoTensor(dev(delta), gr, dev(theta))], [s])(
+        idx, val, count, pulse.workspace())
+    torch.cuda.synchronize()
+    assert oc > 0
     assert read_count(count) == oc
     np.testing.assert_array_equal(h32(idx)[:oc], oi[:oc])
     np.testing.assert_array_equal(hf32(val)[:oc].view(np.uint32), ov[:oc].view(np.uint32))
