@@ -500,18 +500,8 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
 #pragma unroll
     for (int j = 0; j < kVPer; ++j) {
       const uint32_t i = i0 + j;
-      if (i < cnt) {
-        s_off[i] = o;
-        for (uint32_t q = 0; q < npair[j]; ++q) {
-          const uint64_t pos = excl + o + q;
-          if (pos < p.out_capacity) {
-            const bool esc = q + 1 < npair[j];
-            p.drow[pos] = esc ? (uint8_t)255 : (uint8_t)(last[j] >> 16);
-            p.dcol[pos] = esc ? (uint16_t)0 : (uint16_t)(last[j] & 0xFFFFu);
-          }
-        }
-        o += npair[j];
-      }
+      if (i < cnt) s_off[i] = o;
+      o += npair[j];
     }
     __syncthreads();
     // segments starting in this tile: their pair offset and first index
@@ -531,6 +521,43 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
       for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) {
         p.seg_pairs[s] = total;
         p.first[s] = 0u;
+      }
+    }
+    __syncthreads();  // s_idx and s_off are read for the last time
+    // The tile's pairs are one contiguous run [excl, excl + agg32).  Without
+    // long escapes it fits s_idx (as (row field << 16) | column field), and
+    // consecutive lanes write consecutive pairs; otherwise each thread writes
+    // its own entries' pairs.
+    const bool staged = agg32 <= kVTile + 1;
+    o = texcl;
+#pragma unroll
+    for (int j = 0; j < kVPer; ++j) {
+      const uint32_t i = i0 + j;
+      if (i >= cnt) break;
+      for (uint32_t q = 0; q < npair[j]; ++q) {
+        const bool esc = q + 1 < npair[j];
+        const uint32_t pair = esc ? (255u << 16) : last[j];
+        if (staged) {
+          s_idx[o + q] = pair;
+        } else {
+          const uint64_t pos = excl + o + q;
+          if (pos < p.out_capacity) {
+            p.drow[pos] = (uint8_t)(pair >> 16);
+            p.dcol[pos] = (uint16_t)(pair & 0xFFFFu);
+          }
+        }
+      }
+      o += npair[j];
+    }
+    if (staged) {
+      __syncthreads();
+      for (uint32_t q = tid; q < agg32; q += kVT) {
+        const uint64_t pos = excl + q;
+        if (pos < p.out_capacity) {
+          const uint32_t pair = s_idx[q];
+          p.drow[pos] = (uint8_t)(pair >> 16);
+          p.dcol[pos] = (uint16_t)(pair & 0xFFFFu);
+        }
       }
     }
     __syncthreads();
@@ -703,13 +730,10 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
     const uint32_t i0 = (uint32_t)tid * kVPer;
     uint32_t escb[kVPer];
     uint32_t seg_id = 0, C = 1;
-    uint64_t sp = 0, sb = 0;
     uint32_t rst_bits = 0, esc_bits = 0;
     if (i0 < cnt) {
       seg_id = segment_of(p.seg_pairs, p.nseg, q0 + i0);
       C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
-      sp = p.seg_pairs[seg_id];
-      sb = p.seg_begin[seg_id];
     }
     uint32_t seg_at[kVPer];  // segment of each pair (changes only at starts)
 #pragma unroll
@@ -745,8 +769,18 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
     if (i0 < cnt) atomicOr(&s_rf[i0 >> 5], rst_bits << (i0 & 31));
     __syncthreads();
     tile_segmented_sum<true>(p.ws, tk, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
-    // scatter this thread's entries
+    // Pair i's entry lands at seg_begin[s] + 1 + (q0 + i - seg_pairs[s]) -
+    // (escapes before it), s its segment.  The owning thread stores the low
+    // 32 bits of that position in s_pair (no longer needed), thread 0 the
+    // whole position of pair 0 as a reference, and escapes are flagged in
+    // s_seg's place (its segment starts were last read before the sum).  A
+    // tile's positions lie within cnt + nseg < 2^31 of each other, so each is
+    // the reference plus the signed 32-bit difference of the low halves.  The
+    // writes then go out with consecutive lanes on consecutive pairs, whose
+    // entries are consecutive, so they coalesce.
+    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_seg[w] = 0;
     uint32_t cur = 0xFFFFFFFFu;
+    uint64_t sp = 0, sb = 0;
 #pragma unroll
     for (int j = 0; j < kVPer; ++j) {
       const uint32_t i = i0 + j;
@@ -756,8 +790,17 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
         sp = p.seg_pairs[cur];
         sb = p.seg_begin[cur];
       }
-      if ((esc_bits >> j) & 1u) continue;
       const uint64_t pos = sb + 1 + (q0 + i - sp) - escb[j];
+      s_pair[i] = (uint32_t)pos;
+      if (i == 0) s_b = pos;
+    }
+    __syncthreads();
+    if (i0 < cnt) atomicOr(&s_seg[i0 >> 5], esc_bits << (i0 & 31));
+    __syncthreads();
+    const uint64_t ref = s_b;
+    for (uint32_t i = tid; i < cnt; i += kVT) {
+      if (flag_at(s_seg, i)) continue;  // an escape pair has no entry
+      const uint64_t pos = ref + (uint64_t)(int64_t)(int32_t)(s_pair[i] - (uint32_t)ref);
       if (pos < p.capacity) p.idx[pos] = (uint32_t)s_v[i];
     }
     // first entries of the segments starting in this tile (and, in the last
