@@ -422,12 +422,15 @@ __global__ __launch_bounds__(kVT) void varint_sums_kernel(VarintDecParams p) {
 
 // ---------------------------------------------------------------- 2-D COO
 
-// The segment holding entry k: the last segment starting at or before k
-// (several empty segments may share a start), segment 0 for entries before
-// every start.  Whole-thread binary search over the device array.
-__device__ __forceinline__ uint32_t segment_of(const uint64_t* seg_begin, uint32_t nseg, uint64_t k) {
-  uint32_t lo = 0, hi = nseg;  // first start > k lies in [lo, hi]
-  while (lo < hi) {
+// The segment holding element k of a tile: the last segment starting at or
+// before k (several empty segments may share a start), segment 0 for
+// elements before every start.  [lo, hi) are the segments starting in the
+// tile (mark_starts): every earlier segment starts before k and every later
+// one after it, so the binary search runs over that range only, usually one
+// or two segments.
+__device__ __forceinline__ uint32_t segment_in(const uint64_t* seg_begin, uint32_t lo, uint32_t hi,
+                                               uint64_t k) {
+  while (lo < hi) {  // first start > k lies in [lo, hi]
     const uint32_t mid = (lo + hi) >> 1;
     if (seg_begin[mid] <= k) lo = mid + 1;
     else hi = mid;
@@ -460,7 +463,7 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
     const uint32_t i0 = (uint32_t)tid * kVPer;
     uint32_t C = 1, pr = 0, pc = 0;
     if (i0 < cnt) {
-      C = p.cols[segment_of(p.seg_begin, p.nseg, k0 + i0)];
+      C = p.cols[segment_in(p.seg_begin, s_range[0], s_range[1], k0 + i0)];
       C = C > 0 ? C : 1u;
       pr = s_idx[i0] / C;
       pc = s_idx[i0] - pr * C;
@@ -472,7 +475,7 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
       last[j] = 0;
       if (i < cnt) {
         if (flag_at(s_flags, i) && i != i0) {
-          C = p.cols[segment_of(p.seg_begin, p.nseg, k0 + i)];
+          C = p.cols[segment_in(p.seg_begin, s_range[0], s_range[1], k0 + i)];
           C = C > 0 ? C : 1u;
         }
         const uint32_t cur = s_idx[1 + i];
@@ -676,7 +679,7 @@ __global__ __launch_bounds__(kVT) void coo_rows_kernel(CooDecParams p) {
       const bool esc = dr == 255u && p.dcol[q0 + i] == 0;
       uint64_t v = (uint64_t)dr | ((uint64_t)(esc ? 1u : 0u) << 32);
       if (flag_at(s_rf, i)) {  // the segment's first pair: start from its first index's row
-        const uint32_t s = segment_of(p.seg_pairs, p.nseg, q0 + i);
+        const uint32_t s = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
         const uint32_t C = p.cols[s] > 0 ? p.cols[s] : 1u;
         v += p.first[s] / C;
       }
@@ -732,7 +735,7 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
     uint32_t seg_id = 0, C = 1;
     uint32_t rst_bits = 0, esc_bits = 0;
     if (i0 < cnt) {
-      seg_id = segment_of(p.seg_pairs, p.nseg, q0 + i0);
+      seg_id = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i0);
       C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
     }
     uint32_t seg_at[kVPer];  // segment of each pair (changes only at starts)
@@ -744,7 +747,7 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
       if (i >= cnt) continue;
       const bool seg_start = flag_at(s_seg, i);
       if (seg_start && i != i0) {
-        seg_id = segment_of(p.seg_pairs, p.nseg, q0 + i);
+        seg_id = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
         C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
         seg_at[j] = seg_id;
       }
