@@ -347,11 +347,11 @@ int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end
  *   seg_pairs, first, cols   as pulse_coo_encode wrote / read them.
  *   idx           device uint32 [capacity]: entry k of the patch at idx[k];
  *                 entries at or past capacity are not written.
- *   scratch       device, 8 * pair_capacity bytes, 8-byte aligned: per-pair
- *                 state of the first pass.
- * Two passes: the row and escape count of each pair since its segment's
- * start (one segmented running sum), then its flat index (a running sum that
- * restarts at each new-row pair), written at its entry's position.  Requires
+ * One kernel, two running sums chained per tile of pairs: the row and escape
+ * count of each pair since its segment's start (a segmented running sum),
+ * then its flat index (a running sum that restarts at each new-row pair),
+ * written at its entry's position.  The library allocates nothing; the
+ * workspace orders the tiles as for the other ordered kernels.  Requires
  * fewer than 2^22 escapes per segment (a tensor of at most 2^30 rows).  A
  * stream that encode did not write decodes to unspecified indices but no
  * access leaves the buffers.
@@ -359,7 +359,7 @@ int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end
 int pulse_coo_decode(const uint8_t *drow, const uint16_t *dcol, uint64_t pair_capacity,
                      const uint64_t *npairs, const uint64_t *seg_begin, const uint64_t *seg_pairs,
                      uint32_t nseg, const uint32_t *cols, const uint32_t *first,
-                     const uint64_t *nent, uint32_t *idx, uint64_t capacity, uint64_t *scratch,
+                     const uint64_t *nent, uint32_t *idx, uint64_t capacity,
                      void *workspace, size_t workspace_bytes, void *stream);
 
 /*

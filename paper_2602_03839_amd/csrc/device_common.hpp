@@ -37,10 +37,11 @@ namespace pulse {
 //         mod 256.  Every sequence number is published exactly once, in order
 //         of use, so a slot holds either the current lap's word or the previous
 //         lap's, whose tag differs; a stale word reads as "not ready".  A slot
-//         is reused only kSlots tickets later; since at most R <= 8192 tiles
-//         are in flight at once and a tile looks back at most R tiles,
-//         kSlots > 2R + 2 ensures a word is never overwritten while a reader
-//         still needs it.
+//         is reused only kSlots sequence numbers later; since at most R <= 8192
+//         sequence numbers are in flight at once (tiles, or two per tile for a
+//         kernel that chains two scans per tile) and a look-back reaches at
+//         most R of them, kSlots > 2R + 2 ensures a word is never overwritten
+//         while a reader still needs it.
 constexpr int kWordTicket = 0;
 constexpr int kWordGaveUp = 16;
 constexpr int kWordDone = 32;
@@ -240,7 +241,10 @@ struct LookWindow {
   uint64_t w[LK];
 };
 
-template <int LK>
+// STRIDE: sequence numbers per tile.  A tile that runs several chained scans
+// gives each its own sequence number (scan c of tile t: base + STRIDE * t +
+// c); its look-back then visits the predecessors' words of the same scan.
+template <int LK, int STRIDE = 1>
 __device__ __forceinline__ void look_back_issue(uint64_t* ws, const Ticket& tk, int64_t j,
                                                 LookWindow<LK>& win) {
   const int lane = lane_id();
@@ -249,7 +253,8 @@ __device__ __forceinline__ void look_back_issue(uint64_t* ws, const Ticket& tk, 
     const int64_t tj = j - (m * 64 + lane);
     win.w[m] = 0;
     if (tj >= 0) {
-      const uint64_t gj = (tk.seq - (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
+      const uint64_t gj =
+          (tk.seq - (uint64_t)STRIDE * (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
       win.w[m] = __hip_atomic_load(status_slot(ws, gj), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -257,7 +262,7 @@ __device__ __forceinline__ void look_back_issue(uint64_t* ws, const Ticket& tk, 
 
 // WIDE: the aggregates may exceed 32 bits (a packed multi-field value); they
 // are then summed with 64-bit lane shuffles.
-template <int LK, bool WIDE = false>
+template <int LK, bool WIDE = false, int STRIDE = 1>
 __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win) {
   const int lane = lane_id();
   uint64_t excl = 0;
@@ -268,7 +273,8 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
 #pragma unroll
     for (int m = 0; m < LK; ++m) {
       const int64_t tj = j - (m * 64 + lane);
-      const uint64_t gj = (tk.seq - (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
+      const uint64_t gj =
+          (tk.seq - (uint64_t)STRIDE * (uint64_t)((int64_t)tk.tile - tj)) & kSeqMask;
       if (tj >= 0 && ((win.w[m] >> 54) & 0xFFull) != ((gj >> kSlotBits) & 0xFFull))
         win.w[m] = 0;  // stale lap: not ready
       const uint64_t flag = win.w[m] >> 62;
@@ -293,7 +299,8 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
     if (wait_q >= 0) {
       // wait for that one tile, then read the window again
       const int64_t tq = j - wait_q;
-      const uint64_t gq = (tk.seq - (uint64_t)((int64_t)tk.tile - tq)) & kSeqMask;
+      const uint64_t gq =
+          (tk.seq - (uint64_t)STRIDE * (uint64_t)((int64_t)tk.tile - tq)) & kSeqMask;
       uint32_t pause = 0;
       bool ready = false;
       bool gave_up = false;
@@ -323,7 +330,7 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
           __hip_atomic_store(ws + kWordGaveUp, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return excl;
       }
-      look_back_issue<LK>(ws, tk, j, win);
+      look_back_issue<LK, STRIDE>(ws, tk, j, win);
       continue;
     }
     // Every word before the nearest prefix is a tile aggregate (a count of at
@@ -357,7 +364,7 @@ __device__ uint64_t look_back(uint64_t* ws, const Ticket& tk, LookWindow<LK> win
       return excl + (((uint64_t)hi << 32) | lo);
     }
     j -= 64 * LK;
-    look_back_issue<LK>(ws, tk, j, win);
+    look_back_issue<LK, STRIDE>(ws, tk, j, win);
   }
 }
 

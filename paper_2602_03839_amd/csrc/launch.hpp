@@ -285,7 +285,7 @@ struct CooDecParams {
   uint64_t* ws;
   const uint8_t* drow;
   const uint16_t* dcol;
-  uint64_t pair_capacity;      // pairs readable (and scratch size)
+  uint64_t pair_capacity;      // pairs readable
   const uint64_t* npairs;      // device: pairs in the stream
   const uint64_t* seg_begin;   // device [nseg]: entry where each segment starts
   const uint64_t* seg_pairs;   // device [nseg]: pair where each segment starts
@@ -295,7 +295,6 @@ struct CooDecParams {
   const uint64_t* nent;        // device: entries in the patch
   uint32_t* idx;
   uint64_t capacity;
-  uint64_t* scratch;           // device [pair_capacity]: per pair (row, escapes) of pass 1
   uint32_t ntiles;
 };
 

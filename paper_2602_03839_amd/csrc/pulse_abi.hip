@@ -523,17 +523,16 @@ int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end
 int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_capacity,
                      const uint64_t* npairs, const uint64_t* seg_begin, const uint64_t* seg_pairs,
                      uint32_t nseg, const uint32_t* cols, const uint32_t* first,
-                     const uint64_t* nent, uint32_t* idx, uint64_t capacity, uint64_t* scratch,
-                     void* workspace, size_t workspace_bytes, void* stream) {
+                     const uint64_t* nent, uint32_t* idx, uint64_t capacity, void* workspace,
+                     size_t workspace_bytes, void* stream) {
   if (nseg == 0) return fail(PULSE_EINVAL, "coo decode: nseg is 0");
   if (!npairs || !seg_begin || !seg_pairs || !cols || !first || !nent)
     return fail(PULSE_EINVAL, "coo decode: NULL pointer");
-  if (pair_capacity > 0 && (!drow || !dcol || !scratch))
-    return fail(PULSE_EINVAL, "coo decode: drow/dcol/scratch is NULL");
+  if (pair_capacity > 0 && (!drow || !dcol))
+    return fail(PULSE_EINVAL, "coo decode: drow/dcol is NULL");
   if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "coo decode: idx is NULL");
-  if (!aligned(npairs, 8) || !aligned(seg_begin, 8) || !aligned(seg_pairs, 8) || !aligned(nent, 8) ||
-      (scratch && !aligned(scratch, 8)))
-    return fail(PULSE_EALIGN, "coo decode: counters/scratch not 8-byte aligned");
+  if (!aligned(npairs, 8) || !aligned(seg_begin, 8) || !aligned(seg_pairs, 8) || !aligned(nent, 8))
+    return fail(PULSE_EALIGN, "coo decode: counters not 8-byte aligned");
   if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4) || (dcol && !aligned(dcol, 2)))
     return fail(PULSE_EALIGN, "coo decode: idx/cols/first/dcol misaligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
@@ -555,7 +554,6 @@ int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_ca
   p.nent = nent;
   p.idx = idx;
   p.capacity = capacity;
-  p.scratch = scratch;
   p.ntiles = (uint32_t)nt;
   return hip_status(pulse::launch_coo_decode(p, (hipStream_t)stream), "coo decode launch");
 }

@@ -26,11 +26,12 @@
 // per later entry -- (0, column gap) within a row, (rows ahead, column + 1) on
 // a later row -- with (255, 0) escape pairs, each 255 rows, ahead of a gap of
 // more than 255 rows.  An entry's pair count is 1 + its escapes; their ordered
-// exclusive sum places its pairs.  Its decode is two segmented running sums
-// over the pairs: coo_rows_kernel (row and escape count since the segment's
-// start, both restarting at segment starts, packed into one scanned value)
-// and coo_flat_kernel (the flat index, restarting at every new-row pair and
-// segment start, written at the entry's position).
+// exclusive sum places its pairs.  Its decode (coo_decode_kernel) is two
+// segmented running sums over the pairs, both chained in the same pass over
+// pair tiles: the row and escape count since the segment's start (both
+// restarting at segment starts, packed into one scanned value), then the flat
+// index (restarting at every new-row pair and segment start), written at the
+// entry's position.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -96,8 +97,10 @@ __device__ uint32_t wave_lower_bound64(const uint64_t* a, uint32_t n, uint64_t k
 // this block's later tiles, each behind its own look-back -- a chain through
 // every block.  (The encode and sparsify kernels draw four at a time because
 // they publish aggregates iterations ahead of resolving.)
+// A kernel that runs SPT chained scans per tile (SPT sequence numbers per
+// tile) passes SPT, so the next launch starts past all of them.
 template <typename Fn>
-__device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
+__device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn, uint32_t spt = 1) {
   __shared__ uint64_t s_tk;
   uint64_t g0 = 0;  // thread 0 only
   for (;;) {
@@ -112,7 +115,7 @@ __device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
     if (tk.tile >= ntiles) break;
     fn(tk);
   }
-  if (threadIdx.x == 0) finish_launch(ws, g0, ntiles, gridDim.x);
+  if (threadIdx.x == 0) finish_launch(ws, g0, ntiles * spt, gridDim.x);
 }
 
 // Exclusive prefix of the tile's `agg` over the earlier tiles of the launch
@@ -121,7 +124,8 @@ __device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
 // prefix at once; the tile still looks back for its own entries before the
 // restart.
 // WIDE: aggregates may exceed 32 bits (the look-back then sums in 64 bits).
-template <bool WIDE = false>
+// STRIDE: sequence numbers per tile (see look_back_issue).
+template <bool WIDE = false, int STRIDE = 1>
 __device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg, bool restart,
                                     uint64_t incl_known, uint64_t* s_b) {
   if (threadIdx.x < 64) {
@@ -133,8 +137,8 @@ __device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg
       if (lane == 0)
         status_publish(ws, tk.seq, restart ? kFlagPrefix : kFlagAggregate, restart ? incl_known : agg);
       LookWindow<1> win;
-      look_back_issue<1>(ws, tk, (int64_t)tk.tile - 1, win);
-      excl = look_back<1, WIDE>(ws, tk, win);
+      look_back_issue<1, STRIDE>(ws, tk, (int64_t)tk.tile - 1, win);
+      excl = look_back<1, WIDE, STRIDE>(ws, tk, win);
       if (lane == 0 && !restart) status_publish(ws, tk.seq, kFlagPrefix, excl + agg);
     }
     if (lane == 0) *s_b = excl;
@@ -573,7 +577,7 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
 // restart add `carry` from earlier tiles, which chain_exclusive supplies (a
 // tile holding a restart publishes its inclusive tail at once).  s_v ends up
 // holding the sums.  Every thread of the block calls it.
-template <bool WIDE>
+template <bool WIDE, int STRIDE = 1>
 __device__ void tile_segmented_sum(uint64_t* ws, const Ticket& tk, uint64_t* s_v,
                                    const uint32_t* s_rf, uint32_t cnt, uint64_t* s_tsum,
                                    uint32_t* s_trst, uint64_t* s_tail, uint64_t* s_b) {
@@ -638,7 +642,7 @@ __device__ void tile_segmented_sum(uint64_t* ws, const Ticket& tk, uint64_t* s_v
   __syncthreads();
   const bool tile_rst = s_tail[0] != 0u;
   const uint64_t tile_sum = s_tail[1];
-  const uint64_t carry = chain_exclusive<WIDE>(ws, tk, tile_sum, tile_rst, tile_sum, s_b);
+  const uint64_t carry = chain_exclusive<WIDE, STRIDE>(ws, tk, tile_sum, tile_rst, tile_sum, s_b);
   uint64_t acc = s_tsum[tid] + (s_trst[tid] ? 0u : carry);
 #pragma unroll
   for (int j = 0; j < kVPer; ++j) {
@@ -652,52 +656,19 @@ __device__ void tile_segmented_sum(uint64_t* ws, const Ticket& tk, uint64_t* s_v
   __syncthreads();
 }
 
-// Pass 1: per pair, (row since the segment's first entry) | (escapes since
-// the segment's start) << 32, inclusive.  The first pair of a segment starts
-// from the row of the segment's first index.
-__global__ __launch_bounds__(kVT) void coo_rows_kernel(CooDecParams p) {
-  __shared__ uint64_t s_v[kVTile];
-  __shared__ uint32_t s_rf[kVTile / 32];
-  __shared__ uint32_t s_range[2];
-  __shared__ uint64_t s_tsum[kVT];
-  __shared__ uint32_t s_trst[kVT];
-  __shared__ uint64_t s_tail[2];
-  __shared__ uint64_t s_b;
-  const int tid = threadIdx.x;
-  const uint64_t n0 = *p.npairs;
-  const uint64_t np = n0 < p.pair_capacity ? n0 : p.pair_capacity;
-  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
-    const uint64_t q0 = (uint64_t)tk.tile * kVTile;
-    const uint64_t q1 = q0 + kVTile < np ? q0 + kVTile : (q0 < np ? np : q0);
-    const uint32_t cnt = (uint32_t)(q1 - q0);
-    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_rf[w] = 0;
-    __syncthreads();
-    if (tid < 64) mark_starts(p.seg_pairs, p.nseg, q0, q1, s_rf, s_range);
-    __syncthreads();
-    for (uint32_t i = tid; i < cnt; i += kVT) {
-      const uint32_t dr = p.drow[q0 + i];
-      const bool esc = dr == 255u && p.dcol[q0 + i] == 0;
-      uint64_t v = (uint64_t)dr | ((uint64_t)(esc ? 1u : 0u) << 32);
-      if (flag_at(s_rf, i)) {  // the segment's first pair: start from its first index's row
-        const uint32_t s = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
-        const uint32_t C = p.cols[s] > 0 ? p.cols[s] : 1u;
-        v += p.first[s] / C;
-      }
-      s_v[i] = v;
-    }
-    __syncthreads();
-    tile_segmented_sum<true>(p.ws, tk, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
-    for (uint32_t i = tid; i < cnt; i += kVT) p.scratch[q0 + i] = s_v[i];
-    __syncthreads();
-  });
-}
-
-// Pass 2: the flat index of every pair's entry, written at
-// seg_begin[s] + 1 + (pairs before it in the segment) - (escapes before it);
-// each segment's first index goes to seg_begin[s].  A thread takes 16
-// consecutive pairs of the tile: it finds its first pair's segment by binary
-// search and moves to the next segment only at a segment start.
-__global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
+// The decode, one pass over pair tiles with two chained segmented sums per
+// tile (sequence numbers 2t and 2t + 1 of the launch):
+//   1. per pair, (row since the segment's first entry) | (escapes since the
+//      segment's start) << 32, inclusive, restarting at segment starts; the
+//      first pair of a segment starts from the row of its first index;
+//   2. the flat index of every pair's entry, restarting at new-row pairs and
+//      segment starts, written at seg_begin[s] + 1 + (pairs before it in the
+//      segment) - (escapes before it); each segment's first index goes to
+//      seg_begin[s].
+// A thread takes 16 consecutive pairs of the tile for the second sum: it
+// finds its first pair's segment by a search over the tile's segments and
+// moves to the next segment only at a segment start.
+__global__ __launch_bounds__(kVT) void coo_decode_kernel(CooDecParams p) {
   __shared__ uint64_t s_v[kVTile];
   __shared__ uint32_t s_pair[kVTile];     // drow | dcol << 8
   __shared__ uint32_t s_rf[kVTile / 32];
@@ -712,6 +683,9 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
   const uint64_t np = n0 < p.pair_capacity ? n0 : p.pair_capacity;
   const uint64_t nent = *p.nent;
   for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
+    const uint64_t g0 = (tk.seq - tk.tile) & kSeqMask;
+    const Ticket t_rows{tk.tile, (g0 + 2ull * tk.tile) & kSeqMask};
+    const Ticket t_flat{tk.tile, (g0 + 2ull * tk.tile + 1ull) & kSeqMask};
     const uint64_t q0 = (uint64_t)tk.tile * kVTile;
     const uint64_t q1 = q0 + kVTile < np ? q0 + kVTile : (q0 < np ? np : q0);
     const uint32_t cnt = (uint32_t)(q1 - q0);
@@ -719,13 +693,25 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
       s_rf[w] = 0;
       s_seg[w] = 0;
     }
-    for (uint32_t i = tid; i < cnt; i += kVT) {
-      s_v[i] = p.scratch[q0 + i];
+    for (uint32_t i = tid; i < cnt; i += kVT)
       s_pair[i] = (uint32_t)p.drow[q0 + i] | ((uint32_t)p.dcol[q0 + i] << 8);
-    }
     __syncthreads();
     if (tid < 64) mark_starts(p.seg_pairs, p.nseg, q0, q1, s_seg, s_range);
     __syncthreads();
+    // sum 1: row and escape count since the segment's start
+    for (uint32_t i = tid; i < cnt; i += kVT) {
+      const uint32_t pr = s_pair[i];
+      const bool esc = (pr & 0xFFu) == 255u && (pr >> 8) == 0u;
+      uint64_t v = (uint64_t)(pr & 0xFFu) | ((uint64_t)(esc ? 1u : 0u) << 32);
+      if (flag_at(s_seg, i)) {  // the segment's first pair: start from its first index's row
+        const uint32_t s = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
+        const uint32_t C = p.cols[s] > 0 ? p.cols[s] : 1u;
+        v += p.first[s] / C;
+      }
+      s_v[i] = v;
+    }
+    __syncthreads();
+    tile_segmented_sum<true, 2>(p.ws, t_rows, s_v, s_seg, cnt, s_tsum, s_trst, s_tail, &s_b);
     // values and restarts of this thread's pairs: a new-row pair restarts at
     // row * C + column, a segment's first pair at its first index + gap (or,
     // if it starts a new row, as a new-row pair), a same-row pair adds its
@@ -771,7 +757,8 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
     // publish this thread's restart flags (its 16 bits of the tile's bitmap)
     if (i0 < cnt) atomicOr(&s_rf[i0 >> 5], rst_bits << (i0 & 31));
     __syncthreads();
-    tile_segmented_sum<true>(p.ws, tk, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
+    // sum 2: the flat index
+    tile_segmented_sum<true, 2>(p.ws, t_flat, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
     // Pair i's entry lands at seg_begin[s] + 1 + (q0 + i - seg_pairs[s]) -
     // (escapes before it), s its segment.  The owning thread stores the low
     // 32 bits of that position in s_pair (no longer needed), thread 0 the
@@ -822,7 +809,7 @@ __global__ __launch_bounds__(kVT) void coo_flat_kernel(CooDecParams p) {
       }
     }
     __syncthreads();
-  });
+  }, 2u);
 }
 
 uint32_t varint_entry_tile() { return kVTile; }
@@ -859,9 +846,7 @@ hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream) {
 hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream) {
   const uint32_t grid = varint_grid(p.ntiles);
   if (grid == 0) return hipErrorInvalidDevice;
-  hipLaunchKernelGGL(coo_rows_kernel, dim3(grid), dim3(kVT), 0, stream, p);
-  if (hipError_t e = hipGetLastError()) return e;
-  hipLaunchKernelGGL(coo_flat_kernel, dim3(grid), dim3(kVT), 0, stream, p);
+  hipLaunchKernelGGL(coo_decode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -130,7 +130,7 @@ def lib():
             L.pulse_cast_lowp.argtypes = [i32, vp, u64, f32, vp, vp, vp]
             L.pulse_coo_encode.argtypes = [vp, u64, vp, vp, u32, vp, vp, vp, vp, u64, vp, vp, vp,
                                            sz, vp]
-            L.pulse_coo_decode.argtypes = [vp, vp, u64, vp, vp, vp, u32, vp, vp, vp, vp, u64, vp,
+            L.pulse_coo_decode.argtypes = [vp, vp, u64, vp, vp, vp, u32, vp, vp, vp, vp, u64,
                                            vp, sz, vp]
             L.pulse_encode_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_apply_lowp_batch.argtypes = [i32, vp, u32, vp, vp, u64, vp, vp, vp, vp]
@@ -421,15 +421,14 @@ def coo_encode(idx: torch.Tensor, end: torch.Tensor, seg_begin: torch.Tensor, co
 
 def coo_decode(drow: torch.Tensor, dcol: torch.Tensor, npairs: torch.Tensor,
                seg_begin: torch.Tensor, seg_pairs: torch.Tensor, cols: torch.Tensor,
-               first: torch.Tensor, nent: torch.Tensor, idx: torch.Tensor, scratch: torch.Tensor,
+               first: torch.Tensor, nent: torch.Tensor, idx: torch.Tensor,
                ws: torch.Tensor, stream=None) -> None:
     """Indices back from a 2-D COO delta stream (pulse_coo_decode)."""
     pc = min(drow.numel(), dcol.numel())
-    assert scratch.element_size() == 8 and scratch.numel() >= pc
     nseg = seg_begin.numel()
     _check(lib().pulse_coo_decode(_p(drow), _p(dcol), pc, _p(npairs), _p(seg_begin),
                                   _p(seg_pairs), nseg, _p(cols), _p(first), _p(nent), _p(idx),
-                                  idx.numel(), _p(scratch), _p(ws), ws.numel(), _stream(stream)),
+                                  idx.numel(), _p(ws), ws.numel(), _stream(stream)),
            "pulse_coo_decode")
 
 

@@ -169,12 +169,11 @@ def gpu_decode(first, drow, dcol, seg_pairs, seg_begin, cols, nent, ws=None, cap
         torch.zeros(1, dtype=torch.int16, device="cuda")
     cap = nent if cap is None else cap
     idx = torch.full((max(cap, 1),), -1, dtype=torch.int32, device="cuda")
-    scratch = torch.empty(max(P, 1), dtype=torch.int64, device="cuda")
     pulse.coo_decode(d_drow[:P] if P else d_drow[:0], d_dcol[:P] if P else d_dcol[:0], counter(P),
                      dev(np.asarray(seg_begin, dtype=np.uint64)),
                      dev(np.asarray(seg_pairs, dtype=np.uint64)), dev(np.asarray(cols, np.uint32)),
                      dev(np.asarray(first, np.uint32)), counter(nent), idx[:cap] if cap else idx[:0],
-                     scratch, pulse.workspace() if ws is None else ws)
+                     pulse.workspace() if ws is None else ws)
     torch.cuda.synchronize()
     return h32(idx)[:cap]
 
