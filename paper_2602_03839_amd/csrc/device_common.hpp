@@ -1,6 +1,6 @@
 // device_common.hpp -- gfx950 building blocks shared by the libpulse kernels.
 //
-//  * bf16 round-to-nearest-even on FP32 bit patterns (integer form);
+//  * FP32 -> BF16 round-to-nearest-even on the conversion unit;
 //  * wave64 scans and reductions;
 //  * the single-pass ordered scan across workgroups ("decoupled look-back",
 //    Merrill & Garland, NVIDIA tech report NVR-2016-002), written for CDNA:

@@ -5,9 +5,9 @@
 //
 // Tile layout.  A tile is U groups x TBC compute lanes x 8 consecutive
 // elements; group u of lane l covers elements u*TBC*8 + l*8 + [0, 8).  Each lane
-// issues two 16-byte FP32 loads and one 16-byte BF16 load per group (non-
-// temporal: the data is streamed once), so every wave instruction reads 1 KiB
-// of contiguous memory.  Element order inside a tile is group-major, then lane,
+// issues two 16-byte FP32 loads and one 16-byte BF16 load per group (the BF16
+// one non-temporal; see load_group), so every wave instruction reads 1 KiB of
+// contiguous memory.  Element order inside a tile is group-major, then lane,
 // then slot, and the compaction ranks follow that order.
 //
 // Block = NW compute waves + 1 scan wave, persistent over tiles drawn by

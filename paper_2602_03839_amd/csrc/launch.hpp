@@ -15,7 +15,7 @@ static_assert(kMaxBatch <= 64, "the tile -> tensor lookup keeps one tensor per l
 // Tile shapes: compute threads per block (a multiple of 64; one more wave is
 // added for the scan) and 8-element groups per thread.  The defaults give
 // 16-wave blocks (15 compute + 1 scan), one per CU: waves are handed out to
-// the SIMDs in fours, and the LDS value ring of one block takes 150 KiB of the
+// the SIMDs in fours, and the sparsifier's LDS value ring takes 150 KiB of the
 // CU's 160 KiB.  Overridable at build time for tuning sweeps.
 #ifndef PULSE_ENCODE_TB
 #define PULSE_ENCODE_TB 960
