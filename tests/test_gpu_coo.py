@@ -215,3 +215,42 @@ def test_decode_capacity_and_empty():
     out = gpu_decode(np.zeros(3, np.uint32), np.zeros(0, np.uint8), np.zeros(0, np.uint16),
                      np.zeros(3, np.uint64), np.zeros(3, np.uint64), np.array([3, 4, 5], np.uint32), 0)
     assert out.size == 0 and z.size == 0
+
+
+def test_round_trip_on_one_workspace_twice():
+    """The BF16 encode, the COO encode and the COO decode (two chained sums per
+    tile, two sequence numbers of the ring each) back to back on one
+    workspace, twice: every launch must start past the sequence numbers of
+    the one before it."""
+    rng = np.random.default_rng(14)
+    shapes = [(700, 300), (1, 17), (0, 5), (2000, 9), (64, 1024)]
+    cols = np.array([c for _, c in shapes], dtype=np.uint32)
+    descs, want = [], []
+    for r, c in shapes:
+        n = r * c
+        w = (rng.standard_normal(max(n, 1)) * 0.1).astype(np.float32)[:n]
+        w2 = (w - (rng.standard_normal(n) * 3e-3 * np.abs(w)).astype(np.float32)).astype(np.float32)
+        s = oracle.cast(w)
+        k, oi, _ = oracle.encode(w2, s)
+        want.append(oi[:k])
+        descs.append(pulse.EncodeTensor(dev(w2), dev(s), None, 0))
+    want_idx = np.concatenate(want)
+    seg_h = np.cumsum([0] + [x.size for x in want[:-1]]).astype(np.uint64)
+    of, od, oc, osp = oracle.coo_encode(want_idx, seg_h, cols)
+    N = sum(r * c for r, c in shapes)
+    ws = pulse.workspace()
+    idx = torch.zeros(N + 1, dtype=torch.int32, device="cuda")
+    val = torch.zeros(N + 1, dtype=torch.int16, device="cuda")
+    seg = torch.zeros(len(shapes), dtype=torch.int64, device="cuda")
+    for rep in range(2):
+        print(f"coo shared workspace: round {rep}", flush=True)
+        count = counter(0)
+        pulse.EncodeBatch(descs)(idx, val, count, ws, seg_begin=seg)
+        P, gf, gd, gc, gsp = gpu_coo(None, None, cols, out_cap=N + 64, ws=ws, idx_d=idx,
+                                     end_d=count, seg_d=seg)
+        assert P == od.size
+        np.testing.assert_array_equal(gd, od)
+        np.testing.assert_array_equal(gc, oc)
+        np.testing.assert_array_equal(gsp, osp)
+        back = gpu_decode(gf, gd, gc, gsp, seg.cpu().numpy().view(np.uint64), cols, want_idx.size, ws=ws)
+        np.testing.assert_array_equal(back, want_idx)
