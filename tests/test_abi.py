@@ -194,3 +194,42 @@ def test_lowp_validation(L):
     assert lo(FP8, lt, None, 1, A, A, 10, A, None, ws, wsb, None) == EINVAL  # inv_scales
     assert lo(7, lt, sc, 1, A, A, 10, A, None, ws, wsb, None) == EINVAL
     assert lo(FP8, lt, sc, 1, A, A, 10, A, None, ws + 8, wsb, None) == EALIGN
+
+
+def test_stream_validation(L):
+    """The delta-varint and 2-D COO entry points: missing pointers, alignment,
+    an empty segment list and more tiles than one launch holds."""
+    ws, wsb = ws_args(L)
+    big = 1 << 40
+    ve = L.pulse_varint_encode  # idx, capacity, end, seg_begin, nseg, out, out_capacity,
+    #                             seg_bytes, total_bytes, workspace, bytes, stream
+    assert ve(A, 10, None, None, 0, A, 10, None, A, ws, wsb, None) == EINVAL      # end
+    assert ve(None, 10, A, None, 0, A, 10, None, A, ws, wsb, None) == EINVAL      # idx
+    assert ve(A, 10, A, None, 0, None, 10, None, A, ws, wsb, None) == EINVAL      # out
+    assert ve(A, 10, A, None, 2, A, 10, None, A, ws, wsb, None) == EINVAL         # seg_begin
+    assert ve(A, 10, A + 4, None, 0, A, 10, None, A, ws, wsb, None) == EALIGN     # end
+    assert ve(A + 2, 10, A, None, 0, A, 10, None, A, ws, wsb, None) == EALIGN     # idx
+    assert ve(A, big, A, None, 0, A, 10, None, A, ws, wsb, None) == EINVAL        # tiles
+    assert ve(A, 10, A, None, 0, A, 10, None, A, None, wsb, None) == EINVAL       # workspace
+    vd = L.pulse_varint_decode  # in, in_capacity, nbytes, seg_begin, nseg, idx, capacity,
+    #                             count, workspace, bytes, stream
+    assert vd(A, 10, None, None, 0, A, 10, A, ws, wsb, None) == EINVAL            # nbytes
+    assert vd(None, 10, A, None, 0, A, 10, A, ws, wsb, None) == EINVAL            # in
+    assert vd(A, 10, A, None, 0, A + 2, 10, A, ws, wsb, None) == EALIGN           # idx
+    assert vd(A, big, A, None, 0, A, 10, A, ws, wsb, None) == EINVAL              # tiles
+    ce = L.pulse_coo_encode  # idx, capacity, end, seg_begin, nseg, cols, first, drow, dcol,
+    #                          out_capacity, seg_pairs, total_pairs, workspace, bytes, stream
+    assert ce(A, 10, A, A, 0, A, A, A, A, 10, A, A, ws, wsb, None) == EINVAL      # nseg 0
+    assert ce(A, 10, A, A, 1, None, A, A, A, 10, A, A, ws, wsb, None) == EINVAL   # cols
+    assert ce(A, 10, A, A, 1, A, A, A, None, 10, A, A, ws, wsb, None) == EINVAL   # dcol
+    assert ce(A, 10, A, A, 1, A, A, A, A + 1, 10, A, A, ws, wsb, None) == EALIGN  # dcol
+    assert ce(A, big, A, A, 1, A, A, A, A, 10, A, A, ws, wsb, None) == EINVAL     # tiles
+    cd = L.pulse_coo_decode  # drow, dcol, pair_capacity, npairs, seg_begin, seg_pairs, nseg,
+    #                          cols, first, nent, idx, capacity, workspace, bytes, stream
+    assert cd(A, A, 10, A, A, A, 0, A, A, A, A, 10, ws, wsb, None) == EINVAL      # nseg 0
+    assert cd(None, A, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EINVAL   # drow
+    assert cd(A, A, 10, A, A, A, 1, A, A, A, None, 10, ws, wsb, None) == EINVAL   # idx
+    assert cd(A, A, 10, A + 4, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # npairs
+    assert cd(A, A + 1, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # dcol
+    assert cd(A, A, big, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EINVAL     # tiles
+    assert b"coo decode" in L.pulse_last_error()
