@@ -141,8 +141,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the patch codec needs no collectives, and this "
-              "build measures a single MI355X (the design notes describe how it would shard).",
+        print("bench.py measures one GPU only: the patch codec needs no collectives; across GPUs "
+              "each rank would run it on its own shard of the tensors, with no cross-GPU traffic.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -37,7 +37,7 @@
  *   oracle_merkle_root   Merkle Tree Hash) over fixed-size chunks of the
  *                        concatenated BF16 bytes.
  *
- * Readings where the paper is silent (all listed in the design notes):
+ * Readings where the paper is silent:
  *   - A NaN input casts to a quiet NaN that keeps the sign and the leading
  *     payload bits (IEEE 754-2019 6.2.3 NaN propagation; the paper never meets NaN).
  *   - Overflow rounds to +-inf exactly as IEEE RNE with an unbounded exponent.
@@ -325,8 +325,8 @@ int64_t oracle_varint_decode(const uint8_t *in, uint64_t nbytes, uint32_t *out, 
  * as it sits in memory: each BF16 value as its two bytes, low byte first.
  *
  * A single SHA-256 over the whole stream is one long chain of compressions
- * and cannot be split, so the checksum is read as a tree of SHA-256 (the
- * design notes give the reasons): the stream is cut into chunks of
+ * and cannot be split across compute units, so the checksum is read as a
+ * tree of SHA-256: the stream is cut into chunks of
  * `leaf_bytes` bytes (the last one may be shorter) and combined with the
  * Merkle Tree Hash of RFC 6962, Sec. 2.1:
  *     MTH({})      = SHA-256()                        (empty stream)
@@ -518,7 +518,7 @@ void oracle_merkle_root(const uint8_t *digests, uint64_t nleaves, uint8_t root[3
  * mantissa bit: magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6), two codes per byte,
  * the even-indexed value in the low nibble.
  *
- * Readings (listed in the design notes):
+ * Readings where the paper is silent:
  *   - FP8 values carry a per-tensor FP32 scale: the receiver computes with
  *     y = fl32(x * inv_scale) cast to E4M3, rounded to nearest with ties to
  *     the even code, saturating to +-448 (also for +-inf); NaN -> 0x7F with
