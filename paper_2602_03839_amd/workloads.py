@@ -100,7 +100,7 @@ SHAPES = {
     "32b": ModelShape("32b", 5120, 64, 1024, 27648, 152064, tied=False),
 }
 
-C1_N = 1 << 20
+SINGLE_N = 1 << 20
 
 
 def mix_seed(*parts: int) -> int:
@@ -132,7 +132,7 @@ def adam_step_np(w: np.ndarray, u: np.ndarray, lr: float) -> np.ndarray:
     return (w - step).astype(np.float32)
 
 
-def c1_inputs(lr: float = 1e-6, n: int = C1_N, seed: int = 0):
+def single_tensor_inputs(lr: float = 1e-6, n: int = SINGLE_N, seed: int = 0):
     """Single FP32 tensor: default_rng(seed), draws in the order w, m, v.
 
     Returns (w, w_new) as float32 arrays; the snapshot is bf16(w), computed by

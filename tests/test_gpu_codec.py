@@ -120,8 +120,8 @@ def test_cast_exhaustive_all_fp32_patterns():
 # --------------------------------------------------------------------------- encode
 
 def test_encode_c1(ws):
-    """Config c1 (1,048,576 params, lr 1e-6): patch and lossless apply match the oracle."""
-    w, w_new = wl.c1_inputs()
+    """One 1,048,576-element tensor at lr 1e-6: patch and lossless apply match the oracle."""
+    w, w_new = wl.single_tensor_inputs()
     s_or = oracle.cast(w)
     s_d = pulse.cast_bf16(dev(w))
     np.testing.assert_array_equal(h16(s_d), s_or)

@@ -2,10 +2,10 @@
 times: batches of <= 64 tensors, a patch buffer sized for 5% of the set (10%
 for the sparsifier), one workspace for every launch.
 
-* c2 (0.5B-shaped, 494,005,120 params, flat uint32 indices) is compared with
+* the 0.5B-shaped set (494,005,120 params, flat uint32 indices) is compared with
   the oracle in full, element by element, including the fused refresh.
-* c3 (7B-shaped, 20-step chains at lr 3e-7, 1e-6, 3e-6), c4 (32B-shaped, one
-  fused step at lr 1e-6) and c5 (7B-shaped PULSELoCo, 10 rounds) are too large
+* the 7B-shaped chains (20 steps at lr 3e-7, 1e-6, 3e-6), the 32B-shaped set
+  (one fused step at lr 1e-6) and the 7B-shaped PULSELoCo run (10 rounds) are too large
   for the oracle in test time.  They are checked
     (a) at full size against the definition, computed on the GPU with torch's
         own BF16 cast, comparison, nonzero and FP32 add (no kernel of this
@@ -130,7 +130,7 @@ def fresh_memory():
     torch.cuda.empty_cache()
 
 
-def test_c2_full_oracle_parity(fresh_memory):
+def test_05b_full_oracle_parity(fresh_memory):
     """0.5B-shaped set, one fused step at lr 1e-6: patch, segments and refreshed copy
     equal the oracle's for all 494,005,120 parameters."""
     oracle.build()
@@ -171,7 +171,7 @@ def test_c2_full_oracle_parity(fresh_memory):
 
 
 @pytest.mark.parametrize("lr", [3e-7, 1e-6, 3e-6])
-def test_c3_twenty_step_chain(fresh_memory, lr):
+def test_7b_twenty_step_chain(fresh_memory, lr):
     """7B-shaped set, 20 consecutive steps; each step's snapshot is the copy the
     previous patches refreshed.  The standalone apply keeps a second copy."""
     oracle.build()
@@ -223,7 +223,7 @@ def test_c3_twenty_step_chain(fresh_memory, lr):
     assert lo < dens[0] < hi, dens[0]
 
 
-def test_c4_single_fused_step_32b(fresh_memory):
+def test_32b_single_fused_step(fresh_memory):
     """32B-shaped set resident on one GPU: one fused encode+refresh step at lr 1e-6."""
     oracle.build()
     ms = ModelSet("32b")
@@ -257,7 +257,7 @@ def test_c4_single_fused_step_32b(fresh_memory):
         np.testing.assert_array_equal(ms.view(R, i)[a:e].cpu().numpy().view(np.uint16), r)
 
 
-def test_c5_loco_ten_rounds_7b(fresh_memory):
+def test_7b_loco_ten_rounds(fresh_memory):
     """PULSELoCo on the 7B-shaped set: 10 rounds at a fixed tau, residual carried
     in FP32; every round's patch and residual are bit-exact."""
     oracle.build()

@@ -155,7 +155,7 @@ def _bottom_up_root(leaf_digests: np.ndarray) -> bytes:
 
 
 def model_bf16(key: str):
-    """A model-shaped set of BF16 weights (the c2-c4 init of the workloads), one flat
+    """A model-shaped set of BF16 weights (the workloads' model-shaped init), one flat
     int16 buffer with one view per tensor."""
     specs = wl.SHAPES[key].tensors()
     cfg = {"0.5b": 2, "7b": 3, "32b": 4}[key]
@@ -173,10 +173,10 @@ def model_bf16(key: str):
 
 
 @pytest.mark.slow
-def test_c2_full_parity():
+def test_05b_set_full_parity():
     """0.5B-shaped set (218 tensors, 494,005,120 values): every leaf and the root."""
     flat, views, _ = model_bf16("0.5b")
-    print("c2 hash: full parity", flush=True)
+    print("0.5B-shaped hash: full parity", flush=True)
     got_root, got_leaves = gpu_hash(views)
     stream = host_bytes(flat)
     want_root, want_leaves = oracle.tree_hash(stream)
@@ -186,13 +186,13 @@ def test_c2_full_parity():
 
 
 @pytest.mark.slow
-def test_c4_32b_sampled_leaves_and_tree():
+def test_32b_set_sampled_leaves_and_tree():
     """32B-shaped set (579 tensors, 32,763,417,600 values) resident on one GPU:
     512 random leaves and every leaf that holds a tensor boundary against the
     oracle, and the root against the tree built over the GPU's leaf digests."""
     torch.cuda.empty_cache()
     flat, views, offs = model_bf16("32b")
-    print("c4 hash: sampled parity", flush=True)
+    print("32B-shaped hash: sampled parity", flush=True)
     got_root, got_leaves = gpu_hash(views)
     nleaves = pulse.hash_leaf_count(int(offs[-1]))
     assert got_leaves.shape == (nleaves, 32)

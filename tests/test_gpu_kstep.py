@@ -20,7 +20,7 @@ KS = (1, 8, 16, 32)
 
 @pytest.mark.parametrize("lr", [3e-7, 1e-6])
 def test_kstep_patches_along_a_chain(lr):
-    n = wl.C1_N + 333
+    n = wl.SINGLE_N + 333
     rng = np.random.default_rng(42)
     w = rng.normal(0.0, wl.W_VAR ** 0.5, n).astype(np.float32)
     S0 = oracle.cast(w)

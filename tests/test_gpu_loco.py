@@ -90,7 +90,7 @@ def test_loco_overflow_append_base(ws):
 
 
 def test_loco_ten_round_chain(ws):
-    """Config c5's recipe at 2^20 elements: 10 rounds, residual carried on each side."""
+    """The 7B-shaped LoCo recipe at 2^20 elements: 10 rounds, residual carried on each side."""
     rng = np.random.default_rng(12)
     n = 1 << 20
     tau = wl.loco_tau()

@@ -131,7 +131,7 @@ def test_encode_patch_round_trip_with_shared_workspace(ws):
     sizes = [300_000, 17, 0, 1 << 20, 4096 * 3 + 5]
     descs, olists = [], []
     for i, n in enumerate(sizes):
-        w, w_new = wl.c1_inputs(n=max(n, 1), seed=i)
+        w, w_new = wl.single_tensor_inputs(n=max(n, 1), seed=i)
         w, w_new = w[:n], w_new[:n]
         s = oracle.cast(w)
         cnt, oi, _ = oracle.encode(w_new, s)

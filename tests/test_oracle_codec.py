@@ -59,8 +59,8 @@ def test_encode_brute_force_all_masks(oracle_mod, n):
 
 
 def test_encode_counts_and_lossless_on_c1(oracle_mod):
-    """Config c1: nnz == mismatch count, ascending unique indices, lossless apply."""
-    w, w_new = wl.c1_inputs()
+    """One 1,048,576-element tensor: nnz == mismatch count, ascending unique indices, lossless apply."""
+    w, w_new = wl.single_tensor_inputs()
     snap = tcast(w)
     target = tcast(w_new)
     count, idx, val = oracle_mod.encode(w_new, snap)
