@@ -46,6 +46,15 @@
  * call).  Calls that share a workspace must be ordered on one stream; give
  * concurrent streams separate workspaces.  A call that faulted leaves it
  * undefined: zero it again.
+ *
+ * Workspace misuse is detected, not hidden: a workspace that was not
+ * zero-filled can make a tile wait for a predecessor that never publishes.
+ * The kernels then stop waiting (within a fraction of a second), treat the
+ * missing tiles as empty -- so the patch, counts and segment offsets of that
+ * call are wrong -- and raise a flag in the workspace (64-bit word 16, byte
+ * offset 128).  The flag stays raised, and every later call on that workspace
+ * stops waiting at once, until the caller zero-fills the workspace again.
+ * pulse_workspace_status() reads it.
  */
 #ifndef PULSE_H
 #define PULSE_H
@@ -62,11 +71,25 @@ typedef enum pulse_status {
     PULSE_EINVAL = -1, /* NULL required pointer, bad size, workspace too small */
     PULSE_ERANGE = -2, /* index_base + n > 2^32 */
     PULSE_EALIGN = -3, /* a dense stream pointer is not 16-byte aligned */
-    PULSE_EHIP = -4    /* the HIP runtime rejected a launch */
+    PULSE_EHIP = -4,   /* the HIP runtime rejected a launch */
+    PULSE_ESTATE = -5  /* the workspace flag is raised: a look-back gave up */
 } pulse_status;
 
 /* Size in bytes of the workspace that encode and sparsify calls use. */
 size_t pulse_workspace_bytes(void);
+
+/*
+ * pulse_workspace_status -- whether every call on `workspace` since it was
+ * last zero-filled found all its predecessors' status words (see "Workspace
+ * misuse" above).  Synchronises `stream` (the stream the calls were ordered
+ * on), then reads the workspace's flag with a device-to-host copy.
+ *   workspace        as passed to the calls; workspace_bytes its size.
+ * Returns PULSE_OK when the flag is clear, PULSE_ESTATE when it is raised
+ * (the results of the calls since the last zero-fill are unreliable; zero the
+ * workspace before reusing it), PULSE_EINVAL / PULSE_EALIGN for a bad
+ * workspace argument and PULSE_EHIP if the copy fails.
+ */
+int pulse_workspace_status(const void *workspace, size_t workspace_bytes, void *stream);
 
 /* Human-readable name of a pulse_status value (static string). */
 const char *pulse_strerror(int status);

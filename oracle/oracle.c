@@ -56,8 +56,22 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* Scratch allocation that cannot fail silently: the oracle is a checker, so a
+ * missing buffer stops the process with a message instead of producing a
+ * result. */
+static void *oracle_alloc(size_t bytes, int zero)
+{
+    void *p = zero ? calloc(bytes ? bytes : 1, 1) : malloc(bytes ? bytes : 1);
+    if (!p) {
+        fprintf(stderr, "oracle: cannot allocate %zu bytes\n", bytes);
+        abort();
+    }
+    return p;
+}
 
 static float float_from_bits(uint32_t u)
 {
@@ -220,16 +234,13 @@ uint64_t oracle_loco(const float *delta, float *residual, uint64_t n, float tau,
  *
  * Worker r's list is entries [0, count[r]) of idx[r] / val[r], indices of the
  * form index_base + i; an index outside [index_base, index_base + n) is
- * ignored.  Indices within one list are distinct.  Returns 0, or -1 if the
- * scratch vector cannot be allocated.
+ * ignored.  Indices within one list are distinct.  Returns 0.
  */
 int oracle_outer_step(float *theta, float *momentum, uint64_t n, uint32_t index_base,
                       uint32_t nlists, const uint32_t *const *idx, const float *const *val,
                       const uint64_t *count, float mu, float alpha)
 {
-    float *g = (float *)calloc(n ? n : 1, sizeof(float)); /* all +0 */
-    if (!g)
-        return -1;
+    float *g = (float *)oracle_alloc((size_t)n * sizeof(float), 1); /* all +0 */
     for (uint32_t r = 0; r < nlists; r++) {
         for (uint64_t k = 0; k < count[r]; k++) {
             uint32_t j = idx[r][k];
@@ -388,7 +399,7 @@ static void sha256_with(const sha_consts *c, const uint8_t *msg, uint64_t len, u
 {
     /* 5.1.1: append the bit 1, zeros up to 448 mod 512 bits, and the 64-bit length */
     uint64_t padded = ((len + 8) / 64 + 1) * 64;
-    uint8_t *m = calloc(padded, 1);
+    uint8_t *m = oracle_alloc(padded, 1);
     if (len)
         memcpy(m, msg, len);
     m[len] = 0x80;
@@ -452,7 +463,7 @@ void oracle_sha256(const uint8_t *msg, uint64_t len, uint8_t out[32])
 /* leaf hash of RFC 6962: SHA-256 over the byte 0x00 followed by the chunk */
 static void leaf_hash(const sha_consts *c, const uint8_t *chunk, uint64_t len, uint8_t out[32])
 {
-    uint8_t *buf = malloc(len + 1);
+    uint8_t *buf = oracle_alloc(len + 1, 0);
     buf[0] = 0x00;
     if (len)
         memcpy(buf + 1, chunk, len);
@@ -723,9 +734,9 @@ uint64_t oracle_loco_gate_lp(int dtype, float inv_scale, const float *delta, flo
                              uint64_t n, const float *theta, uint32_t index_base, uint32_t *idx,
                              float *val, uint64_t capacity, uint64_t count_in)
 {
-    float *a = malloc((n ? n : 1) * sizeof(float));
-    float *after = malloc((n ? n : 1) * sizeof(float));
-    uint8_t *keep = malloc(n ? n : 1);
+    float *a = oracle_alloc((size_t)n * sizeof(float), 0);
+    float *after = oracle_alloc((size_t)n * sizeof(float), 0);
+    uint8_t *keep = oracle_alloc(n, 0);
     for (uint64_t i = 0; i < n; i++) {
         a[i] = delta[i] + residual[i];
         after[i] = theta[i] - a[i];

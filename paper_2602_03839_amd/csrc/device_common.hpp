@@ -62,14 +62,15 @@ constexpr uint64_t kValueMask = (1ull << 54) - 1;
 // A predecessor is always resident or finished, so a look-back normally waits
 // microseconds.  Only a workspace that was not zero-filled can make a tile
 // wait for one that never runs; after this many polls (well under a second)
-// the wave stops waiting, counts the missing tiles as empty and raises word 1
-// of the workspace, after which no wave of the device waits any more: a
-// misuse yields a wrong patch and a raised flag instead of a hung GPU.
+// the wave stops waiting, counts the missing tiles as empty and raises word
+// kWordGaveUp of the workspace, after which no wave of the device waits any
+// more: a misuse yields a wrong patch and a raised flag instead of a hung GPU.
+// The flag stays raised until the workspace is zero-filled again, and
+// pulse_workspace_status reports it to the host.
 constexpr uint32_t kMaxPolls = 1u << 18;
 
-#ifndef PULSE_LOOKBACK_K
-#define PULSE_LOOKBACK_K 1
-#endif
+// Look-back window: 64 * kLookK predecessors read at once.
+constexpr int kLookK = 1;
 
 __device__ __forceinline__ uint64_t status_word(uint64_t flag, uint64_t g, uint64_t value) {
   return (flag << 62) | (((g >> kSlotBits) & 0xFFull) << 54) | (value & kValueMask);
@@ -183,19 +184,13 @@ constexpr uint64_t kNoTicket = kTicketMask;
 // Tiles per ticket.  A chunk's tiles are processed in consecutive iterations,
 // so the chunk's last aggregate appears kChunk - 1 iterations after its first;
 // with kChunk <= RES + 1 later tiles never wait for it at resolution time.
-#ifndef PULSE_CHUNK
-#define PULSE_CHUNK 4
-#endif
-constexpr uint32_t kChunk = PULSE_CHUNK;
+constexpr uint32_t kChunk = 4;
 
 // Tiles whose loads a block keeps in flight: while a block computes tile T(i),
 // the loads of T(i + 1) .. T(i + kAhead) are outstanding.  A tile is 90 KiB
 // of input at the default shape; one CU needs well over 100 KiB in flight to
 // cover the HBM latency under full load.
-#ifndef PULSE_AHEAD
-#define PULSE_AHEAD 2
-#endif
-constexpr int kAhead = PULSE_AHEAD;
+constexpr int kAhead = 2;
 // LDS ring of tickets: T(i) lives in slot i mod kTkRing.  Compute waves read
 // slots i and i + kAhead in iteration i while the scan wave fills i + kAhead + 1.
 constexpr int kTkRing = kAhead + 2 <= 4 ? 4 : 8;
@@ -499,9 +494,9 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
     if (lane == 0) s_tk[(it + kAhead + 1) & (kTkRing - 1)] = have_last ? take() : kNoTicket;
     // first look-back window of T(i - kResolve), overlapping the compute of T(i)
     const ScanState res = hist[kResolve - 1];
-    LookWindow<PULSE_LOOKBACK_K> win;
+    LookWindow<kLookK> win;
     const bool walk = res.valid && res.tk.tile != 0;
-    if (walk) look_back_issue<PULSE_LOOKBACK_K>(p.ws, res.tk, (int64_t)res.tk.tile - 1, win);
+    if (walk) look_back_issue<kLookK>(p.ws, res.tk, (int64_t)res.tk.tile - 1, win);
     __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + kAhead + 1) in s_tk
     ScanState now;
     now.valid = have_cur;
@@ -525,7 +520,7 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
       if (!walk) {
         excl = count_in;
       } else {
-        excl = look_back<PULSE_LOOKBACK_K>(p.ws, res.tk, win);
+        excl = look_back<kLookK>(p.ws, res.tk, win);
         if (lane == 0) status_publish(p.ws, res.tk.seq, kFlagPrefix, excl + res.agg);
       }
       if (lane == 0) {

@@ -101,15 +101,9 @@ __device__ __forceinline__ void load_group(TileRegs<TBC, U>& r, int u, const Til
 // i + kDefer, after barrier i + kDefer.  Waves leave that write-out and start
 // computing iteration i + kDefer + 1 at different times, so the slot may be
 // refilled only from iteration i + kDefer + 2 on, after the next barrier.
-#ifndef PULSE_SEG_CAP
-#define PULSE_SEG_CAP 64
-#endif
-constexpr uint32_t kSegCap = PULSE_SEG_CAP;
+constexpr uint32_t kSegCap = 64;
 // Iterations from a tile's compute to its resolution and to its write-out.
-#ifndef PULSE_ENCODE_RESOLVE
-#define PULSE_ENCODE_RESOLVE 4
-#endif
-constexpr int kResolve = PULSE_ENCODE_RESOLVE;
+constexpr int kResolve = 4;
 constexpr int kDefer = kResolve + 1;
 constexpr int kWexclRing = wexcl_ring(kResolve);
 constexpr int kSegSlots = kDefer + 2;

@@ -16,33 +16,18 @@ static_assert(kMaxBatch <= 64, "the tile -> tensor lookup keeps one tensor per l
 // added for the scan) and 8-element groups per thread.  The defaults give
 // 16-wave blocks (15 compute + 1 scan), one per CU: waves are handed out to
 // the SIMDs in fours, and the sparsifier's LDS value ring takes 150 KiB of the
-// CU's 160 KiB.  Overridable at build time for tuning sweeps.
-#ifndef PULSE_ENCODE_TB
-#define PULSE_ENCODE_TB 960
-#endif
-#ifndef PULSE_ENCODE_U
-#define PULSE_ENCODE_U 2
-#endif
+// CU's 160 KiB.
 // Refresh writes of a tensor whose inference copy mirrors its snapshot cover
-// whole aligned runs of PULSE_SECTOR_LANES x 8 elements (16 bytes per lane).
+// whole aligned runs of kSectorLanes x 8 elements (16 bytes per lane).
 // 8 lanes = one 128-byte cache line: a scattered write costs about the same
 // HBM time whatever its size up to a line, so whole lines need the fewest
 // write requests (at ~1% density 45% of the lines change, against one request
 // per change for 2-byte writes).
-#ifndef PULSE_SECTOR_LANES
-#define PULSE_SECTOR_LANES 8
-#endif
-#ifndef PULSE_LOCO_TB
-#define PULSE_LOCO_TB 960
-#endif
-#ifndef PULSE_LOCO_U
-#define PULSE_LOCO_U 1
-#endif
-constexpr int kEncodeTB = PULSE_ENCODE_TB;
-constexpr int kEncodeU = PULSE_ENCODE_U;
-constexpr int kSectorLanes = PULSE_SECTOR_LANES;
-constexpr int kLocoTB = PULSE_LOCO_TB;
-constexpr int kLocoU = PULSE_LOCO_U;
+constexpr int kEncodeTB = 960;
+constexpr int kEncodeU = 2;
+constexpr int kSectorLanes = 8;
+constexpr int kLocoTB = 960;
+constexpr int kLocoU = 1;
 
 struct EncodeTensorDesc {
   const float* w_new;

@@ -92,10 +92,7 @@ __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const Lo
 }  // namespace
 
 // Iterations from a tile's compute to its resolution and to its write-out.
-#ifndef PULSE_LOCO_RESOLVE
-#define PULSE_LOCO_RESOLVE 4
-#endif
-constexpr int kResolve = PULSE_LOCO_RESOLVE;
+constexpr int kResolve = 4;
 constexpr int kDefer = kResolve + 1;
 constexpr int kWexclRing = wexcl_ring(kResolve);
 // LDS value buffers (ring).  Each compute thread reads back only the values

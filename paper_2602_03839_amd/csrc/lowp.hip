@@ -143,14 +143,8 @@ __device__ __forceinline__ void lowp_load(LowpRegs& g, const LowpCtx& c, uint64_
 
 }  // namespace
 
-#ifndef PULSE_LOWP_TB
-#define PULSE_LOWP_TB 960
-#endif
-#ifndef PULSE_LOWP_U
-#define PULSE_LOWP_U 3
-#endif
-constexpr int kLowpNW = PULSE_LOWP_TB / 64;
-constexpr int kLowpU = PULSE_LOWP_U;
+constexpr int kLowpNW = 15;
+constexpr int kLowpU = 3;
 constexpr int kLowpResolve = 4;
 constexpr int kLowpDefer = kLowpResolve + 1;
 constexpr int kLowpWexclRing = wexcl_ring(kLowpResolve);

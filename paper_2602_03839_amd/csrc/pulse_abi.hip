@@ -56,9 +56,6 @@ int check_range(uint64_t n, uint32_t index_base, const char* who, uint32_t t) {
 // The refresh target holds the snapshot's bits on entry: it is the snapshot
 // itself, or the caller says it is kept in step with it.
 bool refresh_mirrors(const pulse_encode_tensor& d) {
-#ifdef PULSE_FORCE_MIRROR
-  return true;
-#endif
   return d.refresh == d.snap || (d.flags & PULSE_REFRESH_MIRRORS_SNAP) != 0;
 }
 
@@ -93,6 +90,20 @@ extern "C" {
 
 size_t pulse_workspace_bytes(void) { return pulse::kWorkspaceBytes; }
 
+int pulse_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
+  if (int rc = check_workspace(const_cast<void*>(workspace), workspace_bytes)) return rc;
+  uint64_t flag = 0;
+  const uint64_t* word = static_cast<const uint64_t*>(workspace) + pulse::kWordGaveUp;
+  hipError_t e = hipMemcpyAsync(&flag, word, sizeof flag, hipMemcpyDeviceToHost, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) return fail(PULSE_EHIP, "workspace status: %s", hipGetErrorString(e));
+  if (flag != 0)
+    return fail(PULSE_ESTATE,
+                "a look-back gave up waiting: the workspace was not zero-filled before use; results "
+                "since then are unreliable, zero-fill it again");
+  return ok();
+}
+
 const char* pulse_strerror(int status) {
   switch (status) {
     case PULSE_OK: return "PULSE_OK";
@@ -100,6 +111,7 @@ const char* pulse_strerror(int status) {
     case PULSE_ERANGE: return "PULSE_ERANGE: index range exceeds 32 bits";
     case PULSE_EALIGN: return "PULSE_EALIGN: pointer not aligned";
     case PULSE_EHIP: return "PULSE_EHIP: HIP launch failed";
+    case PULSE_ESTATE: return "PULSE_ESTATE: a look-back gave up waiting (workspace not zero-filled)";
     default: return "unknown pulse status";
   }
 }

@@ -20,8 +20,7 @@ from typing import Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# PULSE_LIB may name another build of the same library (tuning sweeps).
-LIB_PATH = os.environ.get("PULSE_LIB") or os.path.join(_HERE, "libpulse.so")
+LIB_PATH = os.path.join(_HERE, "libpulse.so")
 
 _lock = threading.Lock()
 _lib = None
@@ -38,6 +37,7 @@ class _EncodeTensor(ctypes.Structure):
 
 
 REFRESH_MIRRORS_SNAP = 1  # PULSE_REFRESH_MIRRORS_SNAP
+ESTATE = -5  # PULSE_ESTATE
 
 
 class _ApplyTensor(ctypes.Structure):
@@ -85,6 +85,7 @@ class _HashTensor(ctypes.Structure):
 HASH_LEAF_BYTES = 16384  # PULSE_HASH_LEAF_BYTES
 
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
+           "pulse_workspace_status",
            "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
            "pulse_outer_step", "pulse_outer_step_batch",
@@ -112,6 +113,7 @@ def lib():
             L.pulse_last_error.argtypes = []
             L.pulse_last_error.restype = ctypes.c_char_p
             L.pulse_cast_bf16.argtypes = [vp, vp, u64, vp]
+            L.pulse_workspace_status.argtypes = [vp, sz, vp]
             L.pulse_encode.argtypes = [vp, vp, u64, vp, vp, u64, vp, u32, vp, vp, sz, vp]
             L.pulse_encode_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
             L.pulse_apply.argtypes = [vp, u64, vp, vp, u64, vp, vp, u32, vp, vp]
@@ -149,24 +151,67 @@ def _check(rc: int, what: str):
         raise PulseError(f"{what}: {L.pulse_strerror(rc).decode()} ({L.pulse_last_error().decode()})")
 
 
-def _p(t: Optional[torch.Tensor]):
+def _p(t: Optional[torch.Tensor], name: str = "tensor", esize: Optional[int] = None,
+       numel: Optional[int] = None, min_numel: Optional[int] = None, dtype=None,
+       device=None, optional: bool = True):
+    """Device pointer of `t` after checking what the C ABI cannot see.
+
+    The library trusts sizes and layouts it is given: a buffer shorter than the
+    count passed with it, or a strided view, would make a kernel read or write
+    the wrong memory.  So every tensor must be a contiguous device tensor of the
+    expected element size, length and device; None passes only if `optional`.
+    """
     if t is None:
-        return None
+        if optional:
+            return None
+        raise PulseError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise PulseError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
     if not t.is_cuda:
-        raise PulseError("libpulse takes device tensors")
+        raise PulseError(f"{name} must be a device tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise PulseError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise PulseError(f"{name} must be {dtype}, got {t.dtype}")
+    if esize is not None and t.element_size() != esize:
+        raise PulseError(f"{name} must have {esize}-byte elements, got {t.element_size()}")
+    if numel is not None and t.numel() != numel:
+        raise PulseError(f"{name} has {t.numel()} elements, expected {numel}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise PulseError(f"{name} has {t.numel()} elements, needs at least {min_numel}")
+    if device is not None and t.device != device:
+        raise PulseError(f"{name} is on {t.device}, the call's other tensors on {device}")
     return t.data_ptr()
 
 
-def _stream(stream=None):
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return s.cuda_stream
+def _f32(t, name, numel=None, device=None, optional=False):
+    return _p(t, name, dtype=torch.float32, numel=numel, device=device, optional=optional)
 
 
-def _is16(t: torch.Tensor) -> bool:
-    return t.element_size() == 2
+def _u16(t, name, numel=None, device=None, optional=False):
+    return _p(t, name, esize=2, numel=numel, device=device, optional=optional)
 
 
-def _capacity(idx: torch.Tensor, val: torch.Tensor, capacity: Optional[int]) -> int:
+def _u64(t, name, device=None, min_numel=1, optional=False):
+    return _p(t, name, esize=8, min_numel=min_numel, device=device, optional=optional)
+
+
+def _ws(ws: torch.Tensor, device=None):
+    """Workspace pointer and its size in bytes."""
+    ptr = _p(ws, "workspace", device=device, optional=False)
+    return ptr, ws.numel() * ws.element_size()
+
+
+def _stream(stream=None, device=None):
+    if stream is not None:
+        return stream.cuda_stream
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _capacity(idx: torch.Tensor, val: torch.Tensor, capacity: Optional[int],
+              idx_esize: int, val_esize: int, device=None) -> int:
+    _p(idx, "idx", esize=idx_esize, device=device, optional=False)
+    _p(val, "val", esize=val_esize, device=device, optional=False)
     room = min(idx.numel(), val.numel())
     if capacity is None:
         return room
@@ -184,12 +229,31 @@ def workspace(device=None) -> torch.Tensor:
     return torch.zeros(workspace_bytes(), dtype=torch.uint8, device=device or "cuda")
 
 
+def workspace_status(ws: torch.Tensor, stream=None) -> int:
+    """pulse_workspace_status: 0 if every look-back on `ws` found its
+    predecessors, else PULSE_ESTATE (synchronises the stream)."""
+    ptr, nb = _ws(ws)
+    rc = lib().pulse_workspace_status(ptr, nb, _stream(stream, ws.device))
+    if rc not in (0, ESTATE):
+        _check(rc, "pulse_workspace_status")
+    return rc
+
+
+def check_workspace(ws: torch.Tensor, stream=None) -> None:
+    """Raise PulseError if a call on `ws` gave up waiting in a look-back, which
+    happens only when the workspace was not zero-filled before first use: the
+    patches written since then are not trustworthy, and the workspace must be
+    zero-filled again."""
+    _check(workspace_status(ws, stream), "pulse_workspace_status")
+
+
 def cast_bf16(src: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    assert src.dtype == torch.float32 and src.is_contiguous()
+    _f32(src, "src")
     if out is None:
         out = torch.empty(src.shape, dtype=torch.int16, device=src.device)
-    assert _is16(out) and out.numel() == src.numel() and out.is_contiguous()
-    _check(lib().pulse_cast_bf16(_p(src), _p(out), src.numel(), _stream(stream)), "pulse_cast_bf16")
+    _u16(out, "out", numel=src.numel(), device=src.device)
+    _check(lib().pulse_cast_bf16(src.data_ptr(), out.data_ptr(), src.numel(),
+                                 _stream(stream, src.device)), "pulse_cast_bf16")
     return out
 
 
@@ -197,13 +261,16 @@ def encode(w_new: torch.Tensor, snap: torch.Tensor, idx: torch.Tensor, val: torc
            count: torch.Tensor, ws: torch.Tensor, index_base: int = 0,
            refresh: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
            stream=None) -> None:
-    assert w_new.dtype == torch.float32 and _is16(snap) and _is16(val)
-    assert idx.element_size() == 4 and count.element_size() == 8
-    assert w_new.numel() == snap.numel()
-    cap = _capacity(idx, val, capacity)
-    _check(lib().pulse_encode(_p(w_new), _p(snap), w_new.numel(), _p(idx), _p(val),
-                              cap, _p(count), index_base,
-                              _p(refresh), _p(ws), ws.numel(), _stream(stream)), "pulse_encode")
+    dev = w_new.device
+    n = w_new.numel()
+    pw = _f32(w_new, "w_new")
+    ps = _u16(snap, "snap", numel=n, device=dev)
+    pr = _u16(refresh, "refresh", numel=n, device=dev, optional=True)
+    cap = _capacity(idx, val, capacity, 4, 2, dev)
+    pc = _u64(count, "count", dev)
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_encode(pw, ps, n, idx.data_ptr(), val.data_ptr(), cap, pc, index_base,
+                              pr, pws, nb, _stream(stream, dev)), "pulse_encode")
 
 
 @dataclass
@@ -215,34 +282,49 @@ class EncodeTensor:
     mirrors_snap: bool = False  # refresh holds snap's bits on entry (PULSE_REFRESH_MIRRORS_SNAP)
 
 
+def _batch_device(tensors, first):
+    return first(tensors[0]).device if tensors else None
+
+
 class EncodeBatch:
     """Descriptor array for pulse_encode_batch, built once and reused."""
 
     def __init__(self, tensors: Sequence[EncodeTensor]):
         self.n = len(tensors)
+        self.device = _batch_device(tensors, lambda t: t.w_new)
         arr = (_EncodeTensor * max(1, self.n))()
         for i, t in enumerate(tensors):
-            assert t.w_new.dtype == torch.float32 and _is16(t.snap)
-            assert t.w_new.numel() == t.snap.numel()
-            arr[i] = _EncodeTensor(_p(t.w_new), _p(t.snap), _p(t.refresh), t.w_new.numel(),
-                                   t.index_base, REFRESH_MIRRORS_SNAP if t.mirrors_snap else 0)
+            n = t.w_new.numel()
+            arr[i] = _EncodeTensor(_f32(t.w_new, f"tensor {i} w_new", device=self.device),
+                                   _u16(t.snap, f"tensor {i} snap", numel=n, device=self.device),
+                                   _u16(t.refresh, f"tensor {i} refresh", numel=n,
+                                        device=self.device, optional=True),
+                                   n, t.index_base, REFRESH_MIRRORS_SNAP if t.mirrors_snap else 0)
         self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
-        _check(lib().pulse_encode_batch(self.arr, self.n, _p(idx), _p(val), cap, _p(count),
-                                        _p(seg_begin), _p(ws), ws.numel(), _stream(stream)),
+        dev = self.device
+        cap = _capacity(idx, val, capacity, 4, 2, dev)
+        pws, nb = _ws(ws, dev)
+        _check(lib().pulse_encode_batch(self.arr, self.n, idx.data_ptr(), val.data_ptr(), cap,
+                                        _u64(count, "count", dev),
+                                        _u64(seg_begin, "seg_begin", dev, min_numel=self.n,
+                                             optional=True),
+                                        pws, nb, _stream(stream, dev)),
                "pulse_encode_batch")
 
 
 def apply(dst: torch.Tensor, idx: torch.Tensor, val: torch.Tensor, begin: torch.Tensor,
           end: torch.Tensor, index_base: int = 0, rejected: Optional[torch.Tensor] = None,
           capacity: Optional[int] = None, stream=None) -> None:
-    assert _is16(dst) and _is16(val) and idx.element_size() == 4
-    cap = _capacity(idx, val, capacity)
-    _check(lib().pulse_apply(_p(dst), dst.numel(), _p(idx), _p(val), cap, _p(begin), _p(end),
-                             index_base, _p(rejected), _stream(stream)), "pulse_apply")
+    dev = dst.device
+    pd = _u16(dst, "dst")
+    cap = _capacity(idx, val, capacity, 4, 2, dev)
+    _check(lib().pulse_apply(pd, dst.numel(), idx.data_ptr(), val.data_ptr(), cap,
+                             _u64(begin, "begin", dev), _u64(end, "end", dev), index_base,
+                             _u64(rejected, "rejected", dev, optional=True),
+                             _stream(stream, dev)), "pulse_apply")
 
 
 @dataclass
@@ -254,30 +336,39 @@ class ApplyTensor:
 class ApplyBatch:
     def __init__(self, tensors: Sequence[ApplyTensor]):
         self.n = len(tensors)
+        self.device = _batch_device(tensors, lambda t: t.dst)
         arr = (_ApplyTensor * max(1, self.n))()
         for i, t in enumerate(tensors):
-            assert _is16(t.dst)
-            arr[i] = _ApplyTensor(_p(t.dst), t.dst.numel(), t.index_base)
+            arr[i] = _ApplyTensor(_u16(t.dst, f"tensor {i} dst", device=self.device), t.dst.numel(),
+                                  t.index_base)
         self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, idx, val, seg_begin, end, rejected=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
-        _check(lib().pulse_apply_batch(self.arr, self.n, _p(idx), _p(val), cap, _p(seg_begin),
-                                       _p(end), _p(rejected), _stream(stream)), "pulse_apply_batch")
+        dev = self.device
+        cap = _capacity(idx, val, capacity, 4, 2, dev)
+        _check(lib().pulse_apply_batch(self.arr, self.n, idx.data_ptr(), val.data_ptr(), cap,
+                                       _u64(seg_begin, "seg_begin", dev, min_numel=self.n),
+                                       _u64(end, "end", dev),
+                                       _u64(rejected, "rejected", dev, optional=True),
+                                       _stream(stream, dev)), "pulse_apply_batch")
 
 
 def loco_sparsify(delta: torch.Tensor, residual: torch.Tensor, tau: float, idx: torch.Tensor,
                   val: torch.Tensor, count: torch.Tensor, ws: torch.Tensor,
                   theta: Optional[torch.Tensor] = None, index_base: int = 0,
                   capacity: Optional[int] = None, stream=None) -> None:
-    assert delta.dtype == torch.float32 and residual.dtype == torch.float32
-    assert val.dtype == torch.float32 and idx.element_size() == 4
-    assert delta.numel() == residual.numel()
-    cap = _capacity(idx, val, capacity)
-    _check(lib().pulse_loco_sparsify(_p(delta), _p(residual), delta.numel(), float(tau),
-                                     _p(theta), _p(idx), _p(val), cap,
-                                     _p(count), index_base, _p(ws), ws.numel(), _stream(stream)),
+    dev = delta.device
+    n = delta.numel()
+    pdl = _f32(delta, "delta")
+    pr = _f32(residual, "residual", numel=n, device=dev)
+    pt = _f32(theta, "theta", numel=n, device=dev, optional=True)
+    _f32(val, "val", device=dev)
+    cap = _capacity(idx, val, capacity, 4, 4, dev)
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_loco_sparsify(pdl, pr, n, float(tau), pt, idx.data_ptr(), val.data_ptr(),
+                                     cap, _u64(count, "count", dev), index_base, pws, nb,
+                                     _stream(stream, dev)),
            "pulse_loco_sparsify")
 
 
@@ -289,23 +380,36 @@ class LocoTensor:
     index_base: int = 0
 
 
+def _loco_arr(tensors, device, need_theta=False):
+    arr = (_LocoTensor * max(1, len(tensors)))()
+    for i, t in enumerate(tensors):
+        n = t.delta.numel()
+        arr[i] = _LocoTensor(_f32(t.delta, f"tensor {i} delta", device=device),
+                             _f32(t.residual, f"tensor {i} residual", numel=n, device=device),
+                             _f32(t.theta, f"tensor {i} theta", numel=n, device=device,
+                                  optional=not need_theta),
+                             n, t.index_base)
+    return arr
+
+
 class LocoBatch:
     def __init__(self, tensors: Sequence[LocoTensor]):
         self.n = len(tensors)
-        arr = (_LocoTensor * max(1, self.n))()
-        for i, t in enumerate(tensors):
-            assert t.delta.dtype == torch.float32 and t.residual.dtype == torch.float32
-            assert t.delta.numel() == t.residual.numel()
-            arr[i] = _LocoTensor(_p(t.delta), _p(t.residual), _p(t.theta), t.delta.numel(),
-                                 t.index_base)
-        self.arr = arr
+        self.device = _batch_device(tensors, lambda t: t.delta)
+        self.arr = _loco_arr(tensors, self.device)
         self.keep = list(tensors)
 
     def __call__(self, tau, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
-        _check(lib().pulse_loco_sparsify_batch(self.arr, self.n, float(tau), _p(idx), _p(val),
-                                               cap, _p(count), _p(seg_begin), _p(ws), ws.numel(),
-                                               _stream(stream)), "pulse_loco_sparsify_batch")
+        dev = self.device
+        _f32(val, "val", device=dev)
+        cap = _capacity(idx, val, capacity, 4, 4, dev)
+        pws, nb = _ws(ws, dev)
+        _check(lib().pulse_loco_sparsify_batch(self.arr, self.n, float(tau), idx.data_ptr(),
+                                               val.data_ptr(), cap, _u64(count, "count", dev),
+                                               _u64(seg_begin, "seg_begin", dev, min_numel=self.n,
+                                                    optional=True),
+                                               pws, nb, _stream(stream, dev)),
+               "pulse_loco_sparsify_batch")
 
 
 @dataclass
@@ -322,26 +426,28 @@ class SparseList:
     capacity: Optional[int] = None
 
 
-def _lists(lists: Sequence[SparseList]):
+def _lists(lists: Sequence[SparseList], ntensors: int, device):
     if len(lists) > MAX_LISTS:
         raise PulseError(f"at most {MAX_LISTS} lists per call")
     arr = (_SparseList * max(1, len(lists)))()
     for r, L in enumerate(lists):
-        assert L.idx.element_size() == 4 and L.val.dtype == torch.float32
-        assert L.seg_begin.element_size() == 8 and L.end.element_size() == 8
-        arr[r] = _SparseList(_p(L.idx), _p(L.val), _capacity(L.idx, L.val, L.capacity),
-                             _p(L.seg_begin), _p(L.end))
+        _f32(L.val, f"list {r} val", device=device)
+        cap = _capacity(L.idx, L.val, L.capacity, 4, 4, device)
+        arr[r] = _SparseList(L.idx.data_ptr(), L.val.data_ptr(), cap,
+                             _u64(L.seg_begin, f"list {r} seg_begin", device, min_numel=ntensors),
+                             _u64(L.end, f"list {r} end", device))
     return arr
 
 
 def outer_step(theta: torch.Tensor, momentum: torch.Tensor, lists: Sequence[SparseList],
                mu: float = 0.9, alpha: float = 0.7, index_base: int = 0, stream=None) -> None:
     """PULSELoCo's outer update of one tensor (pulse_outer_step)."""
-    assert theta.dtype == torch.float32 and momentum.dtype == torch.float32
-    assert theta.numel() == momentum.numel()
-    arr = _lists(lists)
-    _check(lib().pulse_outer_step(_p(theta), _p(momentum), theta.numel(), index_base, arr,
-                                  len(lists), float(mu), float(alpha), _stream(stream)),
+    dev = theta.device
+    pt = _f32(theta, "theta")
+    pm = _f32(momentum, "momentum", numel=theta.numel(), device=dev)
+    arr = _lists(lists, 1, dev)
+    _check(lib().pulse_outer_step(pt, pm, theta.numel(), index_base, arr, len(lists), float(mu),
+                                  float(alpha), _stream(stream, dev)),
            "pulse_outer_step")
 
 
@@ -357,19 +463,22 @@ class OuterBatch:
 
     def __init__(self, tensors: Sequence[OuterTensor]):
         self.n = len(tensors)
+        self.device = _batch_device(tensors, lambda t: t.theta)
         arr = (_OuterTensor * max(1, self.n))()
         for i, t in enumerate(tensors):
-            assert t.theta.dtype == torch.float32 and t.momentum.dtype == torch.float32
-            assert t.theta.numel() == t.momentum.numel()
-            arr[i] = _OuterTensor(_p(t.theta), _p(t.momentum), t.theta.numel(), t.index_base)
+            arr[i] = _OuterTensor(_f32(t.theta, f"tensor {i} theta", device=self.device),
+                                  _f32(t.momentum, f"tensor {i} momentum", numel=t.theta.numel(),
+                                       device=self.device),
+                                  t.theta.numel(), t.index_base)
         self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, lists: Sequence[SparseList], mu: float = 0.9, alpha: float = 0.7,
                  stream=None):
-        arr = _lists(lists)
+        dev = self.device
+        arr = _lists(lists, self.n, dev)
         _check(lib().pulse_outer_step_batch(self.arr, self.n, arr, len(lists), float(mu),
-                                            float(alpha), _stream(stream)),
+                                            float(alpha), _stream(stream, dev)),
                "pulse_outer_step_batch")
 
 
@@ -378,28 +487,36 @@ def varint_encode(idx: torch.Tensor, end: torch.Tensor, out: torch.Tensor, total
                   seg_bytes: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
                   stream=None) -> None:
     """Delta-varint stream of a sorted patch's indices (pulse_varint_encode)."""
-    assert idx.element_size() == 4 and out.element_size() == 1
-    assert end.element_size() == 8 and total.element_size() == 8
+    dev = idx.device
+    pi = _p(idx, "idx", esize=4, optional=False)
     cap = idx.numel() if capacity is None else capacity
-    assert 0 <= cap <= idx.numel()
+    if not 0 <= cap <= idx.numel():
+        raise PulseError(f"capacity {cap} exceeds idx ({idx.numel()} entries)")
     nseg = 0 if seg_begin is None else seg_begin.numel()
-    if seg_bytes is not None:
-        assert seg_begin is not None and seg_bytes.numel() >= nseg
-    _check(lib().pulse_varint_encode(_p(idx), cap, _p(end), _p(seg_begin), nseg, _p(out),
-                                     out.numel(), _p(seg_bytes), _p(total), _p(ws), ws.numel(),
-                                     _stream(stream)), "pulse_varint_encode")
+    psb = _u64(seg_begin, "seg_begin", dev, min_numel=0, optional=True)
+    if seg_bytes is not None and seg_begin is None:
+        raise PulseError("seg_bytes needs seg_begin")
+    pby = _u64(seg_bytes, "seg_bytes", dev, min_numel=nseg, optional=True)
+    po = _p(out, "out", esize=1, device=dev, optional=False)
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_varint_encode(pi, cap, _u64(end, "end", dev), psb, nseg, po, out.numel(),
+                                     pby, _u64(total, "total", dev), pws, nb,
+                                     _stream(stream, dev)), "pulse_varint_encode")
 
 
 def varint_decode(stream_bytes: torch.Tensor, nbytes: torch.Tensor, idx: torch.Tensor,
                   count: torch.Tensor, ws: torch.Tensor, seg_begin: Optional[torch.Tensor] = None,
                   stream=None) -> None:
     """Indices back from a delta-varint stream (pulse_varint_decode)."""
-    assert stream_bytes.element_size() == 1 and idx.element_size() == 4
-    assert nbytes.element_size() == 8 and count.element_size() == 8
+    dev = stream_bytes.device
+    pb = _p(stream_bytes, "stream_bytes", esize=1, optional=False)
+    pi = _p(idx, "idx", esize=4, device=dev, optional=False)
     nseg = 0 if seg_begin is None else seg_begin.numel()
-    _check(lib().pulse_varint_decode(_p(stream_bytes), stream_bytes.numel(), _p(nbytes),
-                                     _p(seg_begin), nseg, _p(idx), idx.numel(), _p(count), _p(ws),
-                                     ws.numel(), _stream(stream)), "pulse_varint_decode")
+    psb = _u64(seg_begin, "seg_begin", dev, min_numel=0, optional=True)
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_varint_decode(pb, stream_bytes.numel(), _u64(nbytes, "nbytes", dev), psb,
+                                     nseg, pi, idx.numel(), _u64(count, "count", dev), pws, nb,
+                                     _stream(stream, dev)), "pulse_varint_decode")
 
 
 def coo_encode(idx: torch.Tensor, end: torch.Tensor, seg_begin: torch.Tensor, cols: torch.Tensor,
@@ -407,15 +524,22 @@ def coo_encode(idx: torch.Tensor, end: torch.Tensor, seg_begin: torch.Tensor, co
                seg_pairs: torch.Tensor, total: torch.Tensor, ws: torch.Tensor,
                capacity: Optional[int] = None, stream=None) -> None:
     """2-D COO delta downcast of a sorted patch's indices (pulse_coo_encode)."""
-    assert idx.element_size() == 4 and cols.element_size() == 4 and first.element_size() == 4
-    assert drow.element_size() == 1 and dcol.element_size() == 2
-    assert seg_begin.element_size() == 8 and seg_pairs.element_size() == 8
-    nseg = seg_begin.numel()
-    assert cols.numel() >= nseg and first.numel() >= nseg and seg_pairs.numel() >= nseg
+    dev = idx.device
+    pi = _p(idx, "idx", esize=4, optional=False)
+    nseg = seg_begin.numel() if seg_begin is not None else 0
+    psb = _u64(seg_begin, "seg_begin", dev, min_numel=0)
+    pco = _p(cols, "cols", esize=4, min_numel=nseg, device=dev, optional=False)
+    pfi = _p(first, "first", esize=4, min_numel=nseg, device=dev, optional=False)
+    pdr = _p(drow, "drow", esize=1, device=dev, optional=False)
+    pdc = _p(dcol, "dcol", esize=2, device=dev, optional=False)
+    psp = _u64(seg_pairs, "seg_pairs", dev, min_numel=nseg)
     cap = idx.numel() if capacity is None else capacity
-    _check(lib().pulse_coo_encode(_p(idx), cap, _p(end), _p(seg_begin), nseg, _p(cols), _p(first),
-                                  _p(drow), _p(dcol), min(drow.numel(), dcol.numel()),
-                                  _p(seg_pairs), _p(total), _p(ws), ws.numel(), _stream(stream)),
+    if not 0 <= cap <= idx.numel():
+        raise PulseError(f"capacity {cap} exceeds idx ({idx.numel()} entries)")
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_coo_encode(pi, cap, _u64(end, "end", dev), psb, nseg, pco, pfi, pdr, pdc,
+                                  min(drow.numel(), dcol.numel()), psp, _u64(total, "total", dev),
+                                  pws, nb, _stream(stream, dev)),
            "pulse_coo_encode")
 
 
@@ -424,11 +548,20 @@ def coo_decode(drow: torch.Tensor, dcol: torch.Tensor, npairs: torch.Tensor,
                first: torch.Tensor, nent: torch.Tensor, idx: torch.Tensor,
                ws: torch.Tensor, stream=None) -> None:
     """Indices back from a 2-D COO delta stream (pulse_coo_decode)."""
-    pc = min(drow.numel(), dcol.numel())
-    nseg = seg_begin.numel()
-    _check(lib().pulse_coo_decode(_p(drow), _p(dcol), pc, _p(npairs), _p(seg_begin),
-                                  _p(seg_pairs), nseg, _p(cols), _p(first), _p(nent), _p(idx),
-                                  idx.numel(), _p(ws), ws.numel(), _stream(stream)),
+    dev = idx.device
+    pdr = _p(drow, "drow", esize=1, device=dev, optional=False)
+    pdc = _p(dcol, "dcol", esize=2, device=dev, optional=False)
+    nseg = seg_begin.numel() if seg_begin is not None else 0
+    psb = _u64(seg_begin, "seg_begin", dev, min_numel=0)
+    psp = _u64(seg_pairs, "seg_pairs", dev, min_numel=nseg)
+    pco = _p(cols, "cols", esize=4, min_numel=nseg, device=dev, optional=False)
+    pfi = _p(first, "first", esize=4, min_numel=nseg, device=dev, optional=False)
+    pi = _p(idx, "idx", esize=4, optional=False)
+    pws, nb = _ws(ws, dev)
+    _check(lib().pulse_coo_decode(pdr, pdc, min(drow.numel(), dcol.numel()),
+                                  _u64(npairs, "npairs", dev), psb, psp, nseg, pco, pfi,
+                                  _u64(nent, "nent", dev), pi, idx.numel(), pws, nb,
+                                  _stream(stream, dev)),
            "pulse_coo_decode")
 
 
@@ -436,20 +569,25 @@ def lowp_sizes(dtype: int, n: int):
     """(code bytes, scale bytes) of one tensor's D view."""
     if dtype == FP8_E4M3:
         return n, 0
-    return (n + 1) // 2, (n + 31) // 32
+    if dtype == MXFP4:
+        return (n + 1) // 2, (n + 31) // 32
+    raise PulseError(f"unknown receiver dtype {dtype}")
 
 
 def cast_lowp(dtype: int, src: torch.Tensor, inv_scale: float = 1.0, codes=None, scales=None,
               stream=None):
     """Dense D view of an FP32 tensor: (codes uint8, scales uint8 or None)."""
-    assert src.dtype == torch.float32 and src.is_contiguous()
+    dev = src.device
+    ps = _f32(src, "src")
     nc, ns = lowp_sizes(dtype, src.numel())
     if codes is None:
-        codes = torch.empty(max(nc, 1), dtype=torch.uint8, device=src.device)
+        codes = torch.empty(max(nc, 1), dtype=torch.uint8, device=dev)
     if scales is None and dtype == MXFP4:
-        scales = torch.empty(max(ns, 1), dtype=torch.uint8, device=src.device)
-    _check(lib().pulse_cast_lowp(dtype, _p(src), src.numel(), float(inv_scale), _p(codes),
-                                 _p(scales), _stream(stream)), "pulse_cast_lowp")
+        scales = torch.empty(max(ns, 1), dtype=torch.uint8, device=dev)
+    pc = _p(codes, "codes", esize=1, min_numel=nc, device=dev, optional=False)
+    psc = _p(scales, "scales", esize=1, min_numel=ns, device=dev, optional=dtype != MXFP4)
+    _check(lib().pulse_cast_lowp(dtype, ps, src.numel(), float(inv_scale), pc, psc,
+                                 _stream(stream, dev)), "pulse_cast_lowp")
     return codes, scales
 
 
@@ -467,19 +605,30 @@ class EncodeLowpBatch:
 
     def __init__(self, dtype: int, tensors: Sequence[LowpTensor]):
         self.dtype, self.n = dtype, len(tensors)
+        self.device = _batch_device(tensors, lambda t: t.w_new)
         arr = (_LowpTensor * max(1, self.n))()
         for i, t in enumerate(tensors):
-            assert t.w_new.dtype == torch.float32 and t.snap.element_size() == 1
-            arr[i] = _LowpTensor(_p(t.w_new), _p(t.snap), _p(t.snap_scales), t.w_new.numel(),
-                                 t.index_base, float(t.inv_scale))
+            n = t.w_new.numel()
+            nc, ns = lowp_sizes(dtype, n)
+            arr[i] = _LowpTensor(_f32(t.w_new, f"tensor {i} w_new", device=self.device),
+                                 _p(t.snap, f"tensor {i} snap", esize=1, min_numel=nc,
+                                    device=self.device, optional=False),
+                                 _p(t.snap_scales, f"tensor {i} snap_scales", esize=1,
+                                    min_numel=ns, device=self.device, optional=dtype != MXFP4),
+                                 n, t.index_base, float(t.inv_scale))
         self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
-        _check(lib().pulse_encode_lowp_batch(self.dtype, self.arr, self.n, _p(idx), _p(val), cap,
-                                             _p(count), _p(seg_begin), _p(ws), ws.numel(),
-                                             _stream(stream)), "pulse_encode_lowp_batch")
+        dev = self.device
+        cap = _capacity(idx, val, capacity, 4, 1 if self.dtype == FP8_E4M3 else 2, dev)
+        pws, nb = _ws(ws, dev)
+        _check(lib().pulse_encode_lowp_batch(self.dtype, self.arr, self.n, idx.data_ptr(),
+                                             val.data_ptr(), cap, _u64(count, "count", dev),
+                                             _u64(seg_begin, "seg_begin", dev, min_numel=self.n,
+                                                  optional=True),
+                                             pws, nb, _stream(stream, dev)),
+               "pulse_encode_lowp_batch")
 
 
 @dataclass
@@ -493,17 +642,27 @@ class LowpApplyTensor:
 class ApplyLowpBatch:
     def __init__(self, dtype: int, tensors: Sequence[LowpApplyTensor]):
         self.dtype, self.n = dtype, len(tensors)
+        self.device = _batch_device(tensors, lambda t: t.codes)
         arr = (_LowpApplyTensor * max(1, self.n))()
         for i, t in enumerate(tensors):
-            arr[i] = _LowpApplyTensor(_p(t.codes), _p(t.scales), t.n, t.index_base)
+            nc, ns = lowp_sizes(dtype, t.n)
+            arr[i] = _LowpApplyTensor(_p(t.codes, f"tensor {i} codes", esize=1, min_numel=nc,
+                                         device=self.device, optional=False),
+                                      _p(t.scales, f"tensor {i} scales", esize=1, min_numel=ns,
+                                         device=self.device, optional=dtype != MXFP4),
+                                      t.n, t.index_base)
         self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, idx, val, seg_begin, end, rejected=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
-        _check(lib().pulse_apply_lowp_batch(self.dtype, self.arr, self.n, _p(idx), _p(val), cap,
-                                            _p(seg_begin), _p(end), _p(rejected),
-                                            _stream(stream)), "pulse_apply_lowp_batch")
+        dev = self.device
+        cap = _capacity(idx, val, capacity, 4, 1 if self.dtype == FP8_E4M3 else 2, dev)
+        _check(lib().pulse_apply_lowp_batch(self.dtype, self.arr, self.n, idx.data_ptr(),
+                                            val.data_ptr(), cap,
+                                            _u64(seg_begin, "seg_begin", dev, min_numel=self.n),
+                                            _u64(end, "end", dev),
+                                            _u64(rejected, "rejected", dev, optional=True),
+                                            _stream(stream, dev)), "pulse_apply_lowp_batch")
 
 
 class LocoLowpBatch:
@@ -511,22 +670,25 @@ class LocoLowpBatch:
 
     def __init__(self, dtype: int, tensors: Sequence[LocoTensor], inv_scales=None):
         self.dtype, self.n = dtype, len(tensors)
-        arr = (_LocoTensor * max(1, self.n))()
-        for i, t in enumerate(tensors):
-            assert t.theta is not None
-            arr[i] = _LocoTensor(_p(t.delta), _p(t.residual), _p(t.theta), t.delta.numel(),
-                                 t.index_base)
+        self.device = _batch_device(tensors, lambda t: t.delta)
+        self.arr = _loco_arr(tensors, self.device, need_theta=True)
         sc = list(inv_scales) if inv_scales is not None else [1.0] * self.n
+        if len(sc) != self.n:
+            raise PulseError(f"{len(sc)} inv_scales for {self.n} tensors")
         self.scales = (ctypes.c_float * max(1, self.n))(*sc)
-        self.arr = arr
         self.keep = list(tensors)
 
     def __call__(self, idx, val, count, ws, seg_begin=None, capacity=None, stream=None):
-        cap = _capacity(idx, val, capacity)
+        dev = self.device
+        _f32(val, "val", device=dev)
+        cap = _capacity(idx, val, capacity, 4, 4, dev)
+        pws, nb = _ws(ws, dev)
         _check(lib().pulse_loco_sparsify_lowp_batch(self.dtype, self.arr, self.scales, self.n,
-                                                    _p(idx), _p(val), cap, _p(count),
-                                                    _p(seg_begin), _p(ws), ws.numel(),
-                                                    _stream(stream)),
+                                                    idx.data_ptr(), val.data_ptr(), cap,
+                                                    _u64(count, "count", dev),
+                                                    _u64(seg_begin, "seg_begin", dev,
+                                                         min_numel=self.n, optional=True),
+                                                    pws, nb, _stream(stream, dev)),
                "pulse_loco_sparsify_lowp_batch")
 
 
@@ -544,13 +706,17 @@ class HashBatch:
 
     def __init__(self, tensors: Sequence[torch.Tensor], device=None):
         self.n = len(tensors)
+        dev = device or (tensors[0].device if tensors else torch.device("cuda"))
+        dev = torch.device(dev)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
         arr = (_HashTensor * max(1, self.n))()
         total = 0
         for i, t in enumerate(tensors):
-            assert _is16(t) and t.is_contiguous()
-            arr[i] = _HashTensor(_p(t) if t.numel() else None, t.numel())
+            ptr = _u16(t, f"tensor {i}", device=dev)
+            arr[i] = _HashTensor(ptr if t.numel() else None, t.numel())
             total += t.numel()
-        dev = device or (tensors[0].device if tensors else "cuda")
+        self.device = dev
         self.arr = arr
         self.keep = list(tensors)
         self.total = total
@@ -562,8 +728,9 @@ class HashBatch:
         self.root = torch.empty(32, dtype=torch.uint8, device=dev)
 
     def __call__(self, stream=None) -> torch.Tensor:
-        _check(lib().pulse_hash_tree(self.arr, self.n, _p(self.leaves), _p(self.root),
-                                     _p(self.ws), self.ws.numel(), _stream(stream)),
+        _check(lib().pulse_hash_tree(self.arr, self.n, self.leaves.data_ptr(),
+                                     self.root.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+                                     _stream(stream, self.device)),
                "pulse_hash_tree")
         return self.root
 

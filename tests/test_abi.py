@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 23, names
+    assert len(names) == 24, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name
@@ -39,8 +39,16 @@ def test_exports_every_declared_function(L):
 
 def test_strerror_and_workspace(L):
     assert L.pulse_workspace_bytes() >= 8 * (1 << 16)
-    for rc in (OK, EINVAL, ERANGE, EALIGN, -4):
+    for rc in (OK, EINVAL, ERANGE, EALIGN, -4, pulse.ESTATE):
         assert L.pulse_strerror(rc).decode().startswith("PULSE_")
+    assert b"ESTATE" in L.pulse_strerror(pulse.ESTATE)
+
+
+def test_workspace_status_validation(L):
+    wsb = L.pulse_workspace_bytes()
+    assert L.pulse_workspace_status(None, wsb, None) == EINVAL
+    assert L.pulse_workspace_status(A * 8 + 16, wsb, None) == EALIGN
+    assert L.pulse_workspace_status(A * 8, wsb - 1, None) == EINVAL
 
 
 A = 1 << 20  # fake, 16-byte-aligned "device" address (never touched)
