@@ -55,6 +55,20 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+def build_selfcheck(sanitize: bool = False) -> str:
+    """Compile oracle/selfcheck.c with oracle.c into an executable next to them
+    (with -fsanitize=address,undefined when `sanitize`); it runs the oracle's
+    pins in C and exits 0 when all pass (usage: selfcheck <tests/golden dir>)."""
+    exe = os.path.join(_HERE, "selfcheck_asan" if sanitize else "selfcheck")
+    flags = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=all", "-static-libasan", "-static-libubsan"] if sanitize else ["-O2"]
+    tmp = exe + f".tmp{os.getpid()}"
+    subprocess.check_call(["gcc", "-ffp-contract=off", "-fno-fast-math", "-Wall", *flags, "-o", tmp,
+                           _SRC, os.path.join(_HERE, "selfcheck.c"), "-lm"])
+    os.replace(tmp, exe)
+    return exe
+
+
 def _load():
     global _lib
     with _lock:

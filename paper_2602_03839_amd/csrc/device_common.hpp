@@ -53,6 +53,12 @@ constexpr uint64_t kSlots = 1ull << kSlotBits;
 constexpr int kStatusOffsetWords = 64;            // 512-byte header
 constexpr size_t kWorkspaceBytes = (kStatusOffsetWords + kSlots) * sizeof(uint64_t);
 constexpr uint32_t kMaxTilesPerLaunch = (1u << kTicketBits) - 1;  // < kNoTicket
+// Largest grid of a ticketed launch.  Every block makes one draw past the last
+// tile, so a kernel that draws one tile per ticket (the index-stream kernels)
+// makes up to ntiles + grid draws, all of which must fit the ticket field:
+// those kernels take at most kMaxTicketedTiles tiles per launch.
+constexpr uint32_t kMaxGrid = 1u << 16;
+constexpr uint32_t kMaxTicketedTiles = kMaxTilesPerLaunch - kMaxGrid;
 
 // status word: [63:62] flag, [61:54] lap tag, [53:0] value
 constexpr uint64_t kFlagAggregate = 1;  // value = this tile's own count
@@ -617,7 +623,8 @@ inline int persistent_grid(const void* kernel, int block) {
   int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, 0) != hipSuccess) return 0;
-  const int grid = cus * (per_cu > 0 ? per_cu : 1);
+  int grid = cus * (per_cu > 0 ? per_cu : 1);
+  if (grid > (int)kMaxGrid) grid = (int)kMaxGrid;
   std::lock_guard<std::mutex> g(mu);
   if (used < 64) cache[used++] = Entry{kernel, dev, block, grid};
   return grid;

@@ -446,7 +446,7 @@ int pulse_varint_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* 
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
   const uint64_t tile = pulse::varint_entry_tile();
   const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "varint encode: capacity too large");
+  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "varint encode: capacity too large");
   pulse::VarintEncParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -477,7 +477,7 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   const uint64_t bt = pulse::varint_byte_tile(), et = pulse::varint_entry_tile();
   const uint64_t nt = in_capacity == 0 ? 1 : (in_capacity + bt - 1) / bt;
   const uint64_t nt2 = capacity == 0 ? 1 : (capacity + et - 1) / et;
-  if (nt > pulse::kMaxTilesPerLaunch || nt2 > pulse::kMaxTilesPerLaunch)
+  if (nt > pulse::kMaxTicketedTiles || nt2 > pulse::kMaxTicketedTiles)
     return fail(PULSE_EINVAL, "varint decode: capacity too large");
   pulse::VarintDecParams p;
   memset(&p, 0, sizeof p);
@@ -512,7 +512,7 @@ int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
   const uint64_t tile = pulse::varint_entry_tile();
   const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "coo encode: capacity too large");
+  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "coo encode: capacity too large");
   pulse::CooEncParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -550,7 +550,7 @@ int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_ca
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
   const uint64_t tile = pulse::varint_entry_tile();
   const uint64_t nt = pair_capacity == 0 ? 1 : (pair_capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTilesPerLaunch) return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
+  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
   pulse::CooDecParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;

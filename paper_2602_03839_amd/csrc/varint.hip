@@ -825,7 +825,8 @@ static uint32_t varint_grid(uint32_t ntiles) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  const uint32_t cap = (uint32_t)(cus > 0 ? cus : 1) * 4u;
+  uint32_t cap = (uint32_t)(cus > 0 ? cus : 1) * 4u;
+  if (cap > kMaxGrid) cap = kMaxGrid;
   return ntiles < cap ? ntiles : cap;
 }
 

@@ -96,6 +96,26 @@ def test_mxfp4_cast(n):
     np.testing.assert_array_equal(u8(codes)[: oc.size], oc)
 
 
+@pytest.mark.gpu
+def test_mxfp4_cast_golden_blocks():
+    """The hand-worked OCP MX blocks, each alone and all 12 as one tensor
+    padded to 32 values per block: scale bytes and codes as written."""
+    from test_oracle_lowp import mx_golden
+    cases = mx_golden()
+    for x, scale, want in cases:
+        codes, scales = pulse.cast_lowp(MX, dev(x))
+        assert int(scales[0].item()) == scale, x
+        assert [int(v) for v in oracle.mx_codes(codes.cpu().numpy(), x.size)] == want, x
+    padded = np.zeros(32 * len(cases), dtype=np.float32)
+    for b, (x, _s, _c) in enumerate(cases):
+        padded[32 * b: 32 * b + x.size] = x
+    codes, scales = pulse.cast_lowp(MX, dev(padded))
+    got = oracle.mx_codes(codes.cpu().numpy(), padded.size)
+    for b, (x, scale, want) in enumerate(cases):
+        assert int(scales[b].item()) == scale, x
+        assert [int(v) for v in got[32 * b: 32 * b + x.size]] == want, x
+
+
 def test_mxfp4_cast_every_block_exponent():
     """Blocks whose largest magnitude has every exponent field 0..255 (E from
     -127, clamped, to 126, and infinity), the others drawn over a wide range

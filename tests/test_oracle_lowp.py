@@ -8,6 +8,9 @@ other than itself.
 * MXFP4: a second formulation written here with exact fractions (block
   exponent from frexp, nearest E2M1 magnitude, ties to the even code) on
   random, ragged, zero, subnormal, infinite and NaN blocks.
+* MXFP4: blocks worked by hand from the OCP MX v1.0 conversion rule
+  (tests/golden/mxfp4_examples.txt), each chosen so that the shared exponent
+  E and E + 1 give different scale bytes and codes.
 * The paper's own numbers: Table T-ULP-Scale's tau_D = 2^-(m_D + 1) as the
   relative change a value at a binade start (for MXFP4: at the block maximum)
   absorbs, and |w|_crit = eta / tau_D as printed (tests/golden/tulpscale.txt).
@@ -24,6 +27,19 @@ import torch
 import oracle
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "tulpscale.txt")
+MX_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "mxfp4_examples.txt")
+
+
+def mx_golden():
+    """(values float32, scale byte, codes) of each hand-worked MXFP4 block."""
+    out = []
+    for line in open(MX_GOLDEN):
+        if line.startswith("#") or not line.strip():
+            continue
+        v, sb, cs = (x.strip() for x in line.split("|"))
+        x = np.array([float(t) for t in v.split(",")], dtype=np.float32)
+        out.append((x, int(sb), [int(t, 16) for t in cs.split()]))
+    return out
 
 
 def torch_fp8(y: np.ndarray) -> np.ndarray:
@@ -119,6 +135,16 @@ def mx_blocks(rng):
     for _ in range(60):
         out.append(rng.standard_normal(int(rng.integers(1, 33))) * 10.0 ** rng.integers(-8, 8))
     return [np.asarray(b, dtype=np.float32) for b in out]
+
+
+def test_mxfp4_golden_blocks():
+    cases = mx_golden()
+    assert len(cases) == 12
+    for x, scale, codes in cases:
+        assert len(codes) == x.size
+        c, sc = oracle.cast_mxfp4(x)
+        assert int(sc[0]) == scale, x
+        assert [int(v) for v in oracle.mx_codes(c, x.size)] == codes, x
 
 
 def test_mxfp4_matches_fraction_reference():
