@@ -99,3 +99,83 @@ def generated_patch(key: str, density: float, seed: int, device="cuda"):
     seg = torch.tensor(segs[:-1], dtype=torch.int64, device=device)
     count = torch.tensor([segs[-1]], dtype=torch.int64, device=device)
     return idx, seg, count, segs, specs
+
+
+class HostPool:
+    """Runs oracle checks of many tensors on host threads (the oracle's ctypes
+    calls release the GIL), with the host memory held by queued work bounded.
+
+    submit(nbytes, fn, *args): waits until `nbytes` fit the budget, then runs
+    fn(*args) on a worker; fn returns None or an error message.  close()
+    waits for everything and returns the messages.
+    """
+
+    def __init__(self, workers: int = 12, budget_bytes: float = 64e9):
+        import os
+        import threading
+        from concurrent.futures import ThreadPoolExecutor
+        workers = max(1, min(workers, (os.cpu_count() or 4)))
+        self.ex = ThreadPoolExecutor(max_workers=workers)
+        self.cv = threading.Condition()
+        self.budget = budget_bytes
+        self.used = 0.0
+        self.futs = []
+
+    def submit(self, nbytes: float, fn, *args):
+        nbytes = min(nbytes, self.budget)
+        with self.cv:
+            self.cv.wait_for(lambda: self.used + nbytes <= self.budget)
+            self.used += nbytes
+
+        def run():
+            try:
+                return fn(*args)
+            except Exception as e:  # reported, not raised in the worker
+                return f"{type(e).__name__}: {e}"
+            finally:
+                with self.cv:
+                    self.used -= nbytes
+                    self.cv.notify_all()
+
+        self.futs.append(self.ex.submit(run))
+
+    def close(self):
+        errs = [f.result() for f in self.futs]
+        self.ex.shutdown()
+        return [e for e in errs if e]
+
+
+def encode_parity_job(name, w, s, base, g_idx, g_val, g_r):
+    """Oracle encode (with refresh) of one tensor against the GPU's patch
+    segment and refreshed copy; None when all agree."""
+    import oracle
+    nnz = g_idx.size
+    r = s.copy()
+    cnt, oi, ov = oracle.encode(w, s, index_base=base, capacity=nnz, refresh=r)
+    if cnt != nnz:
+        return f"{name}: count {nnz} vs oracle {cnt}"
+    if not np.array_equal(g_idx, oi[:cnt]):
+        return f"{name}: indices differ"
+    if not np.array_equal(g_val, ov[:cnt]):
+        return f"{name}: values differ"
+    if g_r is not None and not np.array_equal(g_r, r):
+        k = int(np.argmax(g_r != r))
+        return f"{name}: refreshed copy differs first at {k}: {g_r[k]:#06x} vs {r[k]:#06x}"
+    return None
+
+
+def loco_parity_job(name, delta, resid_in, tau, base, g_idx, g_val, g_res):
+    """Oracle sparsify of one tensor (residual resid_in, updated in place)
+    against the GPU's patch segment and residual; None when all agree."""
+    import oracle
+    nnz = g_idx.size
+    cnt, oi, ov = oracle.loco(delta, resid_in, tau, index_base=base, capacity=nnz)
+    if cnt != nnz:
+        return f"{name}: count {nnz} vs oracle {cnt}"
+    if not np.array_equal(g_idx, oi[:cnt]):
+        return f"{name}: indices differ"
+    if not np.array_equal(g_val.view(np.uint32), ov[:cnt].view(np.uint32)):
+        return f"{name}: values differ"
+    if not np.array_equal(g_res.view(np.uint32), resid_in.view(np.uint32)):
+        return f"{name}: residual differs"
+    return None

@@ -245,3 +245,20 @@ def test_stream_validation(L):
     assert cd(A, A + 1, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # dcol
     assert cd(A, A, big, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EINVAL     # tiles
     assert b"coo decode" in L.pulse_last_error()
+
+
+def test_binding_rejects_host_tensors(L):
+    """The binding checks tensors before calling the library: host tensors are
+    refused (this runs without a GPU: nothing reaches a kernel)."""
+    import torch
+    w = torch.zeros(16, dtype=torch.float32)
+    s = torch.zeros(16, dtype=torch.int16)
+    with pytest.raises(pulse.PulseError, match="device tensor"):
+        pulse.cast_bf16(w)
+    with pytest.raises(pulse.PulseError, match="device tensor"):
+        pulse.encode(w, s, torch.zeros(16, dtype=torch.int32), s.clone(),
+                     torch.zeros(1, dtype=torch.int64), torch.zeros(8, dtype=torch.uint8))
+    with pytest.raises(pulse.PulseError, match="device tensor"):
+        pulse.EncodeBatch([pulse.EncodeTensor(w, s)])
+    with pytest.raises(pulse.PulseError, match="torch.Tensor"):
+        pulse.cast_bf16([0.0, 1.0])

@@ -2,15 +2,25 @@
 times: batches of <= 64 tensors, a patch buffer sized for 5% of the set (10%
 for the sparsifier), one workspace for every launch.
 
-* the 0.5B-shaped set (494,005,120 params, flat uint32 indices) is compared with
-  the oracle in full, element by element, including the fused refresh.
-* the 7B-shaped chains (20 steps at lr 3e-7, 1e-6, 3e-6), the 32B-shaped set
-  (one fused step at lr 1e-6) and the 7B-shaped PULSELoCo run (10 rounds) are too large
-  for the oracle in test time.  They are checked
-    (a) at full size against the definition, computed on the GPU with torch's
-        own BF16 cast, comparison, nonzero and FP32 add (no kernel of this
-        library takes part), and
-    (b) on sampled windows, element by element, against the oracle.
+Three forms of the fused refresh are covered: one 2-byte write per change
+("sparse"), whole 128-byte lines of an inference copy that mirrors the
+snapshot ("mirror", the form the benchmark times) and the snapshot refreshed
+in place ("inplace", the chainable form).
+
+* the 0.5B-shaped set (494,005,120 params, flat uint32 indices): every form is
+  compared with the oracle in full, element by element.
+* the 32B-shaped set (one fused step at lr 1e-6): the mirror form is compared
+  with the oracle in full (every tensor's patch segment and refreshed copy,
+  streamed through host threads); the in-place form must give the same patch
+  and leave the snapshot equal to the oracle-checked copy.
+* the 7B-shaped chains (20 steps at lr 3e-7, 1e-6, 3e-6, one refresh form
+  each): every step is checked at full size against the definition, computed
+  on the GPU with torch's own BF16 cast, comparison and nonzero (no kernel of
+  this library takes part), sampled windows against the oracle at steps 1 and
+  20, and step 20 against the oracle in full.
+* the 7B-shaped PULSELoCo run (10 rounds): every round against the definition
+  (torch's FP32 add and compare) at full size, windows against the oracle
+  with its own residual every round, and round 1 against the oracle in full.
 
 Snapshots come from torch's BF16 cast of the masters, so no input of either
 side is produced by the library under test.
@@ -20,6 +30,7 @@ import pytest
 import torch
 
 import oracle
+from gpu_helpers import HostPool, encode_parity_job, loco_parity_job
 from paper_2602_03839_amd import pulse
 from paper_2602_03839_amd import workloads as wl
 
@@ -83,12 +94,40 @@ class ModelSet:
         return out
 
 
-def encode_set(ms, w, S, R, idx, val, count, seg, ws):
+def encode_set(ms, w, S, R, idx, val, count, seg, ws, mirror=False):
+    """One fused step over the set; R may be None, a separate copy (mirror:
+    it equals S on entry, whole-line refresh) or S itself (in place)."""
     count.zero_()
     for a, b in chunks(ms.T):
         pulse.EncodeBatch([pulse.EncodeTensor(ms.view(w, i), ms.view(S, i),
-                                              None if R is None else ms.view(R, i), ms.base(i))
+                                              None if R is None else ms.view(R, i), ms.base(i),
+                                              mirror)
                            for i in range(a, b)])(idx, val, count, ws, seg_begin=seg[a:])
+    pulse.check_workspace(ws)
+
+
+def refresh_target(form, S):
+    """The refresh copy of a form, and whether it mirrors the snapshot."""
+    if form == "inplace":
+        return S, False
+    return S.clone(), form == "mirror"
+
+
+def full_encode_parity(ms, w, S_in, R, idx, val, segs, workers=12):
+    """Every tensor's patch segment and refreshed copy against the oracle's
+    encode of (w, S_in), streamed tensor by tensor through host threads."""
+    pool = HostPool(workers=workers)
+    for i in range(ms.T):
+        lo, hi = segs[i], segs[i + 1]
+        hw = ms.view(w, i).cpu().numpy()
+        hs = ms.view(S_in, i).cpu().numpy().view(np.uint16)
+        gi = idx[lo:hi].cpu().numpy().view(np.uint32)
+        gv = val[lo:hi].cpu().numpy().view(np.uint16)
+        gr = ms.view(R, i).cpu().numpy().view(np.uint16)
+        pool.submit(hw.nbytes + 2 * hs.nbytes + 3 * gi.nbytes, encode_parity_job, f"tensor {i}",
+                    hw, hs, ms.base(i), gi, gv, gr)
+    errs = pool.close()
+    assert not errs, errs[:5]
 
 
 def segments(seg, count):
@@ -130,28 +169,29 @@ def fresh_memory():
     torch.cuda.empty_cache()
 
 
-def test_05b_full_oracle_parity(fresh_memory):
+@pytest.mark.parametrize("form", ["sparse", "mirror", "inplace"])
+def test_05b_full_oracle_parity(fresh_memory, form):
     """0.5B-shaped set, one fused step at lr 1e-6: patch, segments and refreshed copy
-    equal the oracle's for all 494,005,120 parameters."""
+    equal the oracle's for all 494,005,120 parameters, in each refresh form."""
     oracle.build()
     ms = ModelSet("0.5b")
     w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
     S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
     ms.init(w, S)
     ms.step(w, 1e-6, 1)
-    R = S.clone()
+    h_w, h_s = w.cpu().numpy(), S.cpu().numpy().view(np.uint16)  # inputs, before the step
+    R, mirror = refresh_target(form, S)
     cap = ms.N // 20
     idx = torch.empty(cap, dtype=torch.int32, device="cuda")
     val = torch.empty(cap, dtype=torch.int16, device="cuda")
     count = torch.zeros(1, dtype=torch.int64, device="cuda")
     seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
     ws = pulse.workspace()
-    encode_set(ms, w, S, R, idx, val, count, seg, ws)
+    encode_set(ms, w, S, R, idx, val, count, seg, ws, mirror)
     torch.cuda.synchronize()
     segs = segments(seg, count)
     nnz = segs[-1]
     assert 0.007 < nnz / ms.N < 0.012
-    h_w, h_s = w.cpu().numpy(), S.cpu().numpy().view(np.uint16)
     h_idx = idx[:nnz].cpu().numpy().view(np.uint32)
     h_val = val[:nnz].cpu().numpy().view(np.uint16)
     h_r = R.cpu().numpy().view(np.uint16)
@@ -170,17 +210,19 @@ def test_05b_full_oracle_parity(fresh_memory):
     np.testing.assert_array_equal(h_r, o_r)
 
 
-@pytest.mark.parametrize("lr", [3e-7, 1e-6, 3e-6])
-def test_7b_twenty_step_chain(fresh_memory, lr):
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("lr,form", [(3e-7, "sparse"), (1e-6, "inplace"), (3e-6, "mirror")])
+def test_7b_twenty_step_chain(fresh_memory, lr, form):
     """7B-shaped set, 20 consecutive steps; each step's snapshot is the copy the
-    previous patches refreshed.  The standalone apply keeps a second copy."""
+    previous patches refreshed (in place, or a separate copy that the next step
+    takes as its snapshot).  The standalone apply keeps a second copy."""
     oracle.build()
     ms = ModelSet("7b")
     rng = np.random.default_rng(int(lr * 1e9))
     w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
     S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
     ms.init(w, S)
-    R = S.clone()  # refreshed by the fused encode
+    R, mirror = refresh_target(form, S)  # refreshed by the fused encode
     Q = S.clone()  # written by the standalone apply
     cap = ms.N // 20
     idx = torch.empty(cap, dtype=torch.int32, device="cuda")
@@ -196,15 +238,19 @@ def test_7b_twenty_step_chain(fresh_memory, lr):
         sample = t in (1, 20)
         if sample:  # the oracle's snapshot: its own cast of w_{t-1} (a generated input)
             prev = [ww[0] for ww in host_windows(ms, wins, w)]
+        if t == 20:  # the full check's snapshot: torch's cast of w_19
+            S_or = bf16_bits(w)
         ms.step(w, lr, t)
         if sample:
             hw = [(ww[0], oracle.cast(p)) for ww, p in zip(host_windows(ms, wins, w), prev)]
-        encode_set(ms, w, S, R, idx, val, count, seg, ws)
+        S_prev = S.clone() if form == "inplace" else S  # the step's snapshot
+        encode_set(ms, w, S, R, idx, val, count, seg, ws, mirror)
         apply(idx, val, seg, count, rejected=rejected)
         segs = segments(seg, count)
         assert segs[-1] <= cap
         dens.append(segs[-1] / ms.N)
-        check_encode_definition(ms, w, S, idx, val, segs)
+        check_encode_definition(ms, w, S_prev, idx, val, segs)
+        del S_prev
         if sample:
             for (i, a, e), (ww, ss) in zip(wins, hw):
                 r = ss.copy()
@@ -213,7 +259,11 @@ def test_7b_twenty_step_chain(fresh_memory, lr):
                 np.testing.assert_array_equal(gi, oi[:cnt])
                 np.testing.assert_array_equal(gv.view(np.uint16), ov[:cnt])
                 np.testing.assert_array_equal(ms.view(R, i)[a:e].cpu().numpy().view(np.uint16), r)
-        S.copy_(R)  # the next snapshot is the patched copy
+        if t == 20:
+            full_encode_parity(ms, w, S_or, R, idx, val, segs)
+            del S_or
+        if form != "inplace":
+            S.copy_(R)  # the next snapshot is the patched copy
     assert int(rejected.item()) == 0
     for i in range(ms.T):
         want = bf16_bits(ms.view(w, i))
@@ -223,11 +273,14 @@ def test_7b_twenty_step_chain(fresh_memory, lr):
     assert lo < dens[0] < hi, dens[0]
 
 
-def test_32b_single_fused_step(fresh_memory):
-    """32B-shaped set resident on one GPU: one fused encode+refresh step at lr 1e-6."""
+@pytest.mark.timeout(900)
+def test_32b_full_oracle_parity(fresh_memory):
+    """32B-shaped set resident on one GPU: one fused step at lr 1e-6 in the form
+    the benchmark times (an inference copy that mirrors the snapshot), compared
+    with the oracle over all 32,763,417,600 parameters; then the in-place form
+    must emit the same patch and leave the snapshot equal to that copy."""
     oracle.build()
     ms = ModelSet("32b")
-    rng = np.random.default_rng(4)
     w = torch.empty(ms.N, dtype=torch.float32, device="cuda")
     S = torch.empty(ms.N, dtype=torch.int16, device="cuda")
     ms.init(w, S)
@@ -239,27 +292,27 @@ def test_32b_single_fused_step(fresh_memory):
     count = torch.zeros(1, dtype=torch.int64, device="cuda")
     seg = torch.zeros(ms.T, dtype=torch.int64, device="cuda")
     ws = pulse.workspace()
-    wins = ms.windows(rng)
-    hw = host_windows(ms, wins, w, S)
-    encode_set(ms, w, S, R, idx, val, count, seg, ws)
+    encode_set(ms, w, S, R, idx, val, count, seg, ws, mirror=True)
     segs = segments(seg, count)
-    assert 0.007 < segs[-1] / ms.N < 0.012 and segs[-1] <= cap
-    check_encode_definition(ms, w, S, idx, val, segs)
+    nnz = segs[-1]
+    assert 0.007 < nnz / ms.N < 0.012 and nnz <= cap
+    full_encode_parity(ms, w, S, R, idx, val, segs)
+    # the chainable form: same patch, snapshot advanced to the checked copy
+    ref_seg = seg.clone()
+    ref_idx, ref_val = idx[:nnz].clone(), val[:nnz].clone()
+    encode_set(ms, w, S, S, idx, val, count, seg, ws)
+    assert int(count.item()) == nnz
+    assert torch.equal(seg, ref_seg)
+    assert torch.equal(idx[:nnz], ref_idx) and torch.equal(val[:nnz], ref_val)
     for i in range(ms.T):
-        assert torch.equal(ms.view(R, i), bf16_bits(ms.view(w, i))), i
-    for (i, a, e), (ww, ss) in zip(wins, hw):
-        ss = ss.view(np.uint16)
-        r = ss.copy()
-        cnt, oi, ov = oracle.encode(ww, ss, index_base=a, refresh=r)
-        gi, gv = gpu_entries(ms, idx, val, segs, i, a, e)
-        np.testing.assert_array_equal(gi, oi[:cnt])
-        np.testing.assert_array_equal(gv.view(np.uint16), ov[:cnt])
-        np.testing.assert_array_equal(ms.view(R, i)[a:e].cpu().numpy().view(np.uint16), r)
+        assert torch.equal(ms.view(S, i), ms.view(R, i)), i
 
 
+@pytest.mark.timeout(900)
 def test_7b_loco_ten_rounds(fresh_memory):
     """PULSELoCo on the 7B-shaped set: 10 rounds at a fixed tau, residual carried
-    in FP32; every round's patch and residual are bit-exact."""
+    in FP32; every round's patch and residual are bit-exact (round 1 against the
+    oracle over all 7,615,487,488 parameters)."""
     oracle.build()
     ms = ModelSet("7b")
     rng = np.random.default_rng(5)
@@ -301,6 +354,16 @@ def test_7b_loco_ten_rounds(fresh_memory):
             assert torch.equal(val[lo:hi].view(torch.int32), s[nz].view(torch.int32)), (r, i)
             want = torch.where(sel, torch.zeros_like(s), s)
             assert torch.equal(ms.view(e, i).view(torch.int32), want.view(torch.int32)), (r, i)
+        if r == 0:  # the whole set against the oracle (its residual starts at 0)
+            pool = HostPool(workers=12)
+            for i in range(ms.T):
+                lo, hi = segs[i], segs[i + 1]
+                hdl = ms.view(d, i).cpu().numpy()
+                pool.submit(4 * hdl.nbytes, loco_parity_job, f"tensor {i}", hdl,
+                            np.zeros_like(hdl), tau, 0, idx[lo:hi].cpu().numpy().view(np.uint32),
+                            val[lo:hi].cpu().numpy(), ms.view(e, i).cpu().numpy())
+            errs = pool.close()
+            assert not errs, errs[:5]
         for (i, a, ee), dd, res in zip(wins, hd, o_res):
             cnt, oi, ov = oracle.loco(dd, res, tau, index_base=a)
             gi, gv = gpu_entries(ms, idx, val, segs, i, a, ee)

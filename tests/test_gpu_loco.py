@@ -14,7 +14,8 @@ from tests.gpu_helpers import counter, dev, h32, hf32, read_count
 
 pytestmark = pytest.mark.gpu
 
-TILE = 960 * 1 * 8  # sparsify tile (elements) of the default build
+TILE = 960 * 2 * 8  # sparsify tile (elements) of the threshold form
+GATE_TILE = 960 * 1 * 8  # and of the gate forms
 EDGES = sorted({m * t + d for t in (7680, 15360) for m in (1, 3) for d in (-1, 0, 1)})
 
 
@@ -87,6 +88,32 @@ def test_loco_overflow_append_base(ws):
     nnz = int((np.abs(d) >= np.float32(tau)).sum())
     for cap in (7 + nnz, 7 + nnz // 3, 7):
         run_loco(d, e, tau, ws, capacity=cap, count_in=7, index_base=999)
+
+
+@pytest.mark.parametrize("gate", [False, True])
+def test_loco_mixed_segment_overflow(ws, gate):
+    """Tiles where some 512-element wave-groups select more entries than their
+    compaction segment holds (30%) and others few (1%): the write-out mixes
+    entries from the segments with entries read back from the residual, with
+    and without the patch capacity cutting through both kinds of group."""
+    rng = np.random.default_rng(21 + gate)
+    tau = wl.loco_tau()
+    tile = GATE_TILE if gate else TILE
+    n = 3 * tile + 4 * 512 + 77
+    region = (np.arange(n) % tile) // 512
+    dense = (region % 3 == 0) | (region == 7)
+    p = np.where(dense, 0.30, 0.01)
+    big = rng.random(n) < p
+    d = (rng.normal(0, tau / 10, n)).astype(np.float32)
+    d[big] = np.float32(2 * tau) * np.sign(rng.normal(size=big.sum())).astype(np.float32)
+    e = (rng.normal(0, tau / 20, n)).astype(np.float32)
+    theta = None
+    if gate:  # the BF16 gate selects by visibility: theta of the same magnitude as d
+        theta = (rng.normal(0, 1.0, n) * np.float32(tau * 100)).astype(np.float32)
+    nnz = run_loco(d, e, tau, ws, theta=theta)[0]
+    assert nnz > n * 0.05
+    for cap in (nnz // 2, 5):
+        run_loco(d, e, tau, ws, theta=theta, capacity=cap + 3, count_in=3, index_base=17)
 
 
 def test_loco_ten_round_chain(ws):

@@ -76,6 +76,21 @@ def test_encode_counts_and_lossless_on_c1(oracle_mod):
     assert 0.008 < count / w.size < 0.011
 
 
+def test_density_under_both_readings(oracle_mod):
+    """The one-tensor workload at lr 1e-6 under the two readings of N(0, x):
+    variance (the default; ~0.92%, "roughly 1%") and standard deviation (~4.7%,
+    which the 5% patch buffer of the 32B-shaped step still holds)."""
+    dens = {}
+    for reading in wl.READINGS:
+        w, w_new = wl.single_tensor_inputs(reading=reading)
+        count, _, _ = oracle_mod.encode(w_new, tcast(w))
+        dens[reading] = count / w.size
+    assert 0.0085 < dens["variance"] < 0.0100
+    assert 0.044 < dens["std"] < 0.050
+    with pytest.raises(ValueError):
+        wl.sd(1.0, "bogus")
+
+
 def test_encode_chain_lossless(oracle_mod):
     """Prop. lossless along a chain of 12 patches (snapshot refreshed in place)."""
     rng = np.random.default_rng(7)
