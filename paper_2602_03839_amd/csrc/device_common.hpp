@@ -201,6 +201,7 @@ constexpr int kAhead = 2;
 // slots i and i + kAhead in iteration i while the scan wave fills i + kAhead + 1.
 constexpr int kTkRing = kAhead + 2 <= 4 ? 4 : 8;
 static_assert(kAhead >= 1 && kAhead + 2 <= kTkRing, "ticket ring too small");
+// (kernels may keep fewer tiles in flight: any AHEAD in [1, kAhead] fits the ring)
 
 // Ticket word of tile `tile` of the launch whose first tile has sequence g0.
 __device__ __forceinline__ uint64_t make_ticket(uint64_t g0, uint32_t tile, uint32_t ntiles) {
@@ -440,7 +441,7 @@ struct KnownPrefix {
 };
 constexpr uint32_t kNoTile = 0xFFFFFFFFu;
 
-template <int U, int NW, int RES, typename Params>
+template <int U, int NW, int RES, typename Params, int AHEAD = kAhead>
 __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot2,
                                uint32_t* s_wexcl, uint64_t* s_excl2, uint32_t* s_cnt2,
                                uint32_t* s_ovf2, uint32_t seg_cap, KnownPrefix* s_known) {
@@ -475,12 +476,12 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
     }
     pre = draw_ticket(p.ws);
     bool more = true;
-    for (int q = 0; q <= kAhead; ++q) {
+    for (int q = 0; q <= AHEAD; ++q) {
       s_tk[q] = more ? take() : kNoTicket;
       more = decode_ticket(s_tk[q]).tile < p.ntiles;
     }
   }
-  __syncthreads();  // T(0) .. T(kAhead)
+  __syncthreads();  // T(0) .. T(AHEAD)
   // g0 (lane 0 only) comes from the counter itself: a ticket slot may hold
   // kNoTicket when the block's first chunk lies past the last tile, and the
   // sequence base must never move backwards
@@ -496,14 +497,14 @@ __device__ void scan_wave_loop(const Params& p, uint64_t* s_tk, uint32_t* s_wtot
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) break;
-    const bool have_last = ticket_at(s_tk, it + kAhead).tile < p.ntiles;
-    if (lane == 0) s_tk[(it + kAhead + 1) & (kTkRing - 1)] = have_last ? take() : kNoTicket;
+    const bool have_last = ticket_at(s_tk, it + AHEAD).tile < p.ntiles;
+    if (lane == 0) s_tk[(it + AHEAD + 1) & (kTkRing - 1)] = have_last ? take() : kNoTicket;
     // first look-back window of T(i - kResolve), overlapping the compute of T(i)
     const ScanState res = hist[kResolve - 1];
     LookWindow<kLookK> win;
     const bool walk = res.valid && res.tk.tile != 0;
     if (walk) look_back_issue<kLookK>(p.ws, res.tk, (int64_t)res.tk.tile - 1, win);
-    __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + kAhead + 1) in s_tk
+    __syncthreads();  // wave totals of T(i) are in s_wtot[i & 1]; T(i + AHEAD + 1) in s_tk
     ScanState now;
     now.valid = have_cur;
     if (have_cur) {

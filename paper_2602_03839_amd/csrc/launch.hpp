@@ -27,7 +27,6 @@ constexpr int kEncodeTB = 960;
 constexpr int kEncodeU = 2;
 constexpr int kSectorLanes = 8;
 constexpr int kLocoTB = 960;
-constexpr int kLocoU = 1;
 
 struct EncodeTensorDesc {
   const float* w_new;
@@ -73,6 +72,8 @@ struct LocoParams {
   uint64_t* seg_begin;
   float tau;
   int gate_dtype;  // with theta: 0 = BF16 gate, kDtypeFp8 / kDtypeMxfp4 = that receiver's gate
+  int gm;          // kernel form, the same for every launch of a call (sets the tile size):
+                  // 0 = threshold, 1 = BF16 gate, 2 = FP8 gate, 3 = MXFP4 gate
   uint32_t ntiles;
   int ntensors;
   uint32_t tile_begin[kMaxBatch + 1];
@@ -289,7 +290,7 @@ static_assert(sizeof(LocoParams) < 4096, "kernel argument block too large");
 static_assert(sizeof(ApplyParams) < 4096, "kernel argument block too large");
 
 uint32_t encode_tile_elems();
-uint32_t loco_tile_elems();
+uint32_t loco_tile_elems(int gm);
 hipError_t launch_encode(EncodeParams& p, hipStream_t stream);
 hipError_t launch_loco(LocoParams& p, hipStream_t stream);
 hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);

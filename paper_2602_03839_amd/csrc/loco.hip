@@ -7,11 +7,14 @@
 // cast_D(theta) != cast_D(theta - s), for MXFP4 on (block scale, code) pairs.
 //
 // Same persistent, pipelined tile structure and ordered compaction as
-// encode.hip (NW compute waves + 1 scan wave; the loads of the next kAhead
-// tiles are in flight while the scan wave walks back).  The residual of a tile is stored
-// densely right after the selection; the rare selected-but-beyond-capacity
-// entries are patched back to s in the write phase (same lane, same address,
-// so program order keeps the later store).
+// encode.hip (NW compute waves + 1 scan wave; the loads of the next tiles
+// are in flight while the scan wave walks back): each wave compacts its
+// selected entries (offset in the tile, FP32 value) into a small LDS segment
+// per (group, wave), and the block writes a resolved tile's entries to the
+// patch in contiguous runs.  The residual of a tile is stored densely right
+// after the selection; the rare selected-but-beyond-capacity entries are
+// patched back to s in the write phase (by the block that stored them, after
+// the barriers in between, so the later store wins).
 #include "device_common.hpp"
 #include "launch.hpp"
 #include "lowp_cast.hpp"
@@ -95,35 +98,64 @@ __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const Lo
 constexpr int kResolve = 4;
 constexpr int kDefer = kResolve + 1;
 constexpr int kWexclRing = wexcl_ring(kResolve);
-// LDS value buffers (ring).  Each compute thread reads back only the values
-// it staged itself: tile T(i) is staged in slot i mod kValBufs after the
-// write-out of T(i - kDefer) has emptied that slot, so kDefer buffers suffice.
-constexpr int kValBufs = kDefer;
+// Compaction segments, as in encode.hip: kSegCap selected entries per
+// (group, wave) and tile, as a 16-bit offset in the tile and the FP32 value,
+// in kDefer + 2 slots (a slot is filled in iteration i, read after barrier
+// i + kDefer and refilled from iteration i + kDefer + 2 on).  A wave-group
+// covers 512 elements, so 64 entries hold 12.5%: every density of the method.
+constexpr uint32_t kSegCap = 64;
+constexpr int kSegSlots = kDefer + 2;
 
 // What the write-out of a tile needs kDefer iterations after its compute.
+// mask / excl (per lane) and ovf (wave-uniform: groups whose wave-group found
+// more than kSegCap entries) serve only tiles where some segment overflowed.
 template <int U>
 struct LocoDeferred {
   uint64_t e0;
   int k;
   bool valid;
+  uint32_t ovf;
   uint32_t mask;
   uint32_t excl[(U + 1) / 2];
 };
 
+// Shape of each form.  The threshold form streams 12 bytes per element with
+// two groups per lane and one tile of loads in flight (two groups of 64 bytes
+// per lane, 120 KiB per CU); the gate forms also stream theta, so they keep
+// one group per lane and two tiles in flight -- both within the 128 registers
+// a 16-wave block allows.
+constexpr int loco_u(int gm) { return gm == 0 ? 2 : 1; }
+constexpr int loco_ahead(int gm) { return gm == 0 ? 1 : 2; }
+
 // GM: 0 = threshold only, 1 = BF16 gate, 2 = FP8 gate, 3 = MXFP4 gate
 // (tensors without theta use the threshold in every mode).
+//
+// Residual.  The selection is local, emission is not: an entry is emitted only
+// if its patch position, known kDefer iterations later, is below capacity.
+// The residual is therefore written densely at compute time as if every
+// selected entry were emitted (0 there, a elsewhere), and the write-out puts
+// a back for selected entries beyond capacity.  A wave-group whose entries do
+// not fit its segment writes a everywhere instead; its write-out reads the
+// values back from the residual and zeroes the emitted ones.
 template <int NW, int U, int GM>
 __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
   constexpr bool GATE = GM != 0;
+  constexpr int AH = loco_ahead(GM);
   constexpr int TBC = NW * 64;
   constexpr uint32_t TILE = TBC * U * 8;
+  constexpr int NSEG = U * NW;  // wave-groups per tile, group-major
   __shared__ uint64_t s_tk[kTkRing];
   __shared__ uint64_t s_excl[2];
-  __shared__ uint32_t s_wtot[2 * U * NW];
-  __shared__ uint32_t s_wexcl[kWexclRing * U * NW];
-  __shared__ uint4 s_vals[kValBufs][U * TBC * 2];
-  static_assert(U * NW <= 64, "block scan runs on one wave");
+  __shared__ uint32_t s_tcnt[2];
+  __shared__ uint32_t s_tovf[2];
+  __shared__ uint32_t s_wtot[2 * NSEG];
+  __shared__ uint32_t s_wexcl[kWexclRing * NSEG];
+  __shared__ uint16_t s_off[kSegSlots][NSEG][kSegCap];  // offset of the entry in its tile
+  __shared__ float s_val[kSegSlots][NSEG][kSegCap];     // its value a
+  static_assert(NSEG <= 64, "block scan runs on one wave");
   static_assert(U <= 4, "masks of all groups are packed into one register");
+  static_assert(TILE <= 65536, "offsets within a tile are stored in 16 bits");
+  static_assert(kWexclRing >= kDefer + 1, "wave prefixes must outlive the write-out");
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -131,22 +163,22 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
   const float tau = p.tau;
 
   if (wid == NW) {
-    scan_wave_loop<U, NW, kResolve>(p, s_tk, s_wtot, s_wexcl, s_excl, nullptr, nullptr, 0u,
-                                     nullptr);
+    scan_wave_loop<U, NW, kResolve, LocoParams, AH>(p, s_tk, s_wtot, s_wexcl, s_excl, s_tcnt,
+                                                     s_tovf, kSegCap, nullptr);
     return;
   }
 
   // ---------------- compute waves (same schedule as encode_kernel: register
-  // set i mod kAhead holds T(i); compute it group by group while refilling the
-  // registers with T(i + kAhead), then write the entries of T(i - kDefer))
-  __syncthreads();  // T(0) .. T(kAhead) are in s_tk
-  static_assert(kAhead == 1 || kAhead == 2, "one or two register sets");
+  // set i mod AH holds T(i); compute it group by group while refilling the
+  // registers with T(i + AH), then write the entries of T(i - kDefer))
+  __syncthreads();  // T(0) .. T(AH) are in s_tk
+  static_assert(AH == 1 || AH == 2, "one or two register sets");
   const uint32_t lane_begin = owner_lane_begin(p);
   LocoRegs<U, GATE> g0, g1;
   uint64_t e0_0 = 0, e0_1 = 0;
   int k_0 = 0, k_1 = 0;
 #pragma unroll
-  for (int q = 0; q < kAhead; ++q) {
+  for (int q = 0; q < AH; ++q) {
     const Ticket t = ticket_at(s_tk, q);
     if (t.tile < p.ntiles) {
       const LocoCtx c = locate(p, lane_begin, t.tile, TILE);
@@ -157,11 +189,11 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
       (q == 0 ? k_0 : k_1) = c.k;
     }
   }
-  // T(i + kAhead) is looked up right after the barrier that publishes it
+  // T(i + AH) is looked up right after the barrier that publishes it
   LocoCtx cn;
   bool have_next = false, next_full = false;
   auto look_up_next = [&](int i) {
-    const Ticket t = ticket_at(s_tk, i + kAhead);
+    const Ticket t = ticket_at(s_tk, i + AH);
     have_next = t.tile < p.ntiles;
     if (have_next) {
       cn = locate(p, lane_begin, t.tile, TILE);
@@ -180,12 +212,10 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
 #pragma unroll
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) return false;
-    uint32_t mask_packed = 0, excl_packed[(U + 1) / 2];
-    uint4 av[2 * U];  // a = Delta + e of T(i), staged after the write-out
+    uint32_t mask_packed = 0, excl_packed[(U + 1) / 2], ovf = 0;
     if (have_cur) {
-      uint32_t cnt[U];
-      const uint64_t cn_n = p.t[ck].n;
       float* const cres = p.t[ck].residual;
+      const uint64_t cn_n = p.t[ck].n;
       const bool full = ce0 + TILE <= cn_n;
       const bool gate = GATE && p.t[ck].theta != nullptr;
 #pragma unroll
@@ -193,7 +223,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
         const uint64_t e = ce0 + (uint64_t)(u * TBC + tid) * 8;
         const bool vec = full || e + 8 <= cn_n;
         uint32_t m = 0;
-        float a[8], nr[8];
+        float a[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const float dv = __uint_as_float(i < 4 ? get_u32(g.d0[u], i) : get_u32(g.d1[u], i - 4));
@@ -248,75 +278,108 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           for (int i = 0; i < 8; ++i)
             if (!(e + i < cn_n)) m &= ~(1u << i);
         }
+        mask_packed |= m << (8 * u);
+        // lane-exclusive prefix of the group's counts; the wave-group's total
+        const uint32_t cnt = __builtin_popcount(m);
+        const uint32_t incl = wave_incl_scan(cnt);
+        const uint32_t r0 = incl - cnt;
+        if (u % 2 == 0) excl_packed[u >> 1] = r0;
+        else excl_packed[u >> 1] |= r0 << 16;
+        const uint32_t tot = __builtin_amdgcn_readlane(incl, 63);
+        const bool seg_ok = tot <= kSegCap;
+        if (!seg_ok) ovf |= 1u << u;
+        if (lane == 63) s_wtot[(it & 1) * NSEG + u * NW + wid] = tot;
+        // compaction at the entries' rank within the wave-group, and the dense
+        // residual store: 0 where (to be) sent, a elsewhere
+        const uint32_t le = (uint32_t)(u * TBC + tid) * 8;  // offset of slot 0 in the tile
+        if (seg_ok) {
+          uint16_t* const off = s_off[it % kSegSlots][u * NW + wid];
+          float* const val = s_val[it % kSegSlots][u * NW + wid];
+          uint32_t mm = m, r = r0;
+          while (mm) {
+            const int i = __builtin_ctz(mm);
+            mm &= mm - 1;
+            off[r] = (uint16_t)(le + i);
+            val[r] = a[i];
+            ++r;
+          }
+        }
+        const uint32_t zero = seg_ok ? m : 0u;
+        float nr[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) nr[i] = ((m >> i) & 1u) ? 0.0f : a[i];
+        for (int i = 0; i < 8; ++i) nr[i] = ((zero >> i) & 1u) ? 0.0f : a[i];
         if (vec) {
           store16(cres + e, make_uint4(__float_as_uint(nr[0]), __float_as_uint(nr[1]),
-                                              __float_as_uint(nr[2]), __float_as_uint(nr[3])));
+                                       __float_as_uint(nr[2]), __float_as_uint(nr[3])));
           store16(cres + e + 4, make_uint4(__float_as_uint(nr[4]), __float_as_uint(nr[5]),
-                                                  __float_as_uint(nr[6]), __float_as_uint(nr[7])));
+                                           __float_as_uint(nr[6]), __float_as_uint(nr[7])));
         } else {
 #pragma unroll
           for (int i = 0; i < 8; ++i)
             if (e + i < cn_n) cres[e + i] = nr[i];
         }
-        mask_packed |= m << (8 * u);
-        cnt[u] = __builtin_popcount(m);
-        av[2 * u] = make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
-                               __float_as_uint(a[3]));
-        av[2 * u + 1] = make_uint4(__float_as_uint(a[4]), __float_as_uint(a[5]),
-                                   __float_as_uint(a[6]), __float_as_uint(a[7]));
-        // this group's registers are free: start T(i + kAhead)'s loads into them
+        // this group's registers are free: start T(i + AH)'s loads into them
         if (have_next) load_group<TBC, U, GATE>(g, u, cn, tid, next_full);
-      }
-#pragma unroll
-      for (int u = 0; u < U; u += 2) {
-        const uint32_t packed = cnt[u] | (u + 1 < U ? (cnt[u + 1] << 16) : 0u);
-        const uint32_t incl = wave_incl_scan(packed);
-        excl_packed[u >> 1] = incl - packed;
-        if (lane == 63) {
-          s_wtot[(it & 1) * U * NW + u * NW + wid] = incl & 0xFFFFu;
-          if (u + 1 < U) s_wtot[(it & 1) * U * NW + (u + 1) * NW + wid] = incl >> 16;
-        }
       }
     }
     __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
 
     const LocoDeferred<U>& od = hist[kDefer - 1];
     if (od.valid) {
-      const int oi = it - kDefer;
+      const int oi = it - kDefer;  // iteration that computed the tile
       const uint64_t tile_excl = s_excl[oi & 1];
+      const uint32_t tile_cnt = s_tcnt[oi & 1];
+      const bool overflowed = s_tovf[oi & 1] != 0u;
       const uint64_t cap = p.capacity;
       const uint32_t base = p.t[od.k].index_base;
       float* const ores = p.t[od.k].residual;
-      const float* vals = reinterpret_cast<const float*>(s_vals[oi % kValBufs]);
-      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * U * NW;
+      const uint32_t* wexcl = s_wexcl + (oi & (kWexclRing - 1)) * NSEG;
+      if (!overflowed) {
+        // entry j of the tile lies in the last wave-group q whose prefix is <= j
+        const uint32_t tbase = base + (uint32_t)od.e0;
+        for (uint32_t j = tid; j < tile_cnt; j += TBC) {
+          int q = 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
-        if (m == 0) continue;
-        uint64_t pos = tile_excl + wexcl[u * NW + wid] +
-                       ((od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-        const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
-        while (m) {
-          const int i = __builtin_ctz(m);
-          m &= m - 1;
-          const float v = vals[(u * TBC + tid) * 8 + i];
+          for (int step = 32; step > 0; step >>= 1)
+            if (q + step < NSEG && wexcl[q + step] <= j) q += step;
+          const uint64_t pos = tile_excl + j;
+          const uint32_t r = j - wexcl[q];
+          const uint32_t o = s_off[oi % kSegSlots][q][r];
+          const float v = s_val[oi % kSegSlots][q][r];
           if (pos < cap) {
-            p.idx[pos] = base + (uint32_t)(e + i);
+            p.idx[pos] = tbase + o;
             p.val[pos] = v;
           } else {
-            ores[e + i] = v;  // selected but not sent: error feedback keeps it
+            ores[od.e0 + o] = v;  // selected but not sent: error feedback keeps it
           }
-          ++pos;
         }
-      }
-    }
-    if (have_cur) {
+      } else {
+        // some wave-group found more entries than its segment holds: every lane
+        // writes its own entries, from the segment or (for an overflowed
+        // wave-group) from the residual, which then holds a
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        s_vals[it % kValBufs][(u * TBC + tid) * 2] = av[2 * u];
-        s_vals[it % kValBufs][(u * TBC + tid) * 2 + 1] = av[2 * u + 1];
+        for (int u = 0; u < U; ++u) {
+          uint32_t m = (od.mask >> (8 * u)) & 0xFFu;
+          const uint32_t r0 = (od.excl[u >> 1] >> (16 * (u & 1))) & 0xFFFFu;
+          uint64_t pos = tile_excl + wexcl[u * NW + wid] + r0;
+          uint32_t r = r0;
+          const bool seg_ok = ((od.ovf >> u) & 1u) == 0u;
+          const uint64_t e = od.e0 + (uint64_t)(u * TBC + tid) * 8;
+          while (m) {
+            const int i = __builtin_ctz(m);
+            m &= m - 1;
+            const float v = seg_ok ? s_val[oi % kSegSlots][u * NW + wid][r] : ores[e + i];
+            if (pos < cap) {
+              p.idx[pos] = base + (uint32_t)(e + i);
+              p.val[pos] = v;
+              if (!seg_ok) ores[e + i] = 0.0f;
+            } else if (seg_ok) {
+              ores[e + i] = v;
+            }
+            ++pos;
+            ++r;
+          }
+        }
       }
     }
 #pragma unroll
@@ -324,6 +387,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
     hist[0].e0 = ce0;
     hist[0].k = ck;
     hist[0].valid = have_cur;
+    hist[0].ovf = ovf;
     hist[0].mask = mask_packed;
 #pragma unroll
     for (int q = 0; q < (U + 1) / 2; ++q) hist[0].excl[q] = excl_packed[q];
@@ -335,9 +399,9 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
     return true;
   };
 
-  for (int it = 0;; it += kAhead) {
+  for (int it = 0;; it += AH) {
     if (!step(it, g0, e0_0, k_0)) return;
-    if (kAhead == 2 && !step(it + 1, g1, e0_1, k_1)) return;
+    if (AH == 2 && !step(it + 1, g1, e0_1, k_1)) return;
   }
 }
 
@@ -349,7 +413,18 @@ __global__ void loco_empty_segments_kernel(const uint64_t* count, uint64_t* seg_
 
 constexpr int kLocoNW = kLocoTB / 64;
 
-uint32_t loco_tile_elems() { return kLocoTB * kLocoU * 8; }
+uint32_t loco_tile_elems(int gm) { return kLocoTB * loco_u(gm) * 8; }
+
+template <int GM>
+static hipError_t launch_loco_form(const LocoParams& p, hipStream_t stream) {
+  const void* fn = (const void*)loco_kernel<kLocoNW, loco_u(GM), GM>;
+  const int grid_cap = persistent_grid(fn, (kLocoNW + 1) * 64);
+  if (grid_cap <= 0) return hipErrorInvalidConfiguration;
+  const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
+  hipLaunchKernelGGL((loco_kernel<kLocoNW, loco_u(GM), GM>), dim3(grid), dim3((kLocoNW + 1) * 64),
+                     0, stream, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_loco(LocoParams& p, hipStream_t stream) {
   if (p.ntiles == 0) {
@@ -358,24 +433,12 @@ hipError_t launch_loco(LocoParams& p, hipStream_t stream) {
                        (const uint64_t*)p.count, p.seg_begin, (uint32_t)p.ntensors);
     return hipGetLastError();
   }
-  bool gate = false;
-  for (int k = 0; k < p.ntensors; ++k) gate |= p.t[k].theta != nullptr;
-  const int gm = !gate ? 0 : p.gate_dtype == kDtypeFp8 ? 2 : p.gate_dtype == kDtypeMxfp4 ? 3 : 1;
-  const void* fns[4] = {(const void*)loco_kernel<kLocoNW, kLocoU, 0>,
-                        (const void*)loco_kernel<kLocoNW, kLocoU, 1>,
-                        (const void*)loco_kernel<kLocoNW, kLocoU, 2>,
-                        (const void*)loco_kernel<kLocoNW, kLocoU, 3>};
-  const int grid_cap = persistent_grid(fns[gm], (kLocoNW + 1) * 64);
-  if (grid_cap <= 0) return hipErrorInvalidConfiguration;
-  const uint32_t grid = p.ntiles < (uint32_t)grid_cap ? p.ntiles : (uint32_t)grid_cap;
-  const dim3 block((kLocoNW + 1) * 64);
-  switch (gm) {
-    case 0: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 0>), dim3(grid), block, 0, stream, p); break;
-    case 1: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 1>), dim3(grid), block, 0, stream, p); break;
-    case 2: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 2>), dim3(grid), block, 0, stream, p); break;
-    default: hipLaunchKernelGGL((loco_kernel<kLocoNW, kLocoU, 3>), dim3(grid), block, 0, stream, p); break;
+  switch (p.gm) {
+    case 0: return launch_loco_form<0>(p, stream);
+    case 1: return launch_loco_form<1>(p, stream);
+    case 2: return launch_loco_form<2>(p, stream);
+    default: return launch_loco_form<3>(p, stream);
   }
-  return hipGetLastError();
 }
 
 }  // namespace pulse

@@ -279,7 +279,12 @@ int loco_batch(const pulse_loco_tensor* tensors, const float* inv_scales, uint32
       return fail(PULSE_EALIGN, "loco tensor %u: delta/residual/theta not 16-byte aligned", t);
     if (int rc = check_range(d.n, d.index_base, "loco", t)) return rc;
   }
-  const uint32_t tile = pulse::loco_tile_elems();
+  // one kernel form for the whole call, so that every launch uses the same tile
+  bool any_theta = false;
+  for (uint32_t t = 0; t < ntensors; ++t) any_theta |= tensors[t].n > 0 && tensors[t].theta != nullptr;
+  const int gm = !any_theta ? 0 : gate_dtype == pulse::kDtypeFp8 ? 2
+                                 : gate_dtype == pulse::kDtypeMxfp4 ? 3 : 1;
+  const uint32_t tile = pulse::loco_tile_elems(gm);
   uint32_t t0 = 0;
   while (t0 < ntensors) {
     pulse::LocoParams p;
@@ -292,6 +297,7 @@ int loco_batch(const pulse_loco_tensor* tensors, const float* inv_scales, uint32
     p.seg_begin = seg_begin ? seg_begin + t0 : nullptr;
     p.tau = tau;
     p.gate_dtype = gate_dtype;
+    p.gm = gm;
     uint32_t tiles = 0;
     int k = 0;
     while (t0 + k < ntensors && k < pulse::kMaxBatch) {
