@@ -1,5 +1,5 @@
 #!/usr/bin/env python3
-"""Benchmark: the PULSESync patch codec over a whole synthetic parameter set on one MI355X.
+"""Benchmark: the PULSESync patch codec over whole synthetic parameter sets on one MI355X.
 
 One step = one pass of the hot path over every tensor of the parameter set
 (default: the 32B-shaped set, 32,763,417,600 FP32 parameters in 579 tensors):
@@ -7,23 +7,37 @@ the fused encode, which casts the FP32 masters to BF16 (RNE), compares them
 bitwise with the previous BF16 snapshot, compacts the changed positions into
 an index-ordered (uint32 index, bf16 value) patch with its device-side count,
 and writes the changed values into the inference-side BF16 copy in the same
-pass.  That step is the headline.
+pass (whole 128-byte lines of a copy that mirrors the snapshot).  That step is
+the headline.
 
-Also measured, outside the headline: the unfused form (encode, then the
-standalone scatter apply of the patch into the inference copy) and the
-PULSELoCo rounds over the 7B-shaped set (10 rounds, fixed threshold): the
-error-feedback sparsification and the outer step that consumes its patch;
-the patch's delta-varint index stream; and the weight hash (a SHA-256 tree)
-of the refreshed inference copy that a receiver checks.  All inputs are
-generated on the GPU before timing and stay resident in HBM.
+Also measured ("legs"), each on its own synthetic workload:
+  * the 32B-shaped set: the in-place form (the snapshot itself refreshed, the
+    chainable form), the unfused form (encode, then the standalone scatter
+    apply), the same step under the standard-deviation reading of N(0, x)
+    (~4.7% density), the bandwidth ceiling of its read stream, the patch's
+    index streams (delta-varint and 2-D COO downcast) and the weight hash;
+  * the one-tensor workload (1,048,576 parameters) and the 0.5B-shaped set;
+  * the 7B-shaped set chained over 20 steps at lr 3e-7, 1e-6 and 3e-6, the
+    snapshot advanced in place each step;
+  * PULSELoCo on the 7B-shaped set: 10 rounds of the error-feedback
+    sparsification at a fixed threshold and with the threshold re-chosen each
+    round, the BF16-gate form, the outer step, and the bandwidth ceiling of a
+    read-modify-write stream;
+  * FP8/MXFP4 receivers and k-step patches on the 7B-shaped set.
+All inputs are generated on the GPU before timing and stay resident in HBM;
+untimed work between timed steps (restoring a snapshot, the next step's
+masters) sits outside the HIP events that time the steps.
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
-    python bench.py [--steps K] [--warmup W] [--workload 32b|7b|0.5b] [--no-cpu-baseline] [--no-loco]
+    python bench.py [--steps K] [--warmup W] [--workload 32b|7b|0.5b] [--reading variance|std]
+                    [--no-cpu-baseline] [--no-loco] [--no-configs] [--no-varint] [--no-hash]
+                    [--no-receivers] [--no-ceiling] [--no-std-leg]
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import platform
@@ -48,6 +62,9 @@ ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 # schedule step 4 rotates, 2 shifts, 2 XOR3 and 2 adds; 8 adds into the state;
 # 16 byte permutes assembling the message words; 3 of loop control.
 SHA_VALU_PER_BLOCK = 64 * 14 + 48 * 10 + 8 + 16 + 3
+# A 32-bit pattern no generated value holds (a NaN payload): the rmw probe's
+# store keeps every element's own value.
+NEVER = 0x7FC00001
 
 
 def log(*a):
@@ -65,10 +82,25 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-class ParamSet:
-    """Flat FP32 master, BF16 snapshot and BF16 inference copy, with per-tensor views."""
+def chunks(n, k):
+    return [(a, min(a + k, n)) for a in range(0, n, k)]
 
-    def __init__(self, key: str, lr: float, device):
+
+def event_pair():
+    import torch
+    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+
+def median(xs):
+    import numpy as np
+    return float(np.median(np.asarray(xs, dtype=np.float64)))
+
+
+class ParamSet:
+    """Flat FP32 masters and BF16 snapshot of a model-shaped set, per-tensor views,
+    and (optionally) a BF16 inference copy equal to the snapshot."""
+
+    def __init__(self, key: str, lr: float, device, reading: str = "variance", copy: bool = True):
         import torch
         from paper_2602_03839_amd import pulse
         from paper_2602_03839_amd import workloads as wl
@@ -82,25 +114,24 @@ class ParamSet:
             self.offsets.append(o)
             o += n
         self.N = o
+        self.T = len(self.specs)
         self.flat_index = self.N < (1 << 32)
-        cfg = WORKLOAD_IDS[key]
+        self.cfg = WORKLOAD_IDS[key]
+        self.reading = reading
         free, total = torch.cuda.mem_get_info(device)
-        log(f"[bench] {key}: {self.N:,} params in {len(self.specs)} tensors; "
+        log(f"[bench] {key} ({reading} reading): {self.N:,} params in {self.T} tensors; "
             f"device memory free {free / 1e9:.1f} / {total / 1e9:.1f} GB")
         self.w = torch.empty(self.N, dtype=torch.float32, device=device)
         self.S = torch.empty(self.N, dtype=torch.int16, device=device)
         t0 = time.perf_counter()
-        for i, (spec, off, n) in enumerate(zip(self.specs, self.offsets, self.sizes)):
-            wv = self.w[off:off + n]
-            wl.init_weights_(wv, spec, cfg, 0, i)
-            pulse.cast_bf16(wv, out=self.S[off:off + n])
-            wl.adam_step_(wv, lr, cfg, 1, i)
-            if i % 64 == 0:
-                log(f"[bench] generated {i + 1}/{len(self.specs)} tensors")
+        for i, spec in enumerate(self.specs):
+            wv = self.view(self.w, i)
+            wl.init_weights_(wv, spec, self.cfg, 0, i, reading=reading)
+            pulse.cast_bf16(wv, out=self.view(self.S, i))
+            wl.adam_step_(wv, lr, self.cfg, 1, i, reading=reading)
         torch.cuda.synchronize()
-        torch.cuda.empty_cache()
         log(f"[bench] generation {time.perf_counter() - t0:.1f}s")
-        self.R = self.S.clone()
+        self.R = self.S.clone() if copy else None
 
     def view(self, buf, i):
         return buf[self.offsets[i]:self.offsets[i] + self.sizes[i]]
@@ -108,14 +139,90 @@ class ParamSet:
     def base(self, i):
         return self.offsets[i] if self.flat_index else 0
 
+    def batches(self, refresh, mirror):
+        """EncodeBatch per launch; refresh: None, a buffer (mirror: it equals S on
+        entry) or self.S (in place)."""
+        from paper_2602_03839_amd import pulse
+        return [pulse.EncodeBatch([pulse.EncodeTensor(self.view(self.w, i), self.view(self.S, i),
+                                                      None if refresh is None else self.view(refresh, i),
+                                                      self.base(i), mirror)
+                                   for i in range(a, b)]) for a, b in chunks(self.T, CHUNK)]
 
-def chunks(n, k):
-    return [(a, min(a + k, n)) for a in range(0, n, k)]
+
+class Patch:
+    def __init__(self, cap, ntensors, device, fp32=False):
+        import torch
+        self.cap = cap
+        self.idx = torch.empty(max(cap, 1), dtype=torch.int32, device=device)
+        self.val = torch.empty(max(cap, 1), dtype=torch.float32 if fp32 else torch.int16, device=device)
+        self.count = torch.zeros(1, dtype=torch.int64, device=device)
+        self.seg = torch.zeros(max(ntensors, 1), dtype=torch.int64, device=device)
 
 
-def event_pair():
-    import torch
-    return torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+def run_pass(batches, parts, patch, ws, ev=None, stream=None):
+    """One pass over all launches; `ev` = (start, end) events around the launches."""
+    patch.count.zero_()
+    if ev:
+        ev[0].record(stream)
+    for (a, _b), b in zip(parts, batches):
+        b(patch.idx, patch.val, patch.count, ws, seg_begin=patch.seg[a:])
+    if ev:
+        ev[1].record(stream)
+
+
+def timed_reps(fn, reps, warmup, before=None):
+    """Per-rep HIP-event times of fn(ev); `before` runs untimed ahead of each rep."""
+    for _ in range(warmup):
+        if before:
+            before()
+        fn(None)
+    out = []
+    for _ in range(reps):
+        if before:
+            before()
+        ev = event_pair()
+        fn(ev)
+        ev[1].synchronize()
+        out.append(ev[0].elapsed_time(ev[1]))
+    return out
+
+
+def fused_figures(N, nnz, ms, n_launch=None):
+    d = {"ms_per_step": round(ms, 4), "nnz": nnz, "density": round(nnz / N, 6),
+         "GBps_scanned": round(6.0 * N / (ms * 1e-3) / 1e9, 2),
+         "hbm_frac_of_peak": round((6.0 * N + 8.0 * nnz) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    if n_launch:
+        d["launches_per_step"] = n_launch
+    return d
+
+
+class Ceiling:
+    """The bandwidth probes of libpulse_ceiling.so (probe/ceiling.hip)."""
+
+    def __init__(self):
+        path = os.path.join(ROOT, "paper_2602_03839_amd", "libpulse_ceiling.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run `python -m paper_2602_03839_amd.build`")
+        L = ctypes.CDLL(path)
+        vp, u64 = ctypes.c_void_p, ctypes.c_uint64
+        L.ceiling_shapes.restype = ctypes.c_int
+        L.ceiling_covered.argtypes = [ctypes.c_int, ctypes.c_int, u64]
+        L.ceiling_covered.restype = u64
+        L.ceiling_read2.argtypes = [ctypes.c_int, vp, vp, u64, vp, vp]
+        L.ceiling_rmw.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, u64, ctypes.c_uint32, vp]
+        self.L = L
+
+    def best(self, pattern, run, N, bytes_per_elem, reps=3):
+        """Fastest shape: (GB/s, shape label, every shape's GB/s)."""
+        shapes = {}
+        for sh in range(self.L.ceiling_shapes()):
+            for nt in ((0,) if pattern == 0 else (0, 1)):
+                ts = timed_reps(lambda ev: run(sh, nt, ev), reps, 1)
+                cov = self.L.ceiling_covered(pattern, sh, N)
+                shapes[f"shape{sh}" + ("" if pattern == 0 else f"_nt{nt}")] = round(
+                    bytes_per_elem * cov / (median(ts) * 1e-3) / 1e9, 1)
+        label = max(shapes, key=shapes.get)
+        return shapes[label], label, shapes
 
 
 def main():
@@ -124,17 +231,23 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="32b", choices=sorted(WORKLOAD_IDS))
+    ap.add_argument("--reading", default="variance", choices=["variance", "std"],
+                    help="reading of N(0, x) in the workload recipe (headline)")
     ap.add_argument("--lr", type=float, default=1e-6)
     ap.add_argument("--capacity-frac", type=float, default=0.05)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=float, default=1.0e9,
                     help="elements of the parameter set the oracle baseline encodes")
     ap.add_argument("--refresh", default="mirror", choices=["mirror", "sparse"],
-                    help="fused refresh form: whole 128-byte runs of the inference copy, which mirrors "
+                    help="headline refresh form: whole 128-byte runs of the inference copy, which mirrors "
                          "the snapshot (mirror), or one 2-byte write per change (sparse)")
     ap.add_argument("--no-loco", action="store_true", help="skip the PULSELoCo leg")
     ap.add_argument("--loco-rounds", type=int, default=10)
-    ap.add_argument("--no-varint", action="store_true", help="skip the wire-format (delta-varint) leg")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the one-tensor, 0.5B-shaped and 7B-shaped chain legs")
+    ap.add_argument("--no-std-leg", action="store_true", help="skip the std-reading 32B-shaped leg")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the bandwidth-ceiling probes")
+    ap.add_argument("--no-varint", action="store_true", help="skip the wire-format legs")
     ap.add_argument("--no-hash", action="store_true", help="skip the weight-hash leg")
     ap.add_argument("--no-receivers", action="store_true",
                     help="skip the FP8/MXFP4-receiver and k-step legs (7B set)")
@@ -154,6 +267,7 @@ def main():
     torch.cuda.set_device(device)
     pulse.lib()
     stream = torch.cuda.current_stream()
+    ceiling = None if args.no_ceiling else Ceiling()
 
     # A plain copy kernel of known size (bitwise_not over 1 GiB of int32 reads
     # 1 GiB and writes 1 GiB), run once so that a counter-collection run of this
@@ -164,105 +278,162 @@ def main():
     del calib
     torch.cuda.empty_cache()
 
-    ps = ParamSet(args.workload, args.lr, device)
-    T = len(ps.specs)
-    cap = int(args.capacity_frac * ps.N)
-    idx = torch.empty(cap, dtype=torch.int32, device=device)
-    val = torch.empty(cap, dtype=torch.int16, device=device)
-    count = torch.zeros(1, dtype=torch.int64, device=device)
-    seg = torch.zeros(T, dtype=torch.int64, device=device)
+    ps = ParamSet(args.workload, args.lr, device, args.reading)
+    N, T = ps.N, ps.T
+    cap = int(args.capacity_frac * N)
+    patch = Patch(cap, T, device)
     ws = pulse.workspace(device)
-    log(f"[bench] patch capacity {cap:,} entries ({cap * 6 / 1e9:.2f} GB)")
-
     parts = chunks(T, CHUNK)
     n_launch = len(parts)
-    # The inference copy starts as a copy of the snapshot and only ever receives
-    # bf16(w') at the positions the step changes, so it equals the snapshot
-    # everywhere else: the whole-run refresh (PULSE_REFRESH_MIRRORS_SNAP) applies.
-    mirror = args.refresh == "mirror"
-    enc_fused = [pulse.EncodeBatch([pulse.EncodeTensor(ps.view(ps.w, i), ps.view(ps.S, i),
-                                                       ps.view(ps.R, i), ps.base(i), mirror)
-                                    for i in range(a, b)]) for a, b in parts]
-    enc_plain = [pulse.EncodeBatch([pulse.EncodeTensor(ps.view(ps.w, i), ps.view(ps.S, i), None, ps.base(i))
-                                    for i in range(a, b)]) for a, b in parts]
-    app = pulse.ApplyBatch([pulse.ApplyTensor(ps.view(ps.R, i), ps.base(i)) for i in range(T)])
+    log(f"[bench] patch capacity {cap:,} entries ({cap * 6 / 1e9:.2f} GB)")
 
-    def encode_pass(batches, ev=None):
-        """One pass over all tensors; `ev` = (start, end) HIP events around its launches."""
-        count.zero_()
-        if ev:
-            ev[0].record(stream)
-        for (a, _b), b in zip(parts, batches):
-            b(idx, val, count, ws, seg_begin=seg[a:])
-        if ev:
-            ev[1].record(stream)
-
-    def timed_steps(step_fn, make_events):
-        for _ in range(args.warmup):
-            step_fn(None)
-        torch.cuda.synchronize()
-        evs = [make_events() for _ in range(args.steps)]
-        t0 = time.perf_counter()
-        for k in range(args.steps):
-            step_fn(evs[k])
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) * 1e3 / args.steps, evs
-
-    # ---- headline: fused encode + refresh of the inference copy.  Events
+    # ---- headline: fused encode + refresh of the inference copy R.  R starts
+    # as a copy of the snapshot and only ever receives bf16(w') at the
+    # positions the step changes, so it equals the snapshot everywhere else:
+    # the whole-line refresh (PULSE_REFRESH_MIRRORS_SNAP) applies.  Events
     # bracket each step's launches (one pair per step: an event between
     # back-to-back launches would itself add a gap); the average launch
     # duration is the bracketed time over the launches of the step.
-    fused_ms, fused_ev = timed_steps(lambda ev: encode_pass(enc_fused, ev), event_pair)
-    nnz = int(count.item())
+    mirror = args.refresh == "mirror"
+    enc_fused = ps.batches(ps.R, mirror)
+    for _ in range(args.warmup):
+        run_pass(enc_fused, parts, patch, ws)
+    torch.cuda.synchronize()
+    evs = [event_pair() for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        run_pass(enc_fused, parts, patch, ws, evs[k], stream)
+    torch.cuda.synchronize()
+    fused_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    pulse.check_workspace(ws)
+    nnz = int(patch.count.item())
     sent = min(nnz, cap)
     if nnz > cap:
         log(f"[bench] WARNING: patch overflow ({nnz:,} > capacity {cap:,})")
-    step_kernel_ms = np.array([s.elapsed_time(e) for s, e in fused_ev])
+    step_kernel_ms = np.array([s.elapsed_time(e) for s, e in evs])
     fused_kernel_ms = float(step_kernel_ms.mean())
     fused_avg_launch_ms = fused_kernel_ms / n_launch
-    value = 6.0 * ps.N / (fused_ms * 1e-3) / 1e9
-    fused_bytes = 6.0 * ps.N + 8.0 * sent  # FP32 + BF16 read; idx + val + refresh written per entry
+    value = 6.0 * N / (fused_ms * 1e-3) / 1e9
+    fused_bytes = 6.0 * N + 8.0 * sent  # FP32 + BF16 read; idx + val + refresh written per entry
     achieved = fused_bytes / n_launch / (fused_avg_launch_ms * 1e-3) / 1e9
     log(f"[bench] fused encode+refresh {fused_ms:.3f} ms/step ({value:.0f} GB/s scanned); "
-        f"kernels {fused_kernel_ms:.3f} ms over {n_launch} launches; nnz {nnz:,} density {nnz / ps.N:.4%}")
-    seg_fused = seg.clone()
-    idx_head = idx[: min(sent, 1 << 24)].clone()
-    val_head = val[: min(sent, 1 << 24)].clone()
+        f"kernels {fused_kernel_ms:.3f} ms over {n_launch} launches ({achieved:.0f} GB/s, "
+        f"{achieved / HBM_PEAK_GBS:.1%} of HBM); nnz {nnz:,} density {nnz / N:.4%}")
+    seg_fused = patch.seg.clone()
+    idx_head = patch.idx[: min(sent, 1 << 24)].clone()
+    val_head = patch.val[: min(sent, 1 << 24)].clone()
+    legs = {}
 
-    # ---- encode, then the standalone scatter apply (receiver side)
-    def unfused(ev):
-        encode_pass(enc_plain, ev[0] if ev else None)
-        if ev:
-            ev[1][0].record(stream)
-        app(idx, val, seg, count)
-        if ev:
-            ev[1][1].record(stream)
+    # ---- the in-place form: the snapshot itself is refreshed (chainable: the
+    # next step compares against it).  Each rep starts from the step's
+    # snapshot, restored from a copy outside the timed region.
+    R = ps.R
+    R.copy_(ps.S)  # R: the step's snapshot, kept to restore S
+    enc_inplace = ps.batches(ps.S, False)
+    ip = timed_reps(lambda ev: run_pass(enc_inplace, parts, patch, ws, ev, stream),
+                    args.steps, args.warmup, before=lambda: ps.S.copy_(R))
+    ip_ms = median(ip)
+    assert int(patch.count.item()) == nnz, "in-place and mirrored encode disagree on the count"
+    check = pulse.cast_bf16(ps.w[: min(N, 1 << 28)])
+    assert torch.equal(check, ps.S[: check.numel()]), "in-place refresh differs from bf16(w')"
+    ps.S.copy_(R)
+    legs["fused_inplace"] = {**fused_figures(N, sent, ip_ms, n_launch),
+                             "kernel": "encode_kernel (refresh form, refresh == snapshot)",
+                             "avg_launch_ms": round(ip_ms / n_launch, 5)}
+    log(f"[bench] fused encode+refresh in place {ip_ms:.3f} ms/step "
+        f"({legs['fused_inplace']['hbm_frac_of_peak']:.1%} of HBM)")
+    del enc_inplace
 
-    unf_ms, unf_ev = timed_steps(unfused, lambda: (event_pair(), event_pair()))
-    enc_ms = float(np.mean([ev[0][0].elapsed_time(ev[0][1]) for ev in unf_ev]))
-    app_ms = float(np.mean([ev[1][0].elapsed_time(ev[1][1]) for ev in unf_ev]))
+    # ---- encode, then the standalone scatter apply (receiver side) into R
+    enc_plain = ps.batches(None, False)
+    app = pulse.ApplyBatch([pulse.ApplyTensor(ps.view(R, i), ps.base(i)) for i in range(T)])
+    enc_t, app_t = [], []
+    for rep in range(args.warmup + args.steps):
+        ea, eb = event_pair(), event_pair()
+        run_pass(enc_plain, parts, patch, ws, ea, stream)
+        eb[0].record(stream)
+        app(patch.idx, patch.val, patch.seg, patch.count)
+        eb[1].record(stream)
+        eb[1].synchronize()
+        if rep >= args.warmup:
+            enc_t.append(ea[0].elapsed_time(ea[1]))
+            app_t.append(eb[0].elapsed_time(eb[1]))
+    enc_ms, app_ms = median(enc_t), median(app_t)
+    unf_ms = enc_ms + app_ms
     log(f"[bench] encode then apply {unf_ms:.3f} ms/step: encode {enc_ms:.3f} ms, apply {app_ms:.3f} ms")
 
-    # ---- sanity: both forms give the same patch; the inference copy equals bf16(w')
-    assert int(count.item()) == nnz, "fused and plain encode disagree on the count"
-    assert torch.equal(seg, seg_fused), "fused and plain encode disagree on the segments"
-    assert torch.equal(idx[: idx_head.numel()], idx_head) and torch.equal(val[: val_head.numel()], val_head)
-    check = pulse.cast_bf16(ps.w[: min(ps.N, 1 << 28)])
-    assert torch.equal(check, ps.R[: check.numel()]), "inference copy differs from bf16(w')"
+    # ---- sanity: every form gives the same patch; the copies equal bf16(w')
+    assert int(patch.count.item()) == nnz, "fused and plain encode disagree on the count"
+    assert torch.equal(patch.seg, seg_fused), "fused and plain encode disagree on the segments"
+    assert torch.equal(patch.idx[: idx_head.numel()], idx_head)
+    assert torch.equal(patch.val[: val_head.numel()], val_head)
+    assert torch.equal(check, R[: check.numel()]), "applied copy differs from bf16(w')"
+    pulse.check_workspace(ws)
     del check, idx_head, val_head
 
-    # ---- the patch's wire format: delta-varint index stream, encoded and decoded
-    varint = None if args.no_varint else varint_leg(args, ps, idx, count, seg, sent, ws, stream)
+    legs["encode_then_apply"] = {
+        "ms_per_step": round(unf_ms, 4),
+        "GBps_scanned": round(6.0 * N / (unf_ms * 1e-3) / 1e9, 2),
+        "encode_ms": round(enc_ms, 4),
+        "apply_ms": round(app_ms, 4),
+        "encode_hbm_frac_of_peak": round((6.0 * N + 6.0 * sent) / (enc_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "apply_entries_per_s": round(sent / (app_ms * 1e-3), 0),
+        "apply_bytes_per_entry": 8,
+        "hbm_frac_of_peak": round((6.0 * N + 14.0 * sent) / (unf_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+    }
+
+    # ---- the read stream's ceiling on the same buffers (probe/ceiling.hip)
+    ceil = None
+    if ceiling is not None:
+        sink = torch.empty(256 * 1024 * 4, dtype=torch.int32, device=device)
+
+        def read2(sh, _nt, ev):
+            if ev:
+                ev[0].record(stream)
+            rc = ceiling.L.ceiling_read2(sh, ps.w.data_ptr(), ps.S.data_ptr(), N, sink.data_ptr(),
+                                         stream.cuda_stream)
+            if ev:
+                ev[1].record(stream)
+            assert rc == 0, rc
+        gbs, label, shapes = ceiling.best(0, read2, N, 6.0)
+        del sink
+        plain_gbs = (6.0 * N + 6.0 * sent) / (enc_ms * 1e-3) / 1e9
+        ceil = {"read_6B_per_elem_GBps": gbs, "best_shape": label, "shapes_GBps": shapes,
+                "fused_encode_frac_of_ceiling": round(achieved / gbs, 4),
+                "plain_encode_frac_of_ceiling": round(plain_gbs / gbs, 4)}
+        log(f"[bench] read ceiling (4 B FP32 + 2 B BF16 per element) {gbs:.0f} GB/s ({label}); "
+            f"fused encode at {achieved / gbs:.1%}, plain encode at {plain_gbs / gbs:.1%} of it")
+        legs["ceiling"] = ceil
+
+    # ---- the patch's wire format: delta-varint and 2-D COO index streams
+    if not args.no_varint:
+        legs["varint_patch"] = varint_leg(args, ps, patch.idx, patch.seg, sent, ws, stream)
 
     # ---- the weight hash a receiver checks after applying the patch
-    whash = None if args.no_hash else hash_leg(args, ps, stream)
+    if not args.no_hash:
+        legs["weight_hash"] = hash_leg(args, ps, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(ps, args.cpu_sample, idx, val, seg, nnz, cap)
+        cpu = cpu_baseline(ps, args.cpu_sample, patch, nnz, cap)
 
     from paper_2602_03839_amd.traffic import read_summary  # noqa: E402
-    traffic = read_summary(TRAFFIC_FILE) if args.workload == "32b" else None
+    traffic = read_summary(TRAFFIC_FILE) if (args.workload == "32b" and args.reading == "variance"
+                                             and mirror) else None
+    roofline = {
+        "bound": "hbm",
+        "kernel": "encode_kernel (refresh form)",
+        "achieved": round(achieved, 2),
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None if traffic is None else round(traffic, 0),
+        "bytes_per_launch": fused_bytes / n_launch,
+        "avg_launch_ms": round(fused_avg_launch_ms, 5),
+    }
+    if ceil is not None:
+        roofline["measured_read_ceiling_GBps"] = ceil["read_6B_per_elem_GBps"]
+        roofline["frac_of_measured_ceiling"] = ceil["fused_encode_frac_of_ceiling"]
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -278,53 +449,175 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"pulsesync-{args.workload}-shaped fused encode+refresh",
-            "params": ps.N,
+            "params": N,
             "tensors": T,
             "lr": args.lr,
+            "reading": args.reading,
             "nnz": nnz,
-            "patch_density": round(nnz / ps.N, 6),
+            "patch_density": round(nnz / N, 6),
             "hbm_frac_of_peak": round(fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "index_form": "flat uint32" if ps.flat_index else "per-tensor uint32 + segment offsets",
             "patch_capacity": cap,
             "launches_per_step": n_launch,
+            "refresh_form": args.refresh,
         },
-        "roofline": {
-            "bound": "hbm",
-            "kernel": "encode_kernel (refresh form)",
-            "achieved": round(achieved, 2),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None if traffic is None else round(traffic, 0),
-            "bytes_per_launch": fused_bytes / n_launch,
-            "avg_launch_ms": round(fused_avg_launch_ms, 5),
-        },
+        "roofline": roofline,
         "cpu_baseline": cpu,
-        "legs": {
-            "varint_patch": varint,
-            "weight_hash": whash,
-            "encode_then_apply": {
-                "ms_per_step": round(unf_ms, 4),
-                "GBps_scanned": round(6.0 * ps.N / (unf_ms * 1e-3) / 1e9, 2),
-                "encode_ms": round(enc_ms, 4),
-                "apply_ms": round(app_ms, 4),
-                "hbm_frac_of_peak": round((6.0 * ps.N + 14.0 * sent) / (unf_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-            },
-        },
+        "legs": legs,
     }
-    del enc_fused, enc_plain, app, idx, val, ps
+    del enc_fused, enc_plain, app, patch, ps, R
     torch.cuda.empty_cache()
+
+    if not args.no_std_leg and args.workload == "32b" and args.reading == "variance":
+        legs["std_reading_32b"] = std_leg(args, device, stream)
+        torch.cuda.empty_cache()
+    if not args.no_configs:
+        legs["one_tensor"] = one_tensor_leg(args, device, stream)
+        legs["set_0p5b"] = set_leg(args, device, stream, "0.5b")
+        torch.cuda.empty_cache()
+        legs["chain_7b"] = chain_leg(args, device, stream)
+        torch.cuda.empty_cache()
     if not args.no_loco:
-        out["legs"]["loco_7b"] = loco_leg(args, device, stream)
+        legs["loco_7b"] = loco_leg(args, device, stream, ceiling)
+        torch.cuda.empty_cache()
     if not args.no_receivers:
-        out["legs"]["receivers_7b"] = receivers_leg(args, device, stream)
+        legs["receivers_7b"] = receivers_leg(args, device, stream)
     print(json.dumps(out), flush=True)
 
 
-def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
+def std_leg(args, device, stream):
+    """The headline step on the 32B-shaped set generated under the standard-deviation
+    reading of N(0, x) (~4.7% density: the top of the density bracket)."""
+    import torch
+    from paper_2602_03839_amd import pulse
+    ps = ParamSet("32b", args.lr, device, "std")
+    patch = Patch(int(args.capacity_frac * ps.N), ps.T, device)
+    ws = pulse.workspace(device)
+    parts = chunks(ps.T, CHUNK)
+    enc = ps.batches(ps.R, True)
+    ts = timed_reps(lambda ev: run_pass(enc, parts, patch, ws, ev, stream), args.steps, args.warmup)
+    nnz = int(patch.count.item())
+    assert nnz <= patch.cap, "std-reading patch overflow"
+    pulse.check_workspace(ws)
+    d = {**fused_figures(ps.N, nnz, median(ts), len(parts)), "reading": "std",
+         "kernel": "encode_kernel (refresh form, mirrored copy)"}
+    log(f"[bench] std reading 32b: fused {d['ms_per_step']:.3f} ms/step, density {d['density']:.4%}, "
+        f"{d['hbm_frac_of_peak']:.1%} of HBM")
+    del enc, patch, ps
+    return d
+
+
+def one_tensor_leg(args, device, stream):
+    """The one-tensor workload (1,048,576 params, lr 1e-6): fused encode+refresh,
+    and encode then apply; launch-bound, so many reps."""
+    import torch
+    from paper_2602_03839_amd import pulse
+    from paper_2602_03839_amd import workloads as wl
+    w, wn = wl.single_tensor_inputs(args.lr)
+    n = w.size
+    w_d = torch.from_numpy(w).to(device)
+    wn_d = torch.from_numpy(wn).to(device)
+    S = pulse.cast_bf16(w_d)
+    R = S.clone()
+    patch = Patch(n, 1, device)
+    ws = pulse.workspace(device)
+    zero = torch.zeros(1, dtype=torch.int64, device=device)
+    fused = pulse.EncodeBatch([pulse.EncodeTensor(wn_d, S, R, 0, True)])
+    plain = pulse.EncodeBatch([pulse.EncodeTensor(wn_d, S, None, 0)])
+    reps = max(50, args.steps)
+
+    def f_fused(ev):
+        run_pass([fused], [(0, 1)], patch, ws, ev, stream)
+
+    def f_unfused(ev):
+        patch.count.zero_()
+        if ev:
+            ev[0].record(stream)
+        plain(patch.idx, patch.val, patch.count, ws)
+        pulse.apply(R, patch.idx, patch.val, zero, patch.count)
+        if ev:
+            ev[1].record(stream)
+    tf = median(timed_reps(f_fused, reps, 5))
+    tu = median(timed_reps(f_unfused, reps, 5))
+    nnz = int(patch.count.item())
+    assert torch.equal(R, pulse.cast_bf16(wn_d))
+    d = {**fused_figures(n, nnz, tf), "encode_then_apply_ms": round(tu, 4), "params": n,
+         "note": "launch-bound: reported, not gated"}
+    log(f"[bench] one tensor: fused {tf * 1e3:.1f} us, encode+apply {tu * 1e3:.1f} us, "
+        f"density {nnz / n:.4%}")
+    return d
+
+
+def set_leg(args, device, stream, key):
+    """One fused step over every tensor of a model-shaped set (mirrored copy)."""
+    from paper_2602_03839_amd import pulse
+    ps = ParamSet(key, args.lr, device)
+    patch = Patch(int(0.05 * ps.N), ps.T, device)
+    ws = pulse.workspace(device)
+    parts = chunks(ps.T, CHUNK)
+    enc = ps.batches(ps.R, True)
+    ts = timed_reps(lambda ev: run_pass(enc, parts, patch, ws, ev, stream), max(args.steps, 20),
+                    args.warmup)
+    nnz = int(patch.count.item())
+    pulse.check_workspace(ws)
+    d = {**fused_figures(ps.N, nnz, median(ts), len(parts)), "params": ps.N, "tensors": ps.T}
+    log(f"[bench] {key}: fused {d['ms_per_step']:.3f} ms/step over {ps.T} tensors, "
+        f"density {d['density']:.4%}, {d['hbm_frac_of_peak']:.1%} of HBM")
+    del enc, patch, ps
+    return d
+
+
+def chain_leg(args, device, stream):
+    """The 7B-shaped set chained over 20 steps at lr 3e-7, 1e-6 and 3e-6: each step's
+    masters come from the previous step's (untimed Adam-like update), and the fused
+    encode refreshes the snapshot in place, so step t compares against step t-1's
+    output.  Every step is timed."""
+    import torch
+    from paper_2602_03839_amd import pulse
+    from paper_2602_03839_amd import workloads as wl
+    out = {}
+    for lr in (3e-7, 1e-6, 3e-6):
+        ps = ParamSet("7b", lr, device, copy=False)
+        patch = Patch(int(0.05 * ps.N), ps.T, device)
+        ws = pulse.workspace(device)
+        parts = chunks(ps.T, CHUNK)
+        enc = ps.batches(ps.S, False)
+        ms, dens = [], []
+        for t in range(1, 21):
+            if t > 1:
+                for i in range(ps.T):
+                    wl.adam_step_(ps.view(ps.w, i), lr, ps.cfg, t, i)
+            ev = event_pair()
+            run_pass(enc, parts, patch, ws, ev, stream)
+            ev[1].synchronize()
+            ms.append(ev[0].elapsed_time(ev[1]))
+            nnz = int(patch.count.item())
+            assert nnz <= patch.cap
+            dens.append(nnz / ps.N)
+        pulse.check_workspace(ws)
+        chk = pulse.cast_bf16(ps.w[: 1 << 28])
+        assert torch.equal(chk, ps.S[: 1 << 28]), "chained snapshot differs from bf16(w_20)"
+        med = median(ms[1:])
+        nnz_mean = float(sum(dens[1:]) / len(dens[1:])) * ps.N
+        out[f"lr_{lr:g}"] = {
+            "ms_per_step_median": round(med, 4),
+            "ms_first_last": [round(ms[0], 4), round(ms[-1], 4)],
+            "density_first_last": [round(dens[0], 6), round(dens[-1], 6)],
+            "GBps_scanned": round(6.0 * ps.N / (med * 1e-3) / 1e9, 2),
+            "hbm_frac_of_peak": round((6.0 * ps.N + 8.0 * nnz_mean) / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+        log(f"[bench] 7b chain lr {lr:g}: {med:.3f} ms/step in place, density {dens[0]:.4%} -> "
+            f"{dens[-1]:.4%}, {out[f'lr_{lr:g}']['hbm_frac_of_peak']:.1%} of HBM")
+        del enc, patch, ps, chk
+        torch.cuda.empty_cache()
+    out["form"] = "in place (snapshot refreshed), 20 chained steps, masters updated between steps (untimed)"
+    out["params"] = wl.SHAPES["7b"].numel()
+    return out
+
+
+def varint_leg(args, ps, idx, seg, sent, ws, stream):
     """The patch's index stream in the paper's wire format (App. H.2 / F.3): the
     per-tensor segments of the last encode pass, delta-varint encoded and decoded."""
-    import numpy as np
     import torch
     from paper_2602_03839_amd import pulse
 
@@ -356,7 +649,7 @@ def varint_leg(args, ps, idx, count, seg, sent, ws, stream):
     assert nbytes <= bound, (nbytes, bound)
     assert int(got.item()) == sent
     assert torch.equal(back[:sent], idx[:sent]), "varint round trip differs from the patch"
-    enc_ms, dec_ms = float(np.median(te)), float(np.median(td))
+    enc_ms, dec_ms = median(te), median(td)
     coo = coo_leg(args, ps, idx, end, seg, sent, ws, stream)
     enc_bytes = 4.0 * sent + nbytes          # indices read, stream written
     dec_bytes = nbytes + 4.0 * sent * 3      # stream read, differences written, re-read, indices written
@@ -381,7 +674,6 @@ def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
     """The same patch's indices as the paper's 2-D COO delta downcast (App. H.2
     step 4, App. H.4.1): per tensor the first index, then (uint8 row, uint16
     column) pairs with (255, 0) escapes for row gaps over 255."""
-    import numpy as np
     import torch
     from paper_2602_03839_amd import pulse
 
@@ -409,7 +701,7 @@ def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
     assert P <= cap_p
     esc = int(((drow[:P] == 255) & (dcol[:P] == 0)).sum().item())
     nbytes = 3 * P + 4 * T
-    ms = float(np.median(times))
+    ms = median(times)
     # decode (the receiver's Upcast + DeltaDecode) and check the round trip
     back = torch.empty(sent + 1, dtype=torch.int32, device=dev)
     npairs = torch.tensor([P], dtype=torch.int64, device=dev)
@@ -423,7 +715,7 @@ def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
         if r:
             td.append(a.elapsed_time(b))
     assert torch.equal(back[:sent], idx[:sent]), "COO round trip differs from the patch"
-    ms_d = float(np.median(td))
+    ms_d = median(td)
     del back
     log(f"[bench] coo downcast: {sent:,} indices -> {P:,} pairs ({esc:,} escapes), "
         f"{nbytes / 1e6:.1f} MB ({nbytes / max(sent, 1):.3f} B/index); encode {ms:.3f} ms, "
@@ -432,14 +724,13 @@ def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
             "bytes_per_index": round(nbytes / max(sent, 1), 4), "encode_ms": round(ms, 4),
             "decode_ms": round(ms_d, 4),
             "encode_GBps_algorithmic": round((4.0 * sent + nbytes) / ms / 1e6, 2),
+            "decode_GBps_algorithmic": round((nbytes + 4.0 * sent) / ms_d / 1e6, 2),
             "kernels": "coo_encode_kernel; coo_decode_kernel"}
 
 
 def hash_leg(args, ps, stream):
     """Weight hash (App. J.4) of the refreshed BF16 inference copy: a SHA-256 tree
     over 16 KiB chunks of its bytes, the check a receiver runs after a patch."""
-    import numpy as np
-    import torch
     from paper_2602_03839_amd import pulse
 
     batch = pulse.HashBatch([ps.view(ps.R, i) for i in range(len(ps.specs))])
@@ -455,7 +746,7 @@ def hash_leg(args, ps, stream):
         if r:
             times.append(a.elapsed_time(b))
     assert len(roots) == 1, "the weight hash changed between calls on unchanged weights"
-    ms = float(np.median(times))
+    ms = median(times)
     blocks = batch.nleaves * ((pulse.HASH_LEAF_BYTES + 1 + 1 + 8 + 63) // 64)
     tops = blocks * SHA_VALU_PER_BLOCK / (ms * 1e-3) / 1e12
     log(f"[bench] weight hash: {batch.nleaves:,} leaves of 16 KiB in {ms:.3f} ms "
@@ -475,10 +766,13 @@ def hash_leg(args, ps, stream):
     }
 
 
-def loco_leg(args, device, stream):
-    """PULSELoCo rounds over the 7B-shaped set at a fixed threshold: the error-feedback
-    sparsification (Alg. 2, one worker) and the outer step that consumes its patch
-    (SparseSync average over R = 1 worker, outer Nesterov, mu 0.9, alpha 0.7)."""
+def loco_leg(args, device, stream, ceiling):
+    """PULSELoCo rounds over the 7B-shaped set: the error-feedback sparsification
+    (Alg. 2, one worker) at the fixed threshold (chosen once so ~2% of round-1
+    entries survive), then again with the threshold re-chosen every round (a
+    sample quantile of |Delta + e|, so ~2% survive each round), the BF16-gate
+    form, and the outer step that consumes the patch (SparseSync average over
+    R = 1 worker, outer Nesterov, mu 0.9, alpha 0.7)."""
     import numpy as np
     import torch
     from paper_2602_03839_amd import pulse
@@ -494,62 +788,122 @@ def loco_leg(args, device, stream):
     resid = torch.zeros(N, dtype=torch.float32, device=device)
     theta = torch.empty(N, dtype=torch.float32, device=device).normal_(0.0, 0.02 ** 0.5)
     mom = torch.zeros(N, dtype=torch.float32, device=device)
-    cap = N // 10
-    idx = torch.empty(cap, dtype=torch.int32, device=device)
-    val = torch.empty(cap, dtype=torch.float32, device=device)
-    count = torch.zeros(1, dtype=torch.int64, device=device)
-    seg = torch.zeros(T, dtype=torch.int64, device=device)
+    patch = Patch(N // 10, T, device, fp32=True)
     ws = pulse.workspace(device)
     parts = chunks(T, CHUNK)
     view = lambda b, i: b[offs[i]:offs[i + 1]]
-    batches = [pulse.LocoBatch([pulse.LocoTensor(view(delta, i), view(resid, i), None, 0)
-                                for i in range(a, b)]) for a, b in parts]
+    thr = [pulse.LocoBatch([pulse.LocoTensor(view(delta, i), view(resid, i), None, 0)
+                            for i in range(a, b)]) for a, b in parts]
+    gate = [pulse.LocoBatch([pulse.LocoTensor(view(delta, i), view(resid, i), view(theta, i), 0)
+                             for i in range(a, b)]) for a, b in parts]
     outer = pulse.OuterBatch([pulse.OuterTensor(view(theta, i), view(mom, i), 0) for i in range(T)])
-    lists = [pulse.SparseList(idx, val, seg, count, capacity=cap)]
-    ms, ms_outer, dens = [], [], []
-    for r in range(args.loco_rounds):
-        for i in range(T):
-            wl.loco_delta_(view(delta, i), 5, r, i)
-        count.zero_()
-        torch.cuda.synchronize()
-        a, e = event_pair()
-        c, d = event_pair()
-        a.record(stream)
+    lists = [pulse.SparseList(patch.idx, patch.val, patch.seg, patch.count, capacity=patch.cap)]
+    g = torch.Generator(device=device)
+
+    def sparsify(batches, tv, ev):
+        patch.count.zero_()
+        if ev:
+            ev[0].record(stream)
         for (t0, _t1), b in zip(parts, batches):
-            b(tau, idx, val, count, ws, seg_begin=seg[t0:])
-        e.record(stream)
-        c.record(stream)
-        outer(lists, mu=0.9, alpha=0.7)
-        d.record(stream)
-        d.synchronize()
-        ms.append(a.elapsed_time(e))
-        ms_outer.append(c.elapsed_time(d))
-        dens.append(int(count.item()) / N)
+            b(tv, patch.idx, patch.val, patch.count, ws, seg_begin=patch.seg[t0:])
+        if ev:
+            ev[1].record(stream)
+
+    def rounds(per_round_tau):
+        resid.zero_()
+        ms, ms_outer, dens, taus = [], [], [], []
+        for r in range(args.loco_rounds):
+            for i in range(T):
+                wl.loco_delta_(view(delta, i), 5, r, i)
+            tv = tau
+            if per_round_tau:  # ~2% of |Delta + e| this round, from a 2^24-element sample
+                g.manual_seed(1000 + r)
+                pos = torch.randint(0, N, (1 << 24,), device=device, generator=g)
+                a = (delta[pos] + resid[pos]).abs()
+                tv = float(torch.kthvalue(a, int((1.0 - wl.LOCO_KEEP) * a.numel())).values.item())
+                del pos, a
+            torch.cuda.synchronize()
+            ev, eo = event_pair(), event_pair()
+            sparsify(thr, tv, ev)
+            eo[0].record(stream)
+            outer(lists, mu=0.9, alpha=0.7)
+            eo[1].record(stream)
+            eo[1].synchronize()
+            ms.append(ev[0].elapsed_time(ev[1]))
+            ms_outer.append(eo[0].elapsed_time(eo[1]))
+            dens.append(int(patch.count.item()) / N)
+            taus.append(tv)
+        return ms, ms_outer, dens, taus
+
+    ms, ms_outer, dens, _ = rounds(False)
     skip = 1 if len(ms) > 1 else 0
-    med = float(np.median(ms[skip:]))
-    med_outer = float(np.median(ms_outer[skip:]))
+    med = median(ms[skip:])
+    med_outer = median(ms_outer[skip:])
     nnz_mean = float(np.mean(dens[skip:])) * N
     outer_bytes = 16.0 * N + 8.0 * nnz_mean
+    loco_bytes = 12.0 * N + 8.0 * nnz_mean
     log(f"[bench] loco 7b: sparsify median {med:.3f} ms/round ({12.0 * N / med / 1e6:.0f} GB/s at 12 B/param); "
         f"outer step median {med_outer:.3f} ms ({outer_bytes / med_outer / 1e6:.0f} GB/s); "
         f"density {dens[0]:.4%} -> {dens[-1]:.4%}")
-    return {
+    ms_p, _mo, dens_p, taus_p = rounds(True)
+    med_p = median(ms_p[skip:])
+    log(f"[bench] loco 7b, tau re-chosen each round: sparsify median {med_p:.3f} ms/round, density "
+        f"{dens_p[0]:.4%} -> {dens_p[-1]:.4%}")
+    # the gate form (Alg. 2's selection by the BF16 visibility of theta - a)
+    gt = timed_reps(lambda ev: sparsify(gate, 0.0, ev), max(3, args.steps), 1,
+                    before=lambda: resid.zero_())
+    g_ms, g_dens = median(gt), int(patch.count.item()) / N
+    pulse.check_workspace(ws)
+    log(f"[bench] loco 7b, BF16 gate: {g_ms:.3f} ms/round ({16.0 * N / g_ms / 1e6:.0f} GB/s at 16 B/param), "
+        f"density {g_dens:.4%}")
+    out = {
         "params": N,
         "tau": tau,
         "rounds": args.loco_rounds,
         "ms_per_round_median": round(med, 4),
+        "ms_per_round": [round(m, 4) for m in ms],
         "GBps_12B_per_param": round(12.0 * N / med / 1e6, 2),
+        "hbm_frac_of_peak": round(loco_bytes / med / 1e6 / HBM_PEAK_GBS, 4),
         "kernel": "loco_kernel (threshold form)",
         "density_first_last": [round(dens[0], 6), round(dens[-1], 6)],
+        "per_round_tau": {"ms_per_round_median": round(med_p, 4),
+                          "density_first_last": [round(dens_p[0], 6), round(dens_p[-1], 6)],
+                          "tau_first_last": [taus_p[0], taus_p[-1]],
+                          "rule": "tau_r = 98th percentile of |Delta + e| over a 2^24-element sample"},
+        "gate_form": {"ms": round(g_ms, 4), "density": round(g_dens, 6),
+                      "GBps_16B_per_param": round(16.0 * N / g_ms / 1e6, 2),
+                      "hbm_frac_of_peak": round((16.0 * N + 8.0 * g_dens * N) / g_ms / 1e6 / HBM_PEAK_GBS, 4),
+                      "kernel": "loco_kernel (BF16 gate form)"},
         "outer_step": {
             "kernel": "outer_kernel (SparseSync average over 1 worker + outer Nesterov)",
             "ms_per_round_median": round(med_outer, 4),
+            "ms_per_round": [round(m, 4) for m in ms_outer],
             "GBps_algorithmic": round(outer_bytes / med_outer / 1e6, 2),
             "hbm_frac_of_peak": round(outer_bytes / med_outer / 1e6 / HBM_PEAK_GBS, 4),
             "bytes_per_round": outer_bytes,
         },
         "round_ms_median": round(med + med_outer, 4),
     }
+    if ceiling is not None:  # the read-modify-write ceiling on the same buffers (e keeps its values)
+        def rmw(sh, nt, ev):
+            if ev:
+                ev[0].record(stream)
+            rc = ceiling.L.ceiling_rmw(sh, nt, delta.data_ptr(), resid.data_ptr(), N, NEVER,
+                                       stream.cuda_stream)
+            if ev:
+                ev[1].record(stream)
+            assert rc == 0, rc
+        gbs, label, shapes = ceiling.best(1, rmw, N, 12.0)
+        add_ms = median(timed_reps(lambda ev: (ev and ev[0].record(stream),
+                                               torch.add(delta, resid, out=resid),
+                                               ev and ev[1].record(stream)), 3, 1))
+        out["ceiling"] = {"rmw_12B_per_elem_GBps": gbs, "best_shape": label, "shapes_GBps": shapes,
+                          "torch_add_GBps": round(12.0 * N / add_ms / 1e6, 1),
+                          "sparsify_frac_of_ceiling": round(loco_bytes / med / 1e6 / gbs, 4)}
+        log(f"[bench] rmw ceiling (8 B read + 4 B written per element) {gbs:.0f} GB/s ({label}); "
+            f"torch.add {12.0 * N / add_ms / 1e6:.0f} GB/s; sparsify at "
+            f"{out['ceiling']['sparsify_frac_of_ceiling']:.1%} of the ceiling")
+    return out
 
 
 def receivers_leg(args, device, stream):
@@ -645,7 +999,7 @@ def receivers_leg(args, device, stream):
                 ta.append(c.elapsed_time(d))
         nnz = int(count.item())
         assert nnz <= cap, f"{name} patch overflow"
-        ms_e, ms_a = float(np.median(te)), float(np.median(ta))
+        ms_e, ms_a = median(te), median(ta)
         gbs = (per_param[name] * N + per_entry[name] * nnz) / ms_e / 1e6
         log(f"[bench] {name} receiver 7b: encode {ms_e:.3f} ms ({gbs:.0f} GB/s, "
             f"{gbs / HBM_PEAK_GBS:.1%} of HBM), apply {ms_a:.3f} ms, density {nnz / N:.5%}")
@@ -679,7 +1033,8 @@ def receivers_leg(args, device, stream):
                 e.synchronize()
                 times.append(a.elapsed_time(e))
             dens[t] = int(count.item()) / N
-            kms = float(np.median(times))
+            kms = median(times)
+    pulse.check_workspace(ws)
     log(f"[bench] k-step BF16 density vs w_0 (7b): " +
         ", ".join(f"k={k}: {d:.4%}" for k, d in dens.items()) + f"; k=32 encode {kms:.3f} ms")
     out["kstep_bf16"] = {"density": {str(k): round(d, 6) for k, d in dens.items()},
@@ -688,7 +1043,7 @@ def receivers_leg(args, device, stream):
     return out
 
 
-def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
+def cpu_baseline(ps, sample_elems, patch, nnz, cap):
     """The oracle (single-threaded C) on a bounded sample of the same step: encode with refresh."""
     import numpy as np
     import oracle
@@ -700,7 +1055,7 @@ def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
             break
         take.append(i)
         tot += n
-    segs = seg.cpu().numpy().tolist() + [min(nnz, cap)]
+    segs = patch.seg.cpu().numpy().tolist() + [min(nnz, cap)]
     t_enc = 0.0
     parity = True
     for i in take:
@@ -712,8 +1067,8 @@ def cpu_baseline(ps, sample_elems, idx, val, seg, nnz, cap):
         t_enc += (time.perf_counter_ns() - c0) * 1e-9
         b, e = segs[i], segs[i + 1]
         if e <= cap:
-            g_idx = idx[b:e].cpu().numpy().view(np.uint32)
-            g_val = val[b:e].cpu().numpy().view(np.uint16)
+            g_idx = patch.idx[b:e].cpu().numpy().view(np.uint32)
+            g_val = patch.val[b:e].cpu().numpy().view(np.uint16)
             parity &= (e - b == cnt and np.array_equal(g_idx, o_idx[:cnt])
                        and np.array_equal(g_val, o_val[:cnt]))
         parity &= np.array_equal(r, ps.view(ps.R, i).cpu().numpy().view(np.uint16))

@@ -10,6 +10,11 @@ short text summary that bench.py reads back: a figure taken on other sources
 is not reported.
 
     python -m paper_2602_03839_amd.traffic --fetch DIR --write DIR --bench-json FILE --out FILE
+    python -m paper_2602_03839_amd.traffic kernels --dir DIR [--dir DIR ...] --out FILE
+    python -m paper_2602_03839_amd.traffic stats --stats-csv FILE --bench-json FILE --out FILE
+
+The second form tabulates every library kernel's counters per dispatch (any
+counters, one directory per counter pass), with mean durations.
 """
 from __future__ import annotations
 
@@ -74,7 +79,145 @@ def _measure(directory: str, counter: str, n_launch: int):
     return scale, sum(enc) * 1024.0, enc
 
 
+def kernel_label(name: str) -> str:
+    """Short kernel name: template arguments kept, namespace and parameters dropped."""
+    n = name[5:] if name.startswith("void ") else name
+    n = n.replace("pulse::", "")
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):  # the parameter list is the first '(' outside template brackets
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    return n[:cut]
+
+
+def kernel_table(dirs, counters_wanted=None, match="pulse|bitwise_not"):
+    """Per kernel: dispatches, mean duration and the mean of every counter per
+    dispatch over the counter-collection runs in `dirs` (FETCH_SIZE and
+    WRITE_SIZE in bytes, calibrated on the copy kernel; other counters raw)."""
+    import re
+    per = {}   # label -> counter -> [values]
+    dur = {}   # label -> [ns]
+    scale = {}
+    for d in dirs:
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        for f in files:
+            with open(f, newline="") as fh:
+                rows = list(csv.DictReader(fh))
+            calib = {}
+            for r in rows:
+                if CALIB_KERNEL in r["Kernel_Name"] and r["Counter_Name"] in ("FETCH_SIZE", "WRITE_SIZE"):
+                    calib.setdefault(r["Counter_Name"], float(r["Counter_Value"]))
+            for c, v in calib.items():
+                scale[c] = CALIB_BYTES / (v * 1024.0)
+            for r in rows:
+                if not re.search(match, r["Kernel_Name"]):
+                    continue
+                lab = kernel_label(r["Kernel_Name"])
+                c = r["Counter_Name"]
+                if counters_wanted and c not in counters_wanted:
+                    continue
+                v = float(r["Counter_Value"])
+                if c in ("FETCH_SIZE", "WRITE_SIZE"):
+                    v = v * 1024.0 * scale.get(c, 1.0)
+                per.setdefault(lab, {}).setdefault(c, []).append(v)
+                try:
+                    dur.setdefault(lab, {})[(f, r["Dispatch_Id"])] = (
+                        int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+                except (KeyError, ValueError):
+                    pass
+    return per, dur, scale
+
+
+def kernels_main(argv):
+    ap = argparse.ArgumentParser(prog="traffic kernels",
+                                 description="per-kernel counter table from rocprofv3 --pmc runs")
+    ap.add_argument("--dir", action="append", required=True, help="a counter-collection output directory")
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--title", default="per-kernel counters")
+    ap.add_argument("--command", action="append", default=[], help="commands that made the runs")
+    args = ap.parse_args(argv)
+    per, dur, scale = kernel_table(args.dir)
+    counters = sorted({c for v in per.values() for c in v})
+    lines = [f"# {args.title}", "",
+             "Mean per dispatch; FETCH_SIZE / WRITE_SIZE in bytes, each calibrated on the copy kernel "
+             "(bitwise_not over 1 GiB: 1 GiB read, 1 GiB written) of the same run "
+             f"(factors {', '.join(f'{k} {v:.4f}' for k, v in sorted(scale.items()))}); other counters raw.",
+             ""]
+    for c in args.command:
+        lines.append(f"    {c}")
+    lines += ["", "| kernel | dispatches | mean duration (us) | " + " | ".join(counters) + " |",
+              "|---|---|---|" + "---|" * len(counters)]
+    for lab in sorted(per):
+        vals = per[lab]
+        nd = max(len(v) for v in vals.values())
+        ds = list(dur.get(lab, {}).values())
+        md = sum(ds) / len(ds) / 1e3 if ds else float("nan")
+        cells = []
+        for c in counters:
+            v = vals.get(c)
+            cells.append(f"{sum(v) / len(v):.4g}" if v else "")
+        lines.append(f"| {lab} | {nd} | {md:.1f} | " + " | ".join(cells) + " |")
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def stats_main(argv):
+    """Markdown summary of a rocprofv3 --kernel-trace --stats run of bench.py:
+    the library's kernels, and the headline kernel's average beside the
+    benchmark's own event timing of the same run."""
+    import re
+    ap = argparse.ArgumentParser(prog="traffic stats")
+    ap.add_argument("--stats-csv", required=True, help="the run's *_kernel_stats.csv")
+    ap.add_argument("--bench-json", required=True, help="file holding the JSON line bench.py printed")
+    ap.add_argument("--out", required=True)
+    ap.add_argument("--command", action="append", default=[], help="commands that made the run")
+    args = ap.parse_args(argv)
+    with open(args.stats_csv, newline="") as fh:
+        rows = list(csv.DictReader(fh))
+    with open(args.bench_json) as fh:
+        d = json.loads([line for line in fh if line.startswith("{")][-1])
+    keep = re.compile(r"pulse::|bitwise_not|read2_kernel|rmw_kernel")
+    out = ["# rocprofv3 kernel stats of one bench.py run", ""]
+    out += ["Commands (repository root as the working directory):", "```"] + args.command + ["```", ""]
+    out += ["| Kernel | Calls | Avg (ms) | Min (ms) | Max (ms) | Total (ms) |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        if not keep.search(r["Name"]):
+            continue
+        name = "torch bitwise_not over 2^28 int32 (counter calibration copy)" if "bitwise_not" in r["Name"] \
+            else kernel_label(r["Name"]).replace("(anonymous namespace)::", "")
+        out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e6:.4f} | "
+                   f"{float(r['MinNs']) / 1e6:.4f} | {float(r['MaxNs']) / 1e6:.4f} | "
+                   f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+    rf = d["roofline"]
+    out += ["", f"bench.py line of this run: fused step {d['ms_per_step']:.3f} ms; HIP events around each step's "
+                f"{d['config']['launches_per_step']} launches give an average launch of {rf['avg_launch_ms']:.4f} ms, "
+                f"{rf['achieved']:.1f} GB/s = {100 * rf['frac']:.1f}% of 8 TB/s."]
+    head = [r for r in rows if re.search(r"encode_kernel<\d+, \d+, true>", r["Name"])]
+    if head:
+        a = float(head[0]["AverageNs"]) / 1e6
+        out.append(f"rocprofv3 average of `{kernel_label(head[0]['Name'])}` over all its dispatches (the headline "
+                   f"and the in-place leg): {a:.4f} ms.")
+    out += ["", "Launch sizes differ within a step (the last batch of a step holds fewer tensors), so Min/Max span "
+                "the batch sizes.  Kernels outside the library (torch's input generators) are left out."]
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
 def main():
+    import sys
+    if len(sys.argv) > 1 and sys.argv[1] == "kernels":
+        kernels_main(sys.argv[2:])
+        return
+    if len(sys.argv) > 1 and sys.argv[1] == "stats":
+        stats_main(sys.argv[2:])
+        return
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--fetch", required=True, help="output directory of the FETCH_SIZE run")
     ap.add_argument("--write", required=True, help="output directory of the WRITE_SIZE run")
