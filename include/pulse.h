@@ -170,6 +170,28 @@ int pulse_encode_batch(const pulse_encode_tensor *tensors, uint32_t ntensors,
                        void *stream);
 
 /*
+ * pulse_encode_batch_noalloc -- pulse_encode_batch without a workspace
+ * argument, for callers that cannot allocate device memory: code being
+ * captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc.  The call allocates nothing (no hipMalloc/hipFree, no
+ * allocating library routine); its scratch is a 524,800-byte array inside
+ * the library (pulse_workspace_bytes()), one per GPU, held from the first
+ * call on that GPU until the process ends.  Each call first clears the
+ * scratch with a small fill kernel on `stream`, then runs exactly the
+ * launches of pulse_encode_batch, so results are identical to it.
+ *   Arguments and errors: as pulse_encode_batch, less the workspace.  A call
+ *   that would need more scratch than the library holds is rejected with
+ *   PULSE_EINVAL (none does today: the scratch does not grow with n); a
+ *   device index above 63 is rejected with PULSE_EINVAL.
+ *   Concurrency: every call on one GPU shares that GPU's scratch, so calls
+ *   that overlap on one GPU (different streams, or threads) race and give
+ *   wrong patches; order them on one stream.
+ */
+int pulse_encode_batch_noalloc(const pulse_encode_tensor *tensors, uint32_t ntensors,
+                               uint32_t *idx, uint16_t *val, uint64_t capacity,
+                               uint64_t *count, uint64_t *seg_begin, void *stream);
+
+/*
  * pulse_apply -- PULSESync decode of one tensor (Sec. 4.2, Alg. 1 Decode;
  * App. H.5, Alg. 4): dst[idx[k] - index_base] = val[k] for k in
  * [*begin, min(*end, capacity)).  A direct copy of bit patterns, no

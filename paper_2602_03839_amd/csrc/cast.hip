@@ -1,6 +1,6 @@
 // cast.hip -- the dense BF16 view of an FP32 tensor (Sec. 3 "Sparsity
 // metric"; RNE per App. A.2 / App. D).  Eight elements per lane per step:
-// two 16-byte loads, one 16-byte store.
+// two 16-byte loads, one 16-byte store.  Also a plain zero fill.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -33,6 +33,22 @@ hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t 
   if (blocks > 8192) blocks = 8192;
   if (blocks == 0) blocks = 1;
   hipLaunchKernelGGL(cast_kernel, dim3((uint32_t)blocks), dim3(kCastTB), 0, stream, src, dst, n);
+  return hipGetLastError();
+}
+
+// A zero fill by a kernel (the allocation-free encode clears its scratch
+// this way on the caller's stream).
+__global__ __launch_bounds__(kCastTB) void zero_words_kernel(uint64_t* __restrict__ p,
+                                                             uint64_t nwords) {
+  const uint64_t stride = (uint64_t)gridDim.x * kCastTB;
+  for (uint64_t i = (uint64_t)blockIdx.x * kCastTB + threadIdx.x; i < nwords; i += stride) p[i] = 0;
+}
+
+hipError_t launch_zero_words(uint64_t* p, uint64_t nwords, hipStream_t stream) {
+  if (nwords == 0) return hipSuccess;
+  uint64_t blocks = (nwords + kCastTB - 1) / kCastTB;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(zero_words_kernel, dim3((uint32_t)blocks), dim3(kCastTB), 0, stream, p, nwords);
   return hipGetLastError();
 }
 

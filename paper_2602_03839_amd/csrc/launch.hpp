@@ -295,6 +295,8 @@ hipError_t launch_encode(EncodeParams& p, hipStream_t stream);
 hipError_t launch_loco(LocoParams& p, hipStream_t stream);
 hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);
 hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream);
+// p[0 .. nwords) = 0 by a kernel (not a memset, so a captured graph replays it as a kernel)
+hipError_t launch_zero_words(uint64_t* p, uint64_t nwords, hipStream_t stream);
 uint64_t outer_unit_elems();
 uint32_t varint_entry_tile();
 uint32_t varint_byte_tile();

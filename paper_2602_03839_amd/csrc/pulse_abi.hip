@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "../../include/pulse.h"
@@ -125,9 +126,46 @@ int pulse_cast_bf16(const float* src, uint16_t* dst, uint64_t n, void* stream) {
   return hip_status(pulse::launch_cast(src, dst, n, (hipStream_t)stream), "cast launch");
 }
 
-int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, uint32_t* idx,
-                       uint16_t* val, uint64_t capacity, uint64_t* count, uint64_t* seg_begin,
-                       void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+// The allocation-free encode's scratch: a workspace that lives in the
+// library's own device memory, one copy per GPU (a file-scope device array
+// is instantiated on every device the library's code object is loaded on).
+// In host code `scratch` names a host-side stand-in: its device address on
+// the current device comes from hipGetSymbolAddress, taken once per device
+// and kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = pulse::kWorkspaceBytes;  // 512.5 KiB
+static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)];
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];
+
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipError_t e = hipGetDevice(&dev)) return fail(PULSE_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(PULSE_EINVAL, "device %d: the allocation-free entry point serves devices 0-%d", dev,
+                kMaxScratchDevices - 1);
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)))
+      return fail(PULSE_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                  hipGetErrorString(e));
+    if (!p || !aligned(p, 256))
+      return fail(PULSE_EHIP, "scratch on device %d has no 256-byte aligned address", dev);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PULSE_OK;
+}
+
+// A batched encode: argument checks, then the launches on the caller's
+// workspace, or (use_scratch) on the library's scratch after a zero fill of
+// it on the stream.
+int encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, uint32_t* idx,
+                 uint16_t* val, uint64_t capacity, uint64_t* count, uint64_t* seg_begin,
+                 void* workspace, size_t workspace_bytes, bool use_scratch, void* stream) {
   if (ntensors == 0) return ok();
   if (!tensors) return fail(PULSE_EINVAL, "encode: tensors is NULL");
   if (!count) return fail(PULSE_EINVAL, "encode: count is NULL");
@@ -136,7 +174,8 @@ int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, ui
     return fail(PULSE_EALIGN, "encode: count/seg_begin not 8-byte aligned");
   if ((idx && !aligned(idx, 4)) || (val && !aligned(val, 2)))
     return fail(PULSE_EALIGN, "encode: idx/val misaligned");
-  if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
+  if (!use_scratch)
+    if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
   for (uint32_t t = 0; t < ntensors; ++t) {
     const pulse_encode_tensor& d = tensors[t];
     if (d.n == 0) continue;
@@ -152,6 +191,19 @@ int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, ui
     if (int rc = check_range(d.n, d.index_base, "encode", t)) return rc;
   }
 
+  if (use_scratch) {
+    // the call needs pulse_workspace_bytes() of scratch; the library holds
+    // kScratchBytes (equal today: the status ring does not grow with n)
+    if (pulse::kWorkspaceBytes > kScratchBytes)
+      return fail(PULSE_EINVAL, "encode (no allocation): needs %zu bytes of scratch, the library holds %zu",
+                  (size_t)pulse::kWorkspaceBytes, (size_t)kScratchBytes);
+    if (int rc = scratch_address(&workspace)) return rc;
+    workspace_bytes = kScratchBytes;
+    if (int rc = hip_status(pulse::launch_zero_words((uint64_t*)workspace, workspace_bytes / 8,
+                                                     (hipStream_t)stream),
+                            "scratch fill launch"))
+      return rc;
+  }
   const uint32_t tile = pulse::encode_tile_elems();
   uint32_t t0 = 0;
   while (t0 < ntensors) {
@@ -186,6 +238,22 @@ int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, ui
     t0 += k;
   }
   return ok();
+}
+
+}  // namespace
+
+int pulse_encode_batch(const pulse_encode_tensor* tensors, uint32_t ntensors, uint32_t* idx,
+                       uint16_t* val, uint64_t capacity, uint64_t* count, uint64_t* seg_begin,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  return encode_batch(tensors, ntensors, idx, val, capacity, count, seg_begin, workspace,
+                      workspace_bytes, false, stream);
+}
+
+int pulse_encode_batch_noalloc(const pulse_encode_tensor* tensors, uint32_t ntensors,
+                               uint32_t* idx, uint16_t* val, uint64_t capacity, uint64_t* count,
+                               uint64_t* seg_begin, void* stream) {
+  return encode_batch(tensors, ntensors, idx, val, capacity, count, seg_begin, nullptr, 0, true,
+                      stream);
 }
 
 int pulse_encode(const float* w_new, const uint16_t* snap, uint64_t n, uint32_t* idx,

@@ -86,7 +86,8 @@ HASH_LEAF_BYTES = 16384  # PULSE_HASH_LEAF_BYTES
 
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
            "pulse_workspace_status",
-           "pulse_encode", "pulse_encode_batch", "pulse_apply", "pulse_apply_batch",
+           "pulse_encode", "pulse_encode_batch", "pulse_encode_batch_noalloc",
+           "pulse_apply", "pulse_apply_batch",
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
            "pulse_outer_step", "pulse_outer_step_batch",
            "pulse_varint_encode", "pulse_varint_decode",
@@ -116,6 +117,7 @@ def lib():
             L.pulse_workspace_status.argtypes = [vp, sz, vp]
             L.pulse_encode.argtypes = [vp, vp, u64, vp, vp, u64, vp, u32, vp, vp, sz, vp]
             L.pulse_encode_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, sz, vp]
+            L.pulse_encode_batch_noalloc.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp]
             L.pulse_apply.argtypes = [vp, u64, vp, vp, u64, vp, vp, u32, vp, vp]
             L.pulse_apply_batch.argtypes = [vp, u32, vp, vp, u64, vp, vp, vp, vp]
             L.pulse_loco_sparsify.argtypes = [vp, vp, u64, f32, vp, vp, vp, u64, vp, u32, vp, sz, vp]
@@ -313,6 +315,18 @@ class EncodeBatch:
                                              optional=True),
                                         pws, nb, _stream(stream, dev)),
                "pulse_encode_batch")
+
+    def noalloc(self, idx, val, count, seg_begin=None, capacity=None, stream=None):
+        """The same call through pulse_encode_batch_noalloc: no workspace, the
+        library's own scratch (allocates nothing; calls on one GPU must not overlap)."""
+        dev = self.device
+        cap = _capacity(idx, val, capacity, 4, 2, dev)
+        _check(lib().pulse_encode_batch_noalloc(self.arr, self.n, idx.data_ptr(), val.data_ptr(),
+                                                cap, _u64(count, "count", dev),
+                                                _u64(seg_begin, "seg_begin", dev,
+                                                     min_numel=self.n, optional=True),
+                                                _stream(stream, dev)),
+               "pulse_encode_batch_noalloc")
 
 
 def apply(dst: torch.Tensor, idx: torch.Tensor, val: torch.Tensor, begin: torch.Tensor,

@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 24, names
+    assert len(names) == 25, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name
@@ -262,3 +262,20 @@ def test_binding_rejects_host_tensors(L):
         pulse.EncodeBatch([pulse.EncodeTensor(w, s)])
     with pytest.raises(pulse.PulseError, match="torch.Tensor"):
         pulse.cast_bf16([0.0, 1.0])
+
+
+def test_encode_noalloc_validation(L):
+    """The allocation-free encode checks its arguments like pulse_encode_batch
+    (before it looks up its scratch, so nothing here needs a GPU)."""
+    enc = L.pulse_encode_batch_noalloc  # tensors, ntensors, idx, val, capacity, count, seg_begin, stream
+    assert enc(None, 0, None, None, 0, None, None, None) == OK
+    assert enc(None, 1, A, A, 10, A, None, None) == EINVAL
+    t = (pulse._EncodeTensor * 1)()
+    t[0] = pulse._EncodeTensor(A, A, None, 10, 0, 0)
+    assert enc(t, 1, A, A, 10, None, None, None) == EINVAL       # count
+    assert enc(t, 1, A, A, 10, A + 4, None, None) == EALIGN      # count alignment
+    t[0] = pulse._EncodeTensor(A + 4, A, None, 10, 0, 0)
+    assert enc(t, 1, A, A, 10, A, None, None) == EALIGN          # w_new alignment
+    t[0] = pulse._EncodeTensor(A, A, None, 10, (1 << 32) - 5, 0)
+    assert enc(t, 1, A, A, 10, A, None, None) == ERANGE
+    assert b"encode tensor 0" in L.pulse_last_error()
