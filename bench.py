@@ -417,9 +417,10 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(ps, args.cpu_sample, patch, nnz, cap)
 
-    from paper_2602_03839_amd.traffic import read_summary  # noqa: E402
-    traffic = read_summary(TRAFFIC_FILE) if (args.workload == "32b" and args.reading == "variance"
-                                             and mirror) else None
+    from paper_2602_03839_amd.traffic import read_summary_split  # noqa: E402
+    split = read_summary_split(TRAFFIC_FILE) if (args.workload == "32b" and args.reading == "variance"
+                                                 and mirror) else None
+    traffic = None if split is None else split[0] + split[1]
     roofline = {
         "bound": "hbm",
         "kernel": "encode_kernel (refresh form)",
@@ -482,7 +483,31 @@ def main():
         torch.cuda.empty_cache()
     if not args.no_receivers:
         legs["receivers_7b"] = receivers_leg(args, device, stream)
+    rmw = legs.get("loco_7b", {}).get("ceiling")
+    if split is not None and ceil is not None and rmw is not None:
+        roofline["counter_bound"] = counter_bound(split, ceil["read_6B_per_elem_GBps"],
+                                                  rmw["rmw_12B_per_elem_GBps"], fused_avg_launch_ms)
+        cb = roofline["counter_bound"]
+        log(f"[bench] fused launch vs the bound its measured traffic sets: {cb['bound_ms']:.3f} ms bound, "
+            f"{fused_avg_launch_ms:.3f} ms measured ({cb['frac']:.1%})")
     print(json.dumps(out), flush=True)
+
+
+def counter_bound(split, read_gbs, rmw_gbs, launch_ms):
+    """The time one fused launch needs for the HBM traffic its counters measured.
+
+    Two measured streams fix a linear cost per byte: the 2:1 read stream
+    (6 B read per element) gives the read rate a, and the read-modify-write
+    stream (8 B read + 4 B written per element) then gives the marginal cost of
+    a written byte, 4/b = 12/rmw - 8/a.  The launch's FETCH_SIZE and WRITE_SIZE
+    bytes (calibrated per launch) at those rates give its bound."""
+    fetch, write = split
+    a = read_gbs * 1e9
+    per_w = (12.0 / (rmw_gbs * 1e9) - 8.0 / a) / 4.0  # seconds per written byte
+    t = fetch / a + write * per_w
+    return {"fetch_bytes": round(fetch), "write_bytes": round(write),
+            "read_GBps": read_gbs, "write_marginal_GBps": round(1.0 / per_w / 1e9, 1),
+            "bound_ms": round(t * 1e3, 4), "frac": round(t * 1e3 / launch_ms, 4)}
 
 
 def std_leg(args, device, stream):

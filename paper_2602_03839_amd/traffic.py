@@ -41,6 +41,13 @@ def kernel_source_hash() -> str:
 
 def read_summary(path: str):
     """traffic_bytes_per_launch from a summary, or None if missing or taken on other sources."""
+    split = read_summary_split(path)
+    return None if split is None else split[0] + split[1]
+
+
+def read_summary_split(path: str):
+    """(fetch_bytes_per_launch, write_bytes_per_launch) from a summary, or None if
+    missing or taken on other sources."""
     try:
         with open(path) as fh:
             kv = dict(line.split(":", 1) for line in fh if ":" in line and not line.startswith("#"))
@@ -50,7 +57,7 @@ def read_summary(path: str):
     if kv.get("source_hash") != kernel_source_hash():
         return None
     try:
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv["fetch_bytes_per_launch"]), float(kv["write_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -82,7 +89,7 @@ def _measure(directory: str, counter: str, n_launch: int):
 def kernel_label(name: str) -> str:
     """Short kernel name: template arguments kept, namespace and parameters dropped."""
     n = name[5:] if name.startswith("void ") else name
-    n = n.replace("pulse::", "")
+    n = n.replace("pulse::", "").replace("(anonymous namespace)::", "")
     depth, cut = 0, len(n)
     for i, ch in enumerate(n):  # the parameter list is the first '(' outside template brackets
         if ch == "<":
@@ -176,6 +183,7 @@ def stats_main(argv):
     ap.add_argument("--stats-csv", required=True, help="the run's *_kernel_stats.csv")
     ap.add_argument("--bench-json", required=True, help="file holding the JSON line bench.py printed")
     ap.add_argument("--out", required=True)
+    ap.add_argument("--trace-csv", help="the run's *_kernel_trace.csv (per-dispatch durations)")
     ap.add_argument("--command", action="append", default=[], help="commands that made the run")
     args = ap.parse_args(argv)
     with open(args.stats_csv, newline="") as fh:
@@ -198,11 +206,22 @@ def stats_main(argv):
     out += ["", f"bench.py line of this run: fused step {d['ms_per_step']:.3f} ms; HIP events around each step's "
                 f"{d['config']['launches_per_step']} launches give an average launch of {rf['avg_launch_ms']:.4f} ms, "
                 f"{rf['achieved']:.1f} GB/s = {100 * rf['frac']:.1f}% of 8 TB/s."]
-    head = [r for r in rows if re.search(r"encode_kernel<\d+, \d+, true>", r["Name"])]
-    if head:
-        a = float(head[0]["AverageNs"]) / 1e6
-        out.append(f"rocprofv3 average of `{kernel_label(head[0]['Name'])}` over all its dispatches (the headline "
-                   f"and the in-place leg): {a:.4f} ms.")
+    if args.trace_csv:
+        # the headline's dispatches are the first refresh-form encode launches
+        # of the run: warm-up steps, then the timed ones
+        with open(args.trace_csv, newline="") as fh:
+            tr = [r for r in csv.DictReader(fh) if re.search(r"encode_kernel<\d+, \d+, true>", r["Kernel_Name"])]
+        tr.sort(key=lambda r: int(r["Dispatch_Id"]))
+        nl = int(d["config"]["launches_per_step"])
+        first = int(d["warmup"]) * nl
+        timed = tr[first:first + int(d["steps"]) * nl]
+        if timed:
+            a = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in timed) / len(timed) / 1e6
+            out.append(f"rocprofv3 trace, the headline's timed dispatches of `{kernel_label(timed[0]['Kernel_Name'])}` "
+                       f"(dispatches {first + 1}-{first + len(timed)} of that kernel in this run): average {a:.4f} ms, "
+                       f"{100 * abs(a - rf['avg_launch_ms']) / rf['avg_launch_ms']:.1f}% from the events' "
+                       f"{rf['avg_launch_ms']:.4f} ms.  (The stats row above averages that kernel over every leg "
+                       f"that uses it: the in-place, std-reading, one-tensor, 0.5B and 7B-chain legs too.)")
     out += ["", "Launch sizes differ within a step (the last batch of a step holds fewer tensors), so Min/Max span "
                 "the batch sizes.  Kernels outside the library (torch's input generators) are left out."]
     with open(args.out, "w") as fh:
