@@ -343,13 +343,22 @@ int pulse_varint_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *
 /*
  * pulse_varint_decode -- indices back from a delta-varint stream (Alg. 1
  * Decode's DeltaDecode step).
- *   in          device bytes [in_capacity]; *nbytes (device uint64) of them
- *               form the stream.  A stream cut inside a number drops it.
+ *   in          device bytes [in_capacity], 16-byte aligned (EALIGN), with
+ *               in_capacity < 2^40 (EINVAL); *nbytes (device uint64) of them
+ *               form the stream.  A stream cut inside a number drops it; a
+ *               number of more than five bytes (not a uint32 varint) decodes
+ *               to an unspecified value.
  *   seg_begin   NULL (one segment) or device uint64 [nseg]: the entry where
  *               each segment starts (container metadata sent with the stream).
  *   idx         device uint32 [capacity] receiving the indices; entries past
  *               capacity are not written.
  *   count       device uint64: the number of entries in the stream.
+ *   workspace   as for encode.  The decode keeps its per-tile sums in the
+ *               workspace's status ring and leaves them zero, so the workspace
+ *               stays valid for the other ordered kernels on the same stream.
+ * Five launches (count, offsets, segment-start tiles, carries, write): the
+ * stream is read twice and the indices written once; no block waits on
+ * another.
  */
 int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t *nbytes,
                         const uint64_t *seg_begin, uint32_t nseg,
@@ -384,20 +393,22 @@ int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end
 /*
  * pulse_coo_decode -- the indices back from a 2-D COO delta stream (Alg. 1
  * Decode's Upcast and DeltaDecode steps for pulse_coo_encode's format).
- *   drow, dcol    device [pair_capacity]; *npairs (device) of them form the
- *                 stream.
+ *   drow, dcol    device [pair_capacity], both 16-byte aligned (EALIGN),
+ *                 pair_capacity < 2^40 (EINVAL); *npairs (device) of them
+ *                 form the stream.
  *   seg_begin     device [nseg]: the entry where each segment starts; *nent
  *                 (device) the number of entries (container metadata sent
  *                 with the stream, as encode's seg_begin and count).
  *   seg_pairs, first, cols   as pulse_coo_encode wrote / read them.
  *   idx           device uint32 [capacity]: entry k of the patch at idx[k];
  *                 entries at or past capacity are not written.
- * One kernel, two running sums chained per tile of pairs: the row and escape
- * count of each pair since its segment's start (a segmented running sum),
- * then its flat index (a running sum that restarts at each new-row pair),
- * written at its entry's position.  The library allocates nothing; the
- * workspace orders the tiles as for the other ordered kernels.  Requires
- * fewer than 2^22 escapes per segment (a tensor of at most 2^30 rows).  A
+ * Each pair acts on the (row, column) of the entry before it: (0, gap) moves
+ * the column, (dr, c + 1) moves dr rows down to column c, an escape 255 rows
+ * down.  These maps compose, so three launches (fold each tile's pairs, scan
+ * the tile folds, write) give every pair its row, column and escape count since
+ * its segment's start, and its entry lands at seg_begin[s] + 1 + (pairs of s
+ * before it) - (escapes of s before it).  The library allocates nothing: the
+ * per-tile folds live in the workspace's status ring and are left zero.  A
  * stream that encode did not write decodes to unspecified indices but no
  * access leaves the buffers.
  */

@@ -1,0 +1,798 @@
+// decode.hip -- the decoders of the patch's two index streams on gfx950, Alg. 1
+// Decode's DeltaDecode (and Upcast) steps for
+//   * the delta-varint stream (App. H.2 "Index Encoding", App. F.3 "Sparse
+//     stream format"): per segment the first index as it is, then differences,
+//     each an unsigned LEB128 varint;
+//   * the 2-D COO delta downcast (App. H.2 step 4, App. H.4.1 "Type
+//     downscaling"): per segment the first index, then (uint8 row field,
+//     uint16 column field) pairs, with (255, 0) escapes for long row gaps.
+//
+// Both decodes are running sums: an entry's index sums the differences since
+// its segment's start, and its place counts the numbers (or non-escape pairs)
+// before it.  Each is computed reduce-then-scan, so that no block ever waits
+// on another:
+//   1. reduce  one block per tile folds its part of the stream into an
+//              aggregate;
+//   2. scan    one block turns the tile aggregates into exclusive prefixes;
+//   3. write   one block per tile reads its part again, starts from its prefix
+//              and writes the indices, staged in LDS so that consecutive lanes
+//              store consecutive entries.
+// The stream is read twice and the indices written once.  (The single-pass
+// form with a decoupled look-back per tile, as the encoders use, was bound by
+// the look-back latency: 3.3 and 5.7 ms on a 306M-entry patch.)
+//
+// A tile is a whole number of units (4,096 bytes or pairs: 16 per thread of a
+// 256-thread block), as many as keep the tile count at most kMaxDecTiles for
+// the stream's actual length, read from the device.  The aggregates live in
+// the workspace's status ring, two words per tile, and the write pass clears
+// them to zero: the ring's other users (encode, sparsify, the stream
+// encoders) read a zero word as "not published yet", so the workspace can
+// still be shared with them on one stream.
+#include "device_common.hpp"
+#include "launch.hpp"
+
+namespace pulse {
+
+namespace {
+
+constexpr int kDT = 256;                     // threads per block of the tile kernels
+constexpr int kDWaves = kDT / 64;
+constexpr uint32_t kDUnit = kDT * 16;        // bytes (varint) or pairs (COO) per unit
+constexpr uint32_t kMaxDecTiles = 32767;     // two ring words per tile, kSlots words
+constexpr int kST = 1024;                    // threads of the single-block scans
+static_assert(2 * (uint64_t)(kMaxDecTiles + 1) <= kSlots, "tile aggregates exceed the ring");
+
+__device__ __forceinline__ uint64_t* dec_ring(uint64_t* ws) { return ws + kStatusOffsetWords; }
+
+// Tiles of a stream of n units' worth of items: each tile holds `per` units;
+// at least one tile (an empty stream still has segments to finish).
+struct Geo {
+  uint64_t tile;    // items per tile
+  uint32_t ntiles;
+};
+
+__device__ __forceinline__ Geo dec_geometry(uint64_t n) {
+  const uint64_t units = n == 0 ? 1 : (n + kDUnit - 1) / kDUnit;
+  const uint64_t per = (units + kMaxDecTiles - 1) / kMaxDecTiles;
+  Geo g;
+  g.tile = per * kDUnit;
+  g.ntiles = (uint32_t)((units + per - 1) / per);
+  return g;
+}
+
+// ---------------------------------------------------------------- block scans
+//
+// Exclusive scan over the threads of a block, in thread order, of an
+// associative operation comb(earlier, later) with identity T::id(); `carry`
+// comes before thread 0.  *total receives carry combined with every thread's
+// value.  Every thread of the block calls it; s_w holds one value per wave.
+
+// Segmented sum: f = a restart (a segment start) occurred, s = the sum since
+// the last one (or since the start, with no restart).
+struct SegSum {
+  uint32_t f, s;
+  __device__ static SegSum id() { return SegSum{0u, 0u}; }
+};
+__device__ __forceinline__ SegSum comb(SegSum x, SegSum y) {
+  return SegSum{x.f | y.f, y.f ? y.s : x.s + y.s};
+}
+__device__ __forceinline__ SegSum shfl_up(SegSum x, int d) {
+  return SegSum{(uint32_t)__shfl_up((int)x.f, d, 64), (uint32_t)__shfl_up((int)x.s, d, 64)};
+}
+
+// COO state.  Absolute (abs = 1): the current entry's row and column within
+// its tensor, and the escapes since its segment's start.  Relative (abs = 0):
+// the map a run of pairs applies to an absolute state --
+//   row += a;  col = k ? col + b : b;  e += e
+// -- which is how every pair acts: a same-row pair (0, gap) is (k 1, a 0,
+// b gap), a pair dr rows down (dr, col + 1) is (k 0, a dr, b col), an escape
+// (255, 0) is (k 1, a 255, b 0, e 1).  A segment start makes the state
+// absolute again from the segment's first index.  Composition: k = k1 k2,
+// a = a1 + a2, b = k2 ? b1 + b2 : b2, e = e1 + e2.
+struct CooEl {
+  uint32_t abs, k, a, b, e;
+  __device__ static CooEl id() { return CooEl{0u, 1u, 0u, 0u, 0u}; }
+};
+__device__ __forceinline__ CooEl comb(CooEl x, CooEl y) {
+  if (y.abs) return y;
+  CooEl r;
+  r.abs = x.abs;
+  r.k = x.abs ? 1u : (x.k & y.k);
+  r.a = x.a + y.a;
+  r.b = y.k ? x.b + y.b : y.b;
+  r.e = x.e + y.e;
+  return r;
+}
+__device__ __forceinline__ CooEl shfl_up(CooEl x, int d) {
+  CooEl r;
+  r.abs = (uint32_t)__shfl_up((int)x.abs, d, 64);
+  r.k = (uint32_t)__shfl_up((int)x.k, d, 64);
+  r.a = (uint32_t)__shfl_up((int)x.a, d, 64);
+  r.b = (uint32_t)__shfl_up((int)x.b, d, 64);
+  r.e = (uint32_t)__shfl_up((int)x.e, d, 64);
+  return r;
+}
+
+template <int NT, typename T>
+__device__ T block_scan_excl(T v, T carry, T* s_w, T* total) {
+  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
+  T inc = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const T o = shfl_up(inc, d);
+    if (lane >= d) inc = comb(o, inc);
+  }
+  const T before = shfl_up(inc, 1);
+  if (lane == 63) s_w[wid] = inc;
+  __syncthreads();
+  T pre = carry, all = carry;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    const T x = s_w[w];
+    if (w < wid) pre = comb(pre, x);
+    all = comb(all, x);
+  }
+  __syncthreads();  // s_w may be reused
+  *total = all;
+  return lane == 0 ? pre : comb(pre, before);
+}
+
+// Block-wide exclusive sum of one count per thread (thread order).
+__device__ uint32_t block_count_excl(uint32_t v, uint32_t* s_w, uint32_t* total) {
+  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
+  const uint32_t incl = wave_incl_scan(v);
+  if (lane == 63) s_w[wid] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kDWaves; ++w) {
+    const uint32_t x = s_w[w];
+    if (w < wid) before += x;
+    all += x;
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - v;
+}
+
+// First position in [0, n) with a[pos] >= key (a non-decreasing), whole wave.
+__device__ uint32_t lower_bound_wave(const uint64_t* a, uint32_t n, uint64_t key) {
+  const int lane = lane_id();
+  uint32_t lo = 0, hi = n;
+  while (hi - lo > 64) {
+    const uint32_t span = hi - lo;
+    const uint32_t q = lo + (uint32_t)((uint64_t)span * (uint32_t)(lane + 1) / 65u);
+    const uint64_t ge = __ballot(a[q] >= key);
+    if (ge == 0) {
+      lo = (uint32_t)__shfl((int)q, 63, 64) + 1;
+    } else {
+      const int f = __builtin_ctzll(ge);
+      const uint32_t qf = (uint32_t)__shfl((int)q, f, 64);
+      lo = f > 0 ? (uint32_t)__shfl((int)q, f - 1, 64) + 1 : lo;
+      hi = qf;
+    }
+  }
+  const uint32_t q = lo + (uint32_t)lane;
+  const uint64_t ge = __ballot(q < hi && a[q] >= key);
+  return ge == 0 ? hi : lo + (uint32_t)__builtin_ctzll(ge);
+}
+
+// Marks in the LDS bitmap (bit k - k0) every k in [k0, k1) at which a segment
+// starts (starts[s] = k; NULL starts: one segment), and bit 0 when k0 == 0 (the
+// stream's first item always starts one).  [s_range[0], s_range[1]) receives
+// the segments starting there.  Wave 0 only; the bitmap must be zero.
+__device__ void mark_segment_starts(const uint64_t* starts, uint32_t nseg, uint64_t k0, uint64_t k1,
+                                    uint32_t* s_bits, uint32_t* s_range) {
+  const int lane = lane_id();
+  uint32_t lo = 0, hi = 0;
+  if (starts && nseg > 0 && k1 > k0) {
+    lo = lower_bound_wave(starts, nseg, k0);
+    hi = lo;
+    for (uint32_t s = lo + (uint32_t)lane;; s += 64) {
+      const bool in = s < nseg && starts[s] < k1;
+      if (in) {
+        const uint32_t i = (uint32_t)(starts[s] - k0);
+        atomicOr(&s_bits[i >> 5], 1u << (i & 31));
+      }
+      const uint64_t m = __ballot(in);
+      hi += (uint32_t)__builtin_popcountll(m);
+      if (m != ~0ull) break;
+    }
+  }
+  if (lane == 0) {
+    if (k0 == 0 && k1 > 0) atomicOr(&s_bits[0], 1u);
+    s_range[0] = lo;
+    s_range[1] = hi;
+  }
+}
+
+__device__ __forceinline__ bool bit_at(const uint32_t* s_bits, uint32_t i) {
+  return (s_bits[i >> 5] >> (i & 31)) & 1u;
+}
+
+// The segment holding item k: the last segment starting at or before k, among
+// [lo, hi) (those starting in the unit), else the one before lo (0 if none).
+__device__ __forceinline__ uint32_t segment_of(const uint64_t* starts, uint32_t lo, uint32_t hi,
+                                               uint64_t k) {
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (starts[mid] <= k) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo > 0 ? lo - 1 : 0;
+}
+
+// ---------------------------------------------------------------- varint bytes
+
+// Sixteen stream bytes [pos, pos + 16) of a thread (pos a multiple of 16, the
+// stream 16-byte aligned) and the four before them.  Bytes before the stream
+// read as 0 (a terminator: the first number starts at byte 0); bytes at or past
+// n read as 0x80 (a continuation: a number cut by the end has no terminator
+// and is dropped).
+struct Bytes16 {
+  uint32_t h;      // bytes pos - 4 .. pos - 1, the first in the low byte
+  uint32_t w[4];   // bytes pos .. pos + 15
+};
+
+__device__ __forceinline__ Bytes16 load_bytes16(const uint8_t* in, uint64_t pos, uint64_t n) {
+  Bytes16 b;
+  b.h = pos >= 4 ? *reinterpret_cast<const uint32_t*>(in + pos - 4) : 0u;
+  if (pos + 16 <= n) {
+    const uint4 v = load16_stream(in + pos);
+    b.w[0] = v.x;
+    b.w[1] = v.y;
+    b.w[2] = v.z;
+    b.w[3] = v.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t x = 0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint64_t at = pos + (uint64_t)(4 * q + c);
+        const uint32_t byte = at < n ? (uint32_t)in[at] : 0x80u;
+        x |= byte << (8 * c);
+      }
+      b.w[q] = x;
+    }
+  }
+  return b;
+}
+
+__device__ __forceinline__ uint32_t terminators(const Bytes16& b) {
+  uint32_t c = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) c += (uint32_t)__builtin_popcount(~b.w[q] & 0x80808080u);
+  return c;
+}
+
+// Calls emit(value) for every number that ends in the sixteen bytes, in
+// order.  A number starts after a terminator; it ends at most four bytes
+// after its start in a valid stream, so starting the walk four bytes early
+// finds the start of every number that ends in the sixteen.  (A number of
+// more than five bytes is not a uint32 varint; its value is unspecified.)
+template <typename Emit>
+__device__ __forceinline__ void walk_numbers(const Bytes16& b, Emit emit) {
+  uint32_t cur = 0, sh = 0;
+  bool start = true;
+#pragma unroll
+  for (int j = -4; j < 16; ++j) {
+    const uint32_t byte = j < 0 ? (b.h >> (8 * (j + 4))) & 0xFFu : (b.w[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+    const uint32_t v7 = byte & 0x7Fu;
+    if (start) {
+      cur = v7;
+      sh = 7;
+    } else {
+      cur |= sh < 32 ? v7 << sh : 0u;
+      sh += 7;
+    }
+    start = (byte & 0x80u) == 0;
+    if (j >= 0 && start) emit(cur);
+  }
+}
+
+struct VarintLds {
+  uint32_t val[kDUnit];          // the unit's indices, in entry order
+  uint32_t bits[kDUnit / 32];    // segment starts among the unit's entries
+  uint32_t range[2];
+  uint32_t w[kDWaves];
+  SegSum ws[kDWaves];
+};
+
+// One unit of the stream, bytes [u0, u1) (u1 <= n), whose first entry is
+// entry e0.  Returns `carry` (the running sum before the unit) combined with
+// the unit's entries; *cnt receives the unit's entry count.  WRITE: the
+// indices are written.  Every thread of the block calls it.
+template <bool WRITE>
+__device__ SegSum varint_unit(const VarintDecParams& p, uint64_t u0, uint64_t u1, uint64_t n,
+                              uint64_t e0, SegSum carry, uint32_t* cnt, VarintLds& L) {
+  const int tid = (int)threadIdx.x;
+  const uint64_t pos = u0 + 16ull * (uint64_t)tid;
+  Bytes16 b;
+  b.h = 0;
+  b.w[0] = b.w[1] = b.w[2] = b.w[3] = 0x80808080u;  // no bytes: no terminators
+  if (pos < u1) b = load_bytes16(p.in, pos, n);
+  for (uint32_t i = (uint32_t)tid; i < kDUnit / 32; i += kDT) L.bits[i] = 0;
+  uint32_t ucnt;
+  const uint32_t rank = block_count_excl(terminators(b), L.w, &ucnt);  // syncs
+  if (tid < 64) mark_segment_starts(p.seg_begin, p.nseg, e0, e0 + ucnt, L.bits, L.range);
+  __syncthreads();
+  // this thread's running sum since its last restart
+  SegSum mine = SegSum::id();
+  uint32_t k = rank;
+  walk_numbers(b, [&](uint32_t v) {
+    if (bit_at(L.bits, k)) {
+      mine.f = 1u;
+      mine.s = v;
+    } else {
+      mine.s += v;
+    }
+    ++k;
+  });
+  SegSum total;
+  const SegSum before = block_scan_excl<kDT>(mine, carry, L.ws, &total);
+  if (WRITE) {
+    uint32_t acc = before.s;
+    k = rank;
+    walk_numbers(b, [&](uint32_t v) {
+      acc = bit_at(L.bits, k) ? v : acc + v;
+      L.val[k] = acc;
+      ++k;
+    });
+    __syncthreads();
+    for (uint32_t i = (uint32_t)tid; i < ucnt; i += kDT) {
+      const uint64_t e = e0 + i;
+      if (e < p.capacity) p.idx[e] = L.val[i];
+    }
+  }
+  __syncthreads();  // bits, range and val are rewritten by the next unit
+  *cnt = ucnt;
+  return total;
+}
+
+// ---------------------------------------------------------------- COO pairs
+
+// Sixteen pairs [q, q + 16) of a thread (q a multiple of 16; drow and dcol
+// 16-byte aligned); pairs at or past n read as (0, 0) and are not used.
+struct Pairs16 {
+  uint32_t r[4];   // row fields, 4 per word
+  uint32_t c[8];   // column fields, 2 per word
+};
+
+__device__ __forceinline__ Pairs16 load_pairs16(const uint8_t* drow, const uint16_t* dcol, uint64_t q,
+                                                uint64_t n) {
+  Pairs16 x;
+  if (q + 16 <= n) {
+    const uint4 r = load16_stream(drow + q);
+    const uint4 c0 = load16_stream(dcol + q);
+    const uint4 c1 = load16_stream(dcol + q + 8);
+    x.r[0] = r.x; x.r[1] = r.y; x.r[2] = r.z; x.r[3] = r.w;
+    x.c[0] = c0.x; x.c[1] = c0.y; x.c[2] = c0.z; x.c[3] = c0.w;
+    x.c[4] = c1.x; x.c[5] = c1.y; x.c[6] = c1.z; x.c[7] = c1.w;
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) x.r[w] = 0;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) x.c[w] = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (q + (uint64_t)j < n) {
+        x.r[j >> 2] |= (uint32_t)drow[q + j] << (8 * (j & 3));
+        x.c[j >> 1] |= (uint32_t)dcol[q + j] << (16 * (j & 1));
+      }
+    }
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint32_t pair_row(const Pairs16& x, int j) {
+  return (x.r[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+}
+__device__ __forceinline__ uint32_t pair_col(const Pairs16& x, int j) {
+  return (x.c[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+}
+
+// The map of one pair (see CooEl).
+__device__ __forceinline__ CooEl pair_map(uint32_t dr, uint32_t dc) {
+  if (dr == 255u && dc == 0u) return CooEl{0u, 1u, 255u, 0u, 1u};  // escape
+  if (dr == 0u) return CooEl{0u, 1u, 0u, dc, 0u};
+  return CooEl{0u, 0u, dr, dc - 1u, 0u};
+}
+
+// The absolute state at segment s's start: its first index as (row, column).
+__device__ __forceinline__ CooEl segment_state(const CooDecParams& p, uint32_t s, uint32_t* C) {
+  const uint32_t c = p.cols[s];
+  *C = c > 0 ? c : 1u;
+  const uint32_t f = p.first[s];
+  const uint32_t row = f / *C;
+  return CooEl{1u, 1u, row, f - row * *C, 0u};
+}
+
+struct CooLds {
+  uint32_t seg[kDUnit / 32];     // segment starts among the unit's pairs
+  uint32_t esc[kDUnit / 32];     // escape pairs
+  uint32_t range[2];
+  uint64_t ref;                  // the position of the unit's first pair
+  CooEl ws[kDWaves];
+};
+
+// The write pass's staging of a unit's entries.
+struct CooStage {
+  uint32_t val[kDUnit];          // flat index of each pair's entry
+  uint32_t pos[kDUnit];          // low 32 bits of its position
+};
+
+// Writes segment s's first index at its first entry (if it has entries).
+__device__ __forceinline__ void put_first(const CooDecParams& p, uint64_t nent, uint32_t s) {
+  const uint64_t b = p.seg_begin[s];
+  const uint64_t e = s + 1 < p.nseg ? p.seg_begin[s + 1] : nent;
+  if (e > b && b < p.capacity) p.idx[b] = p.first[s];
+}
+
+// One unit of pairs [q0, q1) (q1 <= n).  Returns carry combined with the
+// unit's pairs.  WRITE: the entries are written, and the first index of every
+// segment that starts in the unit (the last unit of the stream also those
+// that start at its end).  Every thread of the block calls it.
+template <bool WRITE>
+__device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint64_t n, uint64_t nent,
+                          CooEl carry, bool last_unit, CooLds& L, CooStage* S) {
+  const int tid = (int)threadIdx.x;
+  const uint64_t q = q0 + 16ull * (uint64_t)tid;
+  for (uint32_t i = (uint32_t)tid; i < kDUnit / 32; i += kDT) {
+    L.seg[i] = 0;
+    L.esc[i] = 0;
+  }
+  Pairs16 x;
+  if (q < q1) x = load_pairs16(p.drow, p.dcol, q, n);
+  __syncthreads();
+  if (tid < 64) mark_segment_starts(p.seg_pairs, p.nseg, q0, q1, L.seg, L.range);
+  __syncthreads();
+  const uint32_t lo = L.range[0], hi = L.range[1];
+  const uint32_t m = q < q1 ? (uint32_t)(q1 - q < 16 ? q1 - q : 16) : 0u;  // this thread's pairs
+  const uint32_t i0 = (uint32_t)tid * 16u;
+  // this thread's map (absolute from its last segment start on)
+  CooEl mine = CooEl::id();
+  uint32_t C = 1;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    if ((uint32_t)j < m) {
+      if (bit_at(L.seg, i0 + j)) mine = segment_state(p, segment_of(p.seg_pairs, lo, hi, q + j), &C);
+      mine = comb(mine, pair_map(pair_row(x, j), pair_col(x, j)));
+    }
+  }
+  CooEl total;
+  const CooEl before = block_scan_excl<kDT>(mine, carry, L.ws, &total);
+  if (WRITE) {
+    // Pair i's entry lands at seg_begin[s] + 1 + (pairs of s before it) -
+    // (escapes of s before it).  Positions of one unit lie within
+    // kDUnit + nseg < 2^31 of each other, so each is kept as its low 32 bits
+    // beside the unit's first position.
+    CooEl st = before;
+    uint32_t s = 0;
+    uint64_t sp = 0, sb = 0;
+    C = 1;
+    uint32_t escb = 0;
+    if (m > 0) {
+      s = segment_of(p.seg_pairs, lo, hi, q);
+      const uint32_t c = p.cols[s];
+      C = c > 0 ? c : 1u;
+      sp = p.seg_pairs[s];
+      sb = p.seg_begin[s];
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if ((uint32_t)j < m) {
+        const uint64_t qj = q + (uint64_t)j;
+        if (bit_at(L.seg, i0 + j)) {
+          s = segment_of(p.seg_pairs, lo, hi, qj);
+          st = segment_state(p, s, &C);
+          sp = p.seg_pairs[s];
+          sb = p.seg_begin[s];
+        }
+        const uint32_t dr = pair_row(x, j), dc = pair_col(x, j);
+        const uint64_t at = sb + 1 + (qj - sp) - st.e;
+        st = comb(st, pair_map(dr, dc));
+        if (dr == 255u && dc == 0u) escb |= 1u << j;
+        S->val[i0 + j] = st.a * C + st.b;
+        S->pos[i0 + j] = (uint32_t)at;
+        if (qj == q0) L.ref = at;
+      }
+    }
+    if (m > 0) atomicOr(&L.esc[i0 >> 5], escb << (i0 & 31));
+    __syncthreads();
+    const uint64_t ref = L.ref;
+    const uint32_t cnt = (uint32_t)(q1 - q0);
+    for (uint32_t i = (uint32_t)tid; i < cnt; i += kDT) {
+      if (bit_at(L.esc, i)) continue;  // an escape has no entry
+      const uint64_t at = ref + (uint64_t)(int64_t)(int32_t)(S->pos[i] - (uint32_t)ref);
+      if (at < p.capacity) p.idx[at] = S->val[i];
+    }
+    if (tid < 64) {
+      for (uint32_t t = lo + (uint32_t)lane_id(); t < hi; t += 64) put_first(p, nent, t);
+      if (last_unit) {
+        const uint32_t from = lower_bound_wave(p.seg_pairs, p.nseg, n);
+        for (uint32_t t = from + (uint32_t)lane_id(); t < p.nseg; t += 64) put_first(p, nent, t);
+      }
+    }
+  }
+  __syncthreads();  // the LDS arrays are rewritten by the next unit
+  return total;
+}
+
+__device__ __forceinline__ void store_el(uint64_t* w, CooEl x) {
+  w[0] = (uint64_t)x.a | ((uint64_t)x.b << 32);
+  w[1] = (uint64_t)x.e | ((uint64_t)x.k << 32) | ((uint64_t)x.abs << 33);
+}
+__device__ __forceinline__ CooEl load_el(const uint64_t* w) {
+  const uint64_t w0 = w[0], w1 = w[1];
+  return CooEl{(uint32_t)(w1 >> 33) & 1u, (uint32_t)(w1 >> 32) & 1u, (uint32_t)w0,
+               (uint32_t)(w0 >> 32), (uint32_t)w1};
+}
+
+// Exclusive scan of n elements in place by one block of kST threads: each
+// thread folds a run of consecutive elements, the runs are scanned, and each
+// thread writes its run's prefixes.  *total (thread 0) receives the fold of all.
+template <typename T, typename Load, typename Store>
+__device__ void single_block_scan(uint32_t n, Load ld, Store st, T* s_w, T* total) {
+  const uint32_t per = (n + kST - 1) / kST;
+  const uint32_t a = (uint32_t)threadIdx.x * per;
+  const uint32_t b = a + per < n ? a + per : n;
+  T run = T::id();
+  for (uint32_t i = a; i < b; ++i) run = comb(run, ld(i));
+  T all;
+  T pre = block_scan_excl<kST>(run, T::id(), s_w, &all);
+  for (uint32_t i = a; i < b; ++i) {
+    const T x = ld(i);
+    st(i, pre);
+    pre = comb(pre, x);
+  }
+  *total = all;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- varint
+//
+// Ring layout: word b holds tile b's (entries | sum << 32), word kMaxDecTiles + 1 + b
+// its first entry (| 1 << 63 once a segment start is known to lie in it).
+
+__global__ __launch_bounds__(kDT) void varint_count_kernel(VarintDecParams p) {
+  __shared__ uint32_t s_w[kDWaves];
+  __shared__ uint32_t s_w2[kDWaves];
+  const uint64_t n0 = *p.nbytes;
+  const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
+  const Geo g = dec_geometry(n);
+  if (blockIdx.x >= g.ntiles) return;
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  uint32_t cnt = 0, sum = 0;
+  for (uint64_t pos = t0 + 16ull * threadIdx.x; pos < t1; pos += 16ull * kDT) {
+    const Bytes16 b = load_bytes16(p.in, pos, n);
+    cnt += terminators(b);
+    walk_numbers(b, [&](uint32_t v) { sum += v; });
+  }
+  // block sums of both
+  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
+  const uint32_t c = __builtin_amdgcn_readlane(wave_incl_scan(cnt), 63);
+  const uint32_t s = __builtin_amdgcn_readlane(wave_incl_scan(sum), 63);
+  if (lane == 0) {
+    s_w[wid] = c;
+    s_w2[wid] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t C = 0, S = 0;
+    for (int w = 0; w < kDWaves; ++w) {
+      C += s_w[w];
+      S += s_w2[w];
+    }
+    dec_ring(p.ws)[blockIdx.x] = (uint64_t)C | ((uint64_t)S << 32);
+  }
+}
+
+// One block: each tile's first entry, and the entry count.
+__global__ __launch_bounds__(kST) void varint_offsets_kernel(VarintDecParams p) {
+  __shared__ uint64_t s_w[kST / 64];
+  const uint64_t n0 = *p.nbytes;
+  const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
+  const Geo g = dec_geometry(n);
+  uint64_t* ring = dec_ring(p.ws);
+  const uint32_t per = (g.ntiles + kST - 1) / kST;
+  const uint32_t a = (uint32_t)threadIdx.x * per;
+  const uint32_t b = a + per < g.ntiles ? a + per : g.ntiles;
+  uint64_t run = 0;
+  for (uint32_t i = a; i < b; ++i) run += (uint32_t)ring[i];
+  // block exclusive sum of the runs (64-bit)
+  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
+  uint64_t inc = run;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint64_t o = __shfl_up(inc, d, 64);
+    if (lane >= d) inc += o;
+  }
+  if (lane == 63) s_w[wid] = inc;
+  __syncthreads();
+  uint64_t pre = inc - run, all = 0;
+  for (int w = 0; w < kST / 64; ++w) {
+    if (w < wid) pre += s_w[w];
+    all += s_w[w];
+  }
+  for (uint32_t i = a; i < b; ++i) {
+    ring[kMaxDecTiles + 1 + i] = pre;
+    pre += (uint32_t)ring[i];
+  }
+  if (threadIdx.x == 0) *p.count = all;
+}
+
+// Tiles that hold a segment start: their sum since the last start in them.
+__global__ __launch_bounds__(kDT) void varint_restarts_kernel(VarintDecParams p) {
+  __shared__ VarintLds L;
+  __shared__ int s_has;
+  const uint64_t n0 = *p.nbytes;
+  const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
+  const Geo g = dec_geometry(n);
+  if (blockIdx.x >= g.ntiles) return;
+  uint64_t* ring = dec_ring(p.ws);
+  const uint64_t e0 = ring[kMaxDecTiles + 1 + blockIdx.x];
+  const uint64_t w0 = ring[blockIdx.x];
+  const uint64_t ecnt = (uint32_t)w0;
+  if (threadIdx.x < 64) {
+    bool has = e0 == 0 && ecnt > 0;
+    if (!has && p.seg_begin && p.nseg > 0) {
+      const uint32_t s = lower_bound_wave(p.seg_begin, p.nseg, e0);
+      has = s < p.nseg && p.seg_begin[s] < e0 + ecnt;
+    }
+    if (threadIdx.x == 0) s_has = has ? 1 : 0;
+  }
+  __syncthreads();
+  if (!s_has) return;  // block-uniform
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  SegSum run = SegSum::id();
+  uint64_t e = e0;
+  for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
+    const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    uint32_t c;
+    run = varint_unit<false>(p, u0, u1, n, e, run, &c, L);
+    e += c;
+  }
+  if (threadIdx.x == 0) {
+    ring[blockIdx.x] = (uint64_t)(uint32_t)w0 | ((uint64_t)run.s << 32);
+    ring[kMaxDecTiles + 1 + blockIdx.x] = e0 | (1ull << 63);
+  }
+}
+
+// One block: the running sum carried into each tile.
+__global__ __launch_bounds__(kST) void varint_carry_kernel(VarintDecParams p) {
+  __shared__ SegSum s_w[kST / 64];
+  const uint64_t n0 = *p.nbytes;
+  const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
+  const Geo g = dec_geometry(n);
+  uint64_t* ring = dec_ring(p.ws);
+  auto ld = [&](uint32_t i) {
+    return SegSum{(uint32_t)(ring[kMaxDecTiles + 1 + i] >> 63), (uint32_t)(ring[i] >> 32)};
+  };
+  auto st = [&](uint32_t i, SegSum c) { ring[i] = (ring[i] & 0xFFFFFFFFull) | ((uint64_t)c.s << 32); };
+  SegSum all;
+  single_block_scan<SegSum>(g.ntiles, ld, st, s_w, &all);
+}
+
+__global__ __launch_bounds__(kDT) void varint_write_kernel(VarintDecParams p) {
+  __shared__ VarintLds L;
+  const uint64_t n0 = *p.nbytes;
+  const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
+  const Geo g = dec_geometry(n);
+  if (blockIdx.x >= g.ntiles) return;
+  uint64_t* ring = dec_ring(p.ws);
+  const uint64_t e0 = ring[kMaxDecTiles + 1 + blockIdx.x] & ~(1ull << 63);
+  SegSum run = SegSum{0u, (uint32_t)(ring[blockIdx.x] >> 32)};
+  __syncthreads();  // every thread has read the tile's words
+  if (threadIdx.x == 0) {
+    ring[blockIdx.x] = 0;
+    ring[kMaxDecTiles + 1 + blockIdx.x] = 0;
+  }
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  uint64_t e = e0;
+  for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
+    const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    uint32_t c;
+    run = varint_unit<true>(p, u0, u1, n, e, run, &c, L);
+    e += c;
+  }
+}
+
+// ---------------------------------------------------------------- COO
+//
+// Ring layout: words 2b, 2b + 1 hold tile b's map, then its exclusive prefix.
+
+__global__ __launch_bounds__(kDT) void coo_reduce_kernel(CooDecParams p) {
+  __shared__ CooLds L;
+  const uint64_t n0 = *p.npairs;
+  const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
+  const uint64_t nent = *p.nent;
+  const Geo g = dec_geometry(n);
+  if (blockIdx.x >= g.ntiles) return;
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  CooEl run = CooEl::id();
+  for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
+    const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    run = coo_unit<false>(p, u0, u1, n, nent, run, false, L, nullptr);
+  }
+  if (threadIdx.x == 0) store_el(dec_ring(p.ws) + 2ull * blockIdx.x, run);
+}
+
+__global__ __launch_bounds__(kST) void coo_scan_kernel(CooDecParams p) {
+  __shared__ CooEl s_w[kST / 64];
+  const uint64_t n0 = *p.npairs;
+  const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
+  const Geo g = dec_geometry(n);
+  uint64_t* ring = dec_ring(p.ws);
+  auto ld = [&](uint32_t i) { return load_el(ring + 2ull * i); };
+  auto st = [&](uint32_t i, CooEl x) { store_el(ring + 2ull * i, x); };
+  CooEl all;
+  single_block_scan<CooEl>(g.ntiles, ld, st, s_w, &all);
+}
+
+__global__ __launch_bounds__(kDT) void coo_write_kernel(CooDecParams p) {
+  __shared__ CooLds L;
+  __shared__ CooStage S;
+  const uint64_t n0 = *p.npairs;
+  const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
+  const uint64_t nent = *p.nent;
+  const Geo g = dec_geometry(n);
+  if (blockIdx.x >= g.ntiles) return;
+  uint64_t* ring = dec_ring(p.ws) + 2ull * blockIdx.x;
+  CooEl run = load_el(ring);
+  __syncthreads();  // every thread has read the tile's words
+  if (threadIdx.x == 0) {
+    ring[0] = 0;
+    ring[1] = 0;
+  }
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  if (t0 >= t1) {  // the empty stream: only the segments' first indices
+    run = coo_unit<true>(p, 0, 0, n, nent, run, true, L, &S);
+    return;
+  }
+  for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
+    const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    run = coo_unit<true>(p, u0, u1, n, nent, run, u1 == n, L, &S);
+  }
+}
+
+// ---------------------------------------------------------------- launch
+
+static uint32_t dec_grid(uint64_t capacity) {
+  const uint64_t units = capacity == 0 ? 1 : (capacity + kDUnit - 1) / kDUnit;
+  return (uint32_t)(units < kMaxDecTiles ? units : kMaxDecTiles);
+}
+
+uint64_t decode_max_items() { return 1ull << 40; }
+
+hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream) {
+  const uint32_t grid = dec_grid(p.in_capacity);
+  hipLaunchKernelGGL(varint_count_kernel, dim3(grid), dim3(kDT), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(varint_offsets_kernel, dim3(1), dim3(kST), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(varint_restarts_kernel, dim3(grid), dim3(kDT), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(varint_carry_kernel, dim3(1), dim3(kST), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(varint_write_kernel, dim3(grid), dim3(kDT), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream) {
+  const uint32_t grid = dec_grid(p.pair_capacity);
+  hipLaunchKernelGGL(coo_reduce_kernel, dim3(grid), dim3(kDT), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(coo_scan_kernel, dim3(1), dim3(kST), 0, stream, p);
+  if (hipError_t e = hipGetLastError()) return e;
+  hipLaunchKernelGGL(coo_write_kernel, dim3(grid), dim3(kDT), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace pulse

@@ -149,8 +149,6 @@ struct VarintDecParams {
   uint32_t* idx;
   uint64_t capacity;           // entries writable in idx
   uint64_t* count;             // device: entries decoded
-  uint32_t ntiles;             // byte tiles
-  uint32_t ntiles2;            // entry tiles
 };
 
 // Receivers that compute in a lower precision D (App. D); kDtypeFp8 and
@@ -281,7 +279,6 @@ struct CooDecParams {
   const uint64_t* nent;        // device: entries in the patch
   uint32_t* idx;
   uint64_t capacity;
-  uint32_t ntiles;
 };
 
 static_assert(sizeof(EncodeParams) < 4096, "kernel argument block too large");
@@ -299,7 +296,8 @@ hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t 
 hipError_t launch_zero_words(uint64_t* p, uint64_t nwords, hipStream_t stream);
 uint64_t outer_unit_elems();
 uint32_t varint_entry_tile();
-uint32_t varint_byte_tile();
+// Largest stream (bytes or pairs) the decoders take.
+uint64_t decode_max_items();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream);

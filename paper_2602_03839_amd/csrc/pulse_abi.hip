@@ -547,12 +547,10 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   if (!aligned(nbytes, 8) || !aligned(count, 8) || (seg_begin && !aligned(seg_begin, 8)))
     return fail(PULSE_EALIGN, "varint decode: counters not 8-byte aligned");
   if (idx && !aligned(idx, 4)) return fail(PULSE_EALIGN, "varint decode: idx misaligned");
+  if (in && !aligned16(in)) return fail(PULSE_EALIGN, "varint decode: in not 16-byte aligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  const uint64_t bt = pulse::varint_byte_tile(), et = pulse::varint_entry_tile();
-  const uint64_t nt = in_capacity == 0 ? 1 : (in_capacity + bt - 1) / bt;
-  const uint64_t nt2 = capacity == 0 ? 1 : (capacity + et - 1) / et;
-  if (nt > pulse::kMaxTicketedTiles || nt2 > pulse::kMaxTicketedTiles)
-    return fail(PULSE_EINVAL, "varint decode: capacity too large");
+  if (in_capacity >= pulse::decode_max_items())
+    return fail(PULSE_EINVAL, "varint decode: in_capacity too large");
   pulse::VarintDecParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -564,8 +562,6 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   p.idx = idx;
   p.capacity = capacity;
   p.count = count;
-  p.ntiles = (uint32_t)nt;
-  p.ntiles2 = (uint32_t)nt2;
   return hip_status(pulse::launch_varint_decode(p, (hipStream_t)stream), "varint decode launch");
 }
 
@@ -619,12 +615,13 @@ int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_ca
   if (capacity > 0 && !idx) return fail(PULSE_EINVAL, "coo decode: idx is NULL");
   if (!aligned(npairs, 8) || !aligned(seg_begin, 8) || !aligned(seg_pairs, 8) || !aligned(nent, 8))
     return fail(PULSE_EALIGN, "coo decode: counters not 8-byte aligned");
-  if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4) || (dcol && !aligned(dcol, 2)))
-    return fail(PULSE_EALIGN, "coo decode: idx/cols/first/dcol misaligned");
+  if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4))
+    return fail(PULSE_EALIGN, "coo decode: idx/cols/first misaligned");
+  if ((drow && !aligned16(drow)) || (dcol && !aligned16(dcol)))
+    return fail(PULSE_EALIGN, "coo decode: drow/dcol not 16-byte aligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  const uint64_t tile = pulse::varint_entry_tile();
-  const uint64_t nt = pair_capacity == 0 ? 1 : (pair_capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
+  if (pair_capacity >= pulse::decode_max_items())
+    return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
   pulse::CooDecParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -640,7 +637,6 @@ int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_ca
   p.nent = nent;
   p.idx = idx;
   p.capacity = capacity;
-  p.ntiles = (uint32_t)nt;
   return hip_status(pulse::launch_coo_decode(p, (hipStream_t)stream), "coo decode launch");
 }
 

@@ -1,37 +1,26 @@
-// varint.hip -- the delta-varint index stream of a sorted patch on gfx950
-// (App. H.2 "Index Encoding": first index as it is, then differences; App. F.3
-// "Sparse stream format": delta-encoded, varint-packed indices).  Each number
-// is an unsigned varint: 7-bit groups, least significant first, every byte but
-// the last carrying 0x80.  A patch of several tensors is a list of segments
-// (one per tensor); every segment restarts with its first index as it is.
+// varint.hip -- the encoders of a sorted patch's two index streams on gfx950:
 //
-// All three kernels are persistent chained scans over tiles drawn by ticket,
-// with the same workspace ticket counter and status ring (and the same
-// decoupled look-back) as encode and sparsify, so they may share a workspace
-// with them on one stream:
-//   varint_encode_kernel   entries -> bytes: per-entry varint lengths, their
-//                          ordered exclusive sum gives each entry's bytes.
-//   varint_gaps_kernel     bytes -> differences at entry positions: the
-//                          ordered count of terminating bytes numbers the
-//                          entries.
-//   varint_sums_kernel     differences -> indices: a segmented running sum,
-//                          restarting at every segment's first entry; a tile
-//                          that holds a restart knows its inclusive sum by
-//                          itself and publishes it as a prefix at once.
-// Each tile is staged in LDS so global loads and stores stay contiguous.
+//   * the delta-varint stream (App. H.2 "Index Encoding": first index as it
+//     is, then differences; App. F.3 "Sparse stream format": delta-encoded,
+//     varint-packed indices).  Each number is an unsigned varint: 7-bit
+//     groups, least significant first, every byte but the last carrying 0x80.
+//     A patch of several tensors is a list of segments (one per tensor);
+//     every segment restarts with its first index as it is.
+//     varint_encode_kernel: per-entry varint lengths, whose ordered exclusive
+//     sum gives each entry's bytes.
+//   * the 2-D COO delta downcast of App. H.2 step 4 / App. H.4.1
+//     (coo_encode_kernel): per tensor (row-major, `cols` columns) the first
+//     index as it is, then one (uint8 row field, uint16 column field) pair per
+//     later entry -- (0, column gap) within a row, (rows ahead, column + 1) on
+//     a later row -- with (255, 0) escape pairs, each 255 rows, ahead of a gap
+//     of more than 255 rows.  An entry's pair count is 1 + its escapes; their
+//     ordered exclusive sum places its pairs.
 //
-// The same machinery writes the 2-D COO delta downcast of App. H.2 step 4 /
-// App. H.4.1 (coo_encode_kernel): per tensor (row-major, `cols` columns) the
-// first index as it is, then one (uint8 row field, uint16 column field) pair
-// per later entry -- (0, column gap) within a row, (rows ahead, column + 1) on
-// a later row -- with (255, 0) escape pairs, each 255 rows, ahead of a gap of
-// more than 255 rows.  An entry's pair count is 1 + its escapes; their ordered
-// exclusive sum places its pairs.  Its decode (coo_decode_kernel) is two
-// segmented running sums over the pairs, both chained in the same pass over
-// pair tiles: the row and escape count since the segment's start (both
-// restarting at segment starts, packed into one scanned value), then the flat
-// index (restarting at every new-row pair and segment start), written at the
-// entry's position.
+// Both are persistent chained scans over tiles drawn by ticket, with the same
+// workspace ticket counter and status ring (and the same decoupled look-back)
+// as encode and sparsify, so they may share a workspace with them on one
+// stream.  Each tile is staged in LDS so global loads and stores stay
+// contiguous.  The decoders are in decode.hip.
 #include "device_common.hpp"
 #include "launch.hpp"
 
@@ -42,7 +31,6 @@ namespace {
 constexpr int kVT = 256;                  // threads per block
 constexpr int kVPer = 16;                 // entries per thread
 constexpr uint32_t kVTile = kVT * kVPer;  // 4096 entries per tile
-constexpr uint32_t kBTile = 8192;         // bytes per decode tile (32 per thread)
 constexpr int kVWaves = kVT / 64;
 
 __device__ __forceinline__ uint32_t varint_len(uint32_t d) {
@@ -90,17 +78,15 @@ __device__ uint32_t wave_lower_bound64(const uint64_t* a, uint32_t n, uint64_t k
   return ge == 0 ? hi : lo + (uint32_t)__builtin_ctzll(ge);
 }
 
-// Persistent ticket loop shared by the three kernels.  fn(tk) processes tile
+// Persistent ticket loop shared by the two encoders.  fn(tk) processes tile
 // tk.tile; every thread of the block calls it.  One tile per ticket: a block
 // publishes a tile's aggregate only when it reaches the tile, so with several
 // tiles per ticket the first tile of the next block's draw would wait for
 // this block's later tiles, each behind its own look-back -- a chain through
 // every block.  (The encode and sparsify kernels draw four at a time because
 // they publish aggregates iterations ahead of resolving.)
-// A kernel that runs SPT chained scans per tile (SPT sequence numbers per
-// tile) passes SPT, so the next launch starts past all of them.
 template <typename Fn>
-__device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn, uint32_t spt = 1) {
+__device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn) {
   __shared__ uint64_t s_tk;
   uint64_t g0 = 0;  // thread 0 only
   for (;;) {
@@ -115,31 +101,23 @@ __device__ void for_each_ticket(uint64_t* ws, uint32_t ntiles, Fn fn, uint32_t s
     if (tk.tile >= ntiles) break;
     fn(tk);
   }
-  if (threadIdx.x == 0) finish_launch(ws, g0, ntiles * spt, gridDim.x);
+  if (threadIdx.x == 0) finish_launch(ws, g0, ntiles, gridDim.x);
 }
 
 // Exclusive prefix of the tile's `agg` over the earlier tiles of the launch
-// (block-uniform result).  With `restart`, the tile's inclusive value is
-// `incl_known` whatever came before (a segment starts in it), published as a
-// prefix at once; the tile still looks back for its own entries before the
-// restart.
-// WIDE: aggregates may exceed 32 bits (the look-back then sums in 64 bits).
-// STRIDE: sequence numbers per tile (see look_back_issue).
-template <bool WIDE = false, int STRIDE = 1>
-__device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg, bool restart,
-                                    uint64_t incl_known, uint64_t* s_b) {
+// (block-uniform result).
+__device__ uint64_t chain_exclusive(uint64_t* ws, const Ticket& tk, uint64_t agg, uint64_t* s_b) {
   if (threadIdx.x < 64) {
     const int lane = lane_id();
     uint64_t excl = 0;
     if (tk.tile == 0) {
-      if (lane == 0) status_publish(ws, tk.seq, kFlagPrefix, restart ? incl_known : agg);
+      if (lane == 0) status_publish(ws, tk.seq, kFlagPrefix, agg);
     } else {
-      if (lane == 0)
-        status_publish(ws, tk.seq, restart ? kFlagPrefix : kFlagAggregate, restart ? incl_known : agg);
+      if (lane == 0) status_publish(ws, tk.seq, kFlagAggregate, agg);
       LookWindow<1> win;
-      look_back_issue<1, STRIDE>(ws, tk, (int64_t)tk.tile - 1, win);
-      excl = look_back<1, WIDE, STRIDE>(ws, tk, win);
-      if (lane == 0 && !restart) status_publish(ws, tk.seq, kFlagPrefix, excl + agg);
+      look_back_issue<1>(ws, tk, (int64_t)tk.tile - 1, win);
+      excl = look_back<1>(ws, tk, win);
+      if (lane == 0) status_publish(ws, tk.seq, kFlagPrefix, excl + agg);
     }
     if (lane == 0) *s_b = excl;
   }
@@ -224,7 +202,7 @@ __global__ __launch_bounds__(kVT) void varint_encode_kernel(VarintEncParams p) {
     uint32_t agg32;
     const uint32_t texcl = block_excl_sum(sum, s_w, &agg32);
     const uint64_t agg = agg32;
-    const uint64_t excl = chain_exclusive(p.ws, tk, agg, false, 0, &s_b);
+    const uint64_t excl = chain_exclusive(p.ws, tk, agg, &s_b);
     // bytes into LDS
     uint32_t o = texcl;
 #pragma unroll
@@ -261,165 +239,6 @@ __global__ __launch_bounds__(kVT) void varint_encode_kernel(VarintEncParams p) {
         for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) p.seg_bytes[s] = total;
       }
     }
-    __syncthreads();
-  });
-}
-
-// ---------------------------------------------------------------- decode, pass 1
-
-__global__ __launch_bounds__(kVT) void varint_gaps_kernel(VarintDecParams p) {
-  __shared__ uint8_t s_in[4 + kBTile];      // 4 bytes before the tile, then the tile
-  __shared__ uint32_t s_gap[kBTile];        // values, in entry order
-  __shared__ uint32_t s_w[kVWaves];
-  __shared__ uint64_t s_b;
-  constexpr int kPer = kBTile / kVT;        // bytes per thread
-  const int tid = threadIdx.x;
-  const uint64_t nb0 = *p.nbytes;
-  const uint64_t nbytes = nb0 < p.in_capacity ? nb0 : p.in_capacity;
-  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
-    const uint64_t b0 = (uint64_t)tk.tile * kBTile;
-    const uint64_t b1 = b0 + kBTile < nbytes ? b0 + kBTile : (b0 < nbytes ? nbytes : b0);
-    const uint32_t cnt = (uint32_t)(b1 - b0);
-    for (uint32_t i = tid; i < cnt; i += kVT) s_in[4 + i] = p.in[b0 + i];
-    if (tid < 4) s_in[tid] = b0 >= 4 - (uint64_t)tid ? p.in[b0 - 4 + tid] : 0u;  // 0: a terminator
-    __syncthreads();
-    // terminating bytes of this thread's run
-    uint32_t nterm = 0;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const uint32_t i = (uint32_t)tid * kPer + j;
-      nterm += (i < cnt && !(s_in[4 + i] & 0x80u)) ? 1u : 0u;
-    }
-    uint32_t agg32;
-    const uint32_t texcl = block_excl_sum(nterm, s_w, &agg32);
-    const uint64_t excl = chain_exclusive(p.ws, tk, agg32, false, 0, &s_b);
-    // the value of each number that ends in this tile (it starts at most 4
-    // bytes earlier, possibly in the previous tile)
-    uint32_t e = texcl;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const uint32_t i = (uint32_t)tid * kPer + j;
-      if (i < cnt && !(s_in[4 + i] & 0x80u)) {
-        int st = (int)i;
-        while (st > (int)i - 4 && (s_in[4 + st - 1] & 0x80u) && (b0 + (uint64_t)st) > 0) --st;
-        uint32_t v = 0;
-        for (int q = st; q <= (int)i; ++q) v |= (uint32_t)(s_in[4 + q] & 0x7Fu) << (7 * (q - st));
-        s_gap[e] = v;
-        ++e;
-      }
-    }
-    __syncthreads();
-    for (uint32_t q = tid; q < agg32; q += kVT) {
-      const uint64_t pos = excl + q;
-      if (pos < p.capacity) p.idx[pos] = s_gap[q];
-    }
-    const bool last = nbytes == 0 ? tk.tile == 0 : (b0 <= nbytes - 1 && nbytes - 1 < b0 + kBTile);
-    if (last && tid == 0) *p.count = excl + agg32;
-    __syncthreads();
-  });
-}
-
-// ---------------------------------------------------------------- decode, pass 2
-
-__global__ __launch_bounds__(kVT) void varint_sums_kernel(VarintDecParams p) {
-  __shared__ uint32_t s_v[kVTile];
-  __shared__ uint32_t s_flags[kVTile / 32];
-  __shared__ uint32_t s_range[2];
-  __shared__ uint32_t s_tsum[kVT];     // per thread: sum since its last restart
-  __shared__ uint32_t s_trst[kVT];     // per thread: has a restart
-  __shared__ uint64_t s_b;
-  __shared__ uint32_t s_tail[2];       // the tile's (has restart, sum after the last one)
-  const int tid = threadIdx.x;
-  const uint64_t c0 = *p.count;
-  const uint64_t nent = c0 < p.capacity ? c0 : p.capacity;
-  for_each_ticket(p.ws, p.ntiles2, [&](const Ticket& tk) {
-    const uint64_t k0 = (uint64_t)tk.tile * kVTile;
-    const uint64_t k1 = k0 + kVTile < nent ? k0 + kVTile : (k0 < nent ? nent : k0);
-    const uint32_t cnt = (uint32_t)(k1 - k0);
-    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_flags[w] = 0;
-    for (uint32_t i = tid; i < cnt; i += kVT) s_v[i] = p.idx[k0 + i];
-    __syncthreads();
-    if (tid < 64) mark_starts(p.seg_begin, p.nseg, k0, k1, s_flags, s_range);
-    __syncthreads();
-    // this thread's run: sum since its last restart
-    uint32_t run = 0;
-    bool rst = false;
-#pragma unroll
-    for (int j = 0; j < kVPer; ++j) {
-      const uint32_t i = (uint32_t)tid * kVPer + j;
-      if (i < cnt) {
-        if (flag_at(s_flags, i)) {
-          run = 0;
-          rst = true;
-        }
-        run += s_v[i];
-      }
-    }
-    s_tsum[tid] = run;
-    s_trst[tid] = rst ? 1u : 0u;
-    __syncthreads();
-    // carry into each thread from the threads before it, within the tile
-    // (the segmented sum of the runs, walked by one wave with 4 runs per lane)
-    if (tid < 64) {
-      uint32_t c = 0;
-      bool r = false;
-      uint32_t vals[4];
-      bool rs[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        vals[q] = s_tsum[tid * 4 + q];
-        rs[q] = s_trst[tid * 4 + q] != 0u;
-        c = rs[q] ? vals[q] : c + vals[q];
-        r = r || rs[q];
-      }
-      // inclusive segmented scan of the lanes' (r, c) pairs
-      uint32_t ic = c;
-      bool ir = r;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t oc = (uint32_t)__shfl_up((int)ic, d, 64);
-        const int orr = __shfl_up(ir ? 1 : 0, d, 64);
-        if (lane_id() >= d && !ir) {
-          ic = oc + ic;
-          ir = orr != 0;
-        }
-      }
-      // exclusive value for each of the lane's 4 threads
-      uint32_t ec = (uint32_t)__shfl_up((int)ic, 1, 64);
-      bool er = __shfl_up(ir ? 1 : 0, 1, 64) != 0;
-      if (lane_id() == 0) {
-        ec = 0;
-        er = false;
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        s_tsum[tid * 4 + q] = ec;            // carry from earlier threads of the tile
-        s_trst[tid * 4 + q] = er ? 1u : 0u;  // ... which started after a restart
-        ec = rs[q] ? vals[q] : ec + vals[q];
-        er = er || rs[q];
-      }
-      if (tid == 63) {
-        s_tail[0] = ir ? 1u : 0u;
-        s_tail[1] = ic;
-      }
-    }
-    __syncthreads();
-    const bool tile_rst = s_tail[0] != 0u;
-    const uint32_t tile_sum = s_tail[1];
-    const uint64_t carry = chain_exclusive(p.ws, tk, tile_sum, tile_rst, tile_sum, &s_b);
-    // indices: before any restart in the tile the carry from earlier tiles applies
-    uint32_t acc = s_tsum[tid] + (s_trst[tid] ? 0u : (uint32_t)carry);
-#pragma unroll
-    for (int j = 0; j < kVPer; ++j) {
-      const uint32_t i = (uint32_t)tid * kVPer + j;
-      if (i < cnt) {
-        if (flag_at(s_flags, i)) acc = 0;
-        acc += s_v[i];
-        s_v[i] = acc;
-      }
-    }
-    __syncthreads();
-    for (uint32_t i = tid; i < cnt; i += kVT) p.idx[k0 + i] = s_v[i];
     __syncthreads();
   });
 }
@@ -502,7 +321,7 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
     }
     uint32_t agg32;
     const uint32_t texcl = block_excl_sum(sum, s_w, &agg32);
-    const uint64_t excl = chain_exclusive(p.ws, tk, agg32, false, 0, &s_b);
+    const uint64_t excl = chain_exclusive(p.ws, tk, agg32, &s_b);
     uint32_t o = texcl;
 #pragma unroll
     for (int j = 0; j < kVPer; ++j) {
@@ -571,249 +390,7 @@ __global__ __launch_bounds__(kVT) void coo_encode_kernel(CooEncParams p) {
   });
 }
 
-// Segmented inclusive running sum of one 64-bit value per element over a tile
-// staged in s_v (cnt elements), restarting at the elements flagged in s_rf:
-// there the sum is the element's own value.  Elements before the tile's first
-// restart add `carry` from earlier tiles, which chain_exclusive supplies (a
-// tile holding a restart publishes its inclusive tail at once).  s_v ends up
-// holding the sums.  Every thread of the block calls it.
-template <bool WIDE, int STRIDE = 1>
-__device__ void tile_segmented_sum(uint64_t* ws, const Ticket& tk, uint64_t* s_v,
-                                   const uint32_t* s_rf, uint32_t cnt, uint64_t* s_tsum,
-                                   uint32_t* s_trst, uint64_t* s_tail, uint64_t* s_b) {
-  const int tid = threadIdx.x;
-  uint64_t run = 0;
-  bool rst = false;
-#pragma unroll
-  for (int j = 0; j < kVPer; ++j) {
-    const uint32_t i = (uint32_t)tid * kVPer + j;
-    if (i < cnt) {
-      if (flag_at(s_rf, i)) {
-        run = 0;
-        rst = true;
-      }
-      run += s_v[i];
-    }
-  }
-  s_tsum[tid] = run;
-  s_trst[tid] = rst ? 1u : 0u;
-  __syncthreads();
-  if (tid < 64) {
-    uint64_t c = 0;
-    bool r = false;
-    uint64_t vals[4];
-    bool rs[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      vals[q] = s_tsum[tid * 4 + q];
-      rs[q] = s_trst[tid * 4 + q] != 0u;
-      c = rs[q] ? vals[q] : c + vals[q];
-      r = r || rs[q];
-    }
-    uint64_t ic = c;
-    bool ir = r;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const uint64_t oc = __shfl_up(ic, d, 64);
-      const int orr = __shfl_up(ir ? 1 : 0, d, 64);
-      if (lane_id() >= d && !ir) {
-        ic = oc + ic;
-        ir = orr != 0;
-      }
-    }
-    uint64_t ec = __shfl_up(ic, 1, 64);
-    bool er = __shfl_up(ir ? 1 : 0, 1, 64) != 0;
-    if (lane_id() == 0) {
-      ec = 0;
-      er = false;
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      s_tsum[tid * 4 + q] = ec;
-      s_trst[tid * 4 + q] = er ? 1u : 0u;
-      ec = rs[q] ? vals[q] : ec + vals[q];
-      er = er || rs[q];
-    }
-    if (tid == 63) {
-      s_tail[0] = ir ? 1u : 0u;
-      s_tail[1] = ic;
-    }
-  }
-  __syncthreads();
-  const bool tile_rst = s_tail[0] != 0u;
-  const uint64_t tile_sum = s_tail[1];
-  const uint64_t carry = chain_exclusive<WIDE, STRIDE>(ws, tk, tile_sum, tile_rst, tile_sum, s_b);
-  uint64_t acc = s_tsum[tid] + (s_trst[tid] ? 0u : carry);
-#pragma unroll
-  for (int j = 0; j < kVPer; ++j) {
-    const uint32_t i = (uint32_t)tid * kVPer + j;
-    if (i < cnt) {
-      if (flag_at(s_rf, i)) acc = 0;
-      acc += s_v[i];
-      s_v[i] = acc;
-    }
-  }
-  __syncthreads();
-}
-
-// The decode, one pass over pair tiles with two chained segmented sums per
-// tile (sequence numbers 2t and 2t + 1 of the launch):
-//   1. per pair, (row since the segment's first entry) | (escapes since the
-//      segment's start) << 32, inclusive, restarting at segment starts; the
-//      first pair of a segment starts from the row of its first index;
-//   2. the flat index of every pair's entry, restarting at new-row pairs and
-//      segment starts, written at seg_begin[s] + 1 + (pairs before it in the
-//      segment) - (escapes before it); each segment's first index goes to
-//      seg_begin[s].
-// A thread takes 16 consecutive pairs of the tile for the second sum: it
-// finds its first pair's segment by a search over the tile's segments and
-// moves to the next segment only at a segment start.
-__global__ __launch_bounds__(kVT) void coo_decode_kernel(CooDecParams p) {
-  __shared__ uint64_t s_v[kVTile];
-  __shared__ uint32_t s_pair[kVTile];     // drow | dcol << 8
-  __shared__ uint32_t s_rf[kVTile / 32];
-  __shared__ uint32_t s_seg[kVTile / 32];
-  __shared__ uint32_t s_range[2];
-  __shared__ uint64_t s_tsum[kVT];
-  __shared__ uint32_t s_trst[kVT];
-  __shared__ uint64_t s_tail[2];
-  __shared__ uint64_t s_b;
-  const int tid = threadIdx.x;
-  const uint64_t n0 = *p.npairs;
-  const uint64_t np = n0 < p.pair_capacity ? n0 : p.pair_capacity;
-  const uint64_t nent = *p.nent;
-  for_each_ticket(p.ws, p.ntiles, [&](const Ticket& tk) {
-    const uint64_t g0 = (tk.seq - tk.tile) & kSeqMask;
-    const Ticket t_rows{tk.tile, (g0 + 2ull * tk.tile) & kSeqMask};
-    const Ticket t_flat{tk.tile, (g0 + 2ull * tk.tile + 1ull) & kSeqMask};
-    const uint64_t q0 = (uint64_t)tk.tile * kVTile;
-    const uint64_t q1 = q0 + kVTile < np ? q0 + kVTile : (q0 < np ? np : q0);
-    const uint32_t cnt = (uint32_t)(q1 - q0);
-    for (uint32_t w = tid; w < kVTile / 32; w += kVT) {
-      s_rf[w] = 0;
-      s_seg[w] = 0;
-    }
-    for (uint32_t i = tid; i < cnt; i += kVT)
-      s_pair[i] = (uint32_t)p.drow[q0 + i] | ((uint32_t)p.dcol[q0 + i] << 8);
-    __syncthreads();
-    if (tid < 64) mark_starts(p.seg_pairs, p.nseg, q0, q1, s_seg, s_range);
-    __syncthreads();
-    // sum 1: row and escape count since the segment's start
-    for (uint32_t i = tid; i < cnt; i += kVT) {
-      const uint32_t pr = s_pair[i];
-      const bool esc = (pr & 0xFFu) == 255u && (pr >> 8) == 0u;
-      uint64_t v = (uint64_t)(pr & 0xFFu) | ((uint64_t)(esc ? 1u : 0u) << 32);
-      if (flag_at(s_seg, i)) {  // the segment's first pair: start from its first index's row
-        const uint32_t s = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
-        const uint32_t C = p.cols[s] > 0 ? p.cols[s] : 1u;
-        v += p.first[s] / C;
-      }
-      s_v[i] = v;
-    }
-    __syncthreads();
-    tile_segmented_sum<true, 2>(p.ws, t_rows, s_v, s_seg, cnt, s_tsum, s_trst, s_tail, &s_b);
-    // values and restarts of this thread's pairs: a new-row pair restarts at
-    // row * C + column, a segment's first pair at its first index + gap (or,
-    // if it starts a new row, as a new-row pair), a same-row pair adds its
-    // gap, an escape adds nothing (the new-row pair after it restarts)
-    const uint32_t i0 = (uint32_t)tid * kVPer;
-    uint32_t escb[kVPer];
-    uint32_t seg_id = 0, C = 1;
-    uint32_t rst_bits = 0, esc_bits = 0;
-    if (i0 < cnt) {
-      seg_id = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i0);
-      C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
-    }
-    uint32_t seg_at[kVPer];  // segment of each pair (changes only at starts)
-#pragma unroll
-    for (int j = 0; j < kVPer; ++j) {
-      const uint32_t i = i0 + j;
-      escb[j] = 0;
-      seg_at[j] = seg_id;
-      if (i >= cnt) continue;
-      const bool seg_start = flag_at(s_seg, i);
-      if (seg_start && i != i0) {
-        seg_id = segment_in(p.seg_pairs, s_range[0], s_range[1], q0 + i);
-        C = p.cols[seg_id] > 0 ? p.cols[seg_id] : 1u;
-        seg_at[j] = seg_id;
-      }
-      const uint32_t pr = s_pair[i];
-      const uint32_t dr = pr & 0xFFu, dc = pr >> 8;
-      const bool esc = dr == 255u && dc == 0;
-      const uint64_t st = s_v[i];
-      escb[j] = (uint32_t)(st >> 32);
-      uint64_t v = esc ? 0 : dc;
-      bool rst = seg_start;
-      if (!esc && dr > 0) {
-        v = (uint64_t)(uint32_t)st * C + dc - 1;
-        rst = true;
-      } else if (seg_start && !esc) {
-        v = (uint64_t)p.first[seg_id] + dc;
-      }
-      if (rst) rst_bits |= 1u << j;
-      if (esc) esc_bits |= 1u << j;
-      s_v[i] = v;
-    }
-    // publish this thread's restart flags (its 16 bits of the tile's bitmap)
-    if (i0 < cnt) atomicOr(&s_rf[i0 >> 5], rst_bits << (i0 & 31));
-    __syncthreads();
-    // sum 2: the flat index
-    tile_segmented_sum<true, 2>(p.ws, t_flat, s_v, s_rf, cnt, s_tsum, s_trst, s_tail, &s_b);
-    // Pair i's entry lands at seg_begin[s] + 1 + (q0 + i - seg_pairs[s]) -
-    // (escapes before it), s its segment.  The owning thread stores the low
-    // 32 bits of that position in s_pair (no longer needed), thread 0 the
-    // whole position of pair 0 as a reference, and escapes are flagged in
-    // s_seg's place (its segment starts were last read before the sum).  A
-    // tile's positions lie within cnt + nseg < 2^31 of each other, so each is
-    // the reference plus the signed 32-bit difference of the low halves.  The
-    // writes then go out with consecutive lanes on consecutive pairs, whose
-    // entries are consecutive, so they coalesce.
-    for (uint32_t w = tid; w < kVTile / 32; w += kVT) s_seg[w] = 0;
-    uint32_t cur = 0xFFFFFFFFu;
-    uint64_t sp = 0, sb = 0;
-#pragma unroll
-    for (int j = 0; j < kVPer; ++j) {
-      const uint32_t i = i0 + j;
-      if (i >= cnt) break;
-      if (seg_at[j] != cur) {
-        cur = seg_at[j];
-        sp = p.seg_pairs[cur];
-        sb = p.seg_begin[cur];
-      }
-      const uint64_t pos = sb + 1 + (q0 + i - sp) - escb[j];
-      s_pair[i] = (uint32_t)pos;
-      if (i == 0) s_b = pos;
-    }
-    __syncthreads();
-    if (i0 < cnt) atomicOr(&s_seg[i0 >> 5], esc_bits << (i0 & 31));
-    __syncthreads();
-    const uint64_t ref = s_b;
-    for (uint32_t i = tid; i < cnt; i += kVT) {
-      if (flag_at(s_seg, i)) continue;  // an escape pair has no entry
-      const uint64_t pos = ref + (uint64_t)(int64_t)(int32_t)(s_pair[i] - (uint32_t)ref);
-      if (pos < p.capacity) p.idx[pos] = (uint32_t)s_v[i];
-    }
-    // first entries of the segments starting in this tile (and, in the last
-    // tile, of those whose pairs start at the end of the stream)
-    if (tid < 64) {
-      auto put_first = [&](uint32_t s) {
-        const uint64_t b = p.seg_begin[s];
-        const uint64_t e = s + 1 < p.nseg ? p.seg_begin[s + 1] : nent;
-        if (e > b && b < p.capacity) p.idx[b] = p.first[s];
-      };
-      for (uint32_t s = s_range[0] + (uint32_t)lane_id(); s < s_range[1]; s += 64) put_first(s);
-      const bool lastt = np == 0 ? tk.tile == 0 : (q0 <= np - 1 && np - 1 < q0 + kVTile);
-      if (lastt) {
-        const uint32_t from = wave_lower_bound64(p.seg_pairs, p.nseg, np);
-        for (uint32_t s = from + (uint32_t)lane_id(); s < p.nseg; s += 64) put_first(s);
-      }
-    }
-    __syncthreads();
-  }, 2u);
-}
-
 uint32_t varint_entry_tile() { return kVTile; }
-uint32_t varint_byte_tile() { return kBTile; }
 
 // Four blocks per CU: each block holds one tile at a time and waits on its
 // look-back, so more tiles in flight hide that latency.  On the 32B-shaped
@@ -841,23 +418,6 @@ hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream) {
   const uint32_t grid = varint_grid(p.ntiles);
   if (grid == 0) return hipErrorInvalidDevice;
   hipLaunchKernelGGL(coo_encode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream) {
-  const uint32_t grid = varint_grid(p.ntiles);
-  if (grid == 0) return hipErrorInvalidDevice;
-  hipLaunchKernelGGL(coo_decode_kernel, dim3(grid), dim3(kVT), 0, stream, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream) {
-  uint32_t grid = varint_grid(p.ntiles);
-  if (grid == 0) return hipErrorInvalidDevice;
-  hipLaunchKernelGGL(varint_gaps_kernel, dim3(grid), dim3(kVT), 0, stream, p);
-  if (hipError_t e = hipGetLastError()) return e;
-  grid = varint_grid(p.ntiles2);
-  hipLaunchKernelGGL(varint_sums_kernel, dim3(grid), dim3(kVT), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -229,6 +229,7 @@ def test_stream_validation(L):
     assert vd(None, 10, A, None, 0, A, 10, A, ws, wsb, None) == EINVAL            # in
     assert vd(A, 10, A, None, 0, A + 2, 10, A, ws, wsb, None) == EALIGN           # idx
     assert vd(A, big, A, None, 0, A, 10, A, ws, wsb, None) == EINVAL              # tiles
+    assert vd(A + 1, 10, A, None, 0, A, 10, A, ws, wsb, None) == EALIGN           # in
     ce = L.pulse_coo_encode  # idx, capacity, end, seg_begin, nseg, cols, first, drow, dcol,
     #                          out_capacity, seg_pairs, total_pairs, workspace, bytes, stream
     assert ce(A, 10, A, A, 0, A, A, A, A, 10, A, A, ws, wsb, None) == EINVAL      # nseg 0
@@ -243,6 +244,8 @@ def test_stream_validation(L):
     assert cd(A, A, 10, A, A, A, 1, A, A, A, None, 10, ws, wsb, None) == EINVAL   # idx
     assert cd(A, A, 10, A + 4, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # npairs
     assert cd(A, A + 1, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # dcol
+    assert cd(A + 8, A, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # drow
+    assert cd(A, A + 2, 10, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EALIGN  # dcol
     assert cd(A, A, big, A, A, A, 1, A, A, A, A, 10, ws, wsb, None) == EINVAL     # tiles
     assert b"coo decode" in L.pulse_last_error()
 

@@ -157,3 +157,35 @@ def test_encode_patch_round_trip_with_shared_workspace(ws):
         stream, _ = segments_stream(olists)
         assert read_count(total) == stream.size
         np.testing.assert_array_equal(out[:stream.size].cpu().numpy(), stream)
+
+
+def test_decode_cut_stream_capacity_and_clean_ring():
+    """A stream cut inside its last number drops that number; entries past the
+    output capacity are not written; and the decode leaves the workspace's
+    status ring zero (its per-tile sums are cleared), so a zero-filled
+    workspace stays zero-filled."""
+    rng = np.random.default_rng(8)
+    segs = [sorted_idx(rng, n, (n + 1) * 3001) for n in (5000, 1, 0, 20_000, 7)]
+    stream, _ = segments_stream(segs)
+    seg_begin = np.concatenate([[0], np.cumsum([s.size for s in segs])[:-1]]).astype(np.int64)
+    idx_all = np.concatenate(segs)
+    assert stream[-1] < 0x80 and stream[-2] >= 0x80  # the last number takes several bytes
+    ws = pulse.workspace()
+    # cut one byte before the end: the last entry is dropped
+    back = torch.full((idx_all.size + 5,), -1, dtype=torch.int32, device="cuda")
+    cnt = counter(0)
+    pulse.varint_decode(dev(stream), counter(stream.size - 1), back, cnt, ws, seg_begin=dev(seg_begin))
+    torch.cuda.synchronize()
+    assert read_count(cnt) == idx_all.size - 1
+    np.testing.assert_array_equal(h32(back)[:idx_all.size - 1], idx_all[:-1])
+    assert (h32(back)[idx_all.size - 1:] == 0xFFFFFFFF).all()
+    # capacity below the entry count
+    cap = idx_all.size // 3 + 11
+    back = torch.full((idx_all.size,), -1, dtype=torch.int32, device="cuda")
+    pulse.varint_decode(dev(stream), counter(stream.size), back[:cap], cnt, ws, seg_begin=dev(seg_begin))
+    torch.cuda.synchronize()
+    assert read_count(cnt) == idx_all.size
+    np.testing.assert_array_equal(h32(back)[:cap], idx_all[:cap])
+    assert (h32(back)[cap:] == 0xFFFFFFFF).all()
+    pulse.check_workspace(ws)
+    assert int(ws.view(torch.int64)[64:].abs().sum().item()) == 0
