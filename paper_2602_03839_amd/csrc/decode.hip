@@ -22,50 +22,20 @@
 // the look-back latency: 3.3 and 5.7 ms on a 306M-entry patch.)
 //
 // A tile is a whole number of units (4,096 bytes or pairs: 16 per thread of a
-// 256-thread block), as many as keep the tile count at most kMaxDecTiles for
+// 256-thread block), as many as keep the tile count at most kMaxStreamTiles for
 // the stream's actual length, read from the device.  The aggregates live in
 // the workspace's status ring, two words per tile, and the write pass clears
 // them to zero: the ring's other users (encode, sparsify, the stream
 // encoders) read a zero word as "not published yet", so the workspace can
 // still be shared with them on one stream.
-#include "device_common.hpp"
 #include "launch.hpp"
+#include "stream_common.hpp"
 
 namespace pulse {
 
+using namespace stream;
+
 namespace {
-
-constexpr int kDT = 256;                     // threads per block of the tile kernels
-constexpr int kDWaves = kDT / 64;
-constexpr uint32_t kDUnit = kDT * 16;        // bytes (varint) or pairs (COO) per unit
-constexpr uint32_t kMaxDecTiles = 32767;     // two ring words per tile, kSlots words
-constexpr int kST = 1024;                    // threads of the single-block scans
-static_assert(2 * (uint64_t)(kMaxDecTiles + 1) <= kSlots, "tile aggregates exceed the ring");
-
-__device__ __forceinline__ uint64_t* dec_ring(uint64_t* ws) { return ws + kStatusOffsetWords; }
-
-// Tiles of a stream of n units' worth of items: each tile holds `per` units;
-// at least one tile (an empty stream still has segments to finish).
-struct Geo {
-  uint64_t tile;    // items per tile
-  uint32_t ntiles;
-};
-
-__device__ __forceinline__ Geo dec_geometry(uint64_t n) {
-  const uint64_t units = n == 0 ? 1 : (n + kDUnit - 1) / kDUnit;
-  const uint64_t per = (units + kMaxDecTiles - 1) / kMaxDecTiles;
-  Geo g;
-  g.tile = per * kDUnit;
-  g.ntiles = (uint32_t)((units + per - 1) / per);
-  return g;
-}
-
-// ---------------------------------------------------------------- block scans
-//
-// Exclusive scan over the threads of a block, in thread order, of an
-// associative operation comb(earlier, later) with identity T::id(); `carry`
-// comes before thread 0.  *total receives carry combined with every thread's
-// value.  Every thread of the block calls it; s_w holds one value per wave.
 
 // Segmented sum: f = a restart (a segment start) occurred, s = the sum since
 // the last one (or since the start, with no restart).
@@ -111,115 +81,6 @@ __device__ __forceinline__ CooEl shfl_up(CooEl x, int d) {
   r.b = (uint32_t)__shfl_up((int)x.b, d, 64);
   r.e = (uint32_t)__shfl_up((int)x.e, d, 64);
   return r;
-}
-
-template <int NT, typename T>
-__device__ T block_scan_excl(T v, T carry, T* s_w, T* total) {
-  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
-  T inc = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const T o = shfl_up(inc, d);
-    if (lane >= d) inc = comb(o, inc);
-  }
-  const T before = shfl_up(inc, 1);
-  if (lane == 63) s_w[wid] = inc;
-  __syncthreads();
-  T pre = carry, all = carry;
-#pragma unroll
-  for (int w = 0; w < NT / 64; ++w) {
-    const T x = s_w[w];
-    if (w < wid) pre = comb(pre, x);
-    all = comb(all, x);
-  }
-  __syncthreads();  // s_w may be reused
-  *total = all;
-  return lane == 0 ? pre : comb(pre, before);
-}
-
-// Block-wide exclusive sum of one count per thread (thread order).
-__device__ uint32_t block_count_excl(uint32_t v, uint32_t* s_w, uint32_t* total) {
-  const int lane = lane_id(), wid = (int)threadIdx.x >> 6;
-  const uint32_t incl = wave_incl_scan(v);
-  if (lane == 63) s_w[wid] = incl;
-  __syncthreads();
-  uint32_t before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kDWaves; ++w) {
-    const uint32_t x = s_w[w];
-    if (w < wid) before += x;
-    all += x;
-  }
-  __syncthreads();
-  *total = all;
-  return before + incl - v;
-}
-
-// First position in [0, n) with a[pos] >= key (a non-decreasing), whole wave.
-__device__ uint32_t lower_bound_wave(const uint64_t* a, uint32_t n, uint64_t key) {
-  const int lane = lane_id();
-  uint32_t lo = 0, hi = n;
-  while (hi - lo > 64) {
-    const uint32_t span = hi - lo;
-    const uint32_t q = lo + (uint32_t)((uint64_t)span * (uint32_t)(lane + 1) / 65u);
-    const uint64_t ge = __ballot(a[q] >= key);
-    if (ge == 0) {
-      lo = (uint32_t)__shfl((int)q, 63, 64) + 1;
-    } else {
-      const int f = __builtin_ctzll(ge);
-      const uint32_t qf = (uint32_t)__shfl((int)q, f, 64);
-      lo = f > 0 ? (uint32_t)__shfl((int)q, f - 1, 64) + 1 : lo;
-      hi = qf;
-    }
-  }
-  const uint32_t q = lo + (uint32_t)lane;
-  const uint64_t ge = __ballot(q < hi && a[q] >= key);
-  return ge == 0 ? hi : lo + (uint32_t)__builtin_ctzll(ge);
-}
-
-// Marks in the LDS bitmap (bit k - k0) every k in [k0, k1) at which a segment
-// starts (starts[s] = k; NULL starts: one segment), and bit 0 when k0 == 0 (the
-// stream's first item always starts one).  [s_range[0], s_range[1]) receives
-// the segments starting there.  Wave 0 only; the bitmap must be zero.
-__device__ void mark_segment_starts(const uint64_t* starts, uint32_t nseg, uint64_t k0, uint64_t k1,
-                                    uint32_t* s_bits, uint32_t* s_range) {
-  const int lane = lane_id();
-  uint32_t lo = 0, hi = 0;
-  if (starts && nseg > 0 && k1 > k0) {
-    lo = lower_bound_wave(starts, nseg, k0);
-    hi = lo;
-    for (uint32_t s = lo + (uint32_t)lane;; s += 64) {
-      const bool in = s < nseg && starts[s] < k1;
-      if (in) {
-        const uint32_t i = (uint32_t)(starts[s] - k0);
-        atomicOr(&s_bits[i >> 5], 1u << (i & 31));
-      }
-      const uint64_t m = __ballot(in);
-      hi += (uint32_t)__builtin_popcountll(m);
-      if (m != ~0ull) break;
-    }
-  }
-  if (lane == 0) {
-    if (k0 == 0 && k1 > 0) atomicOr(&s_bits[0], 1u);
-    s_range[0] = lo;
-    s_range[1] = hi;
-  }
-}
-
-__device__ __forceinline__ bool bit_at(const uint32_t* s_bits, uint32_t i) {
-  return (s_bits[i >> 5] >> (i & 31)) & 1u;
-}
-
-// The segment holding item k: the last segment starting at or before k, among
-// [lo, hi) (those starting in the unit), else the one before lo (0 if none).
-__device__ __forceinline__ uint32_t segment_of(const uint64_t* starts, uint32_t lo, uint32_t hi,
-                                               uint64_t k) {
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (starts[mid] <= k) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo > 0 ? lo - 1 : 0;
 }
 
 // ---------------------------------------------------------------- varint bytes
@@ -292,31 +153,37 @@ __device__ __forceinline__ void walk_numbers(const Bytes16& b, Emit emit) {
 }
 
 struct VarintLds {
-  uint32_t val[kDUnit];          // the unit's indices, in entry order
+  uint32_t val[padded(kDUnit)];  // the unit's indices, in entry order (entry i at pad(i))
   uint32_t bits[kDUnit / 32];    // segment starts among the unit's entries
   uint32_t range[2];
   uint32_t w[kDWaves];
   SegSum ws[kDWaves];
+  SegCache seg;                  // the segments starting among the tile's entries
 };
 
-// One unit of the stream, bytes [u0, u1) (u1 <= n), whose first entry is
-// entry e0.  Returns `carry` (the running sum before the unit) combined with
-// the unit's entries; *cnt receives the unit's entry count.  WRITE: the
-// indices are written.  Every thread of the block calls it.
-template <bool WRITE>
-__device__ SegSum varint_unit(const VarintDecParams& p, uint64_t u0, uint64_t u1, uint64_t n,
-                              uint64_t e0, SegSum carry, uint32_t* cnt, VarintLds& L) {
-  const int tid = (int)threadIdx.x;
-  const uint64_t pos = u0 + 16ull * (uint64_t)tid;
+// This thread's sixteen bytes of the unit starting at u0 (none past u1).
+__device__ __forceinline__ Bytes16 unit_bytes(const VarintDecParams& p, uint64_t u0, uint64_t u1,
+                                              uint64_t n) {
+  const uint64_t pos = u0 + 16ull * threadIdx.x;
   Bytes16 b;
   b.h = 0;
   b.w[0] = b.w[1] = b.w[2] = b.w[3] = 0x80808080u;  // no bytes: no terminators
   if (pos < u1) b = load_bytes16(p.in, pos, n);
+  return b;
+}
+
+// One unit of the stream (this thread's bytes b), whose first entry is entry
+// e0.  Returns `carry` (the running sum before the unit) combined with the
+// unit's entries; *cnt receives the unit's entry count.  WRITE: the indices
+// are written.  Every thread of the block calls it.
+template <bool WRITE>
+__device__ SegSum varint_unit(const VarintDecParams& p, const Bytes16& b, uint64_t e0, SegSum carry,
+                              uint32_t* cnt, VarintLds& L) {
+  const int tid = (int)threadIdx.x;
   for (uint32_t i = (uint32_t)tid; i < kDUnit / 32; i += kDT) L.bits[i] = 0;
   uint32_t ucnt;
   const uint32_t rank = block_count_excl(terminators(b), L.w, &ucnt);  // syncs
-  if (tid < 64) mark_segment_starts(p.seg_begin, p.nseg, e0, e0 + ucnt, L.bits, L.range);
-  __syncthreads();
+  mark_unit_starts(p.seg_begin, L.seg, e0, e0 + ucnt, L.bits, L.range);
   // this thread's running sum since its last restart
   SegSum mine = SegSum::id();
   uint32_t k = rank;
@@ -336,13 +203,13 @@ __device__ SegSum varint_unit(const VarintDecParams& p, uint64_t u0, uint64_t u1
     k = rank;
     walk_numbers(b, [&](uint32_t v) {
       acc = bit_at(L.bits, k) ? v : acc + v;
-      L.val[k] = acc;
+      L.val[pad(k)] = acc;
       ++k;
     });
     __syncthreads();
     for (uint32_t i = (uint32_t)tid; i < ucnt; i += kDT) {
       const uint64_t e = e0 + i;
-      if (e < p.capacity) p.idx[e] = L.val[i];
+      if (e < p.capacity) p.idx[e] = L.val[pad(i)];
     }
   }
   __syncthreads();  // bits, range and val are rewritten by the next unit
@@ -414,13 +281,29 @@ struct CooLds {
   uint32_t range[2];
   uint64_t ref;                  // the position of the unit's first pair
   CooEl ws[kDWaves];
+  SegCache cache;                // the segments whose pairs start in the tile
 };
 
 // The write pass's staging of a unit's entries.
 struct CooStage {
-  uint32_t val[kDUnit];          // flat index of each pair's entry
-  uint32_t pos[kDUnit];          // low 32 bits of its position
+  uint32_t val[padded(kDUnit)];  // flat index of each pair's entry (pair i at pad(i))
+  uint32_t pos[padded(kDUnit)];  // low 32 bits of its position
 };
+
+// This thread's sixteen pairs of the unit starting at q0 (none past q1).
+__device__ __forceinline__ Pairs16 unit_pairs(const CooDecParams& p, uint64_t q0, uint64_t q1, uint64_t n) {
+  const uint64_t q = q0 + 16ull * threadIdx.x;
+  Pairs16 x;
+  if (q < q1) {
+    x = load_pairs16(p.drow, p.dcol, q, n);
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) x.r[w] = 0;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) x.c[w] = 0;
+  }
+  return x;
+}
 
 // Writes segment s's first index at its first entry (if it has entries).
 __device__ __forceinline__ void put_first(const CooDecParams& p, uint64_t nent, uint32_t s) {
@@ -429,24 +312,21 @@ __device__ __forceinline__ void put_first(const CooDecParams& p, uint64_t nent, 
   if (e > b && b < p.capacity) p.idx[b] = p.first[s];
 }
 
-// One unit of pairs [q0, q1) (q1 <= n).  Returns carry combined with the
-// unit's pairs.  WRITE: the entries are written, and the first index of every
-// segment that starts in the unit (the last unit of the stream also those
-// that start at its end).  Every thread of the block calls it.
+// One unit of pairs [q0, q1) (q1 <= n; this thread's pairs x).  Returns carry
+// combined with the unit's pairs.  WRITE: the entries are written, and the
+// first index of every segment that starts in the unit (the last unit of the
+// stream also those that start at its end).  Every thread of the block calls it.
 template <bool WRITE>
-__device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint64_t n, uint64_t nent,
-                          CooEl carry, bool last_unit, CooLds& L, CooStage* S) {
+__device__ CooEl coo_unit(const CooDecParams& p, const Pairs16& x, uint64_t q0, uint64_t q1, uint64_t n,
+                          uint64_t nent, CooEl carry, bool last_unit, CooLds& L, CooStage* S) {
   const int tid = (int)threadIdx.x;
   const uint64_t q = q0 + 16ull * (uint64_t)tid;
   for (uint32_t i = (uint32_t)tid; i < kDUnit / 32; i += kDT) {
     L.seg[i] = 0;
     L.esc[i] = 0;
   }
-  Pairs16 x;
-  if (q < q1) x = load_pairs16(p.drow, p.dcol, q, n);
   __syncthreads();
-  if (tid < 64) mark_segment_starts(p.seg_pairs, p.nseg, q0, q1, L.seg, L.range);
-  __syncthreads();
+  mark_unit_starts(p.seg_pairs, L.cache, q0, q1, L.seg, L.range);
   const uint32_t lo = L.range[0], hi = L.range[1];
   const uint32_t m = q < q1 ? (uint32_t)(q1 - q < 16 ? q1 - q : 16) : 0u;  // this thread's pairs
   const uint32_t i0 = (uint32_t)tid * 16u;
@@ -456,7 +336,8 @@ __device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint6
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     if ((uint32_t)j < m) {
-      if (bit_at(L.seg, i0 + j)) mine = segment_state(p, segment_of(p.seg_pairs, lo, hi, q + j), &C);
+      if (bit_at(L.seg, i0 + j))
+        mine = segment_state(p, segment_of(p.seg_pairs, L.cache, lo, hi, q + j), &C);
       mine = comb(mine, pair_map(pair_row(x, j), pair_col(x, j)));
     }
   }
@@ -473,7 +354,7 @@ __device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint6
     C = 1;
     uint32_t escb = 0;
     if (m > 0) {
-      s = segment_of(p.seg_pairs, lo, hi, q);
+      s = segment_of(p.seg_pairs, L.cache, lo, hi, q);
       const uint32_t c = p.cols[s];
       C = c > 0 ? c : 1u;
       sp = p.seg_pairs[s];
@@ -484,7 +365,7 @@ __device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint6
       if ((uint32_t)j < m) {
         const uint64_t qj = q + (uint64_t)j;
         if (bit_at(L.seg, i0 + j)) {
-          s = segment_of(p.seg_pairs, lo, hi, qj);
+          s = segment_of(p.seg_pairs, L.cache, lo, hi, qj);
           st = segment_state(p, s, &C);
           sp = p.seg_pairs[s];
           sb = p.seg_begin[s];
@@ -493,8 +374,8 @@ __device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint6
         const uint64_t at = sb + 1 + (qj - sp) - st.e;
         st = comb(st, pair_map(dr, dc));
         if (dr == 255u && dc == 0u) escb |= 1u << j;
-        S->val[i0 + j] = st.a * C + st.b;
-        S->pos[i0 + j] = (uint32_t)at;
+        S->val[pad(i0 + j)] = st.a * C + st.b;
+        S->pos[pad(i0 + j)] = (uint32_t)at;
         if (qj == q0) L.ref = at;
       }
     }
@@ -504,8 +385,8 @@ __device__ CooEl coo_unit(const CooDecParams& p, uint64_t q0, uint64_t q1, uint6
     const uint32_t cnt = (uint32_t)(q1 - q0);
     for (uint32_t i = (uint32_t)tid; i < cnt; i += kDT) {
       if (bit_at(L.esc, i)) continue;  // an escape has no entry
-      const uint64_t at = ref + (uint64_t)(int64_t)(int32_t)(S->pos[i] - (uint32_t)ref);
-      if (at < p.capacity) p.idx[at] = S->val[i];
+      const uint64_t at = ref + (uint64_t)(int64_t)(int32_t)(S->pos[pad(i)] - (uint32_t)ref);
+      if (at < p.capacity) p.idx[at] = S->val[pad(i)];
     }
     if (tid < 64) {
       for (uint32_t t = lo + (uint32_t)lane_id(); t < hi; t += 64) put_first(p, nent, t);
@@ -529,31 +410,11 @@ __device__ __forceinline__ CooEl load_el(const uint64_t* w) {
                (uint32_t)(w0 >> 32), (uint32_t)w1};
 }
 
-// Exclusive scan of n elements in place by one block of kST threads: each
-// thread folds a run of consecutive elements, the runs are scanned, and each
-// thread writes its run's prefixes.  *total (thread 0) receives the fold of all.
-template <typename T, typename Load, typename Store>
-__device__ void single_block_scan(uint32_t n, Load ld, Store st, T* s_w, T* total) {
-  const uint32_t per = (n + kST - 1) / kST;
-  const uint32_t a = (uint32_t)threadIdx.x * per;
-  const uint32_t b = a + per < n ? a + per : n;
-  T run = T::id();
-  for (uint32_t i = a; i < b; ++i) run = comb(run, ld(i));
-  T all;
-  T pre = block_scan_excl<kST>(run, T::id(), s_w, &all);
-  for (uint32_t i = a; i < b; ++i) {
-    const T x = ld(i);
-    st(i, pre);
-    pre = comb(pre, x);
-  }
-  *total = all;
-}
-
 }  // namespace
 
 // ---------------------------------------------------------------- varint
 //
-// Ring layout: word b holds tile b's (entries | sum << 32), word kMaxDecTiles + 1 + b
+// Ring layout: word b holds tile b's (entries | sum << 32), word kMaxStreamTiles + 1 + b
 // its first entry (| 1 << 63 once a segment start is known to lie in it).
 
 __global__ __launch_bounds__(kDT) void varint_count_kernel(VarintDecParams p) {
@@ -561,7 +422,7 @@ __global__ __launch_bounds__(kDT) void varint_count_kernel(VarintDecParams p) {
   __shared__ uint32_t s_w2[kDWaves];
   const uint64_t n0 = *p.nbytes;
   const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
-  const Geo g = dec_geometry(n);
+  const Geo g = stream_geometry(n);
   if (blockIdx.x >= g.ntiles) return;
   const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
   const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
@@ -586,7 +447,7 @@ __global__ __launch_bounds__(kDT) void varint_count_kernel(VarintDecParams p) {
       C += s_w[w];
       S += s_w2[w];
     }
-    dec_ring(p.ws)[blockIdx.x] = (uint64_t)C | ((uint64_t)S << 32);
+    stream_ring(p.ws)[blockIdx.x] = (uint64_t)C | ((uint64_t)S << 32);
   }
 }
 
@@ -595,8 +456,8 @@ __global__ __launch_bounds__(kST) void varint_offsets_kernel(VarintDecParams p) 
   __shared__ uint64_t s_w[kST / 64];
   const uint64_t n0 = *p.nbytes;
   const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
-  const Geo g = dec_geometry(n);
-  uint64_t* ring = dec_ring(p.ws);
+  const Geo g = stream_geometry(n);
+  uint64_t* ring = stream_ring(p.ws);
   const uint32_t per = (g.ntiles + kST - 1) / kST;
   const uint32_t a = (uint32_t)threadIdx.x * per;
   const uint32_t b = a + per < g.ntiles ? a + per : g.ntiles;
@@ -618,7 +479,7 @@ __global__ __launch_bounds__(kST) void varint_offsets_kernel(VarintDecParams p) 
     all += s_w[w];
   }
   for (uint32_t i = a; i < b; ++i) {
-    ring[kMaxDecTiles + 1 + i] = pre;
+    ring[kMaxStreamTiles + 1 + i] = pre;
     pre += (uint32_t)ring[i];
   }
   if (threadIdx.x == 0) *p.count = all;
@@ -630,10 +491,10 @@ __global__ __launch_bounds__(kDT) void varint_restarts_kernel(VarintDecParams p)
   __shared__ int s_has;
   const uint64_t n0 = *p.nbytes;
   const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
-  const Geo g = dec_geometry(n);
+  const Geo g = stream_geometry(n);
   if (blockIdx.x >= g.ntiles) return;
-  uint64_t* ring = dec_ring(p.ws);
-  const uint64_t e0 = ring[kMaxDecTiles + 1 + blockIdx.x];
+  uint64_t* ring = stream_ring(p.ws);
+  const uint64_t e0 = ring[kMaxStreamTiles + 1 + blockIdx.x];
   const uint64_t w0 = ring[blockIdx.x];
   const uint64_t ecnt = (uint32_t)w0;
   if (threadIdx.x < 64) {
@@ -648,17 +509,21 @@ __global__ __launch_bounds__(kDT) void varint_restarts_kernel(VarintDecParams p)
   if (!s_has) return;  // block-uniform
   const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
   const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  cache_tile_segments(p.seg_begin, p.nseg, e0, e0 + ecnt, L.seg);
   SegSum run = SegSum::id();
   uint64_t e = e0;
+  Bytes16 b = unit_bytes(p, t0, t1, n);
   for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
     const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    const Bytes16 cur = b;
+    if (u1 < t1) b = unit_bytes(p, u1, u1 + kDUnit < t1 ? u1 + kDUnit : t1, n);  // the next unit's, in flight
     uint32_t c;
-    run = varint_unit<false>(p, u0, u1, n, e, run, &c, L);
+    run = varint_unit<false>(p, cur, e, run, &c, L);
     e += c;
   }
   if (threadIdx.x == 0) {
     ring[blockIdx.x] = (uint64_t)(uint32_t)w0 | ((uint64_t)run.s << 32);
-    ring[kMaxDecTiles + 1 + blockIdx.x] = e0 | (1ull << 63);
+    ring[kMaxStreamTiles + 1 + blockIdx.x] = e0 | (1ull << 63);
   }
 }
 
@@ -667,10 +532,10 @@ __global__ __launch_bounds__(kST) void varint_carry_kernel(VarintDecParams p) {
   __shared__ SegSum s_w[kST / 64];
   const uint64_t n0 = *p.nbytes;
   const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
-  const Geo g = dec_geometry(n);
-  uint64_t* ring = dec_ring(p.ws);
+  const Geo g = stream_geometry(n);
+  uint64_t* ring = stream_ring(p.ws);
   auto ld = [&](uint32_t i) {
-    return SegSum{(uint32_t)(ring[kMaxDecTiles + 1 + i] >> 63), (uint32_t)(ring[i] >> 32)};
+    return SegSum{(uint32_t)(ring[kMaxStreamTiles + 1 + i] >> 63), (uint32_t)(ring[i] >> 32)};
   };
   auto st = [&](uint32_t i, SegSum c) { ring[i] = (ring[i] & 0xFFFFFFFFull) | ((uint64_t)c.s << 32); };
   SegSum all;
@@ -681,23 +546,27 @@ __global__ __launch_bounds__(kDT) void varint_write_kernel(VarintDecParams p) {
   __shared__ VarintLds L;
   const uint64_t n0 = *p.nbytes;
   const uint64_t n = n0 < p.in_capacity ? n0 : p.in_capacity;
-  const Geo g = dec_geometry(n);
+  const Geo g = stream_geometry(n);
   if (blockIdx.x >= g.ntiles) return;
-  uint64_t* ring = dec_ring(p.ws);
-  const uint64_t e0 = ring[kMaxDecTiles + 1 + blockIdx.x] & ~(1ull << 63);
-  SegSum run = SegSum{0u, (uint32_t)(ring[blockIdx.x] >> 32)};
-  __syncthreads();  // every thread has read the tile's words
-  if (threadIdx.x == 0) {
-    ring[blockIdx.x] = 0;
-    ring[kMaxDecTiles + 1 + blockIdx.x] = 0;
-  }
+  uint64_t* ring = stream_ring(p.ws);
+  const uint64_t e0 = ring[kMaxStreamTiles + 1 + blockIdx.x] & ~(1ull << 63);
+  const uint64_t w0 = ring[blockIdx.x];
+  SegSum run = SegSum{0u, (uint32_t)(w0 >> 32)};
   const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
   const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  Bytes16 b = unit_bytes(p, t0, t1, n);
+  cache_tile_segments(p.seg_begin, p.nseg, e0, e0 + (uint32_t)w0, L.seg);  // ends with a barrier:
+  if (threadIdx.x == 0) {                                                  // every thread has read
+    ring[blockIdx.x] = 0;                                                  // the tile's words
+    ring[kMaxStreamTiles + 1 + blockIdx.x] = 0;
+  }
   uint64_t e = e0;
   for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
     const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
+    const Bytes16 cur = b;
+    if (u1 < t1) b = unit_bytes(p, u1, u1 + kDUnit < t1 ? u1 + kDUnit : t1, n);  // the next unit's, in flight
     uint32_t c;
-    run = varint_unit<true>(p, u0, u1, n, e, run, &c, L);
+    run = varint_unit<true>(p, cur, e, run, &c, L);
     e += c;
   }
 }
@@ -711,24 +580,28 @@ __global__ __launch_bounds__(kDT) void coo_reduce_kernel(CooDecParams p) {
   const uint64_t n0 = *p.npairs;
   const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
   const uint64_t nent = *p.nent;
-  const Geo g = dec_geometry(n);
+  const Geo g = stream_geometry(n);
   if (blockIdx.x >= g.ntiles) return;
   const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
   const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  cache_tile_segments(p.seg_pairs, p.nseg, t0, t1, L.cache);
   CooEl run = CooEl::id();
+  Pairs16 x = unit_pairs(p, t0, t1, n);
   for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
     const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
-    run = coo_unit<false>(p, u0, u1, n, nent, run, false, L, nullptr);
+    const Pairs16 cur = x;
+    if (u1 < t1) x = unit_pairs(p, u1, u1 + kDUnit < t1 ? u1 + kDUnit : t1, n);  // the next unit's, in flight
+    run = coo_unit<false>(p, cur, u0, u1, n, nent, run, false, L, nullptr);
   }
-  if (threadIdx.x == 0) store_el(dec_ring(p.ws) + 2ull * blockIdx.x, run);
+  if (threadIdx.x == 0) store_el(stream_ring(p.ws) + 2ull * blockIdx.x, run);
 }
 
 __global__ __launch_bounds__(kST) void coo_scan_kernel(CooDecParams p) {
   __shared__ CooEl s_w[kST / 64];
   const uint64_t n0 = *p.npairs;
   const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
-  const Geo g = dec_geometry(n);
-  uint64_t* ring = dec_ring(p.ws);
+  const Geo g = stream_geometry(n);
+  uint64_t* ring = stream_ring(p.ws);
   auto ld = [&](uint32_t i) { return load_el(ring + 2ull * i); };
   auto st = [&](uint32_t i, CooEl x) { store_el(ring + 2ull * i, x); };
   CooEl all;
@@ -741,38 +614,36 @@ __global__ __launch_bounds__(kDT) void coo_write_kernel(CooDecParams p) {
   const uint64_t n0 = *p.npairs;
   const uint64_t n = n0 < p.pair_capacity ? n0 : p.pair_capacity;
   const uint64_t nent = *p.nent;
-  const Geo g = dec_geometry(n);
+  const Geo g = stream_geometry(n);
   if (blockIdx.x >= g.ntiles) return;
-  uint64_t* ring = dec_ring(p.ws) + 2ull * blockIdx.x;
+  uint64_t* ring = stream_ring(p.ws) + 2ull * blockIdx.x;
   CooEl run = load_el(ring);
-  __syncthreads();  // every thread has read the tile's words
-  if (threadIdx.x == 0) {
+  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
+  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
+  Pairs16 x = unit_pairs(p, t0, t1, n);
+  cache_tile_segments(p.seg_pairs, p.nseg, t0, t1, L.cache);  // ends with a barrier: every
+  if (threadIdx.x == 0) {                                     // thread has read the tile's words
     ring[0] = 0;
     ring[1] = 0;
   }
-  const uint64_t t0 = (uint64_t)blockIdx.x * g.tile;
-  const uint64_t t1 = t0 + g.tile < n ? t0 + g.tile : n;
   if (t0 >= t1) {  // the empty stream: only the segments' first indices
-    run = coo_unit<true>(p, 0, 0, n, nent, run, true, L, &S);
+    run = coo_unit<true>(p, x, 0, 0, n, nent, run, true, L, &S);
     return;
   }
   for (uint64_t u0 = t0; u0 < t1; u0 += kDUnit) {
     const uint64_t u1 = u0 + kDUnit < t1 ? u0 + kDUnit : t1;
-    run = coo_unit<true>(p, u0, u1, n, nent, run, u1 == n, L, &S);
+    const Pairs16 cur = x;
+    if (u1 < t1) x = unit_pairs(p, u1, u1 + kDUnit < t1 ? u1 + kDUnit : t1, n);  // the next unit's, in flight
+    run = coo_unit<true>(p, cur, u0, u1, n, nent, run, u1 == n, L, &S);
   }
 }
 
 // ---------------------------------------------------------------- launch
 
-static uint32_t dec_grid(uint64_t capacity) {
-  const uint64_t units = capacity == 0 ? 1 : (capacity + kDUnit - 1) / kDUnit;
-  return (uint32_t)(units < kMaxDecTiles ? units : kMaxDecTiles);
-}
-
-uint64_t decode_max_items() { return 1ull << 40; }
+uint64_t stream_max_items() { return 1ull << 40; }
 
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream) {
-  const uint32_t grid = dec_grid(p.in_capacity);
+  const uint32_t grid = tile_grid(p.in_capacity);
   hipLaunchKernelGGL(varint_count_kernel, dim3(grid), dim3(kDT), 0, stream, p);
   if (hipError_t e = hipGetLastError()) return e;
   hipLaunchKernelGGL(varint_offsets_kernel, dim3(1), dim3(kST), 0, stream, p);
@@ -786,7 +657,7 @@ hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream) {
 }
 
 hipError_t launch_coo_decode(const CooDecParams& p, hipStream_t stream) {
-  const uint32_t grid = dec_grid(p.pair_capacity);
+  const uint32_t grid = tile_grid(p.pair_capacity);
   hipLaunchKernelGGL(coo_reduce_kernel, dim3(grid), dim3(kDT), 0, stream, p);
   if (hipError_t e = hipGetLastError()) return e;
   hipLaunchKernelGGL(coo_scan_kernel, dim3(1), dim3(kST), 0, stream, p);

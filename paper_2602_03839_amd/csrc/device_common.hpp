@@ -53,12 +53,8 @@ constexpr uint64_t kSlots = 1ull << kSlotBits;
 constexpr int kStatusOffsetWords = 64;            // 512-byte header
 constexpr size_t kWorkspaceBytes = (kStatusOffsetWords + kSlots) * sizeof(uint64_t);
 constexpr uint32_t kMaxTilesPerLaunch = (1u << kTicketBits) - 1;  // < kNoTicket
-// Largest grid of a ticketed launch.  Every block makes one draw past the last
-// tile, so a kernel that draws one tile per ticket (the index-stream kernels)
-// makes up to ntiles + grid draws, all of which must fit the ticket field:
-// those kernels take at most kMaxTicketedTiles tiles per launch.
+// Largest grid of a ticketed launch.
 constexpr uint32_t kMaxGrid = 1u << 16;
-constexpr uint32_t kMaxTicketedTiles = kMaxTilesPerLaunch - kMaxGrid;
 
 // status word: [63:62] flag, [61:54] lap tag, [53:0] value
 constexpr uint64_t kFlagAggregate = 1;  // value = this tile's own count

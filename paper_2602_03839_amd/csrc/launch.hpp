@@ -136,7 +136,6 @@ struct VarintEncParams {
   uint64_t out_capacity;
   uint64_t* seg_bytes;         // device [nseg], may be null
   uint64_t* total;             // device
-  uint32_t ntiles;
 };
 
 struct VarintDecParams {
@@ -262,7 +261,6 @@ struct CooEncParams {
   uint64_t out_capacity;       // pairs writable
   uint64_t* seg_pairs;         // device [nseg]: where each segment's pairs start
   uint64_t* total;             // device: pairs in the stream
-  uint32_t ntiles;
 };
 
 struct CooDecParams {
@@ -295,9 +293,8 @@ hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t 
 // p[0 .. nwords) = 0 by a kernel (not a memset, so a captured graph replays it as a kernel)
 hipError_t launch_zero_words(uint64_t* p, uint64_t nwords, hipStream_t stream);
 uint64_t outer_unit_elems();
-uint32_t varint_entry_tile();
-// Largest stream (bytes or pairs) the decoders take.
-uint64_t decode_max_items();
+// Largest capacity (entries, bytes or pairs) the index-stream kernels take.
+uint64_t stream_max_items();
 hipError_t launch_varint_encode(const VarintEncParams& p, hipStream_t stream);
 hipError_t launch_varint_decode(const VarintDecParams& p, hipStream_t stream);
 hipError_t launch_coo_encode(const CooEncParams& p, hipStream_t stream);

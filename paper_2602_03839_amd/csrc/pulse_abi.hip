@@ -518,9 +518,8 @@ int pulse_varint_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* 
     return fail(PULSE_EALIGN, "varint encode: counters not 8-byte aligned");
   if (idx && !aligned(idx, 4)) return fail(PULSE_EALIGN, "varint encode: idx misaligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  const uint64_t tile = pulse::varint_entry_tile();
-  const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "varint encode: capacity too large");
+  if (capacity >= pulse::stream_max_items())
+    return fail(PULSE_EINVAL, "varint encode: capacity too large");
   pulse::VarintEncParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -533,7 +532,6 @@ int pulse_varint_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* 
   p.out_capacity = out_capacity;
   p.seg_bytes = nseg ? seg_bytes : nullptr;
   p.total = total_bytes;
-  p.ntiles = (uint32_t)nt;
   return hip_status(pulse::launch_varint_encode(p, (hipStream_t)stream), "varint encode launch");
 }
 
@@ -549,7 +547,7 @@ int pulse_varint_decode(const uint8_t* in, uint64_t in_capacity, const uint64_t*
   if (idx && !aligned(idx, 4)) return fail(PULSE_EALIGN, "varint decode: idx misaligned");
   if (in && !aligned16(in)) return fail(PULSE_EALIGN, "varint decode: in not 16-byte aligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  if (in_capacity >= pulse::decode_max_items())
+  if (in_capacity >= pulse::stream_max_items())
     return fail(PULSE_EINVAL, "varint decode: in_capacity too large");
   pulse::VarintDecParams p;
   memset(&p, 0, sizeof p);
@@ -580,9 +578,8 @@ int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end
   if ((idx && !aligned(idx, 4)) || !aligned(cols, 4) || !aligned(first, 4) || (dcol && !aligned(dcol, 2)))
     return fail(PULSE_EALIGN, "coo encode: idx/cols/first/dcol misaligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  const uint64_t tile = pulse::varint_entry_tile();
-  const uint64_t nt = capacity == 0 ? 1 : (capacity + tile - 1) / tile;
-  if (nt > pulse::kMaxTicketedTiles) return fail(PULSE_EINVAL, "coo encode: capacity too large");
+  if (capacity >= pulse::stream_max_items())
+    return fail(PULSE_EINVAL, "coo encode: capacity too large");
   pulse::CooEncParams p;
   memset(&p, 0, sizeof p);
   p.ws = (uint64_t*)workspace;
@@ -598,7 +595,6 @@ int pulse_coo_encode(const uint32_t* idx, uint64_t capacity, const uint64_t* end
   p.out_capacity = out_capacity;
   p.seg_pairs = seg_pairs;
   p.total = total_pairs;
-  p.ntiles = (uint32_t)nt;
   return hip_status(pulse::launch_coo_encode(p, (hipStream_t)stream), "coo encode launch");
 }
 
@@ -620,7 +616,7 @@ int pulse_coo_decode(const uint8_t* drow, const uint16_t* dcol, uint64_t pair_ca
   if ((drow && !aligned16(drow)) || (dcol && !aligned16(dcol)))
     return fail(PULSE_EALIGN, "coo decode: drow/dcol not 16-byte aligned");
   if (int rc = check_workspace(workspace, workspace_bytes)) return rc;
-  if (pair_capacity >= pulse::decode_max_items())
+  if (pair_capacity >= pulse::stream_max_items())
     return fail(PULSE_EINVAL, "coo decode: pair_capacity too large");
   pulse::CooDecParams p;
   memset(&p, 0, sizeof p);

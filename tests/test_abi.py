@@ -218,10 +218,6 @@ def test_stream_validation(L):
     assert ve(A, 10, A + 4, None, 0, A, 10, None, A, ws, wsb, None) == EALIGN     # end
     assert ve(A + 2, 10, A, None, 0, A, 10, None, A, ws, wsb, None) == EALIGN     # idx
     assert ve(A, big, A, None, 0, A, 10, None, A, ws, wsb, None) == EINVAL        # tiles
-    # one tile per ticket and one extra draw per block: the tile count leaves
-    # room for the largest grid (2^16 blocks) in the 24-bit ticket field
-    over = ((1 << 24) - 1 - (1 << 16) + 1) * 4096
-    assert ve(A, over, A, None, 0, A, 10, None, A, ws, wsb, None) == EINVAL       # tiles + grid
     assert ve(A, 10, A, None, 0, A, 10, None, A, None, wsb, None) == EINVAL       # workspace
     vd = L.pulse_varint_decode  # in, in_capacity, nbytes, seg_begin, nseg, idx, capacity,
     #                             count, workspace, bytes, stream

@@ -254,3 +254,31 @@ def test_round_trip_on_one_workspace_twice():
         np.testing.assert_array_equal(gsp, osp)
         back = gpu_decode(gf, gd, gc, gsp, seg.cpu().numpy().view(np.uint64), cols, want_idx.size, ws=ws)
         np.testing.assert_array_equal(back, want_idx)
+
+
+def test_row_split_at_exact_multiples_and_large_indices():
+    """Entries at exact multiples of the column count, one below and one above,
+    and indices near 2^32 - 1, for column counts 1, 2, 3, 4095, 4096, 4097,
+    65521 and 65535: every row and column the encoder derives must be the
+    integer quotient and remainder (the oracle's), and the decode gives the
+    indices back."""
+    idx, seg, cols = [], [], []
+    for C in (1, 2, 3, 4095, 4096, 4097, 65521, 65535):
+        rows = (2**32 - 1) // C
+        picks = set()
+        for r in list(range(0, 40)) + list(range(rows - 40, rows + 1)) + [rows // 2, rows // 3]:
+            for d in (-1, 0, 1):
+                v = r * C + d
+                if 0 <= v < rows * C:
+                    picks.add(v)
+        picks |= {rows * C - 1, rows * C - 2}
+        a = np.array(sorted(picks), dtype=np.uint64).astype(np.uint32)
+        seg.append(sum(x.size for x in idx))
+        idx.append(a)
+        cols.append(C)
+    idx = np.concatenate(idx)
+    seg = np.array(seg, dtype=np.uint64)
+    cols = np.array(cols, dtype=np.uint32)
+    check(idx, seg, cols)
+    f, d, c, sp = oracle.coo_encode(idx, seg, cols)
+    np.testing.assert_array_equal(gpu_decode(f, d, c, sp, seg, cols, idx.size), idx)

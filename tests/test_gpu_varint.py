@@ -189,3 +189,27 @@ def test_decode_cut_stream_capacity_and_clean_ring():
     assert (h32(back)[cap:] == 0xFFFFFFFF).all()
     pulse.check_workspace(ws)
     assert int(ws.view(torch.int64)[64:].abs().sum().item()) == 0
+
+
+def test_long_numbers_past_the_staging_limit(ws):
+    """Thousands of one-entry segments whose indices take five bytes each: a
+    4096-entry unit then holds more bytes than the encoder stages in LDS, and
+    each thread writes its own numbers.  Byte-exact against the oracle, with
+    segment byte offsets, and decoded back."""
+    rng = np.random.default_rng(9)
+    segs = [np.array([int(v)], dtype=np.uint32) for v in rng.integers(1 << 28, 1 << 32, 9000)]
+    segs[100] = np.zeros(0, dtype=np.uint32)
+    segs[5000] = np.sort(rng.choice(1 << 20, 3000, replace=False)).astype(np.uint32)
+    seg_begin = np.concatenate([[0], np.cumsum([s.size for s in segs])[:-1]]).astype(np.int64)
+    want, want_offs = segments_stream(segs)
+    idx_all = np.concatenate(segs)
+    out, total, sbytes = gpu_encode(idx_all, seg_begin, ws)
+    assert total == want.size
+    np.testing.assert_array_equal(out[:total].cpu().numpy(), want)
+    np.testing.assert_array_equal(sbytes.cpu().numpy(), want_offs)
+    back = torch.zeros(idx_all.size, dtype=torch.int32, device="cuda")
+    cnt = counter(0)
+    pulse.varint_decode(out, counter(total), back, cnt, ws, seg_begin=dev(seg_begin))
+    torch.cuda.synchronize()
+    assert read_count(cnt) == idx_all.size
+    np.testing.assert_array_equal(h32(back), idx_all)
