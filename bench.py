@@ -690,7 +690,7 @@ def varint_leg(args, ps, idx, seg, sent, ws, stream):
         "decode_ms": round(dec_ms, 4),
         "encode_GBps_algorithmic": round(enc_bytes / enc_ms / 1e6, 2),
         "decode_GBps_algorithmic": round(dec_bytes / dec_ms / 1e6, 2),
-        "kernels": "varint_encode_kernel; varint_gaps_kernel + varint_sums_kernel",
+        "kernels": "varint_size/place/emit_kernel; varint_count/offsets/restarts/carry/write_kernel",
         "coo_downcast": coo,
     }
 
@@ -750,7 +750,7 @@ def coo_leg(args, ps, idx, end, seg, sent, ws, stream):
             "decode_ms": round(ms_d, 4),
             "encode_GBps_algorithmic": round((4.0 * sent + nbytes) / ms / 1e6, 2),
             "decode_GBps_algorithmic": round((nbytes + 4.0 * sent) / ms_d / 1e6, 2),
-            "kernels": "coo_encode_kernel; coo_decode_kernel"}
+            "kernels": "coo_size/place/emit_kernel; coo_reduce/scan/write_kernel"}
 
 
 def hash_leg(args, ps, stream):
