@@ -282,3 +282,19 @@ def test_row_split_at_exact_multiples_and_large_indices():
     check(idx, seg, cols)
     f, d, c, sp = oracle.coo_encode(idx, seg, cols)
     np.testing.assert_array_equal(gpu_decode(f, d, c, sp, seg, cols, idx.size), idx)
+
+
+def test_thousands_of_small_tensors():
+    """Thousands of tiny tensors (0 to 40 elements, many with one entry or
+    none): a 4096-item unit then holds far more segment starts than a tile
+    keeps in LDS, so the encoder's and decoder's lookups past those go to
+    memory.  Bit-exact against the oracle, and decoded back."""
+    rng = np.random.default_rng(15)
+    shapes = [(int(rng.integers(0, 6)), int(rng.integers(1, 8))) for _ in range(6000)]
+    idx, seg, cols = random_patch(rng, shapes, 0.6)
+    assert idx.size > 3 * TILE
+    check(idx, seg, cols)
+    f, d, c, sp = oracle.coo_encode(idx, seg, cols)
+    np.testing.assert_array_equal(gpu_decode(f, d, c, sp, seg, cols, idx.size), idx)
+    P, gf, gd, gc, gsp = gpu_coo(idx, seg, cols)
+    np.testing.assert_array_equal(gpu_decode(gf, gd, gc, gsp, seg, cols, idx.size), idx)
