@@ -383,6 +383,9 @@ int pulse_varint_decode(const uint8_t *in, uint64_t in_capacity, const uint64_t 
  *   pulse_varint_encode; seg_begin[0] should be 0 (earlier entries count as
  *   segment 0).  cols, first and seg_pairs are device arrays of nseg >= 1
  *   elements.  A stream of P pairs takes 3 P bytes plus 4 bytes per segment.
+ *   Indices must ascend within each segment; an entry below the one before
+ *   it gets one unspecified pair (the stream is then not decodable), and no
+ *   access leaves the buffers.
  */
 int pulse_coo_encode(const uint32_t *idx, uint64_t capacity, const uint64_t *end,
                      const uint64_t *seg_begin, uint32_t nseg, const uint32_t *cols,

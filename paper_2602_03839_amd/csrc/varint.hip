@@ -146,6 +146,10 @@ __device__ __forceinline__ uint32_t coo_pairs(bool start, uint32_t cur, uint32_t
   const uint32_t C = k.C;
   const uint32_t r = div_cols(cur, k), c = cur - r * C;
   const uint32_t pr = div_cols(prev, k), pc = prev - pr * C;
+  if (r < pr) {  // not ascending (outside the contract): one pair, no escapes
+    *last = 0;
+    return 1;
+  }
   const uint32_t dr = r - pr;
   if (dr == 0) {
     *last = c - pc;
@@ -388,7 +392,8 @@ __global__ __launch_bounds__(kST) void coo_place_kernel(CooEncParams p) {
 __global__ __launch_bounds__(kDT) void coo_emit_kernel(CooEncParams p) {
   __shared__ EntryLds L;
   __shared__ uint32_t s_pairs[padded(kDUnit + 1)];  // the unit's pairs, pair q at pad(q)
-  __shared__ uint32_t s_toff[kDT];  // pair offset of each thread's first entry in the unit
+  __shared__ uint64_t s_toff[kDT];  // pair offset of each thread's first entry in the unit
+  __shared__ Sum64 s_w64[kDWaves];
   const int tid = (int)threadIdx.x;
   const uint64_t e0 = *p.end;
   const uint64_t nent = e0 < p.capacity ? e0 : p.capacity;
@@ -424,15 +429,20 @@ __global__ __launch_bounds__(kDT) void coo_emit_kernel(CooEncParams p) {
         sum += coo_pairs(start, L.idx[pad(1 + i)], L.idx[pad(i)], cols, &last);
       }
     }
-    uint32_t upairs;
-    const uint32_t first_off = block_count_excl(sum, L.w, &upairs);
+    // 64-bit offsets: valid lists keep a unit's pairs far below 2^32, but an
+    // unsorted one need not, and positions must stay exact for the bounds
+    // checks below to bound the work
+    Sum64 all;
+    const uint64_t first_off = block_scan_excl<kDT>(Sum64{sum}, Sum64::id(), s_w64, &all).v;
+    const uint64_t upairs = all.v;
     s_toff[tid] = first_off;
     // The unit's pairs are one contiguous run [base, base + upairs).  Without
     // long escapes it fits s_pairs (as row field << 16 | column field) and
     // consecutive lanes write consecutive pairs; otherwise each thread writes
-    // its own entries' pairs.
+    // its own entries' pairs, stopping at the output capacity, so the work
+    // stays bounded by the buffer even for a list outside the contract.
     const bool staged = upairs <= kDUnit + 1;
-    uint32_t o = first_off;
+    uint64_t o = first_off;
     cols = cols0;
 #pragma unroll 4
     for (int j = 0; j < 16; ++j) {
@@ -445,13 +455,12 @@ __global__ __launch_bounds__(kDT) void coo_emit_kernel(CooEncParams p) {
         for (uint32_t q = 0; q < np; ++q) {
           const uint32_t pair = q + 1 < np ? (255u << 16) : last;
           if (staged) {
-            s_pairs[pad(o + q)] = pair;
+            s_pairs[pad((uint32_t)o + q)] = pair;
           } else {
             const uint64_t at = base + o + q;
-            if (at < p.out_capacity) {
-              p.drow[at] = (uint8_t)(pair >> 16);
-              p.dcol[at] = (uint16_t)(pair & 0xFFFFu);
-            }
+            if (at >= p.out_capacity) break;
+            p.drow[at] = (uint8_t)(pair >> 16);
+            p.dcol[at] = (uint16_t)(pair & 0xFFFFu);
           }
         }
         o += np;
@@ -465,7 +474,7 @@ __global__ __launch_bounds__(kDT) void coo_emit_kernel(CooEncParams p) {
         const uint64_t b = start_of(p.seg_begin, L.seg, s);
         const uint64_t e = s + 1 < p.nseg ? p.seg_begin[s + 1] : nent;
         const uint32_t i = (uint32_t)(b - u0);
-        uint32_t off = s_toff[i >> 4];
+        uint64_t off = s_toff[i >> 4];
         for (uint32_t q = i & ~15u; q < i; ++q) {
           uint32_t last;
           const Cols c = make_cols(p.cols[segment_of(p.seg_begin, L.seg, lo, hi, u0 + q)]);
@@ -476,7 +485,7 @@ __global__ __launch_bounds__(kDT) void coo_emit_kernel(CooEncParams p) {
       }
     }
     if (staged) {
-      for (uint32_t q = (uint32_t)tid; q < upairs; q += kDT) {
+      for (uint32_t q = (uint32_t)tid; q < (uint32_t)upairs; q += kDT) {
         const uint64_t at = base + q;
         if (at < p.out_capacity) {
           const uint32_t pair = s_pairs[pad(q)];

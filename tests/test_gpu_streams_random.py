@@ -118,3 +118,78 @@ def test_random_patch_structures(seed):
     coo_case(segs, seg, cols, ws, cut)
     pulse.check_workspace(ws)
     assert int(ws.view(torch.int64)[64:].abs().sum().item()) == 0  # the ring is left zero
+
+
+def test_inputs_outside_the_contract_stay_in_bounds():
+    """Streams the encoders did not write, and unsorted index lists: the
+    results are unspecified (except where the arithmetic still fixes them),
+    but no write leaves the output buffers, the work stays bounded, and the
+    workspace's ring is left zero."""
+    rng = np.random.default_rng(77)
+    ws = pulse.workspace()
+    guard = 4096
+
+    # random bytes as a delta-varint stream: the entry count is still the
+    # number of terminating bytes
+    raw = rng.integers(0, 256, 3_000_017, dtype=np.uint8)
+    nterm = int((raw < 0x80).sum())
+    seg = np.sort(rng.integers(0, 2 * nterm, 300)).astype(np.int64)
+    cap = nterm // 2
+    back = torch.full((cap + guard,), -1, dtype=torch.int32, device="cuda")
+    cnt = counter(0)
+    pulse.varint_decode(dev(raw), counter(raw.size), back[:cap], cnt, ws, seg_begin=dev(seg))
+    torch.cuda.synchronize()
+    assert read_count(cnt) == nterm
+    assert (h32(back)[cap:] == 0xFFFFFFFF).all()
+
+    # random pairs as a 2-D COO stream, with sorted and with shuffled metadata
+    P = 2_000_003
+    drow = torch.from_numpy(rng.integers(0, 256, P, dtype=np.uint8)).cuda()
+    dcol = dev(rng.integers(0, 65536, P).astype(np.uint16))
+    nseg = 500
+    for shuffled in (False, True):
+        sp = np.sort(rng.integers(0, P, nseg)).astype(np.uint64)
+        sb = np.sort(rng.integers(0, 3 * P, nseg)).astype(np.uint64)
+        if shuffled:
+            rng.shuffle(sp)
+            rng.shuffle(sb)
+        cols = rng.integers(0, 70000, nseg).astype(np.uint32)
+        first = rng.integers(0, 1 << 32, nseg, dtype=np.uint64).astype(np.uint32)
+        cap = P // 3
+        out = torch.full((cap + guard,), -1, dtype=torch.int32, device="cuda")
+        pulse.coo_decode(drow, dcol, counter(P), dev(sb), dev(sp), dev(cols), dev(first), counter(3 * P),
+                         out[:cap], ws)
+        torch.cuda.synchronize()
+        assert (h32(out)[cap:] == 0xFFFFFFFF).all()
+
+    # an unsorted index list: the delta-varint stream is still the oracle's
+    # (differences are taken modulo 2^32 on both sides); the COO stream of
+    # steps of billions of rows stops at the output capacity
+    segs = [rng.integers(0, 1 << 32, int(k), dtype=np.uint64).astype(np.uint32) for k in (5000, 0, 1, 7000)]
+    segs.append(np.array([0, 4_000_000_000] * 1000, dtype=np.uint32))
+    seg = np.cumsum([0] + [s.size for s in segs[:-1]]).astype(np.uint64)
+    idx_all = np.concatenate(segs)
+    n = idx_all.size
+    want = np.concatenate([oracle.varint_encode(s) for s in segs])
+    out = torch.zeros(want.size + guard, dtype=torch.uint8, device="cuda")
+    total = counter(0)
+    pulse.varint_encode(dev(idx_all), counter(n), out[:want.size], total, ws,
+                        seg_begin=dev(seg.astype(np.int64)), capacity=n)
+    torch.cuda.synchronize()
+    assert read_count(total) == want.size
+    np.testing.assert_array_equal(out[:want.size].cpu().numpy(), want)
+    assert int(out[want.size:].sum().item()) == 0
+    cols = np.array([1, 7, 3, 65535, 1], dtype=np.uint32)
+    cap = 1_000_000
+    drow = torch.zeros(cap + guard, dtype=torch.uint8, device="cuda")
+    dcol = torch.zeros(cap + guard, dtype=torch.int16, device="cuda")
+    first = torch.zeros(len(segs), dtype=torch.int32, device="cuda")
+    spd = torch.zeros(len(segs), dtype=torch.int64, device="cuda")
+    total = counter(0)
+    pulse.coo_encode(dev(idx_all), counter(n), dev(seg), dev(cols), first, drow[:cap], dcol[:cap], spd,
+                     total, ws)
+    torch.cuda.synchronize()
+    assert read_count(total) > cap  # the alternating tensor's up-steps take ~16.8M escapes each
+    assert int(drow[cap:].sum().item()) == 0 and int(dcol[cap:].abs().sum().item()) == 0
+    pulse.check_workspace(ws)
+    assert int(ws.view(torch.int64)[64:].abs().sum().item()) == 0
