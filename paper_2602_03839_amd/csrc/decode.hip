@@ -9,25 +9,20 @@
 //
 // Both decodes are running sums: an entry's index sums the differences since
 // its segment's start, and its place counts the numbers (or non-escape pairs)
-// before it.  Each is computed reduce-then-scan, so that no block ever waits
-// on another:
-//   1. reduce  one block per tile folds its part of the stream into an
-//              aggregate;
-//   2. scan    one block turns the tile aggregates into exclusive prefixes;
-//   3. write   one block per tile reads its part again, starts from its prefix
-//              and writes the indices, staged in LDS so that consecutive lanes
-//              store consecutive entries.
-// The stream is read twice and the indices written once.  (The single-pass
-// form with a decoupled look-back per tile, as the encoders use, was bound by
-// the look-back latency: 3.3 and 5.7 ms on a 306M-entry patch.)
-//
-// A tile is a whole number of units (4,096 bytes or pairs: 16 per thread of a
-// 256-thread block), as many as keep the tile count at most kMaxStreamTiles for
-// the stream's actual length, read from the device.  The aggregates live in
-// the workspace's status ring, two words per tile, and the write pass clears
-// them to zero: the ring's other users (encode, sparsify, the stream
-// encoders) read a zero word as "not published yet", so the workspace can
-// still be shared with them on one stream.
+// before it.  Each is computed reduce-then-scan over tiles of the stream
+// (stream_common.hpp), so that no block ever waits on another:
+//   * COO: a reduce pass folds each tile's pairs into one map on (row,
+//     column, escapes), one block composes the maps, and a write pass gives
+//     every pair its entry's index and place -- the pairs are read twice;
+//   * delta-varint: a count pass (terminating bytes, plain sum of the
+//     numbers), one block numbering the tiles' first entries, a pass over
+//     only the tiles that hold a segment start (their sum since it), one
+//     block carrying the segmented sums, and a write pass -- the bytes are
+//     read twice, plus once more for the tiles with segment starts.
+// The indices are written once, staged in LDS so that consecutive lanes store
+// consecutive entries.  (The single-pass form with a decoupled look-back per
+// tile was bound by the look-back latency: 3.3 and 5.7 ms on a 306M-entry
+// patch, against 0.7 and 1.1 ms here.)
 #include "launch.hpp"
 #include "stream_common.hpp"
 
