@@ -218,10 +218,10 @@ def test_decode_capacity_and_empty():
 
 
 def test_round_trip_on_one_workspace_twice():
-    """The BF16 encode, the COO encode and the COO decode (two chained sums per
-    tile, two sequence numbers of the ring each) back to back on one
-    workspace, twice: every launch must start past the sequence numbers of
-    the one before it."""
+    """The BF16 encode (tickets and status words in the workspace's ring), the
+    COO encode and the COO decode (tile aggregates in the same ring, cleared
+    to zero after use) back to back on one workspace, twice: each must leave
+    the ring valid for the next."""
     rng = np.random.default_rng(14)
     shapes = [(700, 300), (1, 17), (0, 5), (2000, 9), (64, 1024)]
     cols = np.array([c for _, c in shapes], dtype=np.uint32)
