@@ -53,43 +53,55 @@ struct LocoRegs {
   uint4 t0[GATE ? U : 1], t1[GATE ? U : 1];
 };
 
-// Loads of group u of a tile for lane `cl`; whole tiles (`full`, uniform
-// across the block) take the straight-line 16-byte path.  In the gate form a
-// tensor without theta loads nothing for it (its selection uses tau).
-// Unlike the read-only encode, this pass rewrites the residual densely: with
-// plain (cached) loads and stores it measured 9% faster on the 7B-shaped set
-// than with the non-temporal hints.
+// Stand-in source of the prefetch for lanes with no whole group of 8 in range:
+// zero, never written (global, not constant, memory, so that selecting between
+// it and a tensor keeps the loads global rather than flat).
+__device__ __align__(16) uint32_t zero_group[8];
+
+// Loads of group u of a tile for lane `cl`: always the same 16-byte loads into
+// the same registers, from the tensor where all 8 elements of the lane's group
+// lie in it (`live` and in range), else from zero_group.  No branch chooses
+// between load forms, so the registers need no merge copies, which would make
+// the wave wait for these loads right after issuing them; the lane holding a
+// tensor's ragged tail reads its elements one by one when it computes
+// (element_tail).  In the gate form a tensor without theta reads zeros for it
+// (its selection uses tau).  Unlike the read-only encode, this pass rewrites
+// the residual densely: with plain (cached) loads and stores it measured 9%
+// faster on the 7B-shaped set than with the non-temporal hints.
 template <int TBC, int U, bool GATE>
 __device__ __forceinline__ void load_group(LocoRegs<U, GATE>& g, int u, const LocoCtx& c, int cl,
-                                           bool full) {
+                                           bool live) {
   const uint64_t e = c.e0 + (uint64_t)(u * TBC + cl) * 8;
-  if (full) {
-    g.d0[u] = load16(c.d + e);
-    g.d1[u] = load16(c.d + e + 4);
-    g.r0[u] = load16(c.r + e);
-    g.r1[u] = load16(c.r + e + 4);
-    if (GATE && c.th) {
-      g.t0[u] = load16(c.th + e);
-      g.t1[u] = load16(c.th + e + 4);
-    }
-  } else {
-    uint32_t dv[8], rv[8], tv[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const bool ok = e + i < c.n;
-      dv[i] = ok ? __float_as_uint(c.d[e + i]) : 0u;
-      rv[i] = ok ? __float_as_uint(c.r[e + i]) : 0u;
-      tv[i] = (ok && GATE && c.th) ? __float_as_uint(c.th[e + i]) : 0u;
-    }
-    g.d0[u] = make_uint4(dv[0], dv[1], dv[2], dv[3]);
-    g.d1[u] = make_uint4(dv[4], dv[5], dv[6], dv[7]);
-    g.r0[u] = make_uint4(rv[0], rv[1], rv[2], rv[3]);
-    g.r1[u] = make_uint4(rv[4], rv[5], rv[6], rv[7]);
-    if (GATE) {
-      g.t0[u] = make_uint4(tv[0], tv[1], tv[2], tv[3]);
-      g.t1[u] = make_uint4(tv[4], tv[5], tv[6], tv[7]);
-    }
+  const bool ok = live && e + 8 <= c.n;
+  const uint32_t* const zero = zero_group;
+  const uint32_t* const d = ok ? (const uint32_t*)(c.d + e) : zero;
+  const uint32_t* const r = ok ? (const uint32_t*)(c.r + e) : zero;
+  g.d0[u] = load16(d);
+  g.d1[u] = load16(d + 4);
+  g.r0[u] = load16(r);
+  g.r1[u] = load16(r + 4);
+  if (GATE) {
+    const uint32_t* const t = (ok && c.th) ? (const uint32_t*)(c.th + e) : zero;
+    g.t0[u] = load16(t);
+    g.t1[u] = load16(t + 4);
   }
+}
+
+// Delta, residual and theta of a group that straddles the end of its tensor,
+// element by element (0 past the end).  It ends by waiting for its loads: left
+// outstanding, they would make the common path wait, where the two paths
+// join, for every load issued before them (the next tile's too).
+__device__ __forceinline__ void element_tail(const float* d, const float* r, const float* th,
+                                             uint64_t e, uint64_t n, float (&dv)[8], float (&rv)[8],
+                                             float (&tv)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const bool ok = e + i < n;
+    dv[i] = ok ? d[e + i] : 0.0f;
+    rv[i] = ok ? r[e + i] : 0.0f;
+    tv[i] = (ok && th) ? th[e + i] : 0.0f;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // every counter at zero
 }
 
 }  // namespace
@@ -119,13 +131,14 @@ struct LocoDeferred {
   uint32_t excl[(U + 1) / 2];
 };
 
-// Shape of each form.  The threshold form streams 12 bytes per element with
-// two groups per lane and one tile of loads in flight (two groups of 64 bytes
-// per lane, 120 KiB per CU); the gate forms also stream theta, so they keep
-// one group per lane and two tiles in flight -- both within the 128 registers
-// a 16-wave block allows.
-constexpr int loco_u(int gm) { return gm == 0 ? 2 : 1; }
-constexpr int loco_ahead(int gm) { return gm == 0 ? 1 : 2; }
+// Shape of each form: one group of 8 elements per lane and two tiles of loads
+// in flight (the threshold form streams 12 bytes per element, the gate forms
+// also theta, 16), within the 128 registers a 16-wave block allows.  For the
+// threshold form this measured 3.5-4.5% faster on the 7B-shaped set than two
+// groups per lane with one tile in flight, and than two groups with two tiles
+// (which needs all 128 registers).
+constexpr int loco_u(int) { return 1; }
+constexpr int loco_ahead(int) { return 2; }
 
 // GM: 0 = threshold only, 1 = BF16 gate, 2 = FP8 gate, 3 = MXFP4 gate
 // (tensors without theta use the threshold in every mode).
@@ -182,23 +195,19 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
     const Ticket t = ticket_at(s_tk, q);
     if (t.tile < p.ntiles) {
       const LocoCtx c = locate(p, lane_begin, t.tile, TILE);
-      const bool full = c.e0 + TILE <= c.n;
 #pragma unroll
-      for (int u = 0; u < U; ++u) load_group<TBC, U, GATE>(q == 0 ? g0 : g1, u, c, tid, full);
+      for (int u = 0; u < U; ++u) load_group<TBC, U, GATE>(q == 0 ? g0 : g1, u, c, tid, true);
       (q == 0 ? e0_0 : e0_1) = c.e0;
       (q == 0 ? k_0 : k_1) = c.k;
     }
   }
   // T(i + AH) is looked up right after the barrier that publishes it
-  LocoCtx cn;
-  bool have_next = false, next_full = false;
+  LocoCtx cn{};
+  bool have_next = false;
   auto look_up_next = [&](int i) {
     const Ticket t = ticket_at(s_tk, i + AH);
     have_next = t.tile < p.ntiles;
-    if (have_next) {
-      cn = locate(p, lane_begin, t.tile, TILE);
-      next_full = cn.e0 + TILE <= cn.n;
-    }
+    if (have_next) cn = locate(p, lane_begin, t.tile, TILE);
   };
   look_up_next(0);
   LocoDeferred<U> hist[kDefer];
@@ -213,29 +222,34 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
     for (int d = 0; d < kDefer; ++d) pending |= hist[d].valid;
     if (!pending) return false;
     uint32_t mask_packed = 0, excl_packed[(U + 1) / 2], ovf = 0;
-    if (have_cur) {
+    {
       float* const cres = p.t[ck].residual;
       const uint64_t cn_n = p.t[ck].n;
       const bool full = ce0 + TILE <= cn_n;
       const bool gate = GATE && p.t[ck].theta != nullptr;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
+       if (have_cur) {
         const uint64_t e = ce0 + (uint64_t)(u * TBC + tid) * 8;
         const bool vec = full || e + 8 <= cn_n;
         uint32_t m = 0;
-        float a[8];
+        float dv[8], rv[8], tv[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const float dv = __uint_as_float(i < 4 ? get_u32(g.d0[u], i) : get_u32(g.d1[u], i - 4));
-          const float rv = __uint_as_float(i < 4 ? get_u32(g.r0[u], i) : get_u32(g.r1[u], i - 4));
-          a[i] = dv + rv;
+          dv[i] = __uint_as_float(i < 4 ? get_u32(g.d0[u], i) : get_u32(g.d1[u], i - 4));
+          rv[i] = __uint_as_float(i < 4 ? get_u32(g.r0[u], i) : get_u32(g.r1[u], i - 4));
+          tv[i] = 0.0f;
+          if (GATE) tv[i] = __uint_as_float(get_u32(i < 4 ? g.t0[GATE ? u : 0] : g.t1[GATE ? u : 0], i & 3));
         }
+        if (!vec) element_tail(p.t[ck].delta, cres, gate ? p.t[ck].theta : nullptr, e, cn_n, dv, rv, tv);
+        float a[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a[i] = dv[i] + rv[i];
         if (gate && GM == 1) {
           // selected iff bf16(theta) != bf16(theta - a), pairwise on the cvt unit
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const uint4& tq = j < 2 ? g.t0[GATE ? u : 0] : g.t1[GATE ? u : 0];
-            const uint32_t t_lo = get_u32(tq, (2 * j) & 3), t_hi = get_u32(tq, (2 * j + 1) & 3);
+            const uint32_t t_lo = __float_as_uint(tv[2 * j]), t_hi = __float_as_uint(tv[2 * j + 1]);
             const float after_lo = __uint_as_float(t_lo) - a[2 * j];
             const float after_hi = __uint_as_float(t_hi) - a[2 * j + 1];
             m |= diff2(bf16x2_rne(t_lo, t_hi),
@@ -246,8 +260,7 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           float th[8], af[8];
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
-            const uint4& tq = i < 4 ? g.t0[GATE ? u : 0] : g.t1[GATE ? u : 0];
-            th[i] = __uint_as_float(get_u32(tq, i & 3));
+            th[i] = tv[i];
             af[i] = th[i] - a[i];
           }
           if (GM == 2) {
@@ -318,8 +331,10 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
           for (int i = 0; i < 8; ++i)
             if (e + i < cn_n) cres[e + i] = nr[i];
         }
+       }
         // this group's registers are free: start T(i + AH)'s loads into them
-        if (have_next) load_group<TBC, U, GATE>(g, u, cn, tid, next_full);
+        // (unconditionally, so that they are the only definition of them)
+        load_group<TBC, U, GATE>(g, u, cn, tid, have_next);
       }
     }
     __syncthreads();  // wave totals of T(i) published; prefix of T(i - kDefer) resolved
@@ -337,7 +352,15 @@ __global__ __launch_bounds__((NW + 1) * 64) void loco_kernel(LocoParams p) {
       if (!overflowed) {
         // entry j of the tile lies in the last wave-group q whose prefix is <= j
         const uint32_t tbase = base + (uint32_t)od.e0;
-        for (uint32_t j = tid; j < tile_cnt; j += TBC) {
+        // No segment overflowed, so the tile holds at most NSEG * kSegCap =
+        // U * TBC entries: U rounds, unrolled rather than a loop (a loop of
+        // stores makes hipcc wait for every outstanding load, i.e. the next
+        // tile's, before entering it)
+        static_assert(NSEG * kSegCap == U * TBC, "one entry per thread and round");
+#pragma unroll
+        for (int round = 0; round < U; ++round) {
+          const uint32_t j = (uint32_t)(tid + round * TBC);
+          if (j >= tile_cnt) break;
           int q = 0;
 #pragma unroll
           for (int step = 32; step > 0; step >>= 1)
