@@ -210,6 +210,12 @@ class Ceiling:
         L.ceiling_covered.restype = u64
         L.ceiling_read2.argtypes = [ctypes.c_int, vp, vp, u64, vp, vp]
         L.ceiling_rmw.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp, u64, ctypes.c_uint32, vp]
+        L.ceiling_oneshot_shapes.restype = ctypes.c_int
+        L.ceiling_oneshot_covered.argtypes = [ctypes.c_int, ctypes.c_int, u64]
+        L.ceiling_oneshot_covered.restype = u64
+        L.ceiling_read2_oneshot.argtypes = [ctypes.c_int, vp, vp, u64, vp, vp]
+        L.ceiling_rmw_oneshot.argtypes = [ctypes.c_int, vp, vp, u64, ctypes.c_uint32, vp]
+        L.ceiling_refresh_oneshot.argtypes = [ctypes.c_int, vp, vp, vp, u64, vp]
         self.L = L
 
     def best(self, pattern, run, N, bytes_per_elem, reps=3):
@@ -221,6 +227,17 @@ class Ceiling:
                 cov = self.L.ceiling_covered(pattern, sh, N)
                 shapes[f"shape{sh}" + ("" if pattern == 0 else f"_nt{nt}")] = round(
                     bytes_per_elem * cov / (median(ts) * 1e-3) / 1e9, 1)
+        label = max(shapes, key=shapes.get)
+        return shapes[label], label, shapes
+
+    def best_oneshot(self, pattern, run, N, bytes_per_elem, reps=3):
+        """Fastest one-shot shape (threads per block): (GB/s over N elements of
+        bytes_per_elem each, shape label, every shape's GB/s)."""
+        shapes = {}
+        for sh in range(self.L.ceiling_oneshot_shapes()):
+            ts = timed_reps(lambda ev: run(sh, ev), reps, 1)
+            cov = self.L.ceiling_oneshot_covered(pattern, sh, N)
+            shapes[f"oneshot{sh}"] = round(bytes_per_elem * cov / (median(ts) * 1e-3) / 1e9, 1)
         label = max(shapes, key=shapes.get)
         return shapes[label], label, shapes
 
@@ -396,13 +413,48 @@ def main():
                 ev[1].record(stream)
             assert rc == 0, rc
         gbs, label, shapes = ceiling.best(0, read2, N, 6.0)
+
+        def read2_os(sh, ev):
+            if ev:
+                ev[0].record(stream)
+            rc = ceiling.L.ceiling_read2_oneshot(sh, ps.w.data_ptr(), ps.S.data_ptr(), N,
+                                                 sink.data_ptr(), stream.cuda_stream)
+            if ev:
+                ev[1].record(stream)
+            assert rc == 0, rc
+        os_gbs, os_label, os_shapes = ceiling.best_oneshot(0, read2_os, N, 6.0)
         del sink
+
+        # The fused pass's HBM traffic without its ordering work: the reads, the
+        # cast and compare, and the whole-line refresh of R (which holds
+        # bf16(w') here, so the rewritten lines keep their values).
+        def refresh_os(sh, ev):
+            if ev:
+                ev[0].record(stream)
+            rc = ceiling.L.ceiling_refresh_oneshot(sh, ps.w.data_ptr(), ps.S.data_ptr(),
+                                                   R.data_ptr(), N, stream.cuda_stream)
+            if ev:
+                ev[1].record(stream)
+            assert rc == 0, rc
+        rf_gbs, rf_label, rf_shapes = ceiling.best_oneshot(2, refresh_os, N, 6.0)
+        refresh_ms = 6.0 * N / rf_gbs / 1e6
         plain_gbs = (6.0 * N + 6.0 * sent) / (enc_ms * 1e-3) / 1e9
-        ceil = {"read_6B_per_elem_GBps": gbs, "best_shape": label, "shapes_GBps": shapes,
-                "fused_encode_frac_of_ceiling": round(achieved / gbs, 4),
-                "plain_encode_frac_of_ceiling": round(plain_gbs / gbs, 4)}
-        log(f"[bench] read ceiling (4 B FP32 + 2 B BF16 per element) {gbs:.0f} GB/s ({label}); "
-            f"fused encode at {achieved / gbs:.1%}, plain encode at {plain_gbs / gbs:.1%} of it")
+        read_ceiling = max(gbs, os_gbs)
+        ceil = {"read_6B_per_elem_GBps": read_ceiling,
+                "persistent": {"GBps": gbs, "best_shape": label, "shapes_GBps": shapes},
+                "oneshot": {"GBps": os_gbs, "best_shape": os_label, "shapes_GBps": os_shapes},
+                "refresh_stream": {"ms_per_step": round(refresh_ms, 4), "GBps_6B_per_elem": rf_gbs,
+                                   "best_shape": rf_label, "shapes_GBps": rf_shapes,
+                                   "fused_kernel_ms_per_step": round(fused_kernel_ms, 4),
+                                   "fused_frac_of_refresh_stream": round(refresh_ms / fused_kernel_ms, 4)},
+                "fused_encode_frac_of_ceiling": round(achieved / read_ceiling, 4),
+                "plain_encode_frac_of_ceiling": round(plain_gbs / read_ceiling, 4)}
+        log(f"[bench] read ceiling (4 B FP32 + 2 B BF16 per element) {read_ceiling:.0f} GB/s "
+            f"(persistent {gbs:.0f} {label}, one-shot {os_gbs:.0f} {os_label}); fused encode at "
+            f"{achieved / read_ceiling:.1%}, plain encode at {plain_gbs / read_ceiling:.1%} of it")
+        log(f"[bench] reads + whole-line refresh alone (no compaction, no patch): {refresh_ms:.3f} ms "
+            f"per pass ({rf_label}); the fused kernels take {fused_kernel_ms:.3f} ms "
+            f"({refresh_ms / fused_kernel_ms:.1%} of that stream's speed)")
         legs["ceiling"] = ceil
 
     # ---- the patch's wire format: delta-varint and 2-D COO index streams
@@ -435,6 +487,8 @@ def main():
     if ceil is not None:
         roofline["measured_read_ceiling_GBps"] = ceil["read_6B_per_elem_GBps"]
         roofline["frac_of_measured_ceiling"] = ceil["fused_encode_frac_of_ceiling"]
+        roofline["refresh_stream_ms_per_step"] = ceil["refresh_stream"]["ms_per_step"]
+        roofline["frac_of_refresh_stream"] = ceil["refresh_stream"]["fused_frac_of_refresh_stream"]
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -795,9 +849,11 @@ def loco_leg(args, device, stream, ceiling):
     """PULSELoCo rounds over the 7B-shaped set: the error-feedback sparsification
     (Alg. 2, one worker) at the fixed threshold (chosen once so ~2% of round-1
     entries survive), then again with the threshold re-chosen every round (a
-    sample quantile of |Delta + e|, so ~2% survive each round), the BF16-gate
-    form, and the outer step that consumes the patch (SparseSync average over
-    R = 1 worker, outer Nesterov, mu 0.9, alpha 0.7)."""
+    sample quantile of |Delta + e|, so ~2% survive each round), both in the
+    two-pass form (a workspace with room for its staging area); the one-pass
+    kernel at the fixed threshold; the BF16-gate form; and the outer step that
+    consumes the patch (SparseSync average over R = 1 worker, outer Nesterov,
+    mu 0.9, alpha 0.7)."""
     import numpy as np
     import torch
     from paper_2602_03839_amd import pulse
@@ -814,7 +870,8 @@ def loco_leg(args, device, stream, ceiling):
     theta = torch.empty(N, dtype=torch.float32, device=device).normal_(0.0, 0.02 ** 0.5)
     mom = torch.zeros(N, dtype=torch.float32, device=device)
     patch = Patch(N // 10, T, device, fp32=True)
-    ws = pulse.workspace(device)
+    ws = pulse.workspace(device)           # the one-pass kernel
+    ws2 = pulse.loco_workspace(N, device)  # room for the two-pass form's staging
     parts = chunks(T, CHUNK)
     view = lambda b, i: b[offs[i]:offs[i + 1]]
     thr = [pulse.LocoBatch([pulse.LocoTensor(view(delta, i), view(resid, i), None, 0)
@@ -825,16 +882,16 @@ def loco_leg(args, device, stream, ceiling):
     lists = [pulse.SparseList(patch.idx, patch.val, patch.seg, patch.count, capacity=patch.cap)]
     g = torch.Generator(device=device)
 
-    def sparsify(batches, tv, ev):
+    def sparsify(batches, tv, ev, w=ws):
         patch.count.zero_()
         if ev:
             ev[0].record(stream)
         for (t0, _t1), b in zip(parts, batches):
-            b(tv, patch.idx, patch.val, patch.count, ws, seg_begin=patch.seg[t0:])
+            b(tv, patch.idx, patch.val, patch.count, w, seg_begin=patch.seg[t0:])
         if ev:
             ev[1].record(stream)
 
-    def rounds(per_round_tau):
+    def rounds(per_round_tau, w):
         resid.zero_()
         ms, ms_outer, dens, taus = [], [], [], []
         for r in range(args.loco_rounds):
@@ -849,7 +906,7 @@ def loco_leg(args, device, stream, ceiling):
                 del pos, a
             torch.cuda.synchronize()
             ev, eo = event_pair(), event_pair()
-            sparsify(thr, tv, ev)
+            sparsify(thr, tv, ev, w)
             eo[0].record(stream)
             outer(lists, mu=0.9, alpha=0.7)
             eo[1].record(stream)
@@ -860,7 +917,7 @@ def loco_leg(args, device, stream, ceiling):
             taus.append(tv)
         return ms, ms_outer, dens, taus
 
-    ms, ms_outer, dens, _ = rounds(False)
+    ms, ms_outer, dens, _ = rounds(False, ws2)
     skip = 1 if len(ms) > 1 else 0
     med = median(ms[skip:])
     med_outer = median(ms_outer[skip:])
@@ -870,15 +927,20 @@ def loco_leg(args, device, stream, ceiling):
     log(f"[bench] loco 7b: sparsify median {med:.3f} ms/round ({12.0 * N / med / 1e6:.0f} GB/s at 12 B/param); "
         f"outer step median {med_outer:.3f} ms ({outer_bytes / med_outer / 1e6:.0f} GB/s); "
         f"density {dens[0]:.4%} -> {dens[-1]:.4%}")
-    ms_p, _mo, dens_p, taus_p = rounds(True)
+    ms_p, _mo, dens_p, taus_p = rounds(True, ws2)
     med_p = median(ms_p[skip:])
     log(f"[bench] loco 7b, tau re-chosen each round: sparsify median {med_p:.3f} ms/round, density "
         f"{dens_p[0]:.4%} -> {dens_p[-1]:.4%}")
+    ms_1, _mo1, dens_1, _t1 = rounds(False, ws)
+    med_1 = median(ms_1[skip:])
+    log(f"[bench] loco 7b, one-pass kernel: sparsify median {med_1:.3f} ms/round, density "
+        f"{dens_1[0]:.4%} -> {dens_1[-1]:.4%}")
     # the gate form (Alg. 2's selection by the BF16 visibility of theta - a)
     gt = timed_reps(lambda ev: sparsify(gate, 0.0, ev), max(3, args.steps), 1,
                     before=lambda: resid.zero_())
     g_ms, g_dens = median(gt), int(patch.count.item()) / N
     pulse.check_workspace(ws)
+    pulse.check_workspace(ws2)
     log(f"[bench] loco 7b, BF16 gate: {g_ms:.3f} ms/round ({16.0 * N / g_ms / 1e6:.0f} GB/s at 16 B/param), "
         f"density {g_dens:.4%}")
     out = {
@@ -889,8 +951,11 @@ def loco_leg(args, device, stream, ceiling):
         "ms_per_round": [round(m, 4) for m in ms],
         "GBps_12B_per_param": round(12.0 * N / med / 1e6, 2),
         "hbm_frac_of_peak": round(loco_bytes / med / 1e6 / HBM_PEAK_GBS, 4),
-        "kernel": "loco_kernel (threshold form)",
+        "kernel": "loco_stage_kernel + ordering passes (two-pass threshold form)",
         "density_first_last": [round(dens[0], 6), round(dens[-1], 6)],
+        "one_pass": {"ms_per_round_median": round(med_1, 4),
+                     "ms_per_round": [round(m, 4) for m in ms_1],
+                     "kernel": "loco_kernel (threshold form)"},
         "per_round_tau": {"ms_per_round_median": round(med_p, 4),
                           "density_first_last": [round(dens_p[0], 6), round(dens_p[-1], 6)],
                           "tau_first_last": [taus_p[0], taus_p[-1]],
@@ -919,15 +984,32 @@ def loco_leg(args, device, stream, ceiling):
                 ev[1].record(stream)
             assert rc == 0, rc
         gbs, label, shapes = ceiling.best(1, rmw, N, 12.0)
+
+        def rmw_os(sh, ev):
+            if ev:
+                ev[0].record(stream)
+            rc = ceiling.L.ceiling_rmw_oneshot(sh, delta.data_ptr(), resid.data_ptr(), N, NEVER,
+                                               stream.cuda_stream)
+            if ev:
+                ev[1].record(stream)
+            assert rc == 0, rc
+        os_gbs, os_label, os_shapes = ceiling.best_oneshot(1, rmw_os, N, 12.0)
         add_ms = median(timed_reps(lambda ev: (ev and ev[0].record(stream),
                                                torch.add(delta, resid, out=resid),
                                                ev and ev[1].record(stream)), 3, 1))
-        out["ceiling"] = {"rmw_12B_per_elem_GBps": gbs, "best_shape": label, "shapes_GBps": shapes,
+        best = max(gbs, os_gbs)
+        out["ceiling"] = {"rmw_12B_per_elem_GBps": best,
+                          "persistent": {"GBps": gbs, "best_shape": label, "shapes_GBps": shapes,
+                                         "sparsify_frac": round(loco_bytes / med / 1e6 / gbs, 4)},
+                          "oneshot": {"GBps": os_gbs, "best_shape": os_label, "shapes_GBps": os_shapes,
+                                      "ms_per_round": round(12.0 * N / os_gbs / 1e6, 4)},
                           "torch_add_GBps": round(12.0 * N / add_ms / 1e6, 1),
-                          "sparsify_frac_of_ceiling": round(loco_bytes / med / 1e6 / gbs, 4)}
-        log(f"[bench] rmw ceiling (8 B read + 4 B written per element) {gbs:.0f} GB/s ({label}); "
-            f"torch.add {12.0 * N / add_ms / 1e6:.0f} GB/s; sparsify at "
-            f"{out['ceiling']['sparsify_frac_of_ceiling']:.1%} of the ceiling")
+                          "sparsify_frac_of_ceiling": round(loco_bytes / med / 1e6 / best, 4)}
+        log(f"[bench] rmw ceiling (8 B read + 4 B written per element) {best:.0f} GB/s (persistent "
+            f"{gbs:.0f} {label}, one-shot {os_gbs:.0f} {os_label}); torch.add "
+            f"{12.0 * N / add_ms / 1e6:.0f} GB/s; sparsify at "
+            f"{out['ceiling']['sparsify_frac_of_ceiling']:.1%} of the ceiling, "
+            f"{out['ceiling']['persistent']['sparsify_frac']:.1%} of the persistent probe")
     return out
 
 

@@ -238,6 +238,9 @@ int pulse_apply_batch(const pulse_apply_tensor *tensors, uint32_t ntensors,
  * (e[not I] <- s).  NaN is never selected by the threshold form.
  *   delta, residual (in/out), theta: FP32 [n], 16-byte aligned.
  *   idx, val   FP32 patch with room for `capacity` entries.
+ *   workspace  at least pulse_workspace_bytes() bytes, see above.  With a
+ *              larger one (pulse_loco_workspace_bytes) the threshold form
+ *              runs in two passes, with the same results.
  */
 int pulse_loco_sparsify(const float *delta, float *residual, uint64_t n, float tau,
                         const float *theta, uint32_t *idx, float *val, uint64_t capacity,
@@ -252,6 +255,24 @@ typedef struct pulse_loco_tensor {
     uint64_t n;
     uint32_t index_base;
 } pulse_loco_tensor;
+
+/*
+ * pulse_loco_workspace_bytes -- size of a workspace with which a threshold-
+ * form sparsify call (no theta; pulse_loco_sparsify[_batch]) over tensors of
+ * at most n elements in all runs entirely in its two-pass form.  The first
+ * pass streams Delta and e as many short-lived blocks in address order (the
+ * fastest way this chip streams a read-modify-write), staging each 1,024-
+ * element tile's selected entries in the workspace; the second writes them
+ * to the patch in index order.  The results -- patch, count, seg_begin,
+ * residual -- are bit-identical to the one-pass form's.
+ * The part of the workspace past pulse_workspace_bytes() holds the staging
+ * area and needs no initialisation; the first pulse_workspace_bytes() keep
+ * the rules above (zero-filled once), so one workspace may serve every call
+ * ordered on a stream.  A call whose launch (<= 64 tensors) needs more
+ * staging than the workspace holds runs that launch in one pass; the gate
+ * forms always run in one pass.  About 1 byte of workspace per element.
+ */
+size_t pulse_loco_workspace_bytes(uint64_t n);
 
 /* pulse_loco_sparsify over tensors in order, appended to one patch (see pulse_encode_batch). */
 int pulse_loco_sparsify_batch(const pulse_loco_tensor *tensors, uint32_t ntensors, float tau,

@@ -288,6 +288,17 @@ uint32_t encode_tile_elems();
 uint32_t loco_tile_elems(int gm);
 hipError_t launch_encode(EncodeParams& p, hipStream_t stream);
 hipError_t launch_loco(LocoParams& p, hipStream_t stream);
+
+// Two-pass form of the threshold sparsifier (loco2.hip): tiles of kL2Tile
+// elements, each staging up to kL2Cap selected entries; the ordering passes
+// work on units of kL2Unit tiles.  Its staging area (loco2_scratch_bytes for
+// a launch of ntiles tiles) lies in the caller's workspace past the fixed
+// part.  p.ntiles counts kL2Tile-element tiles.
+constexpr uint32_t kL2Tile = 1024;
+constexpr uint32_t kL2Cap = 128;
+constexpr uint32_t kL2Unit = 256;
+size_t loco2_scratch_bytes(uint32_t ntiles);
+hipError_t launch_loco2(LocoParams& p, void* scratch, hipStream_t stream);
 hipError_t launch_apply(const ApplyParams& p, hipStream_t stream);
 hipError_t launch_cast(const float* src, uint16_t* dst, uint64_t n, hipStream_t stream);
 // p[0 .. nwords) = 0 by a kernel (not a memset, so a captured graph replays it as a kernel)

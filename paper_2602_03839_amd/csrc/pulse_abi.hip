@@ -62,6 +62,20 @@ bool refresh_mirrors(const pulse_encode_tensor& d) {
 
 uint32_t tiles_for(uint64_t n, uint32_t tile) { return (uint32_t)((n + tile - 1) / tile); }
 
+// Largest two-pass launch (in kL2Tile-element tiles) whose staging area fits a
+// workspace of `bytes` bytes; 0 if none does.  Capped so that a launch's grid
+// stays below 2^31 blocks.
+constexpr uint32_t kMaxLoco2Tiles = (1u << 31) - 1;
+
+uint32_t loco2_max_tiles(size_t bytes) {
+  if (bytes <= pulse::kWorkspaceBytes) return 0;
+  const size_t room = bytes - pulse::kWorkspaceBytes;
+  uint64_t m = room / (pulse::kL2Cap * 8 + 4);
+  if (m > kMaxLoco2Tiles) m = kMaxLoco2Tiles;
+  while (m > 0 && pulse::loco2_scratch_bytes((uint32_t)m) > room) --m;
+  return (uint32_t)m;
+}
+
 // Workspace of the weight hash: the tensor table (one entry per tensor plus
 // the end of the stream), one 16 KiB scratch slot per tensor, and two buffers
 // for the tree levels above the leaves (level 1 and level 2; later levels
@@ -90,6 +104,13 @@ HashLayout hash_layout(uint32_t ntensors, uint64_t total_values) {
 extern "C" {
 
 size_t pulse_workspace_bytes(void) { return pulse::kWorkspaceBytes; }
+
+size_t pulse_loco_workspace_bytes(uint64_t n) {
+  // every launch holds at most 64 tensors, each adding at most one partial tile
+  uint64_t tiles = n / pulse::kL2Tile + pulse::kMaxBatch;
+  if (tiles > kMaxLoco2Tiles) tiles = kMaxLoco2Tiles;
+  return pulse::kWorkspaceBytes + pulse::loco2_scratch_bytes((uint32_t)tiles);
+}
 
 int pulse_workspace_status(const void* workspace, size_t workspace_bytes, void* stream) {
   if (int rc = check_workspace(const_cast<void*>(workspace), workspace_bytes)) return rc;
@@ -353,6 +374,11 @@ int loco_batch(const pulse_loco_tensor* tensors, const float* inv_scales, uint32
   const int gm = !any_theta ? 0 : gate_dtype == pulse::kDtypeFp8 ? 2
                                  : gate_dtype == pulse::kDtypeMxfp4 ? 3 : 1;
   const uint32_t tile = pulse::loco_tile_elems(gm);
+  // The threshold form runs in two passes when the workspace has room past
+  // its fixed part for a launch's staging area; a tensor too large for it on
+  // its own takes the one-pass kernel.
+  const uint32_t max2 = gm == 0 ? loco2_max_tiles(workspace_bytes) : 0;
+  void* const scratch = static_cast<uint8_t*>(workspace) + pulse::kWorkspaceBytes;
   uint32_t t0 = 0;
   while (t0 < ntensors) {
     pulse::LocoParams p;
@@ -368,6 +394,32 @@ int loco_batch(const pulse_loco_tensor* tensors, const float* inv_scales, uint32
     p.gm = gm;
     uint32_t tiles = 0;
     int k = 0;
+    if (max2 > 0) {
+      while (t0 + k < ntensors && k < pulse::kMaxBatch) {
+        const pulse_loco_tensor& d = tensors[t0 + k];
+        const uint32_t nt = tiles_for(d.n, pulse::kL2Tile);
+        if ((uint64_t)tiles + nt > max2) break;
+        p.tile_begin[k] = tiles;
+        p.t[k].delta = d.delta;
+        p.t[k].residual = d.residual;
+        p.t[k].theta = d.theta;
+        p.t[k].n = d.n;
+        p.t[k].index_base = d.index_base;
+        p.t[k].inv_scale = 1.0f;
+        tiles += nt;
+        ++k;
+      }
+      if (k > 0) {
+        p.tile_begin[k] = tiles;
+        p.ntensors = k;
+        p.ntiles = tiles;
+        if (int rc = hip_status(pulse::launch_loco2(p, scratch, (hipStream_t)stream),
+                                "loco launch (two-pass)"))
+          return rc;
+        t0 += k;
+        continue;
+      }
+    }
     while (t0 + k < ntensors && k < pulse::kMaxBatch) {
       const pulse_loco_tensor& d = tensors[t0 + k];
       const uint32_t nt = tiles_for(d.n, tile);

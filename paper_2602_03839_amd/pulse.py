@@ -85,7 +85,7 @@ class _HashTensor(ctypes.Structure):
 HASH_LEAF_BYTES = 16384  # PULSE_HASH_LEAF_BYTES
 
 EXPORTS = ("pulse_workspace_bytes", "pulse_strerror", "pulse_last_error", "pulse_cast_bf16",
-           "pulse_workspace_status",
+           "pulse_workspace_status", "pulse_loco_workspace_bytes",
            "pulse_encode", "pulse_encode_batch", "pulse_encode_batch_noalloc",
            "pulse_apply", "pulse_apply_batch",
            "pulse_loco_sparsify", "pulse_loco_sparsify_batch",
@@ -109,6 +109,8 @@ def lib():
             sz = ctypes.c_size_t
             L.pulse_workspace_bytes.argtypes = []
             L.pulse_workspace_bytes.restype = sz
+            L.pulse_loco_workspace_bytes.argtypes = [u64]
+            L.pulse_loco_workspace_bytes.restype = sz
             L.pulse_strerror.argtypes = [i32]
             L.pulse_strerror.restype = ctypes.c_char_p
             L.pulse_last_error.argtypes = []
@@ -141,7 +143,8 @@ def lib():
             L.pulse_loco_sparsify_lowp_batch.argtypes = [i32, vp, vp, u32, vp, vp, u64, vp, vp, vp,
                                                          sz, vp]
             for name in EXPORTS[3:]:
-                if name not in ("pulse_hash_leaf_count", "pulse_hash_workspace_bytes"):
+                if name not in ("pulse_hash_leaf_count", "pulse_hash_workspace_bytes",
+                                "pulse_loco_workspace_bytes"):
                     getattr(L, name).restype = i32
             _lib = L
     return _lib
@@ -229,6 +232,20 @@ def workspace_bytes() -> int:
 def workspace(device=None) -> torch.Tensor:
     """A zero-filled workspace; reuse it for every call ordered on one stream."""
     return torch.zeros(workspace_bytes(), dtype=torch.uint8, device=device or "cuda")
+
+
+def loco_workspace_bytes(n: int) -> int:
+    return int(lib().pulse_loco_workspace_bytes(int(n)))
+
+
+def loco_workspace(n: int, device=None) -> torch.Tensor:
+    """A workspace with which threshold-form sparsify calls over at most n
+    elements run in two passes: the fixed part zero-filled, the staging area
+    past it left as allocated.  It serves every other call as a plain
+    workspace too."""
+    ws = torch.empty(loco_workspace_bytes(n), dtype=torch.uint8, device=device or "cuda")
+    ws[:workspace_bytes()].zero_()
+    return ws
 
 
 def workspace_status(ws: torch.Tensor, stream=None) -> int:

@@ -31,7 +31,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = declared_functions()
-    assert len(names) == 25, names
+    assert len(names) == 26, names
     assert set(names) == set(pulse.EXPORTS)
     for name in names:
         assert hasattr(L, name), name
@@ -42,6 +42,19 @@ def test_strerror_and_workspace(L):
     for rc in (OK, EINVAL, ERANGE, EALIGN, -4, pulse.ESTATE):
         assert L.pulse_strerror(rc).decode().startswith("PULSE_")
     assert b"ESTATE" in L.pulse_strerror(pulse.ESTATE)
+
+
+def test_loco_workspace_size(L):
+    """The two-pass sparsifier's workspace: the fixed part plus, per element,
+    about one byte of staging (a 1,024-element tile stages up to 128 8-byte
+    entries), growing with n and never below the fixed part."""
+    fixed = L.pulse_workspace_bytes()
+    sizes = [L.pulse_loco_workspace_bytes(n) for n in (0, 1, 1024, 1 << 20, 7_615_487_488)]
+    assert all(s > fixed for s in sizes)
+    assert sizes == sorted(sizes)
+    per_elem = (sizes[-1] - fixed) / 7_615_487_488
+    assert 1.0 < per_elem < 1.01, per_elem
+    assert L.pulse_loco_workspace_bytes(1 << 62) > fixed  # clamped, no overflow
 
 
 def test_workspace_status_validation(L):

@@ -1,6 +1,11 @@
 """GPU parity for PULSELoCo sparsification (Alg. 2) against the oracle, bit-exact:
 emitted indices, FP32 values and the FP32 residual, over shapes, thresholds,
-the BF16-gate form, overflow, batches, and a 10-round error-feedback chain."""
+the BF16-gate form, overflow, batches, and a 10-round error-feedback chain.
+
+Every test runs twice: with a plain workspace (the one-pass persistent
+kernel) and with one that has room for the two-pass form's staging area
+(the threshold form then stages 1,024-element tiles and orders them in a
+second pass; the gate forms still run in one pass)."""
 import math
 
 import numpy as np
@@ -19,9 +24,11 @@ GATE_TILE = 960 * 1 * 8  # and of the gate forms
 EDGES = sorted({m * t + d for t in (7680, 15360) for m in (1, 3) for d in (-1, 0, 1)})
 
 
-@pytest.fixture(scope="module")
-def ws():
-    return pulse.workspace()
+@pytest.fixture(scope="module", params=["one_pass", "two_pass"])
+def ws(request):
+    if request.param == "one_pass":
+        return pulse.workspace()
+    return pulse.loco_workspace(1 << 24)
 
 
 def run_loco(delta, res, tau, ws, theta=None, capacity=None, index_base=0, count_in=0):
@@ -175,3 +182,89 @@ def test_loco_batch_with_empty_tensors(ws):
     np.testing.assert_array_equal(hf32(g_val)[:cnt].view(np.uint32), o_val[:cnt].view(np.uint32))
     for (d, e, th, b), desc in zip(host, descs):
         np.testing.assert_array_equal(hf32(desc.residual).view(np.uint32), e.view(np.uint32))
+
+
+L2_TILE = 1024  # tile of the two-pass form
+
+
+@pytest.mark.parametrize("n", [L2_TILE - 1, L2_TILE, L2_TILE + 1, 256 * L2_TILE, 256 * L2_TILE + 1,
+                               300 * L2_TILE + 513])
+def test_loco_two_pass_tile_and_unit_edges(n):
+    """Tile edges of the staging pass and unit edges (256 tiles) of the
+    ordering passes, with an append position and an index base."""
+    rng = np.random.default_rng(n)
+    tau = wl.loco_tau()
+    d = wl.loco_delta_np(rng, n)
+    e = (wl.loco_delta_np(rng, n) * np.float32(0.5)).astype(np.float32)
+    ws2 = pulse.loco_workspace(n)
+    run_loco(d, e, tau, ws2, count_in=11, index_base=5)
+    nnz = int((np.abs(d + e) >= np.float32(tau)).sum())
+    run_loco(d, e, tau, ws2, capacity=11 + nnz // 2, count_in=11, index_base=5)
+
+
+def test_loco_two_pass_dense_tiles():
+    """Tiles that select more than a staging slot holds (128 of 1,024) beside
+    sparse ones, in every mix within a unit, with the capacity cutting
+    through staged tiles, re-derived tiles and the boundary between them."""
+    rng = np.random.default_rng(31)
+    tau = wl.loco_tau()
+    ntile = 600
+    n = ntile * L2_TILE - 77
+    frac = np.repeat(rng.choice([0.001, 0.02, 0.12, 0.13, 0.5, 1.0], ntile), L2_TILE)[:n]
+    big = rng.random(n) < frac
+    d = rng.normal(0, tau / 10, n).astype(np.float32)
+    d[big] = np.float32(2 * tau) * np.sign(rng.normal(size=big.sum())).astype(np.float32)
+    e = rng.normal(0, tau / 20, n).astype(np.float32)
+    ws2 = pulse.loco_workspace(n)
+    nnz = run_loco(d, e, tau, ws2)[0]
+    assert nnz > n * 0.1
+    sel = np.abs(d + e) >= np.float32(tau)
+    per_tile = np.add.reduceat(sel, np.arange(0, n, L2_TILE))
+    assert (per_tile > 128).sum() > 50 and (per_tile <= 128).sum() > 50
+    cuts = np.cumsum(per_tile)
+    for cap in (nnz // 3, int(cuts[per_tile.argmax()]), int(cuts[per_tile.argmax()]) + 1, 3):
+        run_loco(d, e, tau, ws2, capacity=cap + 2, count_in=2, index_base=1)
+
+
+def test_loco_two_pass_batches_and_fallback():
+    """A threshold-form batch of 150 tensors (empty ones first, between and
+    last; more than 64, so several launches) on a workspace sized for the
+    whole call, then on one whose staging area holds only small launches, so
+    that the tensors too large for it take the one-pass kernel in between."""
+    rng = np.random.default_rng(41)
+    sizes = [0, 0, 5, 3 * L2_TILE + 1, 0] + [int(rng.integers(0, 9000)) for _ in range(140)]
+    sizes += [200_003, 0, 1, 70_000, 0]
+    tau = wl.loco_tau()
+    host = []
+    base = 0
+    for n in sizes:
+        d = wl.loco_delta_np(rng, n)
+        e = (wl.loco_delta_np(rng, n) * np.float32(0.7)).astype(np.float32)
+        host.append((d, e, base))
+        base += n
+    cap = base + 4
+    o_idx = np.zeros(cap, np.uint32)
+    o_val = np.zeros(cap, np.float32)
+    cnt, o_seg, o_res = 4, [], []
+    for d, e, b in host:
+        o_seg.append(cnt)
+        r = e.copy()
+        cnt, _, _ = oracle.loco(d, r, tau, index_base=b, capacity=cap, count_in=cnt,
+                                idx_out=o_idx, val_out=o_val)
+        o_res.append(r)
+    for ws2 in (pulse.loco_workspace(base), pulse.loco_workspace(20_000)):
+        mk = lambda a: dev(a) if a.size else torch.empty(0, dtype=torch.float32, device="cuda")
+        descs = [pulse.LocoTensor(mk(d), mk(e), None, b) for d, e, b in host]
+        g_idx = torch.zeros(cap, dtype=torch.int32, device="cuda")
+        g_val = torch.zeros(cap, dtype=torch.float32, device="cuda")
+        g_cnt = counter(4)
+        g_seg = torch.full((len(sizes),), -1, dtype=torch.int64, device="cuda")
+        pulse.LocoBatch(descs)(tau, g_idx, g_val, g_cnt, ws2, seg_begin=g_seg)
+        torch.cuda.synchronize()
+        assert read_count(g_cnt) == cnt
+        np.testing.assert_array_equal(g_seg.cpu().numpy(), np.array(o_seg, np.int64))
+        np.testing.assert_array_equal(h32(g_idx)[4:cnt], o_idx[4:cnt])
+        np.testing.assert_array_equal(hf32(g_val)[4:cnt].view(np.uint32),
+                                      o_val[4:cnt].view(np.uint32))
+        for r, desc in zip(o_res, descs):
+            np.testing.assert_array_equal(hf32(desc.residual).view(np.uint32), r.view(np.uint32))
