@@ -190,7 +190,7 @@ def stats_main(argv):
         rows = list(csv.DictReader(fh))
     with open(args.bench_json) as fh:
         d = json.loads([line for line in fh if line.startswith("{")][-1])
-    keep = re.compile(r"pulse::|bitwise_not|read2_kernel|rmw_kernel")
+    keep = re.compile(r"pulse::|bitwise_not|read2_kernel|rmw_kernel|_oneshot")
     out = ["# rocprofv3 kernel stats of one bench.py run", ""]
     out += ["Commands (repository root as the working directory):", "```"] + args.command + ["```", ""]
     out += ["| Kernel | Calls | Avg (ms) | Min (ms) | Max (ms) | Total (ms) |", "|---|---|---|---|---|---|"]
