@@ -246,9 +246,11 @@ __global__ __launch_bounds__(kL2Threads) void loco_gather_kernel(LocoParams p, S
     if (tb < p.ntiles && tb >= t0 && tb < t0 + kL2Unit) p.seg_begin[tid] = ubase + s_pre[tb - t0];
   }
   const uint64_t cap = p.capacity;
-  // staged tiles: wave w copies tiles w, w + kL2Waves, ..., lanes j and
-  // j + 64 entries j and j + 64 of a slot; kBatch tiles' loads are issued
-  // before their stores, so that a wave keeps 2 * kBatch loads in flight
+  // staged tiles: wave w copies the unit's tiles w * kPerWave onwards (one
+  // run of the patch per wave, so the L2 merges the partial lines where one
+  // tile's entries end and the next one's begin), lanes j and j + 64 entries
+  // j and j + 64 of a slot; kBatch tiles' loads are issued before their
+  // stores, so that a wave keeps 2 * kBatch loads in flight
   constexpr int kBatch = 16;
   constexpr int kPerWave = (int)kL2Unit / kL2Waves;
   static_assert(kPerWave % kBatch == 0, "whole batches");
@@ -258,7 +260,7 @@ __global__ __launch_bounds__(kL2Threads) void loco_gather_kernel(LocoParams p, S
     uint32_t cb[kBatch];
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
-      const int i = wid + kL2Waves * (g + b);
+      const int i = wid * kPerWave + g + b;
       const uint32_t ci = s_cnt[i];
       cb[b] = ci <= kL2Cap ? ci : 0u;  // a flagged tile is handled below
       const Staged* const slot = sc.stage + (uint64_t)(t0 + (uint32_t)i) * kL2Cap;
@@ -270,7 +272,7 @@ __global__ __launch_bounds__(kL2Threads) void loco_gather_kernel(LocoParams p, S
     }
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
-      const int i = wid + kL2Waves * (g + b);
+      const int i = wid * kPerWave + g + b;
       const uint64_t pos0 = ubase + s_pre[i];
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
