@@ -24,12 +24,12 @@
 //   pass 2a (loco_unit_sum_kernel): the counts of each unit of kL2Unit tiles.
 //   pass 2b (loco_unit_scan_kernel, one block): each unit's patch position,
 //     from the append position *count; *count grows by the call's total.
-//   pass 2c (loco_gather_kernel): per unit, each tile's position; each wave
-//     copies whole tiles from their staging slots to the patch (positions at or
-//     past the capacity put s back into the residual: not sent, so error
-//     feedback keeps it); a flagged tile is re-derived from the residual,
-//     which holds s there.  Tensors' patch offsets (seg_begin) are written
-//     here and in pass 2b.
+//   pass 2c (loco_gather_kernel): per unit, each tile's position; the unit's
+//     staged entries are copied to the patch in order, one entry per lane
+//     (positions at or past the capacity put s back into the residual: not
+//     sent, so error feedback keeps it); a flagged tile is re-derived from
+//     the residual, which holds s there.  Tensors' patch offsets (seg_begin)
+//     are written here and in pass 2b.
 //
 // Staging memory is the part of the caller's workspace past the fixed header
 // and status ring (see loco2_scratch_bytes); nothing in the fixed part is
@@ -224,7 +224,9 @@ __global__ __launch_bounds__(kL2Threads) void loco_gather_kernel(LocoParams p, S
   __shared__ uint32_t s_w[kL2Waves];
   __shared__ uint32_t s_pre[kL2Unit];  // entries of the unit before each tile
   __shared__ uint32_t s_cnt[kL2Unit];  // each tile's count
+  __shared__ uint8_t s_map[kL2Unit * kL2Cap];  // tile of each staged entry of the unit
   __shared__ uint32_t s_nbig;
+  static_assert(kL2Unit <= 256, "tile of an entry fits a byte");
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid >> 6;
@@ -246,54 +248,84 @@ __global__ __launch_bounds__(kL2Threads) void loco_gather_kernel(LocoParams p, S
     if (tb < p.ntiles && tb >= t0 && tb < t0 + kL2Unit) p.seg_begin[tid] = ubase + s_pre[tb - t0];
   }
   const uint64_t cap = p.capacity;
-  // staged tiles: wave w copies the unit's tiles w * kPerWave onwards (one
-  // run of the patch per wave, so the L2 merges the partial lines where one
-  // tile's entries end and the next one's begin), lanes j and j + 64 entries
-  // j and j + 64 of a slot; kBatch tiles' loads are issued before their
-  // stores, so that a wave keeps 2 * kBatch loads in flight
-  constexpr int kBatch = 16;
-  constexpr int kPerWave = (int)kL2Unit / kL2Waves;
-  static_assert(kPerWave % kBatch == 0, "whole batches");
-  static_assert(kL2Cap == 128, "two entries per lane and slot");
-  for (int g = 0; g < kPerWave; g += kBatch) {
-    Staged v[kBatch][2];
-    uint32_t cb[kBatch];
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int i = wid * kPerWave + g + b;
+  // Staged entries, in the unit's order, one per lane: entry j of the unit is
+  // taken by thread j mod kL2Threads, so every load and store instruction
+  // covers contiguous entries.  A map in LDS names each staged entry's tile;
+  // it covers the unit only while no tile re-derives its entries (the usual
+  // case), else the per-wave copy below serves the unit.
+  if (s_nbig == 0) {
+    // wave w fills the map for the unit's tiles w * kPerWave onwards
+    constexpr int kPerWave = (int)kL2Unit / kL2Waves;
+    for (int i = wid * kPerWave; i < (wid + 1) * kPerWave; ++i) {
       const uint32_t ci = s_cnt[i];
-      cb[b] = ci <= kL2Cap ? ci : 0u;  // a flagged tile is handled below
-      const Staged* const slot = sc.stage + (uint64_t)(t0 + (uint32_t)i) * kL2Cap;
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const uint32_t j = (uint32_t)lane + 64u * r;
-        v[b][r] = j < cb[b] ? slot[j] : Staged{0u, 0u};
-      }
+      const uint32_t b0 = s_pre[i];
+      for (uint32_t r = (uint32_t)lane; r < ci; r += 64) s_map[b0 + r] = (uint8_t)i;
     }
+    __syncthreads();
+    constexpr int kBatch = 8;
+    for (uint32_t j0 = (uint32_t)tid; j0 < total; j0 += kBatch * kL2Threads) {
+      Staged v[kBatch];
 #pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int i = wid * kPerWave + g + b;
-      const uint64_t pos0 = ubase + s_pre[i];
+      for (int b = 0; b < kBatch; ++b) {
+        const uint32_t j = j0 + (uint32_t)b * kL2Threads;
+        v[b] = Staged{0u, 0u};
+        if (j < total) {
+          const uint32_t i = s_map[j];
+          v[b] = sc.stage[(uint64_t)(t0 + i) * kL2Cap + (j - s_pre[i])];
+        }
+      }
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const uint32_t j = (uint32_t)lane + 64u * r;
-        if (j >= cb[b]) continue;
-        const uint64_t pos = pos0 + j;
+      for (int b = 0; b < kBatch; ++b) {
+        const uint32_t j = j0 + (uint32_t)b * kL2Threads;
+        if (j >= total) break;
+        const uint64_t pos = ubase + j;
         if (pos < cap) {
-          store_nt(p.idx + pos, v[b][r].idx);
-          store_nt(p.val + pos, __uint_as_float(v[b][r].val));
+          store_nt(p.idx + pos, v[b].idx);
+          store_nt(p.val + pos, __uint_as_float(v[b].val));
         } else {
           // selected but not sent: error feedback keeps s
-          const uint32_t tt = t0 + (uint32_t)i;
+          const int kk = tile_owner(p, t0 + s_map[j]);
+          p.t[kk].residual[v[b].idx - p.t[kk].index_base] = __uint_as_float(v[b].val);
+        }
+      }
+    }
+    return;
+  }
+  // A unit with a tile that selected more than a staging slot holds: wave w
+  // copies the staged tiles w * kPerWave onwards, lanes j and j + 64 entries
+  // j and j + 64 of a slot...
+  {
+    constexpr int kPerWave = (int)kL2Unit / kL2Waves;
+    static_assert(kL2Cap == 128, "two entries per lane and slot");
+    for (int i = wid * kPerWave; i < (wid + 1) * kPerWave; ++i) {
+      const uint32_t ci = s_cnt[i];
+      if (ci == 0u || ci > kL2Cap) continue;  // wave-uniform
+      const uint32_t tt = t0 + (uint32_t)i;
+      const Staged* const slot = sc.stage + (uint64_t)tt * kL2Cap;
+      Staged v[2];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const uint32_t j = (uint32_t)lane + 64u * r;
+        v[r] = j < ci ? slot[j] : Staged{0u, 0u};
+      }
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const uint32_t j = (uint32_t)lane + 64u * r;
+        if (j >= ci) continue;
+        const uint64_t pos = ubase + s_pre[i] + j;
+        if (pos < cap) {
+          store_nt(p.idx + pos, v[r].idx);
+          store_nt(p.val + pos, __uint_as_float(v[r].val));
+        } else {
           const int kk = tile_owner(p, tt);
-          p.t[kk].residual[v[b][r].idx - p.t[kk].index_base] = __uint_as_float(v[b][r].val);
+          p.t[kk].residual[v[r].idx - p.t[kk].index_base] = __uint_as_float(v[r].val);
         }
       }
     }
   }
-  if (s_nbig == 0) return;
-  // tiles that selected more than a staging slot holds: their residual holds
-  // s; select again, write the entries in order and zero those that are sent
+  // ...and the block re-derives each such tile from its residual, which
+  // holds s there: select again, write the entries in order and zero those
+  // that are sent
   for (int i = 0; i < (int)kL2Unit; ++i) {
     if (s_cnt[i] <= kL2Cap) continue;  // block-uniform
     const uint32_t tt = t0 + (uint32_t)i;
