@@ -14,15 +14,18 @@ Also measured ("legs"), each on its own synthetic workload:
   * the 32B-shaped set: the in-place form (the snapshot itself refreshed, the
     chainable form), the unfused form (encode, then the standalone scatter
     apply), the same step under the standard-deviation reading of N(0, x)
-    (~4.7% density), the bandwidth ceiling of its read stream, the patch's
-    index streams (delta-varint and 2-D COO downcast) and the weight hash;
+    (~4.7% density), the bandwidth ceilings of its read stream (persistent
+    and one-shot probes) and of the same reads with the whole-line refresh
+    writes and no ordering work, the patch's index streams (delta-varint and
+    2-D COO downcast) and the weight hash;
   * the one-tensor workload (1,048,576 parameters) and the 0.5B-shaped set;
   * the 7B-shaped set chained over 20 steps at lr 3e-7, 1e-6 and 3e-6, the
     snapshot advanced in place each step;
   * PULSELoCo on the 7B-shaped set: 10 rounds of the error-feedback
-    sparsification at a fixed threshold and with the threshold re-chosen each
-    round, the BF16-gate form, the outer step, and the bandwidth ceiling of a
-    read-modify-write stream;
+    sparsification in its two-pass form at a fixed threshold and with the
+    threshold re-chosen each round, the one-pass kernel at the fixed
+    threshold, the BF16-gate form, the outer step, and the bandwidth ceilings
+    of a read-modify-write stream (persistent and one-shot probes, torch.add);
   * FP8/MXFP4 receivers and k-step patches on the 7B-shaped set.
 All inputs are generated on the GPU before timing and stay resident in HBM;
 untimed work between timed steps (restoring a snapshot, the next step's
